@@ -1,0 +1,236 @@
+"""Seeded generators: INT8 per-output-channel weight store, BF16 norms / LM head / KV cache,
+BF16-valued activations, and structured masks.
+
+Every draw uses numpy's PCG64 ``default_rng`` keyed by a list, so a single layer or matrix can be
+regenerated without drawing the ones before it:
+
+* weight matrix m of layer l:  ``default_rng([seed_w, l, m])``, m = 0..6 for wq, wk, wv, wo, wg,
+  wu, wd (row-major ``[out][in]``), N(0, 0.02) in float32;
+* attention / FFN RMSNorm gains of layer l: ``[seed_w, l, 7]`` / ``[seed_w, l, 8]``,
+  BF16(1 + 0.1 N(0, 1)), so that a missing gain multiply is visible;
+* final norm gain: ``[seed_w, L, 0]``; LM head: ``[seed_w, L, 1]``, BF16(N(0, 0.02)) ``[V][d]``;
+* activations: ``[seed_x]``, BF16(N(0, 1)) held in float32;
+* KV cache of layer l: ``[seed_kv, l]``, BF16(N(0, 1)) for positions < pos, K drawn before V.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+from .configs import Shape
+
+__all__ = [
+    "WEIGHT_NAMES", "to_bf16_bits", "bf16_bits_to_f32", "bf16_round", "quantize_rows",
+    "layer_weights", "final_norm", "lm_head", "activations", "kv_prior", "tiny_mask",
+    "budget_mask", "raw_mask", "all_kept_mask", "mask_counts",
+]
+
+WEIGHT_NAMES = ("wq", "wk", "wv", "wo", "wg", "wu", "wd")
+
+
+def to_bf16_bits(a) -> np.ndarray:
+    """float32 -> BF16 bit patterns (uint16), round to nearest even; NaN stays NaN."""
+    a = np.ascontiguousarray(a, dtype=np.float32)
+    u = a.view(np.uint32)
+    lsb = (u >> np.uint32(16)) & np.uint32(1)
+    r = ((u + np.uint32(0x7FFF) + lsb) >> np.uint32(16)).astype(np.uint16)
+    nan = np.isnan(a)
+    if nan.any():
+        r[nan] = np.uint16(0x7FC0)
+    return r
+
+
+def bf16_bits_to_f32(b) -> np.ndarray:
+    b = np.ascontiguousarray(b, dtype=np.uint16)
+    return (b.astype(np.uint32) << np.uint32(16)).view(np.float32)
+
+
+def bf16_round(a) -> np.ndarray:
+    """float32 values rounded to the nearest BF16 value, returned as float32."""
+    return bf16_bits_to_f32(to_bf16_bits(a))
+
+
+def quantize_rows(w: np.ndarray):
+    """Symmetric per-output-row INT8: s_r = max_k |w_rk| / 127 (float32, 1 for an all-zero
+    row), q = clip(rint(w / s_r), -127, 127) with ties to even."""
+    w = np.asarray(w, dtype=np.float32)
+    amax = np.abs(w).max(axis=1)
+    s = (amax / np.float32(127.0)).astype(np.float32)
+    s[amax == 0] = np.float32(1.0)
+    q = np.rint(w / s[:, None])
+    np.clip(q, -127, 127, out=q)
+    return q.astype(np.int8), s
+
+
+def _weight_shapes(sh: Shape):
+    qd, kd = sh.n_q_heads * sh.head_dim, sh.n_kv_heads * sh.head_dim
+    d, f = sh.d_model, sh.d_ffn
+    return {"wq": (qd, d), "wk": (kd, d), "wv": (kd, d), "wo": (d, qd),
+            "wg": (f, d), "wu": (f, d), "wd": (d, f)}
+
+
+def _gain(rng, n):
+    return to_bf16_bits(np.float32(1.0) + np.float32(0.1) * rng.standard_normal(n, dtype=np.float32))
+
+
+def layer_weights(sh: Shape, layer: int, seed_w: int = 0, std: float = 0.02) -> dict:
+    """One decoder layer of the INT8 store.
+
+    Returns ``{name: (int8 [out][in], float32 scale [out])}`` for the seven projections plus
+    ``attn_norm`` / ``ffn_norm`` as BF16 bit patterns ``uint16 [d]``.
+    """
+    out = {}
+    for m, (name, shp) in enumerate(_weight_shapes(sh).items()):
+        rng = np.random.default_rng([seed_w, layer, m])
+        w = rng.standard_normal(shp, dtype=np.float32)
+        w *= np.float32(std)
+        out[name] = quantize_rows(w)
+        del w
+    out["attn_norm"] = _gain(np.random.default_rng([seed_w, layer, 7]), sh.d_model)
+    out["ffn_norm"] = _gain(np.random.default_rng([seed_w, layer, 8]), sh.d_model)
+    return out
+
+
+def final_norm(sh: Shape, seed_w: int = 0) -> np.ndarray:
+    return _gain(np.random.default_rng([seed_w, sh.n_layers, 0]), sh.d_model)
+
+
+def lm_head(sh: Shape, seed_w: int = 0, std: float = 0.02) -> np.ndarray:
+    """BF16 bit patterns ``uint16 [V][d]``."""
+    rng = np.random.default_rng([seed_w, sh.n_layers, 1])
+    w = rng.standard_normal((sh.vocab, sh.d_model), dtype=np.float32)
+    w *= np.float32(std)
+    return to_bf16_bits(w)
+
+
+def activations(n_rows: int, d: int, seed_x: int = 1) -> np.ndarray:
+    """BF16-valued N(0, 1) rows ``float32 [n_rows][d]``."""
+    rng = np.random.default_rng([seed_x])
+    return bf16_round(rng.standard_normal((n_rows, d), dtype=np.float32))
+
+
+def kv_prior(sh: Shape, layer: int, batch: int, pos: int, max_seq: int, seed_kv: int = 2,
+             fill: float = 0.0):
+    """Prior K and V cache contents of one layer as BF16 bits ``uint16 [B][Hkv][S][dh]``.
+
+    Positions < pos hold BF16(N(0, 1)) draws (treated as already rotated keys); positions
+    >= pos hold ``fill`` (use NaN to prove that unwritten rows are never read).
+    """
+    rng = np.random.default_rng([seed_kv, layer])
+    shp = (batch, sh.n_kv_heads, pos, sh.head_dim)
+    kd = rng.standard_normal(shp, dtype=np.float32)
+    vd = rng.standard_normal(shp, dtype=np.float32)
+    full = (batch, sh.n_kv_heads, max_seq, sh.head_dim)
+    fill_bits = to_bf16_bits(np.array([fill], dtype=np.float32))[0]
+    k = np.full(full, fill_bits, dtype=np.uint16)
+    v = np.full(full, fill_bits, dtype=np.uint16)
+    k[:, :, :pos] = to_bf16_bits(kd)
+    v[:, :, :pos] = to_bf16_bits(vd)
+    return k, v
+
+
+# ----------------------------------------------------------------------------------- masks
+
+def all_kept_mask(sh: Shape):
+    L = sh.n_layers
+    return (np.ones((L, sh.n_q_heads), np.uint8), np.ones((L, sh.n_kv_heads), np.uint8),
+            np.ones((L, sh.d_ffn), np.uint8))
+
+
+def tiny_mask(sh: Shape, seed: int = 1):
+    """Drops 2 of 8 query heads (both KV groups stay) and keeps 1024 of 1536 FFN channels,
+    per layer, from ``default_rng(seed)``."""
+    rng = np.random.default_rng(seed)
+    q, kv, f = all_kept_mask(sh)
+    f[:] = 0
+    for l in range(sh.n_layers):
+        drop = rng.choice(sh.n_q_heads, 2, replace=False)
+        q[l, drop] = 0
+        keep = np.sort(rng.choice(sh.d_ffn, sh.d_ffn * 2 // 3, replace=False))
+        f[l, keep] = 1
+    return q, kv, f
+
+
+def raw_mask(sh: Shape, seed: int, p_q=0.7, p_kv=0.8, p_f=0.6):
+    """Independent Bernoulli keep bits per query head, KV group and FFN channel. The result is
+    generally not dependency-closed (a kept head may sit in a dropped group, a kept group may
+    have no kept head), which exercises the closure."""
+    rng = np.random.default_rng([seed, 77])
+    L = sh.n_layers
+    q = (rng.uniform(size=(L, sh.n_q_heads)) < p_q).astype(np.uint8)
+    kv = (rng.uniform(size=(L, sh.n_kv_heads)) < p_kv).astype(np.uint8)
+    f = (rng.uniform(size=(L, sh.d_ffn)) < p_f).astype(np.uint8)
+    return q, kv, f
+
+
+def mask_counts(q, kv, f):
+    """Kept query heads, KV groups and FFN channels per layer of a closed mask."""
+    return q.sum(axis=1), kv.sum(axis=1), f.sum(axis=1)
+
+
+def budget_mask(sh: Shape, seed: int, target: float = 0.57, granule: int = 128):
+    """A structured mask at an active-FLOP budget, drawn per candidate.
+
+    Stands in for the offline mask construction, which is not part of the decode path. Keep
+    probabilities are drawn uniformly in [0.3, 1] per KV group, per query head and per FFN
+    granule of ``granule`` channels, then scaled by one factor (bisection) so that the
+    expected active FLOPs equal ``target`` x dense. Groups, heads and granules are then kept by
+    uniform draws; a head needs its group, and a group with no kept head is dropped. Finally
+    FFN granules are dropped in ascending keep probability while over budget, and added back in
+    descending order while one still fits. The result is dependency-closed by construction.
+    """
+    L, Hq, Hkv = sh.n_layers, sh.n_q_heads, sh.n_kv_heads
+    d, dh, F, r = sh.d_model, sh.head_dim, sh.d_ffn, sh.group_size
+    G = granule
+    assert F % G == 0
+    nG = F // G
+    rng = np.random.default_rng(seed)
+    p_grp = rng.uniform(0.3, 1.0, (L, Hkv))
+    p_head = rng.uniform(0.3, 1.0, (L, Hq))
+    p_ffn = rng.uniform(0.3, 1.0, (L, nG))
+    unit = 4 * d * dh            # one query head or one KV group: its projection rows + columns
+    granule_cost = 6 * d * G      # one FFN granule: gate row, up row and down column per channel
+    dense = L * (unit * (Hq + Hkv) + 6 * d * F)
+    budget = target * dense
+
+    def expected(s):
+        kg = np.minimum(1.0, s * p_grp)
+        kh = np.minimum(1.0, s * p_head).reshape(L, Hkv, r)
+        kf = np.minimum(1.0, s * p_ffn)
+        return unit * float((kg * (1.0 + kh.sum(axis=2))).sum()) + granule_cost * float(kf.sum())
+
+    lo, hi = 0.0, 1.0 / 0.3
+    for _ in range(80):
+        mid = 0.5 * (lo + hi)
+        if expected(mid) > budget:
+            hi = mid
+        else:
+            lo = mid
+    s = lo
+    kg = np.minimum(1.0, s * p_grp)
+    kh = np.minimum(1.0, s * p_head)
+    kf = np.minimum(1.0, s * p_ffn)
+    u_grp = rng.uniform(size=(L, Hkv))
+    u_head = rng.uniform(size=(L, Hq))
+    u_ffn = rng.uniform(size=(L, nG))
+    grp = u_grp < kg
+    head = (u_head < kh) & np.repeat(grp, r, axis=1)
+    grp = grp & head.reshape(L, Hkv, r).any(axis=2)
+    ffn_g = u_ffn < kf
+
+    attn_cost = unit * (int(head.sum()) + int(grp.sum()))
+    cost = attn_cost + granule_cost * int(ffn_g.sum())
+    flat = np.arange(L * nG)
+    pf = p_ffn.ravel()
+    fg = ffn_g.ravel()
+    for idx in np.lexsort((flat, pf)):          # ascending probability, ties by index
+        if cost <= budget:
+            break
+        if fg[idx]:
+            fg[idx] = False
+            cost -= granule_cost
+    for idx in np.lexsort((flat, -pf)):         # descending probability, ties by index
+        if not fg[idx] and cost + granule_cost <= budget:
+            fg[idx] = True
+            cost += granule_cost
+    ffn = np.repeat(fg.reshape(L, nG), G, axis=1)
+    return head.astype(np.uint8), grp.astype(np.uint8), ffn.astype(np.uint8)
