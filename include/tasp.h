@@ -1,0 +1,198 @@
+/*
+ * tasp.h - C ABI of the compiled structured-sparse decoder runtime for MI355X (gfx950).
+ *
+ * A structured mask removes, per decoder layer, whole GQA KV groups together with their query
+ * heads, single query heads inside a kept group, and SwiGLU channels (gate row, up row and down
+ * column together). The mask is closed under those dependencies (paper, Sec. "Dependency-Closed
+ * Masks and Cache-Consistent Routing") and then compiled once into a plan: the retained rows and
+ * columns of every projection are packed into dense contiguous INT8 panels (paper, same section,
+ * and appendix paragraph "Backing-store semantics"), so that every later decode step and prefill
+ * launches only the smaller contractions. The plan stays fixed for prefill and every decode step,
+ * and a KV cache is never reused across plans of different masks (same section).
+ *
+ * Model: Llama-3 style decoder layer. Per layer and token, with residual r (float32):
+ *   n = RMSNorm(r; gamma_attn); [q; k; v] = Wqkv n; RoPE(q, k) at the token position;
+ *   append BF16 k, v to the cache; o = softmax(q K^T / sqrt(d_h)) V per retained head;
+ *   r += Wo o; n2 = RMSNorm(r; gamma_ffn); h = silu(Wg n2) * (Wu n2); r += Wd h.
+ * A stack applies L layers, then logits = W_lm RMSNorm(r; gamma_final) with a dense BF16 LM head.
+ *
+ * Conventions used by every entry point
+ *   - Weights: INT8, row-major [out][in], one float32 scale per output row (W = q * s).
+ *   - Query head h belongs to KV group h / (n_q_heads / n_kv_heads); heads are never regrouped.
+ *   - RoPE: rotate-half pairs (i, i + d_h/2), angle = pos * theta^(-2i/d_h).
+ *   - KV cache: BF16, K and V separate, [n_layers][batch][n_kv_heads][max_seq][head_dim]. Only
+ *     retained groups' rows are read or written. Decode at `pos` writes row `pos` and attends
+ *     over rows 0..pos inclusive, reading the stored BF16 values.
+ *   - Activations x / out: float32; rows of `d_model` (decode: [batch][d_model]).
+ *   - Pointers marked (device) are HIP device pointers; (host) are host pointers.
+ *   - Streams are `hipStream_t` passed as void*; NULL is the default stream.
+ *   - Every device buffer is owned by the caller. The library allocates no device memory and owns
+ *     only a plan's host metadata until tasp_plan_destroy.
+ *   - Errors: all arguments are validated on the host before any work is enqueued; on error
+ *     nothing is enqueued and the status says why. tasp_last_error() gives thread-local detail.
+ *     HIP failures map to TASP_ERR_HIP with the runtime's message. No C++ exception crosses the ABI.
+ */
+#ifndef TASP_H
+#define TASP_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t tasp_status;
+enum {
+  TASP_OK = 0,
+  TASP_ERR_INVALID_ARG = -1,      /* null pointer, negative size, wrong enum value        */
+  TASP_ERR_SHAPE = -2,            /* model or call shape not supported / inconsistent      */
+  TASP_ERR_MASK = -3,             /* mask byte other than 0 or 1                           */
+  TASP_ERR_WORKSPACE = -4,        /* workspace too small or misaligned                     */
+  TASP_ERR_POS_RANGE = -5,        /* pos / pos0 + T outside the cache or the plan's limits */
+  TASP_ERR_CACHE_PLAN_MISMATCH = -6, /* cache bound to a plan of another mask              */
+  TASP_ERR_HIP = -7,              /* HIP runtime error                                     */
+  TASP_ERR_UNSUPPORTED = -8,      /* valid request this build does not implement           */
+  TASP_ERR_INTERNAL = -9          /* device result disagrees with the host's check         */
+};
+
+typedef struct tasp_plan_s* tasp_plan;   /* opaque; immutable after tasp_compile_plan */
+
+/* Model geometry and the plan's capacity limits.
+ *   n_layers >= 1; d_model % 64 == 0; head_dim in {64, 128}; n_q_heads % n_kv_heads == 0 with
+ *   n_q_heads / n_kv_heads <= 8; d_ffn % 16 == 0; vocab = 0 for a bare layer stack (decode
+ *   returns the residual) or > 0 for a stack ending in the BF16 LM head (decode returns logits).
+ *   max_batch in 1..8 (decode batch), max_seq = cache rows per sequence, max_prefill = largest
+ *   prefill chunk T (0: prefill unused, no prefill scratch is reserved). */
+typedef struct {
+  int32_t n_layers, d_model, n_q_heads, n_kv_heads, head_dim, d_ffn, vocab;
+  int32_t max_batch, max_seq, max_prefill;
+  float rms_eps;
+  float reserved0;
+  double rope_theta;
+} tasp_model_desc;
+
+typedef struct {
+  const int8_t* w;        /* (device) int8 [out][in], row-major, 16-byte aligned */
+  const float* scale;     /* (device) float32 [out] */
+} tasp_qmat;
+
+/* One layer of the INT8 store: wq [Hq*dh][d], wk/wv [Hkv*dh][d], wo [d][Hq*dh],
+ * wg/wu [d_ffn][d], wd [d][d_ffn]; attn_norm / ffn_norm are BF16 gains [d] (device). */
+typedef struct {
+  tasp_qmat wq, wk, wv, wo, wg, wu, wd;
+  const uint16_t* attn_norm;
+  const uint16_t* ffn_norm;
+} tasp_layer;
+
+/* The store: layers (host array of n_layers), and for vocab > 0 the final BF16 norm gain [d]
+ * and the dense BF16 LM head [vocab][d] (device). The plan copies what it needs, so the store
+ * may be freed once tasp_compile_plan's stream work has completed. */
+typedef struct {
+  const tasp_layer* layers;
+  const uint16_t* final_norm;
+  const uint16_t* lm_head;
+} tasp_store;
+
+/* Host bytes in {0, 1}: q_keep [n_layers][n_q_heads], kv_keep [n_layers][n_kv_heads] (NULL: all
+ * kept), ffn_keep [n_layers][d_ffn]. A NULL tasp_mask* means the dense (all-kept) plan. A mask
+ * that is not dependency-closed is closed, not rejected: a head in a dropped group is dropped,
+ * and a group with no retained head is dropped. */
+typedef struct {
+  const uint8_t* q_keep;
+  const uint8_t* kv_keep;
+  const uint8_t* ffn_keep;
+} tasp_mask;
+
+/* A caller-owned KV cache (device BF16 arrays, layout above). plan_sig records the plan the
+ * cache contents belong to; it is set by tasp_kv_bind and checked by decode and prefill. */
+typedef struct {
+  void* k;
+  void* v;
+  int32_t batch;          /* sequences in the cache, 1..max_batch */
+  int32_t max_seq;        /* rows per sequence, <= the plan's max_seq */
+  uint64_t plan_sig;
+} tasp_kv_cache;
+
+/* Index lists of tasp_plan_indices. */
+enum { TASP_IDX_Q = 0, TASP_IDX_KV = 1, TASP_IDX_QKVSLOT = 2, TASP_IDX_FFN = 3 };
+/* Panels of tasp_plan_panel. */
+enum { TASP_PANEL_QKV = 0, TASP_PANEL_O = 1, TASP_PANEL_GATE = 2, TASP_PANEL_UP = 3,
+       TASP_PANEL_DOWN = 4 };
+
+/* Workspace bytes that tasp_compile_plan needs for this mask (panels, copies of the gains and
+ * LM head, RoPE table, decode and prefill scratch). The mask is closed on the host to size it. */
+tasp_status tasp_plan_workspace_bytes(const tasp_model_desc* desc, const tasp_mask* mask,
+                                      size_t* bytes);
+
+/* Compile a plan (paper: "packed into contiguous tensors and compiled as static launch plans").
+ * Uploads the mask, runs the closure/index kernel (one workgroup per layer; integer-only), gathers
+ * the retained rows / columns and their scales into the panels inside `workspace` (device, 256-byte
+ * aligned, >= tasp_plan_workspace_bytes), and zeroes the scratch counters. Synchronises `stream`
+ * once to read the index lists back; returns TASP_ERR_INTERNAL if they differ from the host's
+ * closure. The workspace must outlive the plan and must not be shared between plans. */
+tasp_status tasp_compile_plan(const tasp_model_desc* desc, const tasp_store* store,
+                              const tasp_mask* mask, void* workspace, size_t workspace_bytes,
+                              void* stream, tasp_plan* out);
+
+/* Retained counts of one layer after closure: query heads, KV groups, SwiGLU channels. */
+tasp_status tasp_plan_counts(tasp_plan plan, int32_t layer, int32_t* m_q, int32_t* m_kv,
+                             int32_t* n_ffn);
+
+/* Copy one ascending index list of a layer as computed on the device (host dst of cap entries):
+ * TASP_IDX_Q retained query heads, TASP_IDX_KV retained KV groups, TASP_IDX_QKVSLOT the rank of
+ * each retained head's group among the retained groups, TASP_IDX_FFN retained channels. */
+tasp_status tasp_plan_indices(tasp_plan plan, int32_t layer, int32_t which, int32_t* dst,
+                              int32_t cap, int32_t* n);
+
+/* Where a panel of a layer lives: device int8 rows [rows][ld] (columns >= cols are zero) and its
+ * float32 scales [rows]. QKV rows: retained q heads, then K, then V rows of retained groups. */
+tasp_status tasp_plan_panel(tasp_plan plan, int32_t layer, int32_t which, const int8_t** w,
+                            const float** scale, int64_t* rows, int64_t* cols, int64_t* ld);
+
+/* Analytical active-FLOP ratio of the decoder projections (paper, Eqs. flop-attn and flop-mlp;
+ * LM head excluded), retained INT8 weight bytes, float32 scale bytes, and the plan signature
+ * (a hash of the model shape and the closed mask; equal masks give equal signatures). */
+tasp_status tasp_plan_ledger(tasp_plan plan, double* active_flop_ratio, uint64_t* weight_bytes,
+                             uint64_t* scale_bytes, uint64_t* signature);
+
+tasp_status tasp_plan_destroy(tasp_plan plan);
+
+/* Adopt a cache whose rows 0..pos-1 were filled outside the library (already rotated keys) for
+ * this plan: checks its shape and sets cache->plan_sig. */
+tasp_status tasp_kv_bind(tasp_plan plan, tasp_kv_cache* cache);
+
+/* One decode step for cache->batch sequences that share `pos` (prior positions, 0 <= pos <
+ * cache->max_seq). x (device) float32 [batch][d_model]; out (device) float32 [batch][d_model], or
+ * logits [batch][vocab] when the plan has an LM head. x and out may not overlap. Stream-ordered
+ * and asynchronous; launches only the plan's kernels and allocates nothing, so it may be captured
+ * into a HIP graph. Calls on one plan must be ordered (they share the plan's scratch). */
+tasp_status tasp_decode_step(tasp_plan plan, const float* x, tasp_kv_cache* cache, int32_t pos,
+                             float* out, void* stream);
+
+/* Prefill of T tokens of one sequence (cache->batch must be 1) at positions pos0..pos0+T-1,
+ * 1 <= T <= max_prefill, pos0 + T <= cache->max_seq. x (device) float32 [T][d_model]; out
+ * (device) float32 [T][d_model], or logits [T][vocab] with an LM head. Token t attends causally
+ * over rows 0..pos0+t. pos0 == 0 binds the cache to the plan; pos0 > 0 requires it bound. */
+tasp_status tasp_prefill(tasp_plan plan, const float* x, int32_t T, tasp_kv_cache* cache,
+                         int32_t pos0, float* out, void* stream);
+
+/* Profiling variant of tasp_decode_step: records a HIP event pair around every kernel it launches,
+ * synchronises `stream`, and writes each kernel's duration in milliseconds to kernel_ms[i] and a
+ * kernel-kind code to kinds[i] (0 QKV, 1 attention, 2 O, 3 gate/up, 4 down, 5 LM head) for up to
+ * cap kernels; *n receives the number launched. Not capturable (it synchronises). */
+tasp_status tasp_decode_step_timed(tasp_plan plan, const float* x, tasp_kv_cache* cache,
+                                   int32_t pos, float* out, void* stream, float* kernel_ms,
+                                   int32_t* kinds, int32_t cap, int32_t* n);
+
+/* Plain streaming copy of `bytes` (multiple of 16) from src to dst (device): the reference kernel
+ * whose counter readings calibrate memory-traffic measurements. */
+tasp_status tasp_copy_probe(void* dst, const void* src, size_t bytes, void* stream);
+
+const char* tasp_status_string(tasp_status s);
+const char* tasp_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* TASP_H */

@@ -1,0 +1,87 @@
+// Internal launcher interface between the host runtime and the gfx950 kernels.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace tasp {
+
+// ----------------------------------------------------------------- plan compilation
+
+// Closure + ascending index lists for every layer (one workgroup per layer).
+//   q_keep [L][Hq], kv_keep [L][Hkv] (nullable: all kept), ffn_keep [L][F]   (device bytes)
+//   outputs per layer l (device int32): q_idx [l*Hq ..], kv_idx [l*Hkv ..], q_kvslot [l*Hq ..],
+//   slot_start [l*(Hkv+1) ..] (first retained-head position of each retained group, then m_q),
+//   ffn_idx [l*F ..], counts [l*4 ..] = {m_q, m_kv, c, 0}.
+hipError_t launch_closure(const uint8_t* q_keep, const uint8_t* kv_keep, const uint8_t* ffn_keep,
+                          int L, int Hq, int Hkv, int F, int* q_idx, int* kv_idx, int* q_kvslot,
+                          int* slot_start, int* ffn_idx, int* counts, hipStream_t s);
+
+// dst rows [i*dh + e] = src rows [idx[i]*dh + e] for i < n, e < dh; rows of K bytes (K % 16 == 0).
+hipError_t launch_gather_head_rows(int8_t* dst, const int8_t* src, const int* idx, int n, int dh,
+                                   int K, float* dst_scale, const float* src_scale, hipStream_t s);
+// dst rows [i] = src rows [idx[i]] for i < n (rows of K bytes) and the matching scales.
+hipError_t launch_gather_rows(int8_t* dst, const int8_t* src, const int* idx, int n, int K,
+                              float* dst_scale, const float* src_scale, hipStream_t s);
+// dst[r][i*dh + e] = src[r][idx[i]*dh + e] for r < rows; src row stride src_ld, dst stride dst_ld.
+hipError_t launch_gather_head_cols(int8_t* dst, int dst_ld, const int8_t* src, int src_ld,
+                                   const int* idx, int n, int dh, int rows, hipStream_t s);
+// dst[r][j] = src[r][idx[j]] for j < n, zero for n <= j < dst_ld.
+hipError_t launch_gather_cols(int8_t* dst, int dst_ld, const int8_t* src, int src_ld,
+                              const int* idx, int n, int rows, hipStream_t s);
+hipError_t launch_copy(void* dst, const void* src, size_t bytes, hipStream_t s);   // bytes % 16 == 0
+hipError_t launch_fill_zero(void* dst, size_t bytes, hipStream_t s);              // bytes % 4 == 0
+
+// ----------------------------------------------------------------- decode GEMVs
+
+enum GemvMode { GEMV_QKV = 0, GEMV_RESID = 1, GEMV_GATEUP = 2 };
+
+struct GemvArgs {
+  const int8_t* w;       // panel rows [N][ld] (gate/up: gate rows)
+  const int8_t* w2;      // gate/up: up rows [N][ld]
+  const float* scale;    // [N]
+  const float* scale2;   // gate/up: up scales [N]
+  int N;                 // output rows (gate/up: channels)
+  int K;                 // valid columns; columns K..ld-1 of a row are zero
+  int ld;                // row stride in bytes, multiple of 16 and >= K
+  const float* x;        // input rows [B][ldx]
+  int ldx;
+  const uint16_t* gamma; // RMSNorm gain (QKV, gate/up); null: input used as is
+  float eps;
+  const float* resid;    // residual rows [B][ldy] (GEMV_RESID)
+  float* y;              // output rows [B][ldy]
+  int ldy;
+  int B;                 // batch rows (1..8)
+};
+hipError_t launch_gemv(GemvMode mode, const GemvArgs& a, hipStream_t s);
+size_t gemv_lds_bytes(int B, int K);
+
+struct LmHeadArgs {
+  const uint16_t* w;     // BF16 [V][K]
+  int V, K;
+  const float* x; int ldx;
+  const uint16_t* gamma; float eps;
+  float* y; int ldy;     // logits [B][ldy]
+  int B;
+};
+hipError_t launch_lmhead(const LmHeadArgs& a, hipStream_t s);
+
+// ----------------------------------------------------------------- decode attention
+
+struct AttnArgs {
+  const float* qkv; int ld_qkv;    // [B][ld_qkv]: raw q (m_q*dh), k (m_kv*dh), v (m_kv*dh)
+  int m_q, m_kv, dh;
+  const int* kv_idx;               // [m_kv] retained group ids
+  const int* slot_start;           // [m_kv + 1] first head position of each retained group
+  uint16_t* kc; uint16_t* vc;      // this layer's cache base, [B][Hkv][S][dh]
+  int Hkv, S;
+  const float* rope_cos; const float* rope_sin;  // [max_seq][dh/2]
+  int pos, chunk, n_split;
+  float* part;                     // [B][m_kv][n_split][8][dh + 2]
+  int* counters;                   // [B][Hkv], zero between calls
+  float* o; int ld_o;              // [B][ld_o] retained heads in ascending order
+  int B;
+};
+hipError_t launch_attn_decode(const AttnArgs& a, hipStream_t s);
+int attn_max_chunk();
+
+}  // namespace tasp

@@ -1,0 +1,716 @@
+// Host runtime of libtasp: validation, mask closure for sizing and cross-checking, the workspace
+// layout of a plan, plan compilation, and the launch sequences of decode.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "kernels.hpp"
+#include "tasp.h"
+
+struct tasp_plan_s;
+
+namespace {
+
+thread_local std::string g_err;
+
+tasp_status fail(tasp_status s, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return s;
+}
+
+#define HIP_TRY(expr)                                                                   \
+  do {                                                                                  \
+    hipError_t e_ = (expr);                                                             \
+    if (e_ != hipSuccess) return fail(TASP_ERR_HIP, "%s: %s", #expr, hipGetErrorString(e_)); \
+  } while (0)
+
+constexpr size_t kAlign = 256;
+constexpr int kMinChunk = 64;
+constexpr int kAttnTargetBlocks = 1024;
+constexpr size_t kLdsLimit = 160 * 1024 - 1024;
+
+size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+int round_up16(int v) { return (v + 15) / 16 * 16; }
+
+// ----------------------------------------------------------------------- closure on the host
+
+struct Closed {
+  std::vector<uint8_t> q, kv, f;     // closed bits [L][Hq], [L][Hkv], [L][F]
+  std::vector<int> m_q, m_kv, c;
+};
+
+tasp_status check_desc(const tasp_model_desc* d) {
+  if (!d) return fail(TASP_ERR_INVALID_ARG, "desc is NULL");
+  if (d->n_layers < 1 || d->d_model < 16 || d->n_q_heads < 1 || d->n_kv_heads < 1 ||
+      d->d_ffn < 1 || d->vocab < 0 || d->max_batch < 1 || d->max_seq < 1 || d->max_prefill < 0)
+    return fail(TASP_ERR_SHAPE, "non-positive dimension in model desc");
+  if (d->d_model % 16) return fail(TASP_ERR_SHAPE, "d_model %% 16 != 0 (%d)", d->d_model);
+  if (d->head_dim != 64 && d->head_dim != 128)
+    return fail(TASP_ERR_SHAPE, "head_dim must be 64 or 128 (%d)", d->head_dim);
+  if (d->n_q_heads % d->n_kv_heads)
+    return fail(TASP_ERR_SHAPE, "n_q_heads %% n_kv_heads != 0");
+  if (d->n_q_heads / d->n_kv_heads > 8)
+    return fail(TASP_ERR_SHAPE, "more than 8 query heads per KV group");
+  if (d->n_q_heads > 256 || d->n_kv_heads > 64)
+    return fail(TASP_ERR_SHAPE, "at most 256 query heads and 64 KV heads");
+  if (d->d_ffn % 16) return fail(TASP_ERR_SHAPE, "d_ffn %% 16 != 0 (%d)", d->d_ffn);
+  if (d->max_batch > 8) return fail(TASP_ERR_SHAPE, "max_batch > 8");
+  if (!(d->rms_eps > 0.0f) || !(d->rope_theta > 0.0))
+    return fail(TASP_ERR_SHAPE, "rms_eps and rope_theta must be positive");
+  const int widest = std::max({d->d_model, d->n_q_heads * d->head_dim, d->d_ffn});
+  if (tasp::gemv_lds_bytes(d->max_batch, widest) > kLdsLimit)
+    return fail(TASP_ERR_UNSUPPORTED, "max_batch x widest GEMV input exceeds LDS (%d x %d)",
+                d->max_batch, widest);
+  return TASP_OK;
+}
+
+tasp_status host_close(const tasp_model_desc* d, const tasp_mask* m, Closed* out) {
+  const int L = d->n_layers, Hq = d->n_q_heads, Hkv = d->n_kv_heads, F = d->d_ffn;
+  const int r = Hq / Hkv;
+  out->q.assign(size_t(L) * Hq, 1);
+  out->kv.assign(size_t(L) * Hkv, 1);
+  out->f.assign(size_t(L) * F, 1);
+  if (m) {
+    if (!m->q_keep || !m->ffn_keep)
+      return fail(TASP_ERR_INVALID_ARG, "mask q_keep / ffn_keep is NULL");
+    auto check = [](const uint8_t* p, size_t n, const char* what) -> tasp_status {
+      for (size_t i = 0; i < n; ++i)
+        if (p[i] > 1) return fail(TASP_ERR_MASK, "%s[%zu] = %d is not 0 or 1", what, i, int(p[i]));
+      return TASP_OK;
+    };
+    tasp_status s;
+    if ((s = check(m->q_keep, out->q.size(), "q_keep")) != TASP_OK) return s;
+    if (m->kv_keep && (s = check(m->kv_keep, out->kv.size(), "kv_keep")) != TASP_OK) return s;
+    if ((s = check(m->ffn_keep, out->f.size(), "ffn_keep")) != TASP_OK) return s;
+    for (int l = 0; l < L; ++l)
+      for (int h = 0; h < Hq; ++h) {
+        const bool g_in = m->kv_keep ? m->kv_keep[size_t(l) * Hkv + h / r] != 0 : true;
+        out->q[size_t(l) * Hq + h] = (m->q_keep[size_t(l) * Hq + h] != 0) && g_in;
+      }
+    std::memcpy(out->f.data(), m->ffn_keep, out->f.size());
+  }
+  out->m_q.assign(L, 0);
+  out->m_kv.assign(L, 0);
+  out->c.assign(L, 0);
+  for (int l = 0; l < L; ++l) {
+    for (int g = 0; g < Hkv; ++g) {
+      uint8_t any = 0;
+      for (int h = g * r; h < (g + 1) * r; ++h) any |= out->q[size_t(l) * Hq + h];
+      out->kv[size_t(l) * Hkv + g] = any;
+      out->m_kv[l] += any;
+    }
+    for (int h = 0; h < Hq; ++h) out->m_q[l] += out->q[size_t(l) * Hq + h];
+    for (int j = 0; j < F; ++j) out->c[l] += out->f[size_t(l) * F + j];
+  }
+  return TASP_OK;
+}
+
+// ----------------------------------------------------------------------- workspace layout
+
+struct LayerLayout {
+  size_t qkv, s_qkv, o, s_o, g, u, s_g, s_u, dn, s_d, an, fn;
+  int n_qkv, ld_o, ld_d;
+};
+
+struct Layout {
+  std::vector<LayerLayout> layers;
+  size_t mask_q, mask_kv, mask_f;
+  size_t idx_q, idx_kv, idx_slot, idx_slot_start, idx_ffn, counts;
+  size_t final_norm, lm_head, rope_cos, rope_sin;
+  size_t r_mid, r_io0, r_io1, qkv_buf, o_buf, h_buf, part, counters;
+  size_t zero_begin, zero_end;       // scratch cleared at compile
+  size_t total;
+  int n_split_max, ld_qkv, ld_obuf, ld_h;
+};
+
+Layout make_layout(const tasp_model_desc* d, const Closed& c) {
+  Layout Y;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = off;
+    off = align_up(off + bytes, kAlign);
+    return at;
+  };
+  const int L = d->n_layers, D = d->d_model, Hq = d->n_q_heads, Hkv = d->n_kv_heads;
+  const int dh = d->head_dim, F = d->d_ffn, B = d->max_batch;
+  Y.layers.resize(L);
+  for (int l = 0; l < L; ++l) {
+    LayerLayout& P = Y.layers[l];
+    P.n_qkv = (c.m_q[l] + 2 * c.m_kv[l]) * dh;
+    P.ld_o = c.m_q[l] * dh;
+    P.ld_d = round_up16(c.c[l]);
+    P.qkv = take(size_t(P.n_qkv) * D);
+    P.s_qkv = take(size_t(P.n_qkv) * 4);
+    P.o = take(size_t(D) * P.ld_o);
+    P.s_o = take(size_t(D) * 4);
+    P.g = take(size_t(c.c[l]) * D);
+    P.u = take(size_t(c.c[l]) * D);
+    P.s_g = take(size_t(c.c[l]) * 4);
+    P.s_u = take(size_t(c.c[l]) * 4);
+    P.dn = take(size_t(D) * P.ld_d);
+    P.s_d = take(size_t(D) * 4);
+    P.an = take(size_t(D) * 2);
+    P.fn = take(size_t(D) * 2);
+  }
+  Y.mask_q = take(size_t(L) * Hq);
+  Y.mask_kv = take(size_t(L) * Hkv);
+  Y.mask_f = take(size_t(L) * F);
+  Y.idx_q = take(size_t(L) * Hq * 4);
+  Y.idx_kv = take(size_t(L) * Hkv * 4);
+  Y.idx_slot = take(size_t(L) * Hq * 4);
+  Y.idx_slot_start = take(size_t(L) * (Hkv + 1) * 4);
+  Y.idx_ffn = take(size_t(L) * F * 4);
+  Y.counts = take(size_t(L) * 4 * 4);
+  Y.final_norm = d->vocab ? take(size_t(D) * 2) : 0;
+  Y.lm_head = d->vocab ? take(size_t(d->vocab) * D * 2) : 0;
+  Y.rope_cos = take(size_t(d->max_seq) * (dh / 2) * 4);
+  Y.rope_sin = take(size_t(d->max_seq) * (dh / 2) * 4);
+  Y.n_split_max = (d->max_seq + kMinChunk - 1) / kMinChunk;
+  Y.ld_qkv = (Hq + 2 * Hkv) * dh;
+  Y.ld_obuf = Hq * dh;
+  Y.ld_h = round_up16(F);
+  Y.zero_begin = off;
+  Y.r_mid = take(size_t(B) * D * 4);
+  Y.r_io0 = take(size_t(B) * D * 4);
+  Y.r_io1 = take(size_t(B) * D * 4);
+  Y.qkv_buf = take(size_t(B) * Y.ld_qkv * 4);
+  Y.o_buf = take(size_t(B) * Y.ld_obuf * 4);
+  Y.h_buf = take(size_t(B) * Y.ld_h * 4);
+  Y.part = take(size_t(B) * Hkv * Y.n_split_max * 8 * (dh + 2) * 4);
+  Y.counters = take(size_t(B) * Hkv * 4);
+  Y.zero_end = off;
+  Y.total = off;
+  return Y;
+}
+
+uint64_t fnv1a(uint64_t h, const void* p, size_t n) {
+  const uint8_t* b = static_cast<const uint8_t*>(p);
+  for (size_t i = 0; i < n; ++i) {
+    h ^= b[i];
+    h *= 1099511628211ull;
+  }
+  return h;
+}
+
+// Retained per-token FLOPs of one layer (paper, Eqs. flop-attn and flop-mlp).
+double layer_flops(const tasp_model_desc* d, int m_q, int m_kv, int c) {
+  const double D = d->d_model, dh = d->head_dim;
+  return 2.0 * D * dh * (m_q + 2.0 * m_kv) + 2.0 * dh * m_q * D + 6.0 * D * c;
+}
+
+}  // namespace
+
+// ------------------------------------------------------------------------------- the plan
+
+struct LayerPlan {
+  int m_q, m_kv, c, n_qkv, ld_o, ld_d;
+  int8_t *qkv, *o, *g, *u, *dn;
+  float *s_qkv, *s_o, *s_g, *s_u, *s_d;
+  uint16_t *an, *fn;
+  int *d_kv_idx, *d_slot_start;
+  std::vector<int> q_idx, kv_idx, q_kvslot, ffn_idx;
+};
+
+struct tasp_plan_s {
+  tasp_model_desc desc;
+  uint64_t sig;
+  double ratio;
+  uint64_t weight_bytes, scale_bytes;
+  std::vector<LayerPlan> layers;
+  uint16_t *final_norm, *lm_head;
+  float *rope_cos, *rope_sin;
+  float *r_mid, *r_io[2], *qkv_buf, *o_buf, *h_buf, *part;
+  int* counters;
+  int n_split_max, ld_qkv, ld_obuf, ld_h;
+};
+
+namespace {
+
+struct Timer {
+  std::vector<hipEvent_t> ev;
+  std::vector<int> kinds;
+};
+
+template <class F>
+tasp_status run_kernel(Timer* tm, int kind, hipStream_t s, F&& launch) {
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  if (tm) {
+    HIP_TRY(hipEventCreate(&e0));
+    HIP_TRY(hipEventCreate(&e1));
+    tm->ev.push_back(e0);
+    tm->ev.push_back(e1);
+    tm->kinds.push_back(kind);
+    HIP_TRY(hipEventRecord(e0, s));
+  }
+  const hipError_t e = launch();
+  if (e != hipSuccess) return fail(TASP_ERR_HIP, "kernel launch (kind %d): %s", kind, hipGetErrorString(e));
+  if (tm) HIP_TRY(hipEventRecord(e1, s));
+  return TASP_OK;
+}
+
+tasp_status check_cache(const tasp_plan_s* p, const tasp_kv_cache* c) {
+  if (!c) return fail(TASP_ERR_INVALID_ARG, "cache is NULL");
+  if (!c->k || !c->v) return fail(TASP_ERR_INVALID_ARG, "cache k / v is NULL");
+  if (c->batch < 1 || c->batch > p->desc.max_batch)
+    return fail(TASP_ERR_SHAPE, "cache batch %d outside 1..%d", c->batch, p->desc.max_batch);
+  if (c->max_seq < 1 || c->max_seq > p->desc.max_seq)
+    return fail(TASP_ERR_SHAPE, "cache max_seq %d outside 1..%d", c->max_seq, p->desc.max_seq);
+  return TASP_OK;
+}
+
+tasp_status decode_impl(tasp_plan p, const float* x, tasp_kv_cache* cache, int32_t pos,
+                        float* out, void* stream, Timer* tm) {
+  if (!p) return fail(TASP_ERR_INVALID_ARG, "plan is NULL");
+  if (!x || !out) return fail(TASP_ERR_INVALID_ARG, "x / out is NULL");
+  tasp_status st = check_cache(p, cache);
+  if (st != TASP_OK) return st;
+  if (cache->plan_sig != p->sig)
+    return fail(TASP_ERR_CACHE_PLAN_MISMATCH, "cache belongs to plan %016llx, not %016llx",
+                (unsigned long long)cache->plan_sig, (unsigned long long)p->sig);
+  if (pos < 0 || pos >= cache->max_seq)
+    return fail(TASP_ERR_POS_RANGE, "pos %d outside 0..%d", pos, cache->max_seq - 1);
+  const tasp_model_desc& d = p->desc;
+  const int B = cache->batch, D = d.d_model, dh = d.head_dim, L = d.n_layers;
+  const size_t out_elems = size_t(B) * (d.vocab ? d.vocab : D);
+  const char* xb = reinterpret_cast<const char*>(x);
+  const char* ob = reinterpret_cast<const char*>(out);
+  if (ob < xb + size_t(B) * D * 4 && xb < ob + out_elems * 4)
+    return fail(TASP_ERR_INVALID_ARG, "x and out overlap");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const size_t layer_cache = size_t(B) * d.n_kv_heads * cache->max_seq * dh;
+  const int total = pos + 1;
+
+  for (int l = 0; l < L; ++l) {
+    const LayerPlan& P = p->layers[l];
+    const float* in = (l == 0) ? x : p->r_io[(l - 1) & 1];
+    float* lo = (l == L - 1 && d.vocab == 0) ? out : p->r_io[l & 1];
+    if (P.n_qkv > 0) {
+      tasp::GemvArgs a{};
+      a.w = P.qkv; a.scale = P.s_qkv; a.N = P.n_qkv; a.K = D; a.ld = D;
+      a.x = in; a.ldx = D; a.gamma = P.an; a.eps = d.rms_eps; a.y = p->qkv_buf;
+      a.ldy = p->ld_qkv; a.B = B;
+      if ((st = run_kernel(tm, 0, s, [&] { return tasp::launch_gemv(tasp::GEMV_QKV, a, s); })))
+        return st;
+    }
+    if (P.m_kv > 0) {
+      tasp::AttnArgs a{};
+      long want = (long(total) * P.m_kv * B + kAttnTargetBlocks - 1) / kAttnTargetBlocks;
+      int chunk = int(std::min<long>(std::max<long>(want, kMinChunk), tasp::attn_max_chunk()));
+      chunk = (chunk + kMinChunk - 1) / kMinChunk * kMinChunk;
+      a.qkv = p->qkv_buf; a.ld_qkv = p->ld_qkv; a.m_q = P.m_q; a.m_kv = P.m_kv; a.dh = dh;
+      a.kv_idx = P.d_kv_idx; a.slot_start = P.d_slot_start;
+      a.kc = static_cast<uint16_t*>(cache->k) + l * layer_cache;
+      a.vc = static_cast<uint16_t*>(cache->v) + l * layer_cache;
+      a.Hkv = d.n_kv_heads; a.S = cache->max_seq; a.rope_cos = p->rope_cos;
+      a.rope_sin = p->rope_sin; a.pos = pos; a.chunk = chunk;
+      a.n_split = (total + chunk - 1) / chunk; a.part = p->part; a.counters = p->counters;
+      a.o = p->o_buf; a.ld_o = p->ld_obuf; a.B = B;
+      if ((st = run_kernel(tm, 1, s, [&] { return tasp::launch_attn_decode(a, s); }))) return st;
+    }
+    {
+      tasp::GemvArgs a{};
+      a.w = P.o; a.scale = P.s_o; a.N = D; a.K = P.m_q * dh; a.ld = P.ld_o; a.x = p->o_buf;
+      a.ldx = p->ld_obuf; a.resid = in; a.y = p->r_mid; a.ldy = D; a.B = B;
+      if ((st = run_kernel(tm, 2, s, [&] { return tasp::launch_gemv(tasp::GEMV_RESID, a, s); })))
+        return st;
+    }
+    if (P.c > 0) {
+      tasp::GemvArgs a{};
+      a.w = P.g; a.w2 = P.u; a.scale = P.s_g; a.scale2 = P.s_u; a.N = P.c; a.K = D; a.ld = D;
+      a.x = p->r_mid; a.ldx = D; a.gamma = P.fn; a.eps = d.rms_eps; a.y = p->h_buf;
+      a.ldy = p->ld_h; a.B = B;
+      if ((st = run_kernel(tm, 3, s, [&] { return tasp::launch_gemv(tasp::GEMV_GATEUP, a, s); })))
+        return st;
+    }
+    {
+      tasp::GemvArgs a{};
+      a.w = P.dn; a.scale = P.s_d; a.N = D; a.K = P.c; a.ld = P.ld_d; a.x = p->h_buf;
+      a.ldx = p->ld_h; a.resid = p->r_mid; a.y = lo; a.ldy = D; a.B = B;
+      if ((st = run_kernel(tm, 4, s, [&] { return tasp::launch_gemv(tasp::GEMV_RESID, a, s); })))
+        return st;
+    }
+  }
+  if (d.vocab) {
+    tasp::LmHeadArgs a{};
+    a.w = p->lm_head; a.V = d.vocab; a.K = D; a.x = p->r_io[(L - 1) & 1]; a.ldx = D;
+    a.gamma = p->final_norm; a.eps = d.rms_eps; a.y = out; a.ldy = d.vocab; a.B = B;
+    if ((st = run_kernel(tm, 5, s, [&] { return tasp::launch_lmhead(a, s); }))) return st;
+  }
+  return TASP_OK;
+}
+
+}  // namespace
+
+// ------------------------------------------------------------------------------- C ABI
+
+extern "C" {
+
+const char* tasp_status_string(tasp_status s) {
+  switch (s) {
+    case TASP_OK: return "ok";
+    case TASP_ERR_INVALID_ARG: return "invalid argument";
+    case TASP_ERR_SHAPE: return "unsupported or inconsistent shape";
+    case TASP_ERR_MASK: return "mask byte not 0 or 1";
+    case TASP_ERR_WORKSPACE: return "workspace too small or misaligned";
+    case TASP_ERR_POS_RANGE: return "position out of range";
+    case TASP_ERR_CACHE_PLAN_MISMATCH: return "KV cache belongs to another plan";
+    case TASP_ERR_HIP: return "HIP runtime error";
+    case TASP_ERR_UNSUPPORTED: return "unsupported";
+    case TASP_ERR_INTERNAL: return "internal consistency check failed";
+  }
+  return "unknown status";
+}
+
+const char* tasp_last_error(void) { return g_err.c_str(); }
+
+tasp_status tasp_plan_workspace_bytes(const tasp_model_desc* desc, const tasp_mask* mask,
+                                      size_t* bytes) {
+  tasp_status st = check_desc(desc);
+  if (st != TASP_OK) return st;
+  if (!bytes) return fail(TASP_ERR_INVALID_ARG, "bytes is NULL");
+  Closed c;
+  if ((st = host_close(desc, mask, &c)) != TASP_OK) return st;
+  *bytes = make_layout(desc, c).total;
+  return TASP_OK;
+}
+
+tasp_status tasp_compile_plan(const tasp_model_desc* desc, const tasp_store* store,
+                              const tasp_mask* mask, void* workspace, size_t workspace_bytes,
+                              void* stream, tasp_plan* out) {
+  tasp_status st = check_desc(desc);
+  if (st != TASP_OK) return st;
+  if (!store || !store->layers || !out) return fail(TASP_ERR_INVALID_ARG, "store / out is NULL");
+  if (!workspace) return fail(TASP_ERR_INVALID_ARG, "workspace is NULL");
+  if (reinterpret_cast<uintptr_t>(workspace) % kAlign)
+    return fail(TASP_ERR_WORKSPACE, "workspace not %zu-byte aligned", kAlign);
+  const tasp_model_desc& d = *desc;
+  for (int l = 0; l < d.n_layers; ++l) {
+    const tasp_layer& S = store->layers[l];
+    const tasp_qmat* mats[7] = {&S.wq, &S.wk, &S.wv, &S.wo, &S.wg, &S.wu, &S.wd};
+    for (const tasp_qmat* m : mats)
+      if (!m->w || !m->scale) return fail(TASP_ERR_INVALID_ARG, "layer %d: NULL weight", l);
+    if (!S.attn_norm || !S.ffn_norm) return fail(TASP_ERR_INVALID_ARG, "layer %d: NULL gain", l);
+    for (const tasp_qmat* m : mats)
+      if (reinterpret_cast<uintptr_t>(m->w) % 16)
+        return fail(TASP_ERR_INVALID_ARG, "layer %d: weight not 16-byte aligned", l);
+  }
+  if (d.vocab && (!store->final_norm || !store->lm_head))
+    return fail(TASP_ERR_INVALID_ARG, "vocab > 0 but final_norm / lm_head is NULL");
+  Closed c;
+  if ((st = host_close(desc, mask, &c)) != TASP_OK) return st;
+  const Layout Y = make_layout(desc, c);
+  if (workspace_bytes < Y.total)
+    return fail(TASP_ERR_WORKSPACE, "workspace %zu < %zu bytes", workspace_bytes, Y.total);
+
+  const int L = d.n_layers, D = d.d_model, Hq = d.n_q_heads, Hkv = d.n_kv_heads;
+  const int dh = d.head_dim, F = d.d_ffn;
+  char* ws = static_cast<char*>(workspace);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  auto at = [&](size_t off) { return ws + off; };
+
+  // device closure over the caller's (possibly not closed) mask bits
+  std::vector<uint8_t> ones_q, ones_f;
+  const uint8_t* hq = mask ? mask->q_keep : nullptr;
+  const uint8_t* hf = mask ? mask->ffn_keep : nullptr;
+  if (!hq) { ones_q.assign(size_t(L) * Hq, 1); hq = ones_q.data(); }
+  if (!hf) { ones_f.assign(size_t(L) * F, 1); hf = ones_f.data(); }
+  const bool has_kv = mask && mask->kv_keep;
+  HIP_TRY(hipMemcpyAsync(at(Y.mask_q), hq, size_t(L) * Hq, hipMemcpyHostToDevice, s));
+  if (has_kv)
+    HIP_TRY(hipMemcpyAsync(at(Y.mask_kv), mask->kv_keep, size_t(L) * Hkv, hipMemcpyHostToDevice, s));
+  HIP_TRY(hipMemcpyAsync(at(Y.mask_f), hf, size_t(L) * F, hipMemcpyHostToDevice, s));
+  int* dq = reinterpret_cast<int*>(at(Y.idx_q));
+  int* dkv = reinterpret_cast<int*>(at(Y.idx_kv));
+  int* dslot = reinterpret_cast<int*>(at(Y.idx_slot));
+  int* dss = reinterpret_cast<int*>(at(Y.idx_slot_start));
+  int* dffn = reinterpret_cast<int*>(at(Y.idx_ffn));
+  int* dcnt = reinterpret_cast<int*>(at(Y.counts));
+  HIP_TRY(tasp::launch_closure(reinterpret_cast<uint8_t*>(at(Y.mask_q)),
+                               has_kv ? reinterpret_cast<uint8_t*>(at(Y.mask_kv)) : nullptr,
+                               reinterpret_cast<uint8_t*>(at(Y.mask_f)), L, Hq, Hkv, F, dq, dkv,
+                               dslot, dss, dffn, dcnt, s));
+
+  tasp_plan_s* p = new (std::nothrow) tasp_plan_s();
+  if (!p) return fail(TASP_ERR_INTERNAL, "out of host memory");
+  p->desc = d;
+  p->layers.resize(L);
+  for (int l = 0; l < L; ++l) {
+    const LayerLayout& Q = Y.layers[l];
+    const tasp_layer& S = store->layers[l];
+    LayerPlan& P = p->layers[l];
+    P.m_q = c.m_q[l]; P.m_kv = c.m_kv[l]; P.c = c.c[l];
+    P.n_qkv = Q.n_qkv; P.ld_o = Q.ld_o; P.ld_d = Q.ld_d;
+    P.qkv = reinterpret_cast<int8_t*>(at(Q.qkv)); P.s_qkv = reinterpret_cast<float*>(at(Q.s_qkv));
+    P.o = reinterpret_cast<int8_t*>(at(Q.o)); P.s_o = reinterpret_cast<float*>(at(Q.s_o));
+    P.g = reinterpret_cast<int8_t*>(at(Q.g)); P.u = reinterpret_cast<int8_t*>(at(Q.u));
+    P.s_g = reinterpret_cast<float*>(at(Q.s_g)); P.s_u = reinterpret_cast<float*>(at(Q.s_u));
+    P.dn = reinterpret_cast<int8_t*>(at(Q.dn)); P.s_d = reinterpret_cast<float*>(at(Q.s_d));
+    P.an = reinterpret_cast<uint16_t*>(at(Q.an)); P.fn = reinterpret_cast<uint16_t*>(at(Q.fn));
+    P.d_kv_idx = dkv + size_t(l) * Hkv;
+    P.d_slot_start = dss + size_t(l) * (Hkv + 1);
+    const int* lq = dq + size_t(l) * Hq;
+    const int* lkv = dkv + size_t(l) * Hkv;
+    const int* lf = dffn + size_t(l) * F;
+    tasp_status e = TASP_OK;
+    auto chk = [&](hipError_t h) {
+      if (h != hipSuccess && e == TASP_OK) e = fail(TASP_ERR_HIP, "gather: %s", hipGetErrorString(h));
+    };
+    const int mq = P.m_q, mkv = P.m_kv;
+    chk(tasp::launch_gather_head_rows(P.qkv, S.wq.w, lq, mq, dh, D, P.s_qkv, S.wq.scale, s));
+    chk(tasp::launch_gather_head_rows(P.qkv + size_t(mq) * dh * D, S.wk.w, lkv, mkv, dh, D,
+                                      P.s_qkv + mq * dh, S.wk.scale, s));
+    chk(tasp::launch_gather_head_rows(P.qkv + size_t(mq + mkv) * dh * D, S.wv.w, lkv, mkv, dh, D,
+                                      P.s_qkv + (mq + mkv) * dh, S.wv.scale, s));
+    chk(tasp::launch_gather_head_cols(P.o, P.ld_o, S.wo.w, Hq * dh, lq, mq, dh, D, s));
+    chk(tasp::launch_copy(P.s_o, S.wo.scale, size_t(D) * 4, s));
+    chk(tasp::launch_gather_rows(P.g, S.wg.w, lf, P.c, D, P.s_g, S.wg.scale, s));
+    chk(tasp::launch_gather_rows(P.u, S.wu.w, lf, P.c, D, P.s_u, S.wu.scale, s));
+    chk(tasp::launch_gather_cols(P.dn, P.ld_d, S.wd.w, F, lf, P.c, D, s));
+    chk(tasp::launch_copy(P.s_d, S.wd.scale, size_t(D) * 4, s));
+    chk(tasp::launch_copy(P.an, S.attn_norm, size_t(D) * 2, s));
+    chk(tasp::launch_copy(P.fn, S.ffn_norm, size_t(D) * 2, s));
+    if (e != TASP_OK) { (void)hipStreamSynchronize(s); delete p; return e; }
+  }
+  if (d.vocab) {
+    p->final_norm = reinterpret_cast<uint16_t*>(at(Y.final_norm));
+    p->lm_head = reinterpret_cast<uint16_t*>(at(Y.lm_head));
+    hipError_t h = tasp::launch_copy(p->final_norm, store->final_norm, size_t(D) * 2, s);
+    if (h == hipSuccess) h = tasp::launch_copy(p->lm_head, store->lm_head, size_t(d.vocab) * D * 2, s);
+    if (h != hipSuccess) {
+      (void)hipStreamSynchronize(s);
+      delete p;
+      return fail(TASP_ERR_HIP, "LM head copy: %s", hipGetErrorString(h));
+    }
+  } else {
+    p->final_norm = p->lm_head = nullptr;
+  }
+  // rotary table: angle pos * theta^(-2i/dh) evaluated in double, stored as float
+  const int half = dh / 2;
+  std::vector<float> tc(size_t(d.max_seq) * half), ts(size_t(d.max_seq) * half);
+  for (int t = 0; t < d.max_seq; ++t)
+    for (int i = 0; i < half; ++i) {
+      const double ang = double(t) * std::pow(d.rope_theta, -2.0 * i / dh);
+      tc[size_t(t) * half + i] = float(std::cos(ang));
+      ts[size_t(t) * half + i] = float(std::sin(ang));
+    }
+  p->rope_cos = reinterpret_cast<float*>(at(Y.rope_cos));
+  p->rope_sin = reinterpret_cast<float*>(at(Y.rope_sin));
+  hipError_t h = hipMemcpyAsync(p->rope_cos, tc.data(), tc.size() * 4, hipMemcpyHostToDevice, s);
+  if (h == hipSuccess) h = hipMemcpyAsync(p->rope_sin, ts.data(), ts.size() * 4, hipMemcpyHostToDevice, s);
+  if (h == hipSuccess) h = tasp::launch_fill_zero(at(Y.zero_begin), Y.zero_end - Y.zero_begin, s);
+  p->r_mid = reinterpret_cast<float*>(at(Y.r_mid));
+  p->r_io[0] = reinterpret_cast<float*>(at(Y.r_io0));
+  p->r_io[1] = reinterpret_cast<float*>(at(Y.r_io1));
+  p->qkv_buf = reinterpret_cast<float*>(at(Y.qkv_buf));
+  p->o_buf = reinterpret_cast<float*>(at(Y.o_buf));
+  p->h_buf = reinterpret_cast<float*>(at(Y.h_buf));
+  p->part = reinterpret_cast<float*>(at(Y.part));
+  p->counters = reinterpret_cast<int*>(at(Y.counters));
+  p->n_split_max = Y.n_split_max; p->ld_qkv = Y.ld_qkv; p->ld_obuf = Y.ld_obuf; p->ld_h = Y.ld_h;
+
+  // read the device index lists back (the one synchronisation) and check them
+  std::vector<int> hq_idx(size_t(L) * Hq), hkv_idx(size_t(L) * Hkv), hslot(size_t(L) * Hq),
+      hffn(size_t(L) * F), hcnt(size_t(L) * 4);
+  if (h == hipSuccess) h = hipMemcpyAsync(hq_idx.data(), dq, hq_idx.size() * 4, hipMemcpyDeviceToHost, s);
+  if (h == hipSuccess) h = hipMemcpyAsync(hkv_idx.data(), dkv, hkv_idx.size() * 4, hipMemcpyDeviceToHost, s);
+  if (h == hipSuccess) h = hipMemcpyAsync(hslot.data(), dslot, hslot.size() * 4, hipMemcpyDeviceToHost, s);
+  if (h == hipSuccess) h = hipMemcpyAsync(hffn.data(), dffn, hffn.size() * 4, hipMemcpyDeviceToHost, s);
+  if (h == hipSuccess) h = hipMemcpyAsync(hcnt.data(), dcnt, hcnt.size() * 4, hipMemcpyDeviceToHost, s);
+  if (h == hipSuccess) h = hipStreamSynchronize(s);
+  if (h != hipSuccess) {
+    (void)hipStreamSynchronize(s);
+    delete p;
+    return fail(TASP_ERR_HIP, "compile: %s", hipGetErrorString(h));
+  }
+  const int r = Hq / Hkv;
+  for (int l = 0; l < L; ++l) {
+    LayerPlan& P = p->layers[l];
+    if (hcnt[l * 4] != P.m_q || hcnt[l * 4 + 1] != P.m_kv || hcnt[l * 4 + 2] != P.c) {
+      delete p;
+      return fail(TASP_ERR_INTERNAL, "layer %d: device counts (%d,%d,%d) != host (%d,%d,%d)", l,
+                  hcnt[l * 4], hcnt[l * 4 + 1], hcnt[l * 4 + 2], P.m_q, P.m_kv, P.c);
+    }
+    P.q_idx.assign(hq_idx.begin() + size_t(l) * Hq, hq_idx.begin() + size_t(l) * Hq + P.m_q);
+    P.q_kvslot.assign(hslot.begin() + size_t(l) * Hq, hslot.begin() + size_t(l) * Hq + P.m_q);
+    P.kv_idx.assign(hkv_idx.begin() + size_t(l) * Hkv, hkv_idx.begin() + size_t(l) * Hkv + P.m_kv);
+    P.ffn_idx.assign(hffn.begin() + size_t(l) * F, hffn.begin() + size_t(l) * F + P.c);
+    bool ok = true;
+    int k = 0;
+    for (int hh = 0; hh < Hq; ++hh)
+      if (c.q[size_t(l) * Hq + hh]) ok &= (k < P.m_q && P.q_idx[k++] == hh);
+    k = 0;
+    for (int g = 0; g < Hkv; ++g)
+      if (c.kv[size_t(l) * Hkv + g]) ok &= (k < P.m_kv && P.kv_idx[k++] == g);
+    k = 0;
+    for (int j = 0; j < F; ++j)
+      if (c.f[size_t(l) * F + j]) ok &= (k < P.c && P.ffn_idx[k++] == j);
+    for (int i = 0; i < P.m_q && ok; ++i)
+      ok &= P.q_kvslot[i] >= 0 && P.q_kvslot[i] < P.m_kv && P.kv_idx[P.q_kvslot[i]] == P.q_idx[i] / r;
+    if (!ok) {
+      delete p;
+      return fail(TASP_ERR_INTERNAL, "layer %d: device index lists differ from the host closure", l);
+    }
+  }
+  // ledger and signature
+  double num = 0.0, den = 0.0;
+  uint64_t wb = 0, sb = 0;
+  for (int l = 0; l < L; ++l) {
+    const LayerPlan& P = p->layers[l];
+    num += layer_flops(desc, P.m_q, P.m_kv, P.c);
+    den += layer_flops(desc, Hq, Hkv, F);
+    wb += uint64_t(P.n_qkv) * D + uint64_t(D) * P.m_q * dh + 3ull * D * P.c;
+    sb += 4ull * (uint64_t(P.n_qkv) + D + 2ull * P.c + D);
+  }
+  p->ratio = num / den;
+  p->weight_bytes = wb;
+  p->scale_bytes = sb;
+  uint64_t sig = 1469598103934665603ull;
+  const int32_t shape[7] = {d.n_layers, d.d_model, d.n_q_heads, d.n_kv_heads, d.head_dim, d.d_ffn, d.vocab};
+  sig = fnv1a(sig, shape, sizeof shape);
+  sig = fnv1a(sig, c.q.data(), c.q.size());
+  sig = fnv1a(sig, c.kv.data(), c.kv.size());
+  sig = fnv1a(sig, c.f.data(), c.f.size());
+  p->sig = sig ? sig : 1;
+  *out = p;
+  return TASP_OK;
+}
+
+tasp_status tasp_plan_counts(tasp_plan p, int32_t layer, int32_t* m_q, int32_t* m_kv,
+                             int32_t* n_ffn) {
+  if (!p) return fail(TASP_ERR_INVALID_ARG, "plan is NULL");
+  if (layer < 0 || layer >= p->desc.n_layers) return fail(TASP_ERR_INVALID_ARG, "bad layer %d", layer);
+  const LayerPlan& P = p->layers[layer];
+  if (m_q) *m_q = P.m_q;
+  if (m_kv) *m_kv = P.m_kv;
+  if (n_ffn) *n_ffn = P.c;
+  return TASP_OK;
+}
+
+tasp_status tasp_plan_indices(tasp_plan p, int32_t layer, int32_t which, int32_t* dst,
+                              int32_t cap, int32_t* n) {
+  if (!p) return fail(TASP_ERR_INVALID_ARG, "plan is NULL");
+  if (layer < 0 || layer >= p->desc.n_layers) return fail(TASP_ERR_INVALID_ARG, "bad layer %d", layer);
+  const LayerPlan& P = p->layers[layer];
+  const std::vector<int>* v = nullptr;
+  switch (which) {
+    case TASP_IDX_Q: v = &P.q_idx; break;
+    case TASP_IDX_KV: v = &P.kv_idx; break;
+    case TASP_IDX_QKVSLOT: v = &P.q_kvslot; break;
+    case TASP_IDX_FFN: v = &P.ffn_idx; break;
+    default: return fail(TASP_ERR_INVALID_ARG, "bad index list %d", which);
+  }
+  if (n) *n = int32_t(v->size());
+  if (!dst) return TASP_OK;
+  if (cap < int32_t(v->size())) return fail(TASP_ERR_INVALID_ARG, "cap %d < %zu", cap, v->size());
+  std::copy(v->begin(), v->end(), dst);
+  return TASP_OK;
+}
+
+tasp_status tasp_plan_panel(tasp_plan p, int32_t layer, int32_t which, const int8_t** w,
+                            const float** scale, int64_t* rows, int64_t* cols, int64_t* ld) {
+  if (!p) return fail(TASP_ERR_INVALID_ARG, "plan is NULL");
+  if (layer < 0 || layer >= p->desc.n_layers) return fail(TASP_ERR_INVALID_ARG, "bad layer %d", layer);
+  const LayerPlan& P = p->layers[layer];
+  const int D = p->desc.d_model;
+  const int8_t* pw;
+  const float* ps;
+  int64_t r, c, l;
+  switch (which) {
+    case TASP_PANEL_QKV: pw = P.qkv; ps = P.s_qkv; r = P.n_qkv; c = D; l = D; break;
+    case TASP_PANEL_O: pw = P.o; ps = P.s_o; r = D; c = int64_t(P.m_q) * p->desc.head_dim; l = P.ld_o; break;
+    case TASP_PANEL_GATE: pw = P.g; ps = P.s_g; r = P.c; c = D; l = D; break;
+    case TASP_PANEL_UP: pw = P.u; ps = P.s_u; r = P.c; c = D; l = D; break;
+    case TASP_PANEL_DOWN: pw = P.dn; ps = P.s_d; r = D; c = P.c; l = P.ld_d; break;
+    default: return fail(TASP_ERR_INVALID_ARG, "bad panel %d", which);
+  }
+  if (w) *w = pw;
+  if (scale) *scale = ps;
+  if (rows) *rows = r;
+  if (cols) *cols = c;
+  if (ld) *ld = l;
+  return TASP_OK;
+}
+
+tasp_status tasp_plan_ledger(tasp_plan p, double* ratio, uint64_t* weight_bytes,
+                             uint64_t* scale_bytes, uint64_t* signature) {
+  if (!p) return fail(TASP_ERR_INVALID_ARG, "plan is NULL");
+  if (ratio) *ratio = p->ratio;
+  if (weight_bytes) *weight_bytes = p->weight_bytes;
+  if (scale_bytes) *scale_bytes = p->scale_bytes;
+  if (signature) *signature = p->sig;
+  return TASP_OK;
+}
+
+tasp_status tasp_plan_destroy(tasp_plan p) {
+  delete p;
+  return TASP_OK;
+}
+
+tasp_status tasp_kv_bind(tasp_plan p, tasp_kv_cache* cache) {
+  if (!p) return fail(TASP_ERR_INVALID_ARG, "plan is NULL");
+  tasp_status st = check_cache(p, cache);
+  if (st != TASP_OK) return st;
+  cache->plan_sig = p->sig;
+  return TASP_OK;
+}
+
+tasp_status tasp_decode_step(tasp_plan p, const float* x, tasp_kv_cache* cache, int32_t pos,
+                             float* out, void* stream) {
+  return decode_impl(p, x, cache, pos, out, stream, nullptr);
+}
+
+tasp_status tasp_decode_step_timed(tasp_plan p, const float* x, tasp_kv_cache* cache,
+                                   int32_t pos, float* out, void* stream, float* kernel_ms,
+                                   int32_t* kinds, int32_t cap, int32_t* n) {
+  if (!kernel_ms || !kinds || !n) return fail(TASP_ERR_INVALID_ARG, "timing outputs are NULL");
+  Timer tm;
+  tasp_status st = decode_impl(p, x, cache, pos, out, stream, &tm);
+  hipError_t h = hipStreamSynchronize(static_cast<hipStream_t>(stream));
+  const int k = int(tm.kinds.size());
+  if (st == TASP_OK && h == hipSuccess) {
+    for (int i = 0; i < k && i < cap; ++i) {
+      float ms = 0.0f;
+      if (h == hipSuccess) h = hipEventElapsedTime(&ms, tm.ev[2 * i], tm.ev[2 * i + 1]);
+      kernel_ms[i] = ms;
+      kinds[i] = tm.kinds[i];
+    }
+    *n = k;
+  }
+  for (hipEvent_t e : tm.ev) (void)hipEventDestroy(e);
+  if (st != TASP_OK) return st;
+  if (h != hipSuccess) return fail(TASP_ERR_HIP, "timed decode: %s", hipGetErrorString(h));
+  return TASP_OK;
+}
+
+tasp_status tasp_prefill(tasp_plan p, const float* x, int32_t T, tasp_kv_cache* cache,
+                         int32_t pos0, float* out, void* stream) {
+  (void)stream;
+  if (!p) return fail(TASP_ERR_INVALID_ARG, "plan is NULL");
+  if (!x || !out) return fail(TASP_ERR_INVALID_ARG, "x / out is NULL");
+  tasp_status st = check_cache(p, cache);
+  if (st != TASP_OK) return st;
+  if (T < 1 || T > p->desc.max_prefill) return fail(TASP_ERR_SHAPE, "T %d outside 1..%d", T, p->desc.max_prefill);
+  if (pos0 < 0 || pos0 + T > cache->max_seq) return fail(TASP_ERR_POS_RANGE, "pos0 + T beyond the cache");
+  return fail(TASP_ERR_UNSUPPORTED, "prefill is not built yet");
+}
+
+tasp_status tasp_copy_probe(void* dst, const void* src, size_t bytes, void* stream) {
+  if (!dst || !src) return fail(TASP_ERR_INVALID_ARG, "dst / src is NULL");
+  if (bytes % 16) return fail(TASP_ERR_INVALID_ARG, "bytes %% 16 != 0");
+  HIP_TRY(tasp::launch_copy(dst, src, bytes, static_cast<hipStream_t>(stream)));
+  return TASP_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,156 @@
+"""Device-memory plumbing around the C ABI: PyTorch tensors own the INT8 store, the plan
+workspace, activations and the KV cache; this module only builds the ABI structs from them and
+forwards calls. No arithmetic of the decode path happens here.
+"""
+from __future__ import annotations
+
+import ctypes as C
+
+import numpy as np
+import torch
+
+from . import binding as B
+
+WEIGHT_NAMES = ("wq", "wk", "wv", "wo", "wg", "wu", "wd")
+
+
+def model_desc(n_layers, d_model, n_q_heads, n_kv_heads, head_dim, d_ffn, vocab=0, max_batch=1,
+               max_seq=4096, max_prefill=0, rms_eps=1e-5, rope_theta=500000.0):
+    return B.tasp_model_desc(n_layers, d_model, n_q_heads, n_kv_heads, head_dim, d_ffn, vocab,
+                             max_batch, max_seq, max_prefill, rms_eps, 0.0, rope_theta)
+
+
+def desc_from_shape(sh, max_batch=1, max_seq=4096, max_prefill=0):
+    """``sh`` is any object with the Shape fields (n_layers, d_model, ...)."""
+    return model_desc(sh.n_layers, sh.d_model, sh.n_q_heads, sh.n_kv_heads, sh.head_dim, sh.d_ffn,
+                      sh.vocab, max_batch, max_seq, max_prefill, sh.rms_eps, sh.rope_theta)
+
+
+def current_stream():
+    return C.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def _dev(a, device):
+    t = torch.from_numpy(np.ascontiguousarray(a))
+    return t.to(device)
+
+
+class DeviceStore:
+    """The INT8 store on the device. ``layers`` is a list of dicts ``name: (int8 [out][in],
+    float32 [out])`` plus ``attn_norm`` / ``ffn_norm`` BF16 bits (uint16 [d]); a layer may also be
+    given directly as device tensors with the same keys."""
+
+    def __init__(self, layers, final_norm=None, lm_head=None, device="cuda"):
+        self.tensors = []
+        arr = (B.tasp_layer * len(layers))()
+        for i, lay in enumerate(layers):
+            keep = {}
+            for n in WEIGHT_NAMES:
+                w, s = lay[n]
+                w = w if torch.is_tensor(w) else _dev(w, device)
+                s = s if torch.is_tensor(s) else _dev(s, device)
+                keep[n] = (w, s)
+                setattr(arr[i], n, B.tasp_qmat(w.data_ptr(), s.data_ptr()))
+            for n in ("attn_norm", "ffn_norm"):
+                g = lay[n] if torch.is_tensor(lay[n]) else _dev(lay[n], device)
+                keep[n] = g
+                setattr(arr[i], n, g.data_ptr())
+            self.tensors.append(keep)
+        self.final_norm = None if final_norm is None else (
+            final_norm if torch.is_tensor(final_norm) else _dev(final_norm, device))
+        self.lm_head = None if lm_head is None else (
+            lm_head if torch.is_tensor(lm_head) else _dev(lm_head, device))
+        self._layers = arr
+        self.struct = B.tasp_store(arr, self.final_norm.data_ptr() if self.final_norm is not None else None,
+                                   self.lm_head.data_ptr() if self.lm_head is not None else None)
+
+
+def mask_struct(mask):
+    """(q_keep, kv_keep or None, ffn_keep) uint8 numpy arrays -> (tasp_mask, keepalive)."""
+    if mask is None:
+        return None, None
+    q, kv, f = (None if a is None else np.ascontiguousarray(a, dtype=np.uint8) for a in mask)
+    m = B.tasp_mask(q.ctypes.data, None if kv is None else kv.ctypes.data, f.ctypes.data)
+    return C.pointer(m), (q, kv, f, m)
+
+
+class KVCache:
+    """BF16 K and V ``[L][B][Hkv][S][dh]`` owned by torch."""
+
+    def __init__(self, desc, batch, max_seq, device="cuda", fill=0.0):
+        shp = (desc.n_layers, batch, desc.n_kv_heads, max_seq, desc.head_dim)
+        self.k = torch.full(shp, fill, dtype=torch.bfloat16, device=device)
+        self.v = torch.full(shp, fill, dtype=torch.bfloat16, device=device)
+        self.struct = B.tasp_kv_cache(self.k.data_ptr(), self.v.data_ptr(), batch, max_seq, 0)
+
+    def load_layer(self, layer, k_bits, v_bits):
+        """Copy BF16 bit patterns ``uint16 [B][Hkv][S][dh]`` into one layer."""
+        self.k[layer].copy_(torch.from_numpy(np.ascontiguousarray(k_bits)).view(torch.bfloat16))
+        self.v[layer].copy_(torch.from_numpy(np.ascontiguousarray(v_bits)).view(torch.bfloat16))
+
+    def bits(self, which, layer):
+        t = self.k if which == "k" else self.v
+        return t[layer].view(torch.int16).cpu().numpy().view(np.uint16)
+
+
+class Plan:
+    """A compiled plan with its torch-owned workspace."""
+
+    def __init__(self, desc, store, mask=None, stream=None, device="cuda"):
+        self.desc = desc
+        self.store = store
+        mptr, self._mask_keep = mask_struct(mask)
+        self.ws_bytes = B.tasp_plan_workspace_bytes(desc, mptr)
+        self.ws = torch.empty(self.ws_bytes + 256, dtype=torch.uint8, device=device)
+        off = (-self.ws.data_ptr()) % 256
+        self.ws_base = self.ws.data_ptr() + off
+        self.ws_off = off
+        self.handle = B.tasp_compile_plan(desc, store.struct, mptr, self.ws_base, self.ws_bytes,
+                                          stream if stream is not None else current_stream())
+
+    def __del__(self):
+        h = getattr(self, "handle", None)
+        if h:
+            try:
+                B.tasp_plan_destroy(h)
+            except Exception:
+                pass
+            self.handle = None
+
+    def counts(self, layer):
+        return B.tasp_plan_counts(self.handle, layer)
+
+    def indices(self, layer, which):
+        return B.tasp_plan_indices(self.handle, layer, which)
+
+    def ledger(self):
+        ratio, wb, sb, sig = B.tasp_plan_ledger(self.handle)
+        return {"active_flop_ratio": ratio, "weight_bytes": wb, "scale_bytes": sb, "signature": sig}
+
+    def _view(self, ptr, nbytes, dtype):
+        start = ptr - self.ws.data_ptr()
+        return self.ws[start:start + nbytes].view(dtype)
+
+    def panel(self, layer, which):
+        """(int8 rows [rows][ld], float32 scales [rows]) as views into the workspace."""
+        w, s, rows, cols, ld = B.tasp_plan_panel(self.handle, layer, which)
+        if rows * ld == 0:
+            return torch.empty((rows, ld), dtype=torch.int8), torch.empty(rows), cols
+        wt = self._view(w, rows * ld, torch.int8).view(rows, ld)
+        st = self._view(s, rows * 4, torch.float32)
+        return wt, st, cols
+
+    def bind(self, cache):
+        B.tasp_kv_bind(self.handle, cache.struct)
+
+    def decode(self, x, cache, pos, out, stream=None):
+        B.tasp_decode_step(self.handle, x.data_ptr(), cache.struct, pos, out.data_ptr(),
+                           stream if stream is not None else current_stream())
+
+    def decode_timed(self, x, cache, pos, out, stream=None):
+        return B.tasp_decode_step_timed(self.handle, x.data_ptr(), cache.struct, pos, out.data_ptr(),
+                                        stream if stream is not None else current_stream())
+
+    def prefill(self, x, T, cache, pos0, out, stream=None):
+        B.tasp_prefill(self.handle, x.data_ptr(), T, cache.struct, pos0, out.data_ptr(),
+                       stream if stream is not None else current_stream())

@@ -1,0 +1,109 @@
+"""The C-ABI library loads, exports every entry point that include/tasp.h declares, and rejects
+bad arguments on the host before enqueuing any GPU work (no GPU needed)."""
+import ctypes as C
+import os
+import re
+
+import numpy as np
+import pytest
+
+from paper_2609_29499_amd import binding as B
+from paper_2609_29499_amd import session as S
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _lib():
+    if not os.path.exists(B.LIB_PATH):
+        pytest.fail("libtasp.so is not built (run __graft_entry__.build())")
+    return B.load()
+
+
+def test_every_declared_symbol_is_exported():
+    lib = _lib()
+    header = open(os.path.join(ROOT, "include", "tasp.h")).read()
+    declared = set(re.findall(r"^\s*(?:tasp_status|const char\*)\s+(tasp_\w+)\s*\(", header, re.M))
+    assert declared == set(B.EXPORTS)
+    for name in declared:
+        assert hasattr(lib, name), name
+
+
+def _desc(**kw):
+    base = dict(n_layers=1, d_model=512, n_q_heads=8, n_kv_heads=2, head_dim=64, d_ffn=1536,
+                max_seq=256)
+    base.update(kw)
+    return S.model_desc(**base)
+
+
+def test_workspace_bytes_scales_with_mask():
+    _lib()
+    d = _desc()
+    dense = B.tasp_plan_workspace_bytes(d, None)
+    q = np.ones((1, 8), np.uint8)
+    q[0, :4] = 0                                           # group 0 dropped entirely
+    f = np.zeros((1, 1536), np.uint8)
+    f[0, :512] = 1
+    m, keep = S.mask_struct((q, None, f))
+    sparse = B.tasp_plan_workspace_bytes(d, m)
+    assert sparse < dense
+    # retained bytes shrink by at least the dropped panels: 2/3 of FFN rows, 4 q heads + 1 group
+    dropped = 3 * 512 * 1024 + (4 * 64 + 2 * 64) * 512 + 512 * 4 * 64
+    assert dense - sparse >= dropped
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(head_dim=96), "TASP_ERR_SHAPE"),
+    (dict(n_q_heads=6, n_kv_heads=4), "TASP_ERR_SHAPE"),
+    (dict(n_q_heads=32, n_kv_heads=2), "TASP_ERR_SHAPE"),      # 16 heads per group
+    (dict(d_model=520), "TASP_ERR_SHAPE"),
+    (dict(max_batch=9), "TASP_ERR_SHAPE"),
+    (dict(n_layers=0), "TASP_ERR_SHAPE"),
+    (dict(d_ffn=8192, max_batch=8), "TASP_ERR_UNSUPPORTED"),
+])
+def test_bad_desc_rejected(kw, status):
+    _lib()
+    with pytest.raises(B.TaspError) as e:
+        B.tasp_plan_workspace_bytes(_desc(**kw), None)
+    assert B.STATUS[e.value.status] == status
+
+
+def test_bad_mask_byte_rejected():
+    _lib()
+    q = np.ones((1, 8), np.uint8)
+    q[0, 3] = 2
+    m, keep = S.mask_struct((q, None, np.ones((1, 1536), np.uint8)))
+    with pytest.raises(B.TaspError) as e:
+        B.tasp_plan_workspace_bytes(_desc(), m)
+    assert e.value.status == -3 and "q_keep[3]" in str(e.value)
+
+
+def test_compile_rejects_null_and_small_workspace():
+    lib = _lib()
+    d = _desc()
+    store = B.tasp_store(None, None, None)
+    plan = C.c_void_p()
+    st = lib.tasp_compile_plan(C.byref(d), C.byref(store), None, C.c_void_p(256), 1 << 30, None,
+                               C.byref(plan))
+    assert st == -1
+    layers = (B.tasp_layer * 1)()
+    for n in S.WEIGHT_NAMES:
+        setattr(layers[0], n, B.tasp_qmat(4096, 4096))
+    layers[0].attn_norm = layers[0].ffn_norm = 4096
+    store = B.tasp_store(layers, None, None)
+    st = lib.tasp_compile_plan(C.byref(d), C.byref(store), None, C.c_void_p(256), 1024, None,
+                               C.byref(plan))
+    assert st == -4 and b"workspace" in lib.tasp_last_error()
+    st = lib.tasp_compile_plan(C.byref(d), C.byref(store), None, C.c_void_p(100), 1 << 40, None,
+                               C.byref(plan))
+    assert st == -4 and b"aligned" in lib.tasp_last_error()
+
+
+def test_calls_on_null_plan_fail_cleanly():
+    lib = _lib()
+    cache = B.tasp_kv_cache(None, None, 1, 16, 0)
+    assert lib.tasp_decode_step(None, None, C.byref(cache), 0, None, None) == -1
+    assert lib.tasp_prefill(None, None, 1, C.byref(cache), 0, None, None) == -1
+    assert lib.tasp_kv_bind(None, C.byref(cache)) == -1
+    assert lib.tasp_plan_ledger(None, None, None, None, None) == -1
+    assert lib.tasp_copy_probe(None, None, 16, None) == -1
+    assert lib.tasp_status_string(-6) == b"KV cache belongs to another plan"

@@ -1,0 +1,245 @@
+"""GPU parity of the compiled decode path against the CPU oracle, through the C ABI.
+
+Integer work (closure, index lists, panels) must be bit-exact; floating-point outputs must meet
+max|err| <= 1e-2 max|ref| and sum|err| / sum|ref| <= 2e-3 (tests.helpers.assert_parity)."""
+import numpy as np
+import pytest
+import torch
+
+import synth
+from oracle import compact, reference as ref
+from paper_2609_29499_amd import binding as B
+from paper_2609_29499_amd import session as S
+from tests.gpu_case import Case
+from tests.helpers import assert_parity, rel_errors
+
+pytestmark = pytest.mark.gpu
+
+SMALL = synth.tiny_shape(d=256, hq=8, hkv=2, dh=64, f=640, theta=500000.0)
+SMALL128 = synth.tiny_shape(d=512, hq=16, hkv=4, dh=128, f=1024, theta=500000.0)
+
+
+@pytest.fixture(scope="module", autouse=True)
+def gpu():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    B.load()
+
+
+def _flush(msg):
+    print(msg, flush=True)
+
+
+def _check_indices(case):
+    sh = case.sh
+    qc, kvc, fc = case.closed
+    for l in range(sh.n_layers):
+        qi, kvi, slot, fi = ref.index_lists(qc[l], kvc[l], fc[l], sh.group_size)
+        assert case.plan.indices(l, B.IDX_Q) == qi.tolist()
+        assert case.plan.indices(l, B.IDX_KV) == kvi.tolist()
+        assert case.plan.indices(l, B.IDX_QKVSLOT) == slot.tolist()
+        assert case.plan.indices(l, B.IDX_FFN) == fi.tolist()
+        assert case.plan.counts(l) == (len(qi), len(kvi), len(fi))
+
+
+@pytest.mark.parametrize("which", ["tiny_mask", "dense", "raw1", "raw2"])
+def test_closure_indices_and_ledger_bit_exact(which):
+    _flush(f"case closure {which}")
+    sh = synth.TINY.with_layers(3)
+    mask = {"tiny_mask": synth.tiny_mask(sh), "dense": None, "raw1": synth.raw_mask(sh, 1),
+            "raw2": synth.raw_mask(sh, 2, p_q=0.3, p_kv=0.5)}[which]
+    case = Case(sh, mask, batch=1, pos=4)
+    _check_indices(case)
+    counts = synth.mask_counts(*case.closed)
+    led = case.plan.ledger()
+    assert led["active_flop_ratio"] == pytest.approx(ref.active_flop_ratio(sh, counts), rel=1e-14)
+    nb = ref.decode_bytes(sh, counts, batch=1, pos=0)
+    assert led["weight_bytes"] == nb["weights"] and led["scale_bytes"] == nb["scales"]
+
+
+def test_budget_masks_8b_indices():
+    sh = synth.LLAMA3_8B.with_layers(32, vocab=0)
+    for seed in (1, 2):
+        q, kv, f = synth.budget_mask(sh, seed)
+        desc = S.desc_from_shape(sh, max_seq=16)
+        # closure/index lists on a store of one shared layer repeated: only indices are checked
+        lay = synth.layer_weights(sh.with_layers(1), 0)
+        dev = {k: tuple(torch.from_numpy(a).cuda() for a in v) if isinstance(v, tuple)
+               else torch.from_numpy(v).cuda() for k, v in lay.items()}
+        store = S.DeviceStore([dev] * sh.n_layers)
+        plan = S.Plan(desc, store, (q, kv, f))
+        closed = ref.close_mask(q, kv, f, sh.group_size)
+        for l in range(0, 32, 7):
+            qi, kvi, slot, fi = ref.index_lists(closed[0][l], closed[1][l], closed[2][l], sh.group_size)
+            assert plan.indices(l, B.IDX_Q) == qi.tolist()
+            assert plan.indices(l, B.IDX_KV) == kvi.tolist()
+            assert plan.indices(l, B.IDX_QKVSLOT) == slot.tolist()
+            assert plan.indices(l, B.IDX_FFN) == fi.tolist()
+        del plan, store
+        torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("sh", [synth.TINY, SMALL128], ids=["tiny", "dh128"])
+def test_panels_byte_exact(sh):
+    _flush(f"case panels {sh.d_model}")
+    mask = synth.tiny_mask(sh) if sh is synth.TINY else synth.raw_mask(sh, 3)
+    case = Case(sh, mask, batch=1, pos=2)
+    qc, kvc, fc = case.closed
+    pn = compact.compact_panels(case.store[0], qc[0], kvc[0], fc[0], sh)
+    for which, key in ((B.PANEL_QKV, "qkv"), (B.PANEL_O, "o"), (B.PANEL_GATE, "gate"),
+                       (B.PANEL_UP, "up"), (B.PANEL_DOWN, "down")):
+        w, s, cols = case.plan.panel(0, which)
+        w = w.cpu().numpy()
+        s = s.cpu().numpy()
+        assert cols == pn[key].shape[1]
+        assert np.array_equal(w[:, :cols], pn[key]), key
+        assert not w[:, cols:].any(), key                     # padding columns are zero
+        assert np.array_equal(s, pn[key + "_scale"]), key
+
+
+def _decode_case(sh, mask, batch, pos, max_seq=None, **kw):
+    case = Case(sh, mask, batch, pos, max_seq=max_seq, **kw)
+    got = case.run()
+    want = case.oracle()
+    return case, got, want
+
+
+def _check_cache_rows(case):
+    """Row pos of retained groups holds the BF16 new k / v; all other rows are untouched."""
+    sh, pos = case.sh, case.pos
+    for l in range(sh.n_layers):
+        kvc = case.closed[1][l]
+        for which, idx in (("k", 0), ("v", 1)):
+            dev = case.cache.bits(which, l)
+            prior = case.priors[l][idx]
+            # rows below pos unchanged (bit-exact), other groups and rows above pos still NaN
+            assert np.array_equal(dev[:, kvc, :pos], prior[:, kvc, :pos])
+            assert (dev[:, ~kvc] == 0x7FC0).all()
+            assert (dev[:, :, pos + 1:] == 0x7FC0).all()
+            new = synth.bf16_bits_to_f32(dev[:, kvc, pos]).astype(np.float64)
+            want = case.oracle_caches[l][idx][:, kvc, pos]
+            if new.size:
+                assert_parity(new, want, what=f"cache {which} layer {l}")
+
+
+@pytest.mark.parametrize("masked", [True, False], ids=["tiny_mask", "dense"])
+def test_tiny_layer_decode(masked):
+    """The tiny single layer: 6/8 heads, 1024/1536 channels, 128 prior positions; plus dense."""
+    _flush(f"case tiny decode masked={masked}")
+    sh = synth.TINY
+    case, got, want = _decode_case(sh, synth.tiny_mask(sh) if masked else None, 1, 128)
+    m, s = assert_parity(got, want, what="tiny layer")
+    _flush(f"  max_rel={m:.2e} sum_rel={s:.2e}")
+    _check_cache_rows(case)
+
+
+@pytest.mark.parametrize("seed,batch", [(1, 1), (2, 3), (5, 2)])
+def test_raw_masks_and_batches(seed, batch):
+    _flush(f"case raw mask seed={seed} batch={batch}")
+    sh = SMALL.with_layers(2)
+    case, got, want = _decode_case(sh, synth.raw_mask(sh, seed, p_q=0.5, p_kv=0.7), batch, 77,
+                                   max_seq=100)
+    assert_parity(got, want, what="raw mask")
+    _check_cache_rows(case)
+
+
+def test_head_dim_128_ragged_groups():
+    _flush("case dh128 ragged")
+    sh = SMALL128.with_layers(2)
+    q, kv, f = synth.all_kept_mask(sh)
+    q[0, [1, 2, 3, 5, 10, 11]] = 0               # groups keep 1, 3, 2 and 4 heads
+    kv[1, 2] = 0
+    q[1, :3] = 0
+    f[0, 100:777] = 0
+    case, got, want = _decode_case(sh, (q, kv, f), 2, 300, max_seq=333)
+    assert_parity(got, want, what="dh128")
+    _check_cache_rows(case)
+
+
+@pytest.mark.parametrize("what", ["no_heads", "no_ffn", "nothing"])
+def test_empty_modules(what):
+    _flush(f"case empty {what}")
+    sh = SMALL.with_layers(2)
+    q, kv, f = synth.all_kept_mask(sh)
+    if what in ("no_heads", "nothing"):
+        q[0] = 0
+    if what in ("no_ffn", "nothing"):
+        f[1] = 0
+    case, got, want = _decode_case(sh, (q, kv, f), 1, 9, max_seq=16)
+    assert_parity(got, want, what=what)
+
+
+@pytest.mark.parametrize("pos", [0, 1, 63, 64, 65, 511])
+def test_positions_and_split_boundaries(pos):
+    _flush(f"case pos={pos}")
+    sh = SMALL
+    case, got, want = _decode_case(sh, synth.raw_mask(sh, 4), 1, pos, max_seq=512)
+    assert_parity(got, want, what=f"pos {pos}")
+    _check_cache_rows(case)
+
+
+def test_stack_with_lm_head_logits():
+    _flush("case stack + lm head")
+    sh = synth.tiny_shape(d=256, hq=8, hkv=2, dh=64, f=512, layers=3, vocab=3000)
+    case, got, want = _decode_case(sh, synth.raw_mask(sh, 6), 2, 40, max_seq=48)
+    m, s = assert_parity(got, want, what="logits")
+    assert (got.argmax(axis=1) == want.argmax(axis=1)).all()
+    assert np.abs(got - want).max() < 2e-3 * max(1.0, np.abs(want).max())
+
+
+def test_llama3_8b_layer_full_size():
+    """One Llama-3-8B-shaped layer at 2048 prior positions: seed-1 budget mask and dense."""
+    sh = synth.LLAMA3_8B.with_layers(1, vocab=0)
+    store = [synth.layer_weights(sh, 0)]
+    for mask in (synth.budget_mask(sh, 1), None):
+        _flush(f"case 8b layer masked={mask is not None}")
+        case, got, want = _decode_case(sh, mask, 1, 2048, store=store)
+        m, s = assert_parity(got, want, what="8b layer")
+        _flush(f"  max_rel={m:.2e} sum_rel={s:.2e}")
+        _check_cache_rows(case)
+        del case
+        torch.cuda.empty_cache()
+
+
+def test_repeat_and_graph_replay_are_stable():
+    """Repeated decode (self-resetting counters) and HIP-graph replays give the eager result."""
+    _flush("case repeat + graph")
+    sh = SMALL
+    case = Case(sh, synth.raw_mask(sh, 7), 1, 200, max_seq=256)
+    first = case.run()
+    for _ in range(3):
+        assert np.array_equal(case.run(), first)
+    g = torch.cuda.CUDAGraph()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        case.plan.decode(case.xd, case.cache, case.pos, case.out, stream=S.current_stream())
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    with torch.cuda.graph(g):
+        case.plan.decode(case.xd, case.cache, case.pos, case.out, stream=S.current_stream())
+    for _ in range(3):
+        case.out.fill_(float("nan"))
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert np.array_equal(case.out.cpu().numpy().astype(np.float64), first)
+
+
+def test_cache_plan_binding_errors():
+    _flush("case errors")
+    sh = SMALL
+    a = Case(sh, synth.raw_mask(sh, 1), 1, 5, max_seq=8)
+    b_mask = synth.raw_mask(sh, 2)
+    plan_b = S.Plan(a.desc, a.dstore, b_mask)
+    with pytest.raises(B.TaspError) as e:
+        plan_b.decode(a.xd, a.cache, a.pos, a.out)
+    assert e.value.status == -6
+    same = S.Plan(a.desc, a.dstore, a.mask)
+    assert same.ledger()["signature"] == a.plan.ledger()["signature"]
+    assert plan_b.ledger()["signature"] != a.plan.ledger()["signature"]
+    with pytest.raises(B.TaspError) as e:
+        a.plan.decode(a.xd, a.cache, 8, a.out)
+    assert e.value.status == -5
+    with pytest.raises(B.TaspError) as e:
+        a.plan.decode(a.xd, a.cache, 2, a.xd)
+    assert e.value.status == -1
