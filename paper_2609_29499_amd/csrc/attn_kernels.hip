@@ -2,16 +2,22 @@
 //
 // Grid (n_split, m_kv, B): workgroup (s, j, b) serves retained group slot j of sequence b over
 // cache rows [s*chunk, min((s+1)*chunk, pos+1)) for all of that group's retained query heads
-// (1..8), so each K/V row is read from HBM once for every head that uses it. The workgroup
-//   1. rotates its heads' raw q (RoPE at pos, table from the plan) into LDS, pre-scaled by
-//      log2(e)/sqrt(d_h) so the softmax works in base 2;
-//   2. if its range holds row pos: rotates the new k, rounds k and v to BF16, appends them to the
-//      cache and keeps the rounded values in LDS (the same values later steps will read);
-//   3. scores: d_h/8 lanes share one cache row (16-byte loads), dot products reduced with
-//      shuffles inside the lane group, scores kept in LDS;
-//   4. exact softmax of its range (max, exp2, sum), then P V with the same row mapping;
-//   5. writes (max, sum, unnormalised output) per head; the last workgroup of the group (atomic
-//      counter, reset by that workgroup) merges the ranges by log-sum-exp and writes o.
+// (1..8), so each K/V row is read from HBM once for every head that uses it. The slot -> group
+// and slot -> head-range tables of the layer travel inside the kernel arguments, so the cache
+// loads do not wait for an index load. The workgroup
+//   1. issues the K and V loads of its first 128-row sub-block, then rotates its heads' raw q
+//      (RoPE at pos, table from the plan) into LDS, pre-scaled by log2(e)/sqrt(d_h) so the
+//      softmax works in base 2; if its range holds row pos it also rotates the new k, rounds k
+//      and v to BF16, appends them to the cache and keeps the rounded values in LDS (the values
+//      every later step reads);
+//   2. per sub-block: d_h/8 lanes share a cache row (16-byte loads; rows outside the range use an
+//      out-of-range buffer offset, so no branch sits around a load); the per-row dot products are
+//      reduced across the row's lanes with DPP, and an online softmax (running max and sum per
+//      head, rescaled accumulators) folds the sub-block into P V. The head count is a template
+//      parameter, so every per-head loop is unrolled and independent chains interleave;
+//   3. writes (max, sum, unnormalised output) per head when the range is split; a second, small
+//      kernel merges the ranges by log-sum-exp and writes o (a kernel boundary is the cheapest
+//      device-wide ordering here: an in-kernel fence + counter costs more than the merge itself).
 #include "device_common.hpp"
 #include "kernels.hpp"
 
@@ -19,143 +25,222 @@ namespace tasp {
 namespace {
 
 constexpr int kMaxHeads = 8;
-constexpr int kMaxChunk = 512;
+constexpr int kSub = 128;              // rows per sub-block
+constexpr int kMaxSplit = 256;
+constexpr int kMergeBatch = 32;
+
+__device__ __forceinline__ void unpack_bf16x8(const int4& w, float (&f)[8]) {
+  f[0] = bf16_lo(uint32_t(w.x)); f[1] = bf16_hi(uint32_t(w.x));
+  f[2] = bf16_lo(uint32_t(w.y)); f[3] = bf16_hi(uint32_t(w.y));
+  f[4] = bf16_lo(uint32_t(w.z)); f[5] = bf16_hi(uint32_t(w.z));
+  f[6] = bf16_lo(uint32_t(w.w)); f[7] = bf16_hi(uint32_t(w.w));
+}
+
+__device__ __forceinline__ float4 rope4(const float4& a, const float4& b, const float4& c,
+                                        const float4& s, bool first_half) {
+  // first half: a cos - b sin (b = partner); second half: a cos + b sin
+  const float sg = first_half ? -1.0f : 1.0f;
+  return make_float4(fmaf(sg * b.x, s.x, a.x * c.x), fmaf(sg * b.y, s.y, a.y * c.y),
+                     fmaf(sg * b.z, s.z, a.z * c.z), fmaf(sg * b.w, s.w, a.w * c.w));
+}
 
 template <int DH>
-__global__ __launch_bounds__(kBlock) void attn_decode_kernel(AttnArgs a) {
+struct AttnSmem {
+  float q_s[kMaxHeads][DH];
+  float sc[kMaxHeads][kSub];
+  float red[4][kMaxHeads][DH];
+  float knew[DH];
+  float vnew[DH];
+  float m_s[kMaxHeads], l_s[kMaxHeads], al_s[kMaxHeads];
+};
+
+template <int LPR>
+__device__ __forceinline__ float row_group_sum(float v) {
+  return LPR == 16 ? row16_sum(v) : row8_sum(v);
+}
+
+template <int DH, int NH>
+__device__ __forceinline__ void attn_body(const AttnArgs& a, AttnSmem<DH>& sm, int s, int j,
+                                          int b) {
   constexpr int LPR = DH / 8;          // lanes per cache row
   constexpr int RPW = kWave / LPR;     // rows per wave per step
   constexpr int RPB = RPW * 4;         // rows per workgroup per step
+  constexpr int U = kSub / RPB;        // steps per sub-block
   constexpr int HALF = DH / 2;
-  __shared__ float q_s[kMaxHeads][DH];
-  __shared__ float sc[kMaxHeads][kMaxChunk];
-  __shared__ float red[4][kMaxHeads][DH];
-  __shared__ float knew[DH], vnew[DH];
-  __shared__ float m_s[kMaxHeads], l_s[kMaxHeads];
-  __shared__ int last_flag;
-
-  const int s = blockIdx.x, j = blockIdx.y, b = blockIdx.z;
+  constexpr int Q4 = DH / 4;           // float4 per head row
+  constexpr int PS = DH + 4;           // partial record: max, sum, pad, DH accumulators
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int g = a.kv_idx[j];
   const int h0 = a.slot_start[j];
-  const int nh = a.slot_start[j + 1] - h0;
   const int t0 = s * a.chunk;
   const int t1 = min(t0 + a.chunk, a.pos + 1);
-  const int n = t1 - t0;
   const float* qkv = a.qkv + size_t(b) * a.ld_qkv;
-  const float* cs = a.rope_cos + size_t(a.pos) * HALF;
-  const float* sn = a.rope_sin + size_t(a.pos) * HALF;
-  const float qscale = kLog2e * rsqrtf(float(DH));
   const size_t row_base = (size_t(b) * a.Hkv + g) * a.S;
   uint16_t* kc = a.kc + row_base * DH;
   uint16_t* vc = a.vc + row_base * DH;
   const bool has_new = (t1 == a.pos + 1);
-
-  // 1-2. rotary embedding of the heads' queries and, in the last range, the new key
-  for (int i = tid; i < nh * DH; i += kBlock) {
-    const int h = i / DH, e = i % DH;
-    const float* qh = qkv + size_t(h0 + h) * DH;
-    const int p = e % HALF;
-    const float v = (e < HALF) ? qh[e] * cs[p] - qh[e + HALF] * sn[p]
-                               : qh[e] * cs[p] + qh[e - HALF] * sn[p];
-    q_s[h][e] = v * qscale;
-  }
-  if (has_new && tid < DH) {
-    const float* kh = qkv + size_t(a.m_q + j) * DH;
-    const float* vh = qkv + size_t(a.m_q + a.m_kv + j) * DH;
-    const int e = tid, p = e % HALF;
-    const float kr = (e < HALF) ? kh[e] * cs[p] - kh[e + HALF] * sn[p]
-                                : kh[e] * cs[p] + kh[e - HALF] * sn[p];
-    const uint16_t kb = f32_to_bf16(kr), vb = f32_to_bf16(vh[e]);
-    kc[size_t(a.pos) * DH + e] = kb;
-    vc[size_t(a.pos) * DH + e] = vb;
-    knew[e] = bf16_to_f32(kb);
-    vnew[e] = bf16_to_f32(vb);
-  }
-  __syncthreads();
-
+  // this group's cache rows 0..pos-1 (row pos is taken from LDS)
+  const uint32_t group_bytes = uint32_t(a.pos) * DH * 2u;
+  const __amdgpu_buffer_rsrc_t rk = make_rsrc(kc, group_bytes);
+  const __amdgpu_buffer_rsrc_t rv = make_rsrc(vc, group_bytes);
   const int lr = lane % LPR;           // dims [8 lr, 8 lr + 8)
   const int rb = wave * RPW + lane / LPR;
-  float qr[kMaxHeads][8];
-#pragma unroll
-  for (int h = 0; h < kMaxHeads; ++h)
-#pragma unroll
-    for (int i = 0; i < 8; ++i) qr[h][i] = (h < nh) ? q_s[h][lr * 8 + i] : 0.0f;
+  auto row_off = [&](int t) -> uint32_t {
+    return (t < t1 && t < a.pos) ? uint32_t(t) * (DH * 2u) + uint32_t(lr) * 16u : kOOB;
+  };
 
-  // 3. scores
-  for (int t = t0 + rb; t - rb < t1; t += RPB) {
-    float kf[8];
-    const bool valid = t < t1;
-    if (valid && t == a.pos) {
+  int4 kw[U], vw[U];
 #pragma unroll
-      for (int i = 0; i < 8; ++i) kf[i] = knew[lr * 8 + i];
-    } else if (valid) {
-      const uint4 w = *reinterpret_cast<const uint4*>(kc + size_t(t) * DH + lr * 8);
-      kf[0] = bf16_lo(w.x); kf[1] = bf16_hi(w.x); kf[2] = bf16_lo(w.y); kf[3] = bf16_hi(w.y);
-      kf[4] = bf16_lo(w.z); kf[5] = bf16_hi(w.z); kf[6] = bf16_lo(w.w); kf[7] = bf16_hi(w.w);
-    } else {
+  for (int u = 0; u < U; ++u) {
+    kw[u] = buf_load16(rk, row_off(t0 + rb + u * RPB));
+    vw[u] = buf_load16(rv, row_off(t0 + rb + u * RPB));
+  }
+
+  // 1. RoPE of the queries (and of the new key): item (h, i4) rotates float4 i4 of the first half
+  //    with its partner in the second half
+  {
+    const float4* cs4 = reinterpret_cast<const float4*>(a.rope_cos + size_t(a.pos) * HALF);
+    const float4* sn4 = reinterpret_cast<const float4*>(a.rope_sin + size_t(a.pos) * HALF);
+    const float qscale = kLog2e * rsqrtf(float(DH));
+    constexpr int H4 = HALF / 4;
+    const int nitems = (NH + (has_new ? 1 : 0)) * H4;
+    if (tid < nitems) {
+      const int h = tid / H4, i4 = tid % H4;
+      const bool is_k = h == NH;
+      const float* src = is_k ? qkv + size_t(a.m_q + j) * DH : qkv + size_t(h0 + h) * DH;
+      const float4 x1 = reinterpret_cast<const float4*>(src)[i4];
+      const float4 x2 = reinterpret_cast<const float4*>(src)[i4 + H4];
+      const float4 c = cs4[i4], sn = sn4[i4];
+      float4 y1 = rope4(x1, x2, c, sn, true), y2 = rope4(x2, x1, c, sn, false);
+      if (!is_k) {
+        y1.x *= qscale; y1.y *= qscale; y1.z *= qscale; y1.w *= qscale;
+        y2.x *= qscale; y2.y *= qscale; y2.z *= qscale; y2.w *= qscale;
+        reinterpret_cast<float4*>(sm.q_s[h])[i4] = y1;
+        reinterpret_cast<float4*>(sm.q_s[h])[i4 + H4] = y2;
+      } else {
+        const float e1[4] = {y1.x, y1.y, y1.z, y1.w}, e2[4] = {y2.x, y2.y, y2.z, y2.w};
 #pragma unroll
-      for (int i = 0; i < 8; ++i) kf[i] = 0.0f;
+        for (int q = 0; q < 4; ++q) {
+          const uint16_t b1 = f32_to_bf16(e1[q]), b2 = f32_to_bf16(e2[q]);
+          kc[size_t(a.pos) * DH + i4 * 4 + q] = b1;
+          kc[size_t(a.pos) * DH + HALF + i4 * 4 + q] = b2;
+          sm.knew[i4 * 4 + q] = bf16_to_f32(b1);
+          sm.knew[HALF + i4 * 4 + q] = bf16_to_f32(b2);
+        }
+      }
     }
+    if (has_new && tid >= 128 && tid < 128 + Q4) {
+      const int i4 = tid - 128;
+      const float4 v = reinterpret_cast<const float4*>(qkv + size_t(a.m_q + a.m_kv + j) * DH)[i4];
+      const float e[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
-    for (int h = 0; h < kMaxHeads; ++h) {
-      if (h >= nh) break;
-      float d = 0.0f;
-#pragma unroll
-      for (int i = 0; i < 8; ++i) d = fmaf(qr[h][i], kf[i], d);
-#pragma unroll
-      for (int m = LPR / 2; m >= 1; m >>= 1) d += __shfl_xor(d, m, kWave);
-      if (valid && lr == 0) sc[h][t - t0] = d;
+      for (int q = 0; q < 4; ++q) {
+        const uint16_t bv = f32_to_bf16(e[q]);
+        vc[size_t(a.pos) * DH + i4 * 4 + q] = bv;
+        sm.vnew[i4 * 4 + q] = bf16_to_f32(bv);
+      }
+    }
+    if (tid < NH) {
+      sm.m_s[tid] = -INFINITY;
+      sm.l_s[tid] = 0.0f;
     }
   }
   __syncthreads();
 
-  // 4. softmax of this range, one wave per head
-  for (int h = wave; h < nh; h += 4) {
-    float mx = -INFINITY;
-    for (int t = lane; t < n; t += kWave) mx = fmaxf(mx, sc[h][t]);
-    mx = wave_max(mx);
-    float sum = 0.0f;
-    for (int t = lane; t < n; t += kWave) {
-      const float p = exp2f(sc[h][t] - mx);
-      sc[h][t] = p;
-      sum += p;
-    }
-    sum = wave_sum(sum);
-    if (lane == 0) {
-      m_s[h] = mx;
-      l_s[h] = sum;
-    }
-  }
-  __syncthreads();
-
-  float acc[kMaxHeads][8];
+  float qr[NH][8];
 #pragma unroll
-  for (int h = 0; h < kMaxHeads; ++h)
+  for (int h = 0; h < NH; ++h)
+#pragma unroll
+    for (int i = 0; i < 8; ++i) qr[h][i] = sm.q_s[h][lr * 8 + i];
+  float acc[NH][8];
+#pragma unroll
+  for (int h = 0; h < NH; ++h)
 #pragma unroll
     for (int i = 0; i < 8; ++i) acc[h][i] = 0.0f;
-  for (int t = t0 + rb; t < t1; t += RPB) {
-    float vf[8];
-    if (t == a.pos) {
+
+  // 2. sub-blocks with an online softmax
+  for (int tb = t0; tb < t1; tb += kSub) {
+    if (tb != t0) {
 #pragma unroll
-      for (int i = 0; i < 8; ++i) vf[i] = vnew[lr * 8 + i];
-    } else {
-      const uint4 w = *reinterpret_cast<const uint4*>(vc + size_t(t) * DH + lr * 8);
-      vf[0] = bf16_lo(w.x); vf[1] = bf16_hi(w.x); vf[2] = bf16_lo(w.y); vf[3] = bf16_hi(w.y);
-      vf[4] = bf16_lo(w.z); vf[5] = bf16_hi(w.z); vf[6] = bf16_lo(w.w); vf[7] = bf16_hi(w.w);
+      for (int u = 0; u < U; ++u) {
+        kw[u] = buf_load16(rk, row_off(tb + rb + u * RPB));
+        vw[u] = buf_load16(rv, row_off(tb + rb + u * RPB));
+      }
+    }
+    float d[U][NH];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int t = tb + rb + u * RPB;
+      float kf[8];
+      unpack_bf16x8(kw[u], kf);
+      if (has_new && t == a.pos) {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) kf[i] = sm.knew[lr * 8 + i];
+      }
+#pragma unroll
+      for (int h = 0; h < NH; ++h) {
+        float x = 0.0f;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) x = fmaf(qr[h][i], kf[i], x);
+        d[u][h] = x;
+      }
     }
 #pragma unroll
-    for (int h = 0; h < kMaxHeads; ++h) {
-      if (h >= nh) break;
-      const float p = sc[h][t - t0];
+    for (int u = 0; u < U; ++u)
 #pragma unroll
-      for (int i = 0; i < 8; ++i) acc[h][i] = fmaf(p, vf[i], acc[h][i]);
+      for (int h = 0; h < NH; ++h) d[u][h] = row_group_sum<LPR>(d[u][h]);
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int t = tb + rb + u * RPB;
+      if (lr == 0) {
+#pragma unroll
+        for (int h = 0; h < NH; ++h) sm.sc[h][t - tb] = (t < t1) ? d[u][h] : -INFINITY;
+      }
     }
+    __syncthreads();
+    for (int h = wave; h < NH; h += 4) {
+      const float v0 = sm.sc[h][lane], v1 = sm.sc[h][lane + 64];
+      const float mo = sm.m_s[h];
+      const float mn = fmaxf(mo, wave_max(fmaxf(v0, v1)));
+      const float p0 = exp2f(v0 - mn), p1 = exp2f(v1 - mn);
+      sm.sc[h][lane] = p0;
+      sm.sc[h][lane + 64] = p1;
+      const float sum = wave_sum(p0 + p1);
+      if (lane == 0) {
+        const float al = exp2f(mo - mn);
+        sm.al_s[h] = al;
+        sm.l_s[h] = sm.l_s[h] * al + sum;
+        sm.m_s[h] = mn;
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int h = 0; h < NH; ++h) {
+      const float al = sm.al_s[h];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) acc[h][i] *= al;
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int t = tb + rb + u * RPB;
+      float vf[8];
+      unpack_bf16x8(vw[u], vf);
+      if (has_new && t == a.pos) {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) vf[i] = sm.vnew[lr * 8 + i];
+      }
+#pragma unroll
+      for (int h = 0; h < NH; ++h) {
+        const float p = sm.sc[h][t - tb];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) acc[h][i] = fmaf(p, vf[i], acc[h][i]);
+      }
+    }
+    __syncthreads();
   }
   // reduce over the rows of a wave (lanes that share lr), then over the 4 waves in LDS
 #pragma unroll
-  for (int h = 0; h < kMaxHeads; ++h) {
-    if (h >= nh) break;
+  for (int h = 0; h < NH; ++h)
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
       float v = acc[h][i];
@@ -163,60 +248,98 @@ __global__ __launch_bounds__(kBlock) void attn_decode_kernel(AttnArgs a) {
       for (int m = LPR; m < kWave; m <<= 1) v += __shfl_xor(v, m, kWave);
       acc[h][i] = v;
     }
-  }
   if (lane < LPR) {
 #pragma unroll
-    for (int h = 0; h < kMaxHeads; ++h) {
-      if (h >= nh) break;
+    for (int h = 0; h < NH; ++h)
 #pragma unroll
-      for (int i = 0; i < 8; ++i) red[wave][h][lr * 8 + i] = acc[h][i];
-    }
+      for (int i = 0; i < 8; ++i) sm.red[wave][h][lr * 8 + i] = acc[h][i];
   }
   __syncthreads();
 
   float* ob = a.o + size_t(b) * a.ld_o;
   if (a.n_split == 1) {
-    for (int i = tid; i < nh * DH; i += kBlock) {
+    for (int i = tid; i < NH * DH; i += kBlock) {
       const int h = i / DH, e = i % DH;
-      const float v = red[0][h][e] + red[1][h][e] + red[2][h][e] + red[3][h][e];
-      ob[size_t(h0 + h) * DH + e] = v / l_s[h];
+      const float v = sm.red[0][h][e] + sm.red[1][h][e] + sm.red[2][h][e] + sm.red[3][h][e];
+      ob[size_t(h0 + h) * DH + e] = v / sm.l_s[h];
     }
     return;
   }
-
-  // 5. partial results, then the last workgroup of this group merges them
-  constexpr int PS = DH + 2;
+  // 3. partial results: record per (split, head) = [max, sum, 0, 0, acc[DH]] (float4-aligned)
   float* part = a.part + (size_t(b) * a.m_kv + j) * size_t(a.n_split) * kMaxHeads * PS;
-  for (int i = tid; i < nh * DH; i += kBlock) {
-    const int h = i / DH, e = i % DH;
-    part[(size_t(s) * kMaxHeads + h) * PS + 2 + e] =
-        red[0][h][e] + red[1][h][e] + red[2][h][e] + red[3][h][e];
+  for (int i = tid; i < NH * Q4; i += kBlock) {
+    const int h = i / Q4, e4 = i % Q4;
+    float4 v;
+    v.x = sm.red[0][h][4 * e4 + 0] + sm.red[1][h][4 * e4 + 0] + sm.red[2][h][4 * e4 + 0] + sm.red[3][h][4 * e4 + 0];
+    v.y = sm.red[0][h][4 * e4 + 1] + sm.red[1][h][4 * e4 + 1] + sm.red[2][h][4 * e4 + 1] + sm.red[3][h][4 * e4 + 1];
+    v.z = sm.red[0][h][4 * e4 + 2] + sm.red[1][h][4 * e4 + 2] + sm.red[2][h][4 * e4 + 2] + sm.red[3][h][4 * e4 + 2];
+    v.w = sm.red[0][h][4 * e4 + 3] + sm.red[1][h][4 * e4 + 3] + sm.red[2][h][4 * e4 + 3] + sm.red[3][h][4 * e4 + 3];
+    reinterpret_cast<float4*>(part + (size_t(s) * kMaxHeads + h) * PS + 4)[e4] = v;
   }
-  if (tid < nh) {
-    part[(size_t(s) * kMaxHeads + tid) * PS + 0] = m_s[tid];
-    part[(size_t(s) * kMaxHeads + tid) * PS + 1] = l_s[tid];
+  if (tid < NH)
+    *reinterpret_cast<float2*>(part + (size_t(s) * kMaxHeads + tid) * PS) =
+        make_float2(sm.m_s[tid], sm.l_s[tid]);
+}
+
+template <int DH>
+__global__ __launch_bounds__(kBlock) void attn_decode_kernel(AttnArgs a) {
+  __shared__ __attribute__((aligned(16))) AttnSmem<DH> sm;
+  const int s = blockIdx.x, j = blockIdx.y, b = blockIdx.z;
+  switch (a.slot_start[j + 1] - a.slot_start[j]) {
+    case 1: attn_body<DH, 1>(a, sm, s, j, b); break;
+    case 2: attn_body<DH, 2>(a, sm, s, j, b); break;
+    case 3: attn_body<DH, 3>(a, sm, s, j, b); break;
+    case 4: attn_body<DH, 4>(a, sm, s, j, b); break;
+    case 5: attn_body<DH, 5>(a, sm, s, j, b); break;
+    case 6: attn_body<DH, 6>(a, sm, s, j, b); break;
+    case 7: attn_body<DH, 7>(a, sm, s, j, b); break;
+    case 8: attn_body<DH, 8>(a, sm, s, j, b); break;
   }
-  __threadfence();
-  __syncthreads();
-  int* cnt = a.counters + size_t(b) * a.Hkv + j;
-  if (tid == 0) last_flag = (atomicAdd(cnt, 1) == a.n_split - 1);
-  __syncthreads();
-  if (!last_flag) return;
-  __threadfence();
-  for (int i = tid; i < nh * DH; i += kBlock) {
-    const int h = i / DH, e = i % DH;
-    float M = -INFINITY;
-    for (int k = 0; k < a.n_split; ++k) M = fmaxf(M, ld_coherent(&part[(size_t(k) * kMaxHeads + h) * PS]));
-    float L = 0.0f, A = 0.0f;
-    for (int k = 0; k < a.n_split; ++k) {
-      const float* pk = &part[(size_t(k) * kMaxHeads + h) * PS];
-      const float w = exp2f(ld_coherent(pk) - M);
-      L = fmaf(ld_coherent(pk + 1), w, L);
-      A = fmaf(ld_coherent(pk + 2 + e), w, A);
+}
+
+// Merge of the split partials of one (group slot, sequence): thread (h, e4) combines 4 output dims
+// of one head over all splits, kMergeBatch records in flight at once, with a running
+// log-sum-exp across batches. The kernel boundary makes the partials visible.
+template <int DH>
+__global__ __launch_bounds__(kBlock) void attn_merge_kernel(AttnArgs a) {
+  constexpr int Q4 = DH / 4;
+  constexpr int PS = DH + 4;
+  const int j = blockIdx.x, b = blockIdx.y, tid = threadIdx.x;
+  const int h0 = a.slot_start[j];
+  const int nh = a.slot_start[j + 1] - h0;
+  if (tid >= nh * Q4) return;
+  const int h = tid / Q4, e4 = tid % Q4;
+  const float* part = a.part + (size_t(b) * a.m_kv + j) * size_t(a.n_split) * kMaxHeads * PS;
+  float M = -INFINITY, L = 0.0f;
+  float4 A = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+  for (int k0 = 0; k0 < a.n_split; k0 += kMergeBatch) {
+    float2 ml[kMergeBatch];
+    float4 av[kMergeBatch];
+#pragma unroll
+    for (int q = 0; q < kMergeBatch; ++q) {
+      const float* rec = part + (size_t(min(k0 + q, a.n_split - 1)) * kMaxHeads + h) * PS;
+      ml[q] = *reinterpret_cast<const float2*>(rec);
+      av[q] = reinterpret_cast<const float4*>(rec + 4)[e4];
     }
-    ob[size_t(h0 + h) * DH + e] = A / L;
+    float bm = M;
+#pragma unroll
+    for (int q = 0; q < kMergeBatch; ++q) bm = fmaxf(bm, ml[q].x);
+    const float rs = exp2f(M - bm);             // rescale what was merged so far
+    L *= rs;
+    A.x *= rs; A.y *= rs; A.z *= rs; A.w *= rs;
+#pragma unroll
+    for (int q = 0; q < kMergeBatch; ++q) {
+      const float w = (k0 + q < a.n_split) ? exp2f(ml[q].x - bm) : 0.0f;
+      L = fmaf(ml[q].y, w, L);
+      A.x = fmaf(av[q].x, w, A.x); A.y = fmaf(av[q].y, w, A.y);
+      A.z = fmaf(av[q].z, w, A.z); A.w = fmaf(av[q].w, w, A.w);
+    }
+    M = bm;
   }
-  if (tid == 0) *cnt = 0;
+  const float inv = 1.0f / L;
+  float* ob = a.o + size_t(b) * a.ld_o;
+  reinterpret_cast<float4*>(ob + size_t(h0 + h) * DH)[e4] =
+      make_float4(A.x * inv, A.y * inv, A.z * inv, A.w * inv);
 }
 
 }  // namespace
@@ -230,9 +353,16 @@ hipError_t launch_attn_decode(const AttnArgs& a, hipStream_t s) {
     hipLaunchKernelGGL(attn_decode_kernel<64>, grid, dim3(kBlock), 0, s, a);
   else
     return hipErrorInvalidValue;
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || a.n_split == 1) return e;
+  if (a.dh == 128)
+    hipLaunchKernelGGL(attn_merge_kernel<128>, dim3(a.m_kv, a.B), dim3(kBlock), 0, s, a);
+  else
+    hipLaunchKernelGGL(attn_merge_kernel<64>, dim3(a.m_kv, a.B), dim3(kBlock), 0, s, a);
   return hipGetLastError();
 }
 
-int attn_max_chunk() { return kMaxChunk; }
+int attn_min_chunk() { return kSub; }
+int attn_max_split() { return kMaxSplit; }
 
 }  // namespace tasp

@@ -1,22 +1,30 @@
-// Decode-time GEMVs over compacted panels: y = s * (P x) with INT8 P, float32 x and float32
-// accumulation, memory-bound on the panel stream.
+// Decode-time GEMVs over compacted panels: y = s * (P x), float32 x and float32 accumulation,
+// INT8 panels for the projections and the dense BF16 LM head. All of them are bound by the panel
+// stream from HBM.
 //
-// Layout of the work: a workgroup stages its input vector (RMS-normalised in the prologue when a
-// gain is given) in LDS once, then each wave walks row groups (4 rows, or 2 SwiGLU channels =
-// 2 gate + 2 up rows) in a grid-stride loop. For a row group a lane issues 16-byte loads at chunk
-// offset 16*lane of every 1 KiB chunk of each row, so a wave reads whole contiguous KiB; 4 chunks
-// x 4 rows are in flight per lane before any arithmetic. Dequantisation happens in registers:
-// each int8 byte b is XOR-ed with 0x80 so that v_cvt_f32_ubyte gives b + 128 exactly, and the
-// bias is removed once per row as 128 * sum(x). The per-row scale is applied after the wave
-// reduction, together with the fused epilogue (plain store, residual add, or SwiGLU).
+// Work decomposition: rows are taken in groups of 4 (for gate/up: 2 SwiGLU channels = 2 gate + 2
+// up rows). A tile is one group x 4 KiB of each of its rows (4 chunks of 1 KiB; a wave reads
+// whole contiguous KiB, 16 bytes per lane). Each wave owns a contiguous range of whole groups and
+// walks its tiles with two register buffers in ping-pong: the next tile's 16 buffer loads are in
+// flight while the current tile is dequantised and accumulated, so arithmetic overlaps the stream.
+// Loads are branch-free: lanes past a row end and tiles past the wave's range use an
+// out-of-range buffer offset, which returns zeros without memory traffic. The first tile is
+// issued before the prologue stages the input vector in LDS (RMS-normalised when a gain is
+// given, the inverse RMS being applied in the epilogue), and the epilogue's per-row operands
+// (scales, residual) are wave-uniform scalar loads, which do not queue behind the vector loads.
+//
+// INT8 dequantisation happens in registers: each byte b is XOR-ed with 0x80 so that
+// v_cvt_f32_ubyte gives b + 128 exactly; the bias is removed once per row as 128 * sum(x); the
+// per-row scale is applied after the wave reduction, fused with the epilogue (store, residual
+// add or SwiGLU). BF16 weights are widened by a shift.
 #include "device_common.hpp"
 #include "kernels.hpp"
 
 namespace tasp {
 namespace {
 
-constexpr int kRowsPerGroup = 4;
-constexpr int kChunksInFlight = 4;
+constexpr int kR = 4;             // rows per group
+constexpr int kC = 4;             // 1 KiB chunks per tile
 constexpr int kWgPerCu = 2;
 constexpr int kNumCu = 256;
 
@@ -28,265 +36,249 @@ __device__ __forceinline__ void fma_bytes(float& acc, uint32_t word, const float
   acc = fmaf(float(u >> 24), x.w, acc);
 }
 
-// Stage B input rows of K floats into LDS (swizzled, zero padded to KP) and return sum(x) per row.
+__device__ __forceinline__ void fma_bf16x4(float& acc, uint32_t w0, uint32_t w1, const float4& x) {
+  acc = fmaf(bf16_lo(w0), x.x, acc);
+  acc = fmaf(bf16_hi(w0), x.y, acc);
+  acc = fmaf(bf16_lo(w1), x.z, acc);
+  acc = fmaf(bf16_hi(w1), x.w, acc);
+}
+
+// Stage B input rows of K floats into LDS (swizzled, zero padded to KP).
+// Thread t owns the float4 at columns 1024 i + 4 t (i < KP / 1024); loads are issued in
+// batches of 4 before any use. With a gain the LDS holds x * gamma and the row's inverse RMS is
+// returned in xscale (applied after the dot product: W (c x) = c (W x)); without, xscale = 1.
+// For INT8 rows bias = 128 * sum of the staged values (removes the +128 of the byte conversion).
 template <int B, bool NORM, bool I8>
 __device__ __forceinline__ void stage_inputs(const float* __restrict__ x, int ldx, int K, int KP,
                                              const uint16_t* __restrict__ gamma, float eps,
-                                             float* xs, float* red, float* sumx) {
+                                             float* xs, float* red2, float* xscale, float* bias) {
+  constexpr int kBatch = 4;
   const int tid = threadIdx.x;
+  const int n4 = (K + 3) >> 2;                          // float4 slots holding valid columns
+  const int npass = KP >> 10;
+  const __amdgpu_buffer_rsrc_t rg = make_rsrc(gamma, uint32_t(NORM ? K : 0) * 2u);
 #pragma unroll
   for (int b = 0; b < B; ++b) {
-    const float* xr = x + size_t(b) * ldx;
-    float inv = 1.0f;
-    if (NORM) {
-      float ss = 0.0f;
-      for (int k = tid; k < K; k += kBlock) {
-        const float v = xr[k];
-        ss = fmaf(v, v, ss);
+    const __amdgpu_buffer_rsrc_t rx = make_rsrc(x + size_t(b) * ldx, uint32_t(n4) * 16u);
+    float ss = 0.0f, sx = 0.0f;
+    for (int i0 = 0; i0 < npass; i0 += kBatch) {
+      int4 xv[kBatch];
+      int2 gv[kBatch];
+#pragma unroll
+      for (int u = 0; u < kBatch; ++u) {
+        const int c4 = ((i0 + u) << 8) + tid;           // float4 index
+        xv[u] = buf_load16(rx, c4 < n4 ? uint32_t(c4) * 16u : kOOB);
+        if (NORM)
+          gv[u] = __builtin_bit_cast(int2, __builtin_amdgcn_raw_buffer_load_b64(
+                                               rg, c4 < n4 ? int(uint32_t(c4) * 8u) : int(kOOB), 0, 0));
       }
-      ss = block_sum(ss, red);
-      inv = rsqrtf(ss / float(K) + eps);
-    }
-    float sx = 0.0f;
-    for (int k = tid; k < KP; k += kBlock) {
-      float v = 0.0f;
-      if (k < K) {
-        v = xr[k];
-        if (NORM) v = (v * inv) * bf16_to_f32(gamma[k]);
+#pragma unroll
+      for (int u = 0; u < kBatch; ++u) {
+        const int i = i0 + u;
+        if (i >= npass) break;
+        const int k = (i << 10) + (tid << 2);
+        float4 v = __builtin_bit_cast(float4, xv[u]);
+        // columns K.. of a partial float4 are zero
+        if (k + 0 >= K) v.x = 0.0f;
+        if (k + 1 >= K) v.y = 0.0f;
+        if (k + 2 >= K) v.z = 0.0f;
+        if (k + 3 >= K) v.w = 0.0f;
+        if (NORM) {
+          ss = fmaf(v.x, v.x, fmaf(v.y, v.y, fmaf(v.z, v.z, fmaf(v.w, v.w, ss))));
+          v.x *= bf16_lo(uint32_t(gv[u].x));
+          v.y *= bf16_hi(uint32_t(gv[u].x));
+          v.z *= bf16_lo(uint32_t(gv[u].y));
+          v.w *= bf16_hi(uint32_t(gv[u].y));
+        }
+        sx += (v.x + v.y) + (v.z + v.w);
+        *reinterpret_cast<float4*>(xs + size_t(b) * KP + (I8 ? xs_slot_i8(k) : xs_slot_bf16(k))) = v;
       }
-      xs[size_t(b) * KP + (I8 ? xs_slot_i8(k) : xs_slot_bf16(k))] = v;
-      sx += v;
     }
-    sumx[b] = block_sum(sx, red);
+    // one block reduction for both sums
+    ss = wave_sum(ss);
+    sx = wave_sum(sx);
+    __syncthreads();
+    if ((tid & 63) == 0) {
+      red2[(tid >> 6) * 2] = ss;
+      red2[(tid >> 6) * 2 + 1] = sx;
+    }
+    __syncthreads();
+    const float tss = red2[0] + red2[2] + red2[4] + red2[6];
+    const float tsx = red2[1] + red2[3] + red2[5] + red2[7];
+    xscale[b] = NORM ? rsqrtf(tss / float(K) + eps) : 1.0f;
+    bias[b] = I8 ? 128.0f * tsx : 0.0f;
   }
   __syncthreads();
 }
 
 template <int B, int MODE>
-__global__ __launch_bounds__(kBlock) void gemv_i8_kernel(GemvArgs a) {
+__global__ __launch_bounds__(kBlock) void gemv_kernel(GemvArgs a) {
+  constexpr bool BF = (MODE == GEMV_LMHEAD);
+  constexpr bool NORM = (MODE != GEMV_RESID);
+  constexpr int CPC = BF ? 512 : 1024;                 // columns per 1 KiB chunk
+  constexpr int LCOL = BF ? 8 : 16;                    // columns per lane load
   extern __shared__ __attribute__((aligned(16))) float xs[];
-  __shared__ float red[4];
-  const int K = a.K;
+  __shared__ float red2[8];
+  const float* __restrict__ scale = a.scale;
+  const float* __restrict__ scale2 = a.scale2;
+  const float* __restrict__ resid = a.resid;
+  const int K = a.K, N = a.N;
   const int KP = (K + 1023) & ~1023;
-  float sumx[B];
-  stage_inputs<B, MODE != GEMV_RESID, true>(a.x, a.ldx, K, KP, a.gamma, a.eps, xs, red, sumx);
-
+  const int nchunks = (K + CPC - 1) / CPC;
+  // tiles per group; at least one, so that an empty input (no retained heads or channels) still
+  // writes the epilogue (residual + 0)
+  const int KB = max(1, (nchunks + kC - 1) / kC);
   const int lane = threadIdx.x & 63;
-  const int wave = blockIdx.x * (kBlock / kWave) + (threadIdx.x >> 6);
+  const int wave = __builtin_amdgcn_readfirstlane(blockIdx.x * (kBlock / kWave) + (threadIdx.x >> 6));
   const int nwaves = gridDim.x * (kBlock / kWave);
-  const int per_group = (MODE == GEMV_GATEUP) ? 2 : kRowsPerGroup;
-  const int n_groups = (a.N + per_group - 1) / per_group;
-  const int nchunks = (K + 1023) >> 10;
+  const int per_group = (MODE == GEMV_GATEUP) ? 2 : kR;
+  const int G = (N + per_group - 1) / per_group;
+  const int g0 = int((long(wave) * G) / nwaves), g1 = int((long(wave + 1) * G) / nwaves);
+  const int t_begin = g0 * KB, t_end = g1 * KB;
+  const uint32_t row_bytes = BF ? uint32_t(K) * 2u : uint32_t(a.ld);
+  const __amdgpu_buffer_rsrc_t rw = make_rsrc(a.w, uint32_t(N) * row_bytes);
+  const __amdgpu_buffer_rsrc_t rw2 =
+      make_rsrc(MODE == GEMV_GATEUP ? a.w2 : a.w, uint32_t(N) * row_bytes);
 
-  for (int gi = wave; gi < n_groups; gi += nwaves) {
-    const int8_t* rp[kRowsPerGroup];
-    bool rv[kRowsPerGroup];
-    int row0;
-    if (MODE == GEMV_GATEUP) {
-      row0 = gi * 2;
+  auto row_of = [&](int gi, int r) {
+    return (MODE == GEMV_GATEUP) ? gi * 2 + (r & 1) : gi * kR + r;
+  };
+  auto issue = [&](int t, int4 (&w)[kC][kR]) {
+    const bool ok_t = t < t_end;
+    const int gi = ok_t ? t / KB : 0;
+    const int kb = t - gi * KB;
 #pragma unroll
-      for (int r = 0; r < kRowsPerGroup; ++r) {
-        const int ch = row0 + (r & 1);
-        rv[r] = ch < a.N;
-        rp[r] = (r < 2 ? a.w : a.w2) + size_t(rv[r] ? ch : 0) * a.ld;
-      }
-    } else {
-      row0 = gi * kRowsPerGroup;
+    for (int u = 0; u < kC; ++u) {
+      const int k = (kb * kC + u) * CPC + lane * LCOL;
 #pragma unroll
-      for (int r = 0; r < kRowsPerGroup; ++r) {
-        rv[r] = row0 + r < a.N;
-        rp[r] = a.w + size_t(rv[r] ? row0 + r : 0) * a.ld;
-      }
-    }
-    float acc[B][kRowsPerGroup];
-#pragma unroll
-    for (int b = 0; b < B; ++b)
-#pragma unroll
-      for (int r = 0; r < kRowsPerGroup; ++r) acc[b][r] = 0.0f;
-
-    for (int c0 = 0; c0 < nchunks; c0 += kChunksInFlight) {
-      int4 wv[kChunksInFlight][kRowsPerGroup];
-#pragma unroll
-      for (int u = 0; u < kChunksInFlight; ++u) {
-        const int k = ((c0 + u) << 10) + (lane << 4);
-#pragma unroll
-        for (int r = 0; r < kRowsPerGroup; ++r) {
-          if (rv[r] && c0 + u < nchunks && k < K)
-            wv[u][r] = *reinterpret_cast<const int4*>(rp[r] + k);
-          else
-            wv[u][r] = make_int4(int(0x80808080u), int(0x80808080u), int(0x80808080u),
-                                 int(0x80808080u));
-        }
-      }
-#pragma unroll
-      for (int u = 0; u < kChunksInFlight; ++u) {
-        const int c = c0 + u;
-        if (c >= nchunks) break;
-#pragma unroll
-        for (int b = 0; b < B; ++b) {
-          const float4* xp =
-              reinterpret_cast<const float4*>(xs + size_t(b) * KP) + ((c << 2) << 6) + lane;
-          const float4 x0 = xp[0], x1 = xp[64], x2 = xp[128], x3 = xp[192];
-#pragma unroll
-          for (int r = 0; r < kRowsPerGroup; ++r) {
-            fma_bytes(acc[b][r], uint32_t(wv[u][r].x), x0);
-            fma_bytes(acc[b][r], uint32_t(wv[u][r].y), x1);
-            fma_bytes(acc[b][r], uint32_t(wv[u][r].z), x2);
-            fma_bytes(acc[b][r], uint32_t(wv[u][r].w), x3);
-          }
-        }
+      for (int r = 0; r < kR; ++r) {
+        const int row = row_of(gi, r);
+        const bool ok = ok_t && (row < N) && (k < K);
+        const uint32_t off = ok ? uint32_t(row) * row_bytes + uint32_t(k) * (BF ? 2u : 1u) : kOOB;
+        w[u][r] = buf_load16((MODE == GEMV_GATEUP && r >= 2) ? rw2 : rw, off);
       }
     }
+  };
 
-#pragma unroll
-    for (int b = 0; b < B; ++b)
-#pragma unroll
-      for (int r = 0; r < kRowsPerGroup; ++r) acc[b][r] = wave_sum(acc[b][r]);
+  int4 wa[kC][kR], wb[kC][kR];
+  issue(t_begin, wa);                                   // in flight during the prologue
 
-    if (lane == 0) {
+  float xscale[B], bias[B];
+  stage_inputs<B, NORM, !BF>(a.x, a.ldx, K, KP, a.gamma, a.eps, xs, red2, xscale, bias);
+
+  float acc[B][kR];
+  float s1[kR], s2[2], res[B][kR];
+  auto process = [&](const int4 (&w)[kC][kR], int t) {
+    const int gi = t / KB;
+    const int kb = t - gi * KB;
+    const int row0 = row_of(gi, 0);
+    if (kb == 0) {
+#pragma unroll
+      for (int b = 0; b < B; ++b)
+#pragma unroll
+        for (int r = 0; r < kR; ++r) acc[b][r] = 0.0f;
+      // epilogue operands: wave-uniform addresses -> scalar loads
+#pragma unroll
+      for (int r = 0; r < kR; ++r) {
+        const int row = min(MODE == GEMV_GATEUP ? row0 + (r & 1) : row0 + r, N - 1);
+        s1[r] = BF ? 1.0f : scale[row];
+        if (MODE == GEMV_GATEUP && r < 2) s2[r] = scale2[row];
+#pragma unroll
+        for (int b = 0; b < B; ++b)
+          res[b][r] = (MODE == GEMV_RESID) ? resid[size_t(b) * a.ldy + row] : 0.0f;
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < kC; ++u) {
+      const int c = kb * kC + u;
+      if (c >= nchunks) break;
 #pragma unroll
       for (int b = 0; b < B; ++b) {
-        if (b >= a.B) break;
-        const float bias = 128.0f * sumx[b];
-        float* yb = a.y + size_t(b) * a.ldy;
-        if (MODE == GEMV_GATEUP) {
+        if (BF) {
+          const float4* xp = reinterpret_cast<const float4*>(xs + size_t(b) * KP) + ((c << 1) << 6) + lane;
+          const float4 x0 = xp[0], x1 = xp[64];
 #pragma unroll
-          for (int r = 0; r < 2; ++r) {
-            if (!rv[r]) continue;
-            const int ch = row0 + r;
-            const float g = a.scale[ch] * (acc[b][r] - bias);
-            const float u = a.scale2[ch] * (acc[b][r + 2] - bias);
-            yb[ch] = g / (1.0f + exp2f(-g * kLog2e)) * u;
+          for (int r = 0; r < kR; ++r) {
+            fma_bf16x4(acc[b][r], uint32_t(w[u][r].x), uint32_t(w[u][r].y), x0);
+            fma_bf16x4(acc[b][r], uint32_t(w[u][r].z), uint32_t(w[u][r].w), x1);
           }
         } else {
+          const float4* xp = reinterpret_cast<const float4*>(xs + size_t(b) * KP) + ((c << 2) << 6) + lane;
+          const float4 x0 = xp[0], x1 = xp[64], x2 = xp[128], x3 = xp[192];
 #pragma unroll
-          for (int r = 0; r < kRowsPerGroup; ++r) {
-            if (!rv[r]) continue;
-            const int row = row0 + r;
-            const float v = a.scale[row] * (acc[b][r] - bias);
-            if (MODE == GEMV_RESID)
-              yb[row] = a.resid[size_t(b) * a.ldy + row] + v;
-            else
-              yb[row] = v;
+          for (int r = 0; r < kR; ++r) {
+            fma_bytes(acc[b][r], uint32_t(w[u][r].x), x0);
+            fma_bytes(acc[b][r], uint32_t(w[u][r].y), x1);
+            fma_bytes(acc[b][r], uint32_t(w[u][r].z), x2);
+            fma_bytes(acc[b][r], uint32_t(w[u][r].w), x3);
           }
         }
       }
     }
+    if (kb != KB - 1) return;
+    float tot[B][kR];
+#pragma unroll
+    for (int b = 0; b < B; ++b)
+#pragma unroll
+      for (int r = 0; r < kR; ++r) tot[b][r] = wave_sum(acc[b][r]);
+    if (lane != 0) return;
+#pragma unroll
+    for (int b = 0; b < B; ++b) {
+      float* yb = a.y + size_t(b) * a.ldy;
+      if (MODE == GEMV_GATEUP) {
+#pragma unroll
+        for (int r = 0; r < 2; ++r) {
+          const int ch = row0 + r;
+          if (ch >= N) continue;
+          const float g = s1[r] * xscale[b] * (tot[b][r] - bias[b]);
+          const float u = s2[r] * xscale[b] * (tot[b][r + 2] - bias[b]);
+          yb[ch] = g / (1.0f + exp2f(-g * kLog2e)) * u;
+        }
+      } else {
+#pragma unroll
+        for (int r = 0; r < kR; ++r) {
+          const int row = row0 + r;
+          if (row >= N) continue;
+          yb[row] = res[b][r] + s1[r] * xscale[b] * (tot[b][r] - bias[b]);
+        }
+      }
+    }
+  };
+
+  for (int t = t_begin; t < t_end; t += 2) {
+    issue(t + 1, wb);
+    process(wa, t);
+    issue(t + 2, wa);
+    if (t + 1 < t_end) process(wb, t + 1);
   }
 }
 
-// Dense BF16 LM head: logits = W_lm RMSNorm(r). A 16-byte lane load holds 8 BF16 weights.
-template <int B>
-__global__ __launch_bounds__(kBlock) void lmhead_kernel(LmHeadArgs a) {
-  extern __shared__ __attribute__((aligned(16))) float xs[];
-  __shared__ float red[4];
-  const int K = a.K;
-  const int KP = (K + 511) & ~511;
-  float sumx[B];
-  stage_inputs<B, true, false>(a.x, a.ldx, K, KP, a.gamma, a.eps, xs, red, sumx);
-  const int lane = threadIdx.x & 63;
-  const int wave = blockIdx.x * (kBlock / kWave) + (threadIdx.x >> 6);
-  const int nwaves = gridDim.x * (kBlock / kWave);
-  const int n_groups = (a.V + kRowsPerGroup - 1) / kRowsPerGroup;
-  const int nchunks = (K + 511) >> 9;
-  for (int gi = wave; gi < n_groups; gi += nwaves) {
-    const int row0 = gi * kRowsPerGroup;
-    const uint16_t* rp[kRowsPerGroup];
-    bool rv[kRowsPerGroup];
-#pragma unroll
-    for (int r = 0; r < kRowsPerGroup; ++r) {
-      rv[r] = row0 + r < a.V;
-      rp[r] = a.w + size_t(rv[r] ? row0 + r : 0) * K;
-    }
-    float acc[B][kRowsPerGroup];
-#pragma unroll
-    for (int b = 0; b < B; ++b)
-#pragma unroll
-      for (int r = 0; r < kRowsPerGroup; ++r) acc[b][r] = 0.0f;
-    for (int c0 = 0; c0 < nchunks; c0 += kChunksInFlight) {
-      int4 wv[kChunksInFlight][kRowsPerGroup];
-#pragma unroll
-      for (int u = 0; u < kChunksInFlight; ++u) {
-        const int k = ((c0 + u) << 9) + (lane << 3);
-#pragma unroll
-        for (int r = 0; r < kRowsPerGroup; ++r) {
-          if (rv[r] && c0 + u < nchunks && k < K)
-            wv[u][r] = *reinterpret_cast<const int4*>(rp[r] + k);
-          else
-            wv[u][r] = make_int4(0, 0, 0, 0);
-        }
-      }
-#pragma unroll
-      for (int u = 0; u < kChunksInFlight; ++u) {
-        const int c = c0 + u;
-        if (c >= nchunks) break;
-#pragma unroll
-        for (int b = 0; b < B; ++b) {
-          const float4* xp =
-              reinterpret_cast<const float4*>(xs + size_t(b) * KP) + ((c << 1) << 6) + lane;
-          const float4 x0 = xp[0], x1 = xp[64];
-#pragma unroll
-          for (int r = 0; r < kRowsPerGroup; ++r) {
-            const uint32_t w0 = wv[u][r].x, w1 = wv[u][r].y, w2 = wv[u][r].z, w3 = wv[u][r].w;
-            float s = acc[b][r];
-            s = fmaf(bf16_lo(w0), x0.x, s);
-            s = fmaf(bf16_hi(w0), x0.y, s);
-            s = fmaf(bf16_lo(w1), x0.z, s);
-            s = fmaf(bf16_hi(w1), x0.w, s);
-            s = fmaf(bf16_lo(w2), x1.x, s);
-            s = fmaf(bf16_hi(w2), x1.y, s);
-            s = fmaf(bf16_lo(w3), x1.z, s);
-            s = fmaf(bf16_hi(w3), x1.w, s);
-            acc[b][r] = s;
-          }
-        }
-      }
-    }
-#pragma unroll
-    for (int b = 0; b < B; ++b)
-#pragma unroll
-      for (int r = 0; r < kRowsPerGroup; ++r) acc[b][r] = wave_sum(acc[b][r]);
-    if (lane == 0) {
-#pragma unroll
-      for (int b = 0; b < B; ++b) {
-        if (b >= a.B) break;
-#pragma unroll
-        for (int r = 0; r < kRowsPerGroup; ++r)
-          if (rv[r]) a.y[size_t(b) * a.ldy + row0 + r] = acc[b][r];
-      }
-    }
-  }
+int gemv_grid(int n_groups) {
+  int waves = n_groups;
+  if (waves > kNumCu * kWgPerCu * 4) waves = kNumCu * kWgPerCu * 4;
+  int grid = (waves + 3) / 4;
+  return grid < 1 ? 1 : grid;
 }
 
 template <int B>
 hipError_t launch_gemv_b(GemvMode mode, const GemvArgs& a, hipStream_t s) {
-  const int per_group = (mode == GEMV_GATEUP) ? 2 : kRowsPerGroup;
-  const int n_groups = (a.N + per_group - 1) / per_group;
-  int grid = (n_groups + 3) / 4;
-  if (grid > kNumCu * kWgPerCu) grid = kNumCu * kWgPerCu;
-  if (grid < 1) grid = 1;
+  const int per_group = (mode == GEMV_GATEUP) ? 2 : kR;
+  const int grid = gemv_grid((a.N + per_group - 1) / per_group);
   const size_t lds = gemv_lds_bytes(B, a.K);
   switch (mode) {
     case GEMV_QKV:
-      hipLaunchKernelGGL((gemv_i8_kernel<B, GEMV_QKV>), dim3(grid), dim3(kBlock), lds, s, a);
+      hipLaunchKernelGGL((gemv_kernel<B, GEMV_QKV>), dim3(grid), dim3(kBlock), lds, s, a);
       break;
     case GEMV_RESID:
-      hipLaunchKernelGGL((gemv_i8_kernel<B, GEMV_RESID>), dim3(grid), dim3(kBlock), lds, s, a);
+      hipLaunchKernelGGL((gemv_kernel<B, GEMV_RESID>), dim3(grid), dim3(kBlock), lds, s, a);
       break;
     case GEMV_GATEUP:
-      hipLaunchKernelGGL((gemv_i8_kernel<B, GEMV_GATEUP>), dim3(grid), dim3(kBlock), lds, s, a);
+      hipLaunchKernelGGL((gemv_kernel<B, GEMV_GATEUP>), dim3(grid), dim3(kBlock), lds, s, a);
+      break;
+    case GEMV_LMHEAD:
+      hipLaunchKernelGGL((gemv_kernel<B, GEMV_LMHEAD>), dim3(grid), dim3(kBlock), lds, s, a);
       break;
   }
-  return hipGetLastError();
-}
-
-template <int B>
-hipError_t launch_lmhead_b(const LmHeadArgs& a, hipStream_t s) {
-  const int n_groups = (a.V + kRowsPerGroup - 1) / kRowsPerGroup;
-  int grid = (n_groups + 3) / 4;
-  if (grid > kNumCu * kWgPerCu) grid = kNumCu * kWgPerCu;
-  const size_t lds = size_t(B) * ((a.K + 511) & ~511) * sizeof(float);
-  hipLaunchKernelGGL((lmhead_kernel<B>), dim3(grid), dim3(kBlock), lds, s, a);
   return hipGetLastError();
 }
 
@@ -304,20 +296,6 @@ hipError_t launch_gemv(GemvMode mode, const GemvArgs& a, hipStream_t s) {
     case 6: return launch_gemv_b<6>(mode, a, s);
     case 7: return launch_gemv_b<7>(mode, a, s);
     case 8: return launch_gemv_b<8>(mode, a, s);
-  }
-  return hipErrorInvalidValue;
-}
-
-hipError_t launch_lmhead(const LmHeadArgs& a, hipStream_t s) {
-  switch (a.B) {
-    case 1: return launch_lmhead_b<1>(a, s);
-    case 2: return launch_lmhead_b<2>(a, s);
-    case 3: return launch_lmhead_b<3>(a, s);
-    case 4: return launch_lmhead_b<4>(a, s);
-    case 5: return launch_lmhead_b<5>(a, s);
-    case 6: return launch_lmhead_b<6>(a, s);
-    case 7: return launch_lmhead_b<7>(a, s);
-    case 8: return launch_lmhead_b<8>(a, s);
   }
   return hipErrorInvalidValue;
 }

@@ -33,19 +33,22 @@ hipError_t launch_fill_zero(void* dst, size_t bytes, hipStream_t s);            
 
 // ----------------------------------------------------------------- decode GEMVs
 
-enum GemvMode { GEMV_QKV = 0, GEMV_RESID = 1, GEMV_GATEUP = 2 };
+// GEMV_QKV: RMSNorm prologue, plain store; GEMV_RESID: residual add; GEMV_GATEUP: RMSNorm
+// prologue, SwiGLU epilogue over paired gate / up rows; GEMV_LMHEAD: RMSNorm prologue, BF16
+// weights (w holds BF16 rows of K elements), plain store.
+enum GemvMode { GEMV_QKV = 0, GEMV_RESID = 1, GEMV_GATEUP = 2, GEMV_LMHEAD = 3 };
 
 struct GemvArgs {
-  const int8_t* w;       // panel rows [N][ld] (gate/up: gate rows)
-  const int8_t* w2;      // gate/up: up rows [N][ld]
-  const float* scale;    // [N]
+  const void* w;         // panel rows [N][ld] (gate/up: gate rows; LM head: BF16 [N][K])
+  const void* w2;        // gate/up: up rows [N][ld]
+  const float* scale;    // [N] (unused by the LM head)
   const float* scale2;   // gate/up: up scales [N]
   int N;                 // output rows (gate/up: channels)
-  int K;                 // valid columns; columns K..ld-1 of a row are zero
-  int ld;                // row stride in bytes, multiple of 16 and >= K
+  int K;                 // valid columns; INT8 columns K..ld-1 of a row are zero
+  int ld;                // INT8 row stride in bytes, multiple of 16 and >= K
   const float* x;        // input rows [B][ldx]
   int ldx;
-  const uint16_t* gamma; // RMSNorm gain (QKV, gate/up); null: input used as is
+  const uint16_t* gamma; // RMSNorm gain (QKV, gate/up, LM head); null for GEMV_RESID
   float eps;
   const float* resid;    // residual rows [B][ldy] (GEMV_RESID)
   float* y;              // output rows [B][ldy]
@@ -55,33 +58,25 @@ struct GemvArgs {
 hipError_t launch_gemv(GemvMode mode, const GemvArgs& a, hipStream_t s);
 size_t gemv_lds_bytes(int B, int K);
 
-struct LmHeadArgs {
-  const uint16_t* w;     // BF16 [V][K]
-  int V, K;
-  const float* x; int ldx;
-  const uint16_t* gamma; float eps;
-  float* y; int ldy;     // logits [B][ldy]
-  int B;
-};
-hipError_t launch_lmhead(const LmHeadArgs& a, hipStream_t s);
-
 // ----------------------------------------------------------------- decode attention
 
 struct AttnArgs {
   const float* qkv; int ld_qkv;    // [B][ld_qkv]: raw q (m_q*dh), k (m_kv*dh), v (m_kv*dh)
   int m_q, m_kv, dh;
-  const int* kv_idx;               // [m_kv] retained group ids
-  const int* slot_start;           // [m_kv + 1] first head position of each retained group
+  int kv_idx[64];                  // retained group ids (first m_kv entries)
+  int slot_start[65];              // first retained-head position of each group slot, then m_q
   uint16_t* kc; uint16_t* vc;      // this layer's cache base, [B][Hkv][S][dh]
   int Hkv, S;
   const float* rope_cos; const float* rope_sin;  // [max_seq][dh/2]
   int pos, chunk, n_split;
-  float* part;                     // [B][m_kv][n_split][8][dh + 2]
-  int* counters;                   // [B][Hkv], zero between calls
+  float* part;                     // [B][m_kv][n_split][8][dh + 4] when n_split > 1
   float* o; int ld_o;              // [B][ld_o] retained heads in ascending order
   int B;
 };
+// Split-KV partial attention (writes o directly when n_split == 1), then, for n_split > 1, the
+// log-sum-exp merge of the partials into o.
 hipError_t launch_attn_decode(const AttnArgs& a, hipStream_t s);
-int attn_max_chunk();
+int attn_min_chunk();   // rows per split are a multiple of this
+int attn_max_split();
 
 }  // namespace tasp

@@ -134,10 +134,19 @@ __global__ __launch_bounds__(kBlock) void gather_cols_kernel(
   for (int j = threadIdx.x; j < dst_ld; j += kBlock) d[j] = (j < n) ? s[idx[j]] : int8_t(0);
 }
 
+// Streaming copy with 4 independent 16-byte loads in flight per thread.
 __global__ __launch_bounds__(kBlock) void copy_kernel(int4* __restrict__ dst,
                                                       const int4* __restrict__ src, size_t n) {
   const size_t stride = size_t(gridDim.x) * kBlock;
-  for (size_t i = size_t(blockIdx.x) * kBlock + threadIdx.x; i < n; i += stride) dst[i] = src[i];
+  size_t i = size_t(blockIdx.x) * kBlock + threadIdx.x;
+  for (; i + 3 * stride < n; i += 4 * stride) {
+    const int4 a = src[i], b = src[i + stride], c = src[i + 2 * stride], d = src[i + 3 * stride];
+    dst[i] = a;
+    dst[i + stride] = b;
+    dst[i + 2 * stride] = c;
+    dst[i + 3 * stride] = d;
+  }
+  for (; i < n; i += stride) dst[i] = src[i];
 }
 
 __global__ __launch_bounds__(kBlock) void fill_zero_kernel(uint32_t* __restrict__ dst, size_t n) {
@@ -147,7 +156,7 @@ __global__ __launch_bounds__(kBlock) void fill_zero_kernel(uint32_t* __restrict_
 
 int grid_for(size_t n) {
   size_t g = (n + kBlock - 1) / kBlock;
-  if (g > 8192) g = 8192;
+  if (g > 2048) g = 2048;
   return g ? int(g) : 1;
 }
 

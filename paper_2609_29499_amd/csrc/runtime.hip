@@ -37,7 +37,6 @@ tasp_status fail(tasp_status s, const char* fmt, ...) {
   } while (0)
 
 constexpr size_t kAlign = 256;
-constexpr int kMinChunk = 64;
 constexpr int kAttnTargetBlocks = 1024;
 constexpr size_t kLdsLimit = 160 * 1024 - 1024;
 
@@ -69,6 +68,12 @@ tasp_status check_desc(const tasp_model_desc* d) {
   if (d->max_batch > 8) return fail(TASP_ERR_SHAPE, "max_batch > 8");
   if (!(d->rms_eps > 0.0f) || !(d->rope_theta > 0.0))
     return fail(TASP_ERR_SHAPE, "rms_eps and rope_theta must be positive");
+  // every panel (and the BF16 LM head) must be addressable by a 31-bit buffer offset
+  const double big = double(1u << 31) - 1.0;
+  const double D = d->d_model, qkv_rows = double(d->n_q_heads + 2 * d->n_kv_heads) * d->head_dim;
+  if (qkv_rows * D > big || double(d->d_ffn) * D > big || D * d->n_q_heads * d->head_dim > big ||
+      double(d->vocab) * D * 2.0 > big)
+    return fail(TASP_ERR_SHAPE, "a weight panel exceeds 2^31 bytes");
   const int widest = std::max({d->d_model, d->n_q_heads * d->head_dim, d->d_ffn});
   if (tasp::gemv_lds_bytes(d->max_batch, widest) > kLdsLimit)
     return fail(TASP_ERR_UNSUPPORTED, "max_batch x widest GEMV input exceeds LDS (%d x %d)",
@@ -129,7 +134,7 @@ struct Layout {
   size_t mask_q, mask_kv, mask_f;
   size_t idx_q, idx_kv, idx_slot, idx_slot_start, idx_ffn, counts;
   size_t final_norm, lm_head, rope_cos, rope_sin;
-  size_t r_mid, r_io0, r_io1, qkv_buf, o_buf, h_buf, part, counters;
+  size_t r_mid, r_io0, r_io1, qkv_buf, o_buf, h_buf, part;
   size_t zero_begin, zero_end;       // scratch cleared at compile
   size_t total;
   int n_split_max, ld_qkv, ld_obuf, ld_h;
@@ -177,7 +182,8 @@ Layout make_layout(const tasp_model_desc* d, const Closed& c) {
   Y.lm_head = d->vocab ? take(size_t(d->vocab) * D * 2) : 0;
   Y.rope_cos = take(size_t(d->max_seq) * (dh / 2) * 4);
   Y.rope_sin = take(size_t(d->max_seq) * (dh / 2) * 4);
-  Y.n_split_max = (d->max_seq + kMinChunk - 1) / kMinChunk;
+  Y.n_split_max = std::min((d->max_seq + tasp::attn_min_chunk() - 1) / tasp::attn_min_chunk(),
+                           tasp::attn_max_split());
   Y.ld_qkv = (Hq + 2 * Hkv) * dh;
   Y.ld_obuf = Hq * dh;
   Y.ld_h = round_up16(F);
@@ -188,8 +194,7 @@ Layout make_layout(const tasp_model_desc* d, const Closed& c) {
   Y.qkv_buf = take(size_t(B) * Y.ld_qkv * 4);
   Y.o_buf = take(size_t(B) * Y.ld_obuf * 4);
   Y.h_buf = take(size_t(B) * Y.ld_h * 4);
-  Y.part = take(size_t(B) * Hkv * Y.n_split_max * 8 * (dh + 2) * 4);
-  Y.counters = take(size_t(B) * Hkv * 4);
+  Y.part = take(size_t(B) * Hkv * Y.n_split_max * 8 * (dh + 4) * 4);
   Y.zero_end = off;
   Y.total = off;
   return Y;
@@ -219,8 +224,7 @@ struct LayerPlan {
   int8_t *qkv, *o, *g, *u, *dn;
   float *s_qkv, *s_o, *s_g, *s_u, *s_d;
   uint16_t *an, *fn;
-  int *d_kv_idx, *d_slot_start;
-  std::vector<int> q_idx, kv_idx, q_kvslot, ffn_idx;
+  std::vector<int> q_idx, kv_idx, q_kvslot, ffn_idx, slot_start;
 };
 
 struct tasp_plan_s {
@@ -232,7 +236,6 @@ struct tasp_plan_s {
   uint16_t *final_norm, *lm_head;
   float *rope_cos, *rope_sin;
   float *r_mid, *r_io[2], *qkv_buf, *o_buf, *h_buf, *part;
-  int* counters;
   int n_split_max, ld_qkv, ld_obuf, ld_h;
 };
 
@@ -306,16 +309,21 @@ tasp_status decode_impl(tasp_plan p, const float* x, tasp_kv_cache* cache, int32
     }
     if (P.m_kv > 0) {
       tasp::AttnArgs a{};
-      long want = (long(total) * P.m_kv * B + kAttnTargetBlocks - 1) / kAttnTargetBlocks;
-      int chunk = int(std::min<long>(std::max<long>(want, kMinChunk), tasp::attn_max_chunk()));
-      chunk = (chunk + kMinChunk - 1) / kMinChunk * kMinChunk;
+      // rows per split: a multiple of the kernel's sub-block, large enough that about
+      // kAttnTargetBlocks workgroups run and that the split count stays within the merge's limit
+      const long sub = tasp::attn_min_chunk();
+      const long want = (long(total) * P.m_kv * B + kAttnTargetBlocks - 1) / kAttnTargetBlocks;
+      const long need = (long(total) + tasp::attn_max_split() - 1) / tasp::attn_max_split();
+      long chunk = std::max<long>(std::max(want, need), sub);
+      chunk = (chunk + sub - 1) / sub * sub;
       a.qkv = p->qkv_buf; a.ld_qkv = p->ld_qkv; a.m_q = P.m_q; a.m_kv = P.m_kv; a.dh = dh;
-      a.kv_idx = P.d_kv_idx; a.slot_start = P.d_slot_start;
+      for (int q = 0; q < P.m_kv; ++q) a.kv_idx[q] = P.kv_idx[q];
+      for (int q = 0; q <= P.m_kv; ++q) a.slot_start[q] = P.slot_start[q];
       a.kc = static_cast<uint16_t*>(cache->k) + l * layer_cache;
       a.vc = static_cast<uint16_t*>(cache->v) + l * layer_cache;
       a.Hkv = d.n_kv_heads; a.S = cache->max_seq; a.rope_cos = p->rope_cos;
-      a.rope_sin = p->rope_sin; a.pos = pos; a.chunk = chunk;
-      a.n_split = (total + chunk - 1) / chunk; a.part = p->part; a.counters = p->counters;
+      a.rope_sin = p->rope_sin; a.pos = pos; a.chunk = int(chunk);
+      a.n_split = int((total + chunk - 1) / chunk); a.part = p->part;
       a.o = p->o_buf; a.ld_o = p->ld_obuf; a.B = B;
       if ((st = run_kernel(tm, 1, s, [&] { return tasp::launch_attn_decode(a, s); }))) return st;
     }
@@ -343,10 +351,11 @@ tasp_status decode_impl(tasp_plan p, const float* x, tasp_kv_cache* cache, int32
     }
   }
   if (d.vocab) {
-    tasp::LmHeadArgs a{};
-    a.w = p->lm_head; a.V = d.vocab; a.K = D; a.x = p->r_io[(L - 1) & 1]; a.ldx = D;
-    a.gamma = p->final_norm; a.eps = d.rms_eps; a.y = out; a.ldy = d.vocab; a.B = B;
-    if ((st = run_kernel(tm, 5, s, [&] { return tasp::launch_lmhead(a, s); }))) return st;
+    tasp::GemvArgs a{};
+    a.w = p->lm_head; a.N = d.vocab; a.K = D; a.ld = 2 * D; a.x = p->r_io[(L - 1) & 1];
+    a.ldx = D; a.gamma = p->final_norm; a.eps = d.rms_eps; a.y = out; a.ldy = d.vocab; a.B = B;
+    if ((st = run_kernel(tm, 5, s, [&] { return tasp::launch_gemv(tasp::GEMV_LMHEAD, a, s); })))
+      return st;
   }
   return TASP_OK;
 }
@@ -458,8 +467,6 @@ tasp_status tasp_compile_plan(const tasp_model_desc* desc, const tasp_store* sto
     P.s_g = reinterpret_cast<float*>(at(Q.s_g)); P.s_u = reinterpret_cast<float*>(at(Q.s_u));
     P.dn = reinterpret_cast<int8_t*>(at(Q.dn)); P.s_d = reinterpret_cast<float*>(at(Q.s_d));
     P.an = reinterpret_cast<uint16_t*>(at(Q.an)); P.fn = reinterpret_cast<uint16_t*>(at(Q.fn));
-    P.d_kv_idx = dkv + size_t(l) * Hkv;
-    P.d_slot_start = dss + size_t(l) * (Hkv + 1);
     const int* lq = dq + size_t(l) * Hq;
     const int* lkv = dkv + size_t(l) * Hkv;
     const int* lf = dffn + size_t(l) * F;
@@ -517,7 +524,6 @@ tasp_status tasp_compile_plan(const tasp_model_desc* desc, const tasp_store* sto
   p->o_buf = reinterpret_cast<float*>(at(Y.o_buf));
   p->h_buf = reinterpret_cast<float*>(at(Y.h_buf));
   p->part = reinterpret_cast<float*>(at(Y.part));
-  p->counters = reinterpret_cast<int*>(at(Y.counters));
   p->n_split_max = Y.n_split_max; p->ld_qkv = Y.ld_qkv; p->ld_obuf = Y.ld_obuf; p->ld_h = Y.ld_h;
 
   // read the device index lists back (the one synchronisation) and check them
@@ -558,6 +564,18 @@ tasp_status tasp_compile_plan(const tasp_model_desc* desc, const tasp_store* sto
       if (c.f[size_t(l) * F + j]) ok &= (k < P.c && P.ffn_idx[k++] == j);
     for (int i = 0; i < P.m_q && ok; ++i)
       ok &= P.q_kvslot[i] >= 0 && P.q_kvslot[i] < P.m_kv && P.kv_idx[P.q_kvslot[i]] == P.q_idx[i] / r;
+    // slot j's heads are the run of the ascending head list whose slot is j
+    P.slot_start.assign(size_t(P.m_kv) + 1, 0);
+    for (int jj = 0; jj <= P.m_kv; ++jj)
+      for (int i = 0; i < P.m_q; ++i) P.slot_start[jj] += (P.q_kvslot[i] < jj);
+    for (int jj = 0; jj < P.m_kv && ok; ++jj) ok &= P.slot_start[jj + 1] > P.slot_start[jj];
+    std::vector<int> dev_ss(size_t(Hkv) + 1);
+    if (ok && hipMemcpy(dev_ss.data(), dss + size_t(l) * (Hkv + 1), (P.m_kv + 1) * sizeof(int),
+                        hipMemcpyDeviceToHost) == hipSuccess) {
+      for (int jj = 0; jj <= P.m_kv; ++jj) ok &= dev_ss[jj] == P.slot_start[jj];
+    } else {
+      ok = false;
+    }
     if (!ok) {
       delete p;
       return fail(TASP_ERR_INTERNAL, "layer %d: device index lists differ from the host closure", l);
