@@ -5,10 +5,10 @@
  * heads, single query heads inside a kept group, and SwiGLU channels (gate row, up row and down
  * column together). The mask is closed under those dependencies (paper, Sec. "Dependency-Closed
  * Masks and Cache-Consistent Routing") and then compiled once into a plan: the retained rows and
- * columns of every projection are packed into dense contiguous INT8 panels (paper, same section,
- * and appendix paragraph "Backing-store semantics"), so that every later decode step and prefill
- * launches only the smaller contractions. The plan stays fixed for prefill and every decode step,
- * and a KV cache is never reused across plans of different masks (same section).
+ * columns of every projection are copied into dense INT8 panels (same section, and the appendix
+ * paragraph "Backing-store semantics"), so that every later decode step and prefill launches only
+ * the smaller contractions. One plan serves a whole request, its prefill and all of its decode
+ * steps; a cache filled under one mask is refused by a plan of another mask (same section).
  *
  * Model: Llama-3 style decoder layer. Per layer and token, with residual r (float32):
  *   n = RMSNorm(r; gamma_attn); [q; k; v] = Wqkv n; RoPE(q, k) at the token position;
@@ -59,7 +59,7 @@ enum {
 typedef struct tasp_plan_s* tasp_plan;   /* opaque; immutable after tasp_compile_plan */
 
 /* Model geometry and the plan's capacity limits.
- *   n_layers >= 1; d_model % 64 == 0; head_dim in {64, 128}; n_q_heads % n_kv_heads == 0 with
+ *   n_layers >= 1; d_model % 16 == 0; head_dim in {64, 128}; n_q_heads % n_kv_heads == 0 with
  *   n_q_heads / n_kv_heads <= 8; d_ffn % 16 == 0; vocab = 0 for a bare layer stack (decode
  *   returns the residual) or > 0 for a stack ending in the BF16 LM head (decode returns logits).
  *   max_batch in 1..8 (decode batch), max_seq = cache rows per sequence, max_prefill = largest
@@ -125,10 +125,10 @@ enum { TASP_PANEL_QKV = 0, TASP_PANEL_O = 1, TASP_PANEL_GATE = 2, TASP_PANEL_UP 
 tasp_status tasp_plan_workspace_bytes(const tasp_model_desc* desc, const tasp_mask* mask,
                                       size_t* bytes);
 
-/* Compile a plan (paper: "packed into contiguous tensors and compiled as static launch plans").
- * Uploads the mask, runs the closure/index kernel (one workgroup per layer; integer-only), gathers
+/* Compile a plan (paper, Sec. "Dependency-Closed Masks and Cache-Consistent Routing": one
+ * compiled launch plan per mask over the INT8 store). Uploads the mask, runs the closure/index kernel (one workgroup per layer; integer-only), gathers
  * the retained rows / columns and their scales into the panels inside `workspace` (device, 256-byte
- * aligned, >= tasp_plan_workspace_bytes), and zeroes the scratch counters. Synchronises `stream`
+ * aligned, >= tasp_plan_workspace_bytes), and zeroes the decode scratch. Synchronises `stream`
  * once to read the index lists back; returns TASP_ERR_INTERNAL if they differ from the host's
  * closure. The workspace must outlive the plan and must not be shared between plans. */
 tasp_status tasp_compile_plan(const tasp_model_desc* desc, const tasp_store* store,
@@ -184,6 +184,17 @@ tasp_status tasp_prefill(tasp_plan plan, const float* x, int32_t T, tasp_kv_cach
 tasp_status tasp_decode_step_timed(tasp_plan plan, const float* x, tasp_kv_cache* cache,
                                    int32_t pos, float* out, void* stream, float* kernel_ms,
                                    int32_t* kinds, int32_t cap, int32_t* n);
+
+/* Profiling: average duration of one stage kernel, measured as n_plans * reps back-to-back launches
+ * between two HIP events on `stream`. Stage `kind` 3 is the gate/up GEMV (RMSNorm + SwiGLU; reads
+ * the plan's post-attention residual, writes its SwiGLU scratch) and 4 the down GEMV (writes the
+ * plan's scratch, not a caller buffer) of layer `layer`. Launch i uses plans[i % n_plans], so
+ * distinct plan copies keep every launch streaming its panel from HBM rather than from cache. Each
+ * plan must have run a tasp_decode_step with batch `batch` (its scratch holds the stage's input).
+ * Synchronises `stream`; writes the mean milliseconds per launch. Not capturable. */
+tasp_status tasp_profile_stage(const tasp_plan* plans, int32_t n_plans, int32_t layer,
+                               int32_t kind, int32_t batch, int32_t reps, void* stream,
+                               float* ms_per_launch);
 
 /* Plain streaming copy of `bytes` (multiple of 16) from src to dst (device): the reference kernel
  * whose counter readings calibrate memory-traffic measurements. */

@@ -42,9 +42,9 @@ __all__ = [
 
 def close_mask(q_keep, kv_keep, ffn_keep, group_size):
     """Dependency closure of a structured mask (Sec. "Dependency-Closed Masks and
-    Cache-Consistent Routing"): in grouped-query attention a KV head stays active whenever any
-    query head it serves is kept, and query heads are never moved to another group; the SwiGLU
-    gate row, up row and down column of a channel are kept or removed together.
+    Cache-Consistent Routing"). Under grouped-query attention a KV group is needed exactly when at
+    least one of its own query heads survives, and a head keeps its original group; a SwiGLU
+    channel is a unit made of its gate row, its up row and its down column.
 
     Inputs are 0/1 arrays ``[L][H_q]``, ``[L][H_kv]`` (None: all kept) and ``[L][d_f]``.
     Returns boolean arrays (q', kv', ffn') with q' = q AND kv[g(h)], kv'[g] = OR_{g(h)=g} q'[h].

@@ -25,7 +25,7 @@ KERNEL_KINDS = {0: "qkv_gemv", 1: "attention", 2: "o_gemv", 3: "gateup_gemv", 4:
 EXPORTS = ["tasp_plan_workspace_bytes", "tasp_compile_plan", "tasp_plan_counts",
            "tasp_plan_indices", "tasp_plan_panel", "tasp_plan_ledger", "tasp_plan_destroy",
            "tasp_kv_bind", "tasp_decode_step", "tasp_prefill", "tasp_decode_step_timed",
-           "tasp_copy_probe", "tasp_status_string", "tasp_last_error"]
+           "tasp_profile_stage", "tasp_copy_probe", "tasp_status_string", "tasp_last_error"]
 
 
 class TaspError(RuntimeError):
@@ -94,6 +94,7 @@ def load(path: str = LIB_PATH):
         "tasp_prefill": [P, P, I32, C.POINTER(tasp_kv_cache), I32, P, P],
         "tasp_decode_step_timed": [P, P, C.POINTER(tasp_kv_cache), I32, P, P, C.POINTER(C.c_float),
                                    C.POINTER(I32), I32, C.POINTER(I32)],
+        "tasp_profile_stage": [C.POINTER(P), I32, I32, I32, I32, I32, P, C.POINTER(C.c_float)],
         "tasp_copy_probe": [P, P, SZ, P],
     }
     for name, args in sig.items():
@@ -180,6 +181,13 @@ def tasp_decode_step_timed(plan, x_ptr, cache, pos, out_ptr, stream, cap=4096):
     _check(load().tasp_decode_step_timed(plan, x_ptr, C.byref(cache), pos, out_ptr, stream, ms,
                                          kinds, cap, C.byref(n)))
     return [(KERNEL_KINDS[kinds[i]], ms[i]) for i in range(n.value)]
+
+
+def tasp_profile_stage(plans, layer, kind, batch, reps, stream):
+    arr = (C.c_void_p * len(plans))(*[p.value if isinstance(p, C.c_void_p) else p for p in plans])
+    ms = C.c_float()
+    _check(load().tasp_profile_stage(arr, len(plans), layer, kind, batch, reps, stream, C.byref(ms)))
+    return ms.value
 
 
 def tasp_copy_probe(dst_ptr, src_ptr, nbytes, stream):

@@ -273,6 +273,27 @@ tasp_status check_cache(const tasp_plan_s* p, const tasp_kv_cache* c) {
   return TASP_OK;
 }
 
+// gate/up GEMV of layer l: RMSNorm(r_mid) -> SwiGLU scratch
+tasp::GemvArgs gateup_args(const tasp_plan_s* p, int l, int B) {
+  const LayerPlan& P = p->layers[l];
+  const int D = p->desc.d_model;
+  tasp::GemvArgs a{};
+  a.w = P.g; a.w2 = P.u; a.scale = P.s_g; a.scale2 = P.s_u; a.N = P.c; a.K = D; a.ld = D;
+  a.x = p->r_mid; a.ldx = D; a.gamma = P.fn; a.eps = p->desc.rms_eps; a.y = p->h_buf;
+  a.ldy = p->ld_h; a.B = B;
+  return a;
+}
+
+// down GEMV of layer l: r_mid + Wd h -> y
+tasp::GemvArgs down_args(const tasp_plan_s* p, int l, int B, float* y) {
+  const LayerPlan& P = p->layers[l];
+  const int D = p->desc.d_model;
+  tasp::GemvArgs a{};
+  a.w = P.dn; a.scale = P.s_d; a.N = D; a.K = P.c; a.ld = P.ld_d; a.x = p->h_buf;
+  a.ldx = p->ld_h; a.resid = p->r_mid; a.y = y; a.ldy = D; a.B = B;
+  return a;
+}
+
 tasp_status decode_impl(tasp_plan p, const float* x, tasp_kv_cache* cache, int32_t pos,
                         float* out, void* stream, Timer* tm) {
   if (!p) return fail(TASP_ERR_INVALID_ARG, "plan is NULL");
@@ -335,17 +356,12 @@ tasp_status decode_impl(tasp_plan p, const float* x, tasp_kv_cache* cache, int32
         return st;
     }
     if (P.c > 0) {
-      tasp::GemvArgs a{};
-      a.w = P.g; a.w2 = P.u; a.scale = P.s_g; a.scale2 = P.s_u; a.N = P.c; a.K = D; a.ld = D;
-      a.x = p->r_mid; a.ldx = D; a.gamma = P.fn; a.eps = d.rms_eps; a.y = p->h_buf;
-      a.ldy = p->ld_h; a.B = B;
+      const tasp::GemvArgs a = gateup_args(p, l, B);
       if ((st = run_kernel(tm, 3, s, [&] { return tasp::launch_gemv(tasp::GEMV_GATEUP, a, s); })))
         return st;
     }
     {
-      tasp::GemvArgs a{};
-      a.w = P.dn; a.scale = P.s_d; a.N = D; a.K = P.c; a.ld = P.ld_d; a.x = p->h_buf;
-      a.ldx = p->ld_h; a.resid = p->r_mid; a.y = lo; a.ldy = D; a.B = B;
+      const tasp::GemvArgs a = down_args(p, l, B, lo);
       if ((st = run_kernel(tm, 4, s, [&] { return tasp::launch_gemv(tasp::GEMV_RESID, a, s); })))
         return st;
     }
@@ -722,6 +738,41 @@ tasp_status tasp_prefill(tasp_plan p, const float* x, int32_t T, tasp_kv_cache* 
   if (T < 1 || T > p->desc.max_prefill) return fail(TASP_ERR_SHAPE, "T %d outside 1..%d", T, p->desc.max_prefill);
   if (pos0 < 0 || pos0 + T > cache->max_seq) return fail(TASP_ERR_POS_RANGE, "pos0 + T beyond the cache");
   return fail(TASP_ERR_UNSUPPORTED, "prefill is not built yet");
+}
+
+tasp_status tasp_profile_stage(const tasp_plan* plans, int32_t n_plans, int32_t layer,
+                               int32_t kind, int32_t batch, int32_t reps, void* stream,
+                               float* ms_per_launch) {
+  if (!plans || n_plans < 1 || reps < 1 || !ms_per_launch)
+    return fail(TASP_ERR_INVALID_ARG, "plans / n_plans / reps / ms_per_launch");
+  if (kind != 3 && kind != 4) return fail(TASP_ERR_UNSUPPORTED, "stage kind %d is not profiled", kind);
+  std::vector<tasp::GemvArgs> args(n_plans);
+  for (int i = 0; i < n_plans; ++i) {
+    const tasp_plan_s* p = plans[i];
+    if (!p) return fail(TASP_ERR_INVALID_ARG, "plans[%d] is NULL", i);
+    if (layer < 0 || layer >= p->desc.n_layers) return fail(TASP_ERR_INVALID_ARG, "bad layer %d", layer);
+    if (batch < 1 || batch > p->desc.max_batch) return fail(TASP_ERR_SHAPE, "bad batch %d", batch);
+    if (kind == 3 && p->layers[layer].c == 0) return fail(TASP_ERR_SHAPE, "layer has no FFN channels");
+    args[i] = (kind == 3) ? gateup_args(p, layer, batch)
+                          : down_args(p, layer, batch, p->r_io[layer & 1]);
+  }
+  const tasp::GemvMode mode = (kind == 3) ? tasp::GEMV_GATEUP : tasp::GEMV_RESID;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  hipEvent_t e0, e1;
+  HIP_TRY(hipEventCreate(&e0));
+  HIP_TRY(hipEventCreate(&e1));
+  hipError_t h = hipEventRecord(e0, s);
+  for (int r = 0; r < reps && h == hipSuccess; ++r)
+    for (int i = 0; i < n_plans && h == hipSuccess; ++i) h = tasp::launch_gemv(mode, args[i], s);
+  if (h == hipSuccess) h = hipEventRecord(e1, s);
+  if (h == hipSuccess) h = hipEventSynchronize(e1);
+  float ms = 0.0f;
+  if (h == hipSuccess) h = hipEventElapsedTime(&ms, e0, e1);
+  (void)hipEventDestroy(e0);
+  (void)hipEventDestroy(e1);
+  if (h != hipSuccess) return fail(TASP_ERR_HIP, "profile: %s", hipGetErrorString(h));
+  *ms_per_launch = ms / float(reps * n_plans);
+  return TASP_OK;
 }
 
 tasp_status tasp_copy_probe(void* dst, const void* src, size_t bytes, void* stream) {

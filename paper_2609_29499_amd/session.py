@@ -9,7 +9,7 @@ import ctypes as C
 import numpy as np
 import torch
 
-from . import binding as B
+from . import binding as B  # noqa: F401  (re-exported for callers)
 
 WEIGHT_NAMES = ("wq", "wk", "wv", "wo", "wg", "wu", "wd")
 

@@ -1,9 +1,9 @@
 """Pins for the oracle's mask closure, index lists and FLOP/byte ledgers.
 
-Closure (Sec. "Dependency-Closed Masks and Cache-Consistent Routing"): a KV head is active
-whenever any query head it serves is retained; query heads are never reassigned across groups;
-gate/up rows and down columns are retained together. The closure is checked exhaustively on a
-tiny layer against properties that any correct closure has, and on hand-derived cases.
+Closure (Sec. "Dependency-Closed Masks and Cache-Consistent Routing"): a KV group is needed
+exactly when one of its own query heads survives, heads keep their group, and a SwiGLU channel is
+one unit (gate row, up row, down column). The closure is checked exhaustively on a tiny layer
+against properties that any correct closure has, and on hand-derived cases.
 """
 import itertools
 import json
