@@ -178,6 +178,116 @@ def copy_probe_gbps(torch, B, nbytes=1 << 30, reps=10):
     return 2 * nbytes / (ms * 1e-3) / 1e9
 
 
+def device_layer(torch, sh, gen):
+    """One decoder layer of the INT8 store drawn on the GPU: N(0, 0.02) rows quantised to INT8 with
+    one float32 scale per row (max |w| / 127), BF16(1 + 0.1 N(0, 1)) gains. Used for stacks, whose
+    stores (5-70 GB) are too large to draw on the host."""
+    qd, kd, d, f = sh.n_q_heads * sh.head_dim, sh.n_kv_heads * sh.head_dim, sh.d_model, sh.d_ffn
+    out = {}
+    for name, (rows, cols) in (("wq", (qd, d)), ("wk", (kd, d)), ("wv", (kd, d)), ("wo", (d, qd)),
+                               ("wg", (f, d)), ("wu", (f, d)), ("wd", (d, f))):
+        w = torch.randn(rows, cols, generator=gen, device="cuda") * 0.02
+        s = (w.abs().amax(dim=1) / 127.0).clamp_min(1e-30)
+        q = torch.round(w / s[:, None]).clamp_(-127, 127).to(torch.int8)
+        out[name] = (q, s.float().contiguous())
+        del w
+    for name in ("attn_norm", "ffn_norm"):
+        g = (1.0 + 0.1 * torch.randn(d, generator=gen, device="cuda")).to(torch.bfloat16)
+        out[name] = g.view(torch.int16)
+    return out
+
+
+def bench_stack(args, wl):
+    """ms/token of a full decode step (all layers + final norm + BF16 LM head) for the dense plan and
+    every seeded mask, batch 1, cache at wl.pos prior positions."""
+    import torch
+    import synth
+    from paper_2609_29499_amd import binding as B
+    from paper_2609_29499_amd import session as S
+    from oracle import reference as ref
+    sh, pos = wl.shape, wl.pos
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(0)
+    t0 = time.time()
+    layers = [device_layer(torch, sh, gen) for _ in range(sh.n_layers)]
+    fnorm = (1.0 + 0.1 * torch.randn(sh.d_model, generator=gen, device="cuda")).to(torch.bfloat16).view(torch.int16)
+    lm = (0.02 * torch.randn(sh.vocab, sh.d_model, generator=gen, device="cuda")).to(torch.bfloat16).view(torch.int16)
+    store = S.DeviceStore(layers, fnorm, lm)
+    desc = S.desc_from_shape(sh, max_batch=1, max_seq=pos + 1)
+    torch.cuda.synchronize()
+    print(f"[bench] {wl.name}: store drawn in {time.time() - t0:.1f}s", file=sys.stderr, flush=True)
+    plans = [("dense", None)] + [(f"mask{sd}", synth.budget_mask(sh, sd)) for sd in wl.mask_seeds]
+    x = torch.randn(1, sh.d_model, generator=gen, device="cuda").to(torch.bfloat16).float()
+    out = torch.empty(1, sh.vocab, device="cuda")
+    rows = []
+    # one plan at a time: the store plus the largest plan (the dense copy) bound device memory
+    for name, m in plans:
+        plan = S.Plan(desc, store, m)
+        cache = S.KVCache(desc, 1, pos + 1)
+        for l in range(sh.n_layers):
+            cache.k[l, :, :, :pos].normal_(generator=gen)
+            cache.v[l, :, :, :pos].normal_(generator=gen)
+        plan.bind(cache)
+        for _ in range(3):
+            plan.decode(x, cache, pos, out)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        st = torch.cuda.Stream()
+        st.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(st):
+            plan.decode(x, cache, pos, out, stream=S.current_stream())
+        torch.cuda.current_stream().wait_stream(st)
+        torch.cuda.synchronize()
+        with torch.cuda.graph(g):
+            plan.decode(x, cache, pos, out, stream=S.current_stream())
+        for _ in range(args.warmup):
+            g.replay()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(args.steps):
+            g.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / args.steps
+        counts = [plan.counts(l) for l in range(sh.n_layers)]
+        cnt = [np.array([c[i] for c in counts]) for i in range(3)]
+        nb = ref.decode_bytes(sh, cnt, 1, pos, lm_head=True)
+        led = plan.ledger()
+        rows.append({"plan": name, "ms_per_token": round(ms, 5), "bytes": nb["total"],
+                     "GBps": round(nb["total"] / (ms * 1e-3) / 1e9, 1),
+                     "active_flop_ratio": round(led["active_flop_ratio"], 4)})
+        print(f"[bench] {name}: {ms:.4f} ms/token, {rows[-1]['GBps']} GB/s", file=sys.stderr, flush=True)
+        del cache, g, plan
+        torch.cuda.empty_cache()
+    dense = rows[0]
+    sparse = rows[1:]
+    mean_sparse = float(np.mean([r["ms_per_token"] for r in sparse]))
+    bts = np.array([r["bytes"] for r in rows], float)
+    tms = np.array([r["ms_per_token"] for r in rows], float)
+    slope, icpt = np.polyfit(bts, tms, 1)
+    pred = slope * bts + icpt
+    r2 = 1.0 - float(((tms - pred) ** 2).sum() / ((tms - tms.mean()) ** 2).sum())
+    line = {
+        "metric": METRIC, "value": round(mean_sparse, 5), "unit": "ms/token", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(mean_sparse, 5),
+        "higher_is_better": False, "scaling": "weak", "vs_baseline": None, "dtype": "int8w-f32",
+        "data": "synthetic",
+        "config": {"workload": wl.name, "d_model": sh.d_model, "layers": sh.n_layers,
+                   "vocab": sh.vocab, "batch": 1, "pos": pos, "masks": list(wl.mask_seeds)},
+        "dense_ms_per_token": dense["ms_per_token"],
+        "speedup_vs_dense": round(dense["ms_per_token"] / mean_sparse, 4),
+        "plans": rows,
+        "time_vs_bytes": {"slope_ms_per_GB": round(slope * 1e9, 4), "intercept_ms": round(icpt, 4),
+                          "r2": round(r2, 4)},
+        "achieved_GBps": round(float(np.mean([r["GBps"] for r in sparse])), 1),
+        "hbm_frac": round(float(np.mean([r["GBps"] for r in sparse])) / PEAK_GBPS, 4),
+        "paper_context": "45.2 -> 31.3 ms/token dense vs compiled sparse, Llama-3-70B, INT8/BF16, one A100 80GB",
+        "roofline": None, "cpu_baseline": None,
+    }
+    print(json.dumps(line), flush=True)
+
+
 def load_traffic(kernel_hash):
     """HBM traffic of the gate/up GEMV from the committed counter summary, if it was taken on the
     current kernel source."""
@@ -208,6 +318,9 @@ def main():
     B.load()
     wl = synth.WORKLOADS[args.workload]
     sh, pos = wl.shape, wl.pos
+    if sh.n_layers > 1 and wl.batch == 1 and wl.prefill_tokens == 0:
+        bench_stack(args, wl)
+        return
     if sh.n_layers != 1 or wl.batch != 1:
         print(json.dumps({"error": f"workload {args.workload} is not a single-layer batch-1 decode"}))
         sys.exit(2)

@@ -27,6 +27,7 @@ constexpr int kR = 4;             // rows per group
 constexpr int kC = 4;             // 1 KiB chunks per tile
 constexpr int kWgPerCu = 2;
 constexpr int kNumCu = 256;
+constexpr size_t kMaxGemvLds = 159 * 1024;     // gfx950: 160 KiB of LDS per workgroup, minus statics
 
 __device__ __forceinline__ void fma_bytes(float& acc, uint32_t word, const float4& x) {
   const uint32_t u = word ^ 0x80808080u;
@@ -260,26 +261,30 @@ int gemv_grid(int n_groups) {
   return grid < 1 ? 1 : grid;
 }
 
+template <int B, int MODE>
+hipError_t launch_mode(const GemvArgs& a, int grid, size_t lds, hipStream_t s) {
+  // dynamic LDS above 64 KiB must be allowed per kernel; done once per instantiation
+  static const hipError_t attr = hipFuncSetAttribute(
+      reinterpret_cast<const void*>(&gemv_kernel<B, MODE>),
+      hipFuncAttributeMaxDynamicSharedMemorySize, int(kMaxGemvLds));
+  if (attr != hipSuccess) return attr;
+  hipLaunchKernelGGL((gemv_kernel<B, MODE>), dim3(grid), dim3(kBlock), lds, s, a);
+  return hipGetLastError();
+}
+
 template <int B>
 hipError_t launch_gemv_b(GemvMode mode, const GemvArgs& a, hipStream_t s) {
   const int per_group = (mode == GEMV_GATEUP) ? 2 : kR;
   const int grid = gemv_grid((a.N + per_group - 1) / per_group);
   const size_t lds = gemv_lds_bytes(B, a.K);
+  if (lds > kMaxGemvLds) return hipErrorInvalidValue;
   switch (mode) {
-    case GEMV_QKV:
-      hipLaunchKernelGGL((gemv_kernel<B, GEMV_QKV>), dim3(grid), dim3(kBlock), lds, s, a);
-      break;
-    case GEMV_RESID:
-      hipLaunchKernelGGL((gemv_kernel<B, GEMV_RESID>), dim3(grid), dim3(kBlock), lds, s, a);
-      break;
-    case GEMV_GATEUP:
-      hipLaunchKernelGGL((gemv_kernel<B, GEMV_GATEUP>), dim3(grid), dim3(kBlock), lds, s, a);
-      break;
-    case GEMV_LMHEAD:
-      hipLaunchKernelGGL((gemv_kernel<B, GEMV_LMHEAD>), dim3(grid), dim3(kBlock), lds, s, a);
-      break;
+    case GEMV_QKV: return launch_mode<B, GEMV_QKV>(a, grid, lds, s);
+    case GEMV_RESID: return launch_mode<B, GEMV_RESID>(a, grid, lds, s);
+    case GEMV_GATEUP: return launch_mode<B, GEMV_GATEUP>(a, grid, lds, s);
+    case GEMV_LMHEAD: return launch_mode<B, GEMV_LMHEAD>(a, grid, lds, s);
   }
-  return hipGetLastError();
+  return hipErrorInvalidValue;
 }
 
 }  // namespace

@@ -38,7 +38,7 @@ tasp_status fail(tasp_status s, const char* fmt, ...) {
 
 constexpr size_t kAlign = 256;
 constexpr int kAttnTargetBlocks = 1024;
-constexpr size_t kLdsLimit = 160 * 1024 - 1024;
+constexpr size_t kLdsLimit = 159 * 1024;
 
 size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 int round_up16(int v) { return (v + 15) / 16 * 16; }

@@ -200,6 +200,44 @@ def test_llama3_8b_layer_full_size():
         torch.cuda.empty_cache()
 
 
+@pytest.mark.parametrize("batch,f", [(1, 24576), (2, 12288)])
+def test_wide_ffn_group_of_eight(batch, f):
+    """Eight query heads per KV group and a down-projection input wider than 64 KiB of LDS
+    (24576 channels at batch 1, 2 x 12288 at batch 2) on a narrow model."""
+    _flush(f"case wide ffn batch={batch} f={f}")
+    sh = synth.tiny_shape(d=256, hq=16, hkv=2, dh=128, f=f, theta=500000.0)
+    q, kv, ff = synth.all_kept_mask(sh)
+    q[0, 3] = 0
+    ff[0, ::7] = 0
+    case, got, want = _decode_case(sh, (q, kv, ff), batch, 70, max_seq=80)
+    assert_parity(got, want, what="wide ffn")
+    _check_cache_rows(case)
+
+
+@pytest.mark.timeout(600)
+def test_llama3_70b_layer_full_size():
+    """One Llama-3-70B-shaped layer (8192, 64/8 heads, 28672): 8 query heads per KV group and a
+    112 KiB down-projection input in LDS; seed-1 budget mask, 4096 prior positions."""
+    _flush("case 70b layer")
+    sh = synth.LLAMA3_70B.with_layers(1, vocab=0)
+    case, got, want = _decode_case(sh, synth.budget_mask(sh, 1), 1, 4096)
+    m, s = assert_parity(got, want, what="70b layer")
+    _flush(f"  max_rel={m:.2e} sum_rel={s:.2e}")
+    _check_cache_rows(case)
+
+
+def test_llama3_8b_two_layer_stack_with_lm_head():
+    """Full Llama-3-8B width: two layers under seed-2 budget masks, the dense BF16 LM head over
+    the 128256-token vocabulary, 512 prior positions, batch 2; logits and greedy tokens."""
+    _flush("case 8b 2-layer stack + lm head")
+    sh = synth.LLAMA3_8B.with_layers(2)
+    case, got, want = _decode_case(sh, synth.budget_mask(sh, 2), 2, 512)
+    m, s = assert_parity(got, want, what="8b stack logits")
+    _flush(f"  max_rel={m:.2e} sum_rel={s:.2e}")
+    assert (got.argmax(axis=1) == want.argmax(axis=1)).all()
+    assert np.abs(got - want).max() < 2e-3 * max(1.0, np.abs(want).max())
+
+
 def test_repeat_and_graph_replay_are_stable():
     """Repeated decode (self-resetting counters) and HIP-graph replays give the eager result."""
     _flush("case repeat + graph")
