@@ -20,7 +20,7 @@ STATUS = {0: "TASP_OK", -1: "TASP_ERR_INVALID_ARG", -2: "TASP_ERR_SHAPE", -3: "T
 IDX_Q, IDX_KV, IDX_QKVSLOT, IDX_FFN = 0, 1, 2, 3
 PANEL_QKV, PANEL_O, PANEL_GATE, PANEL_UP, PANEL_DOWN = 0, 1, 2, 3, 4
 KERNEL_KINDS = {0: "qkv_gemv", 1: "attention", 2: "o_gemv", 3: "gateup_gemv", 4: "down_gemv",
-                5: "lmhead_gemv"}
+                5: "lmhead_gemv", 6: "operand_prep"}
 
 EXPORTS = ["tasp_plan_workspace_bytes", "tasp_compile_plan", "tasp_plan_counts",
            "tasp_plan_indices", "tasp_plan_panel", "tasp_plan_ledger", "tasp_plan_destroy",

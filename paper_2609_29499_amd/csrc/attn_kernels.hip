@@ -59,6 +59,18 @@ __device__ __forceinline__ float row_group_sum(float v) {
   return LPR == 16 ? row16_sum(v) : row8_sum(v);
 }
 
+// One attention output element: float32 row b of o, or the hi/lo BF16 operand of the batched
+// projections (rows 2b and 2b + 1).
+__device__ __forceinline__ void store_o(const AttnArgs& a, int b, int col, float v) {
+  if (a.o_hl) {
+    const uint16_t hi = f32_to_bf16(v);
+    a.o_hl[size_t(2 * b) * a.ld_ohl + col] = hi;
+    a.o_hl[size_t(2 * b + 1) * a.ld_ohl + col] = f32_to_bf16(v - bf16_to_f32(hi));
+  } else {
+    a.o[size_t(b) * a.ld_o + col] = v;
+  }
+}
+
 template <int DH, int NH>
 __device__ __forceinline__ void attn_body(const AttnArgs& a, AttnSmem<DH>& sm, int s, int j,
                                           int b) {
@@ -256,12 +268,11 @@ __device__ __forceinline__ void attn_body(const AttnArgs& a, AttnSmem<DH>& sm, i
   }
   __syncthreads();
 
-  float* ob = a.o + size_t(b) * a.ld_o;
   if (a.n_split == 1) {
     for (int i = tid; i < NH * DH; i += kBlock) {
       const int h = i / DH, e = i % DH;
       const float v = sm.red[0][h][e] + sm.red[1][h][e] + sm.red[2][h][e] + sm.red[3][h][e];
-      ob[size_t(h0 + h) * DH + e] = v / sm.l_s[h];
+      store_o(a, b, (h0 + h) * DH + e, v / sm.l_s[h]);
     }
     return;
   }
@@ -337,6 +348,14 @@ __global__ __launch_bounds__(kBlock) void attn_merge_kernel(AttnArgs a) {
     M = bm;
   }
   const float inv = 1.0f / L;
+  if (a.o_hl) {
+    const int col = (h0 + h) * DH + 4 * e4;
+    store_o(a, b, col + 0, A.x * inv);
+    store_o(a, b, col + 1, A.y * inv);
+    store_o(a, b, col + 2, A.z * inv);
+    store_o(a, b, col + 3, A.w * inv);
+    return;
+  }
   float* ob = a.o + size_t(b) * a.ld_o;
   reinterpret_cast<float4*>(ob + size_t(h0 + h) * DH)[e4] =
       make_float4(A.x * inv, A.y * inv, A.z * inv, A.w * inv);

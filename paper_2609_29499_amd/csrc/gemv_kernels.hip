@@ -292,17 +292,9 @@ hipError_t launch_gemv_b(GemvMode mode, const GemvArgs& a, hipStream_t s) {
 size_t gemv_lds_bytes(int B, int K) { return size_t(B) * ((K + 1023) & ~1023) * sizeof(float); }
 
 hipError_t launch_gemv(GemvMode mode, const GemvArgs& a, hipStream_t s) {
-  switch (a.B) {
-    case 1: return launch_gemv_b<1>(mode, a, s);
-    case 2: return launch_gemv_b<2>(mode, a, s);
-    case 3: return launch_gemv_b<3>(mode, a, s);
-    case 4: return launch_gemv_b<4>(mode, a, s);
-    case 5: return launch_gemv_b<5>(mode, a, s);
-    case 6: return launch_gemv_b<6>(mode, a, s);
-    case 7: return launch_gemv_b<7>(mode, a, s);
-    case 8: return launch_gemv_b<8>(mode, a, s);
-  }
-  return hipErrorInvalidValue;
+  // one sequence; batches of 2..8 run on the matrix cores
+  if (a.B != 1) return hipErrorInvalidValue;
+  return launch_gemv_b<1>(mode, a, s);
 }
 
 }  // namespace tasp

@@ -53,10 +53,41 @@ struct GemvArgs {
   const float* resid;    // residual rows [B][ldy] (GEMV_RESID)
   float* y;              // output rows [B][ldy]
   int ldy;
-  int B;                 // batch rows (1..8)
+  int B;                 // batch rows (1; larger batches use the MFMA kernels)
 };
 hipError_t launch_gemv(GemvMode mode, const GemvArgs& a, hipStream_t s);
 size_t gemv_lds_bytes(int B, int K);
+
+// ----------------------------------------------------------------- batched decode on MFMA
+
+// Batch 2..8. Activations are a [16][ldx] BF16 operand: row 2b = bf16(v), row 2b+1 =
+// bf16(v - bf16(v)) for sequence b (rows >= 2B unused); ldx % 64 == 0, ldx >= K.
+// MM_QKV: plain store; MM_RESID: residual add, optionally writing the next operand (x * gamma_next)
+// and per-16-row sums of squares; MM_GATEUP: SwiGLU of paired gate / up rows into the next operand;
+// MM_LMHEAD: BF16 weights [N][ld], plain store. The inverse RMS of sequence b is
+// rsqrt(inv_d * sum(ssq[b][0..n_ssq)) + eps) when ssq is given, else 1.
+enum MfmaMode { MM_QKV = 0, MM_RESID = 1, MM_GATEUP = 2, MM_LMHEAD = 3 };
+
+struct MfmaArgs {
+  const void* w;              // panel rows [N][ld] (gate/up: gate rows)
+  uint32_t w2_off;            // gate/up: byte offset of the up rows from w
+  const float* scale;         // [N]
+  const float* scale2;        // gate/up: up scales
+  int N, K, ld;               // rows (gate/up: channels), valid columns, row stride (elements)
+  const uint16_t* x; int ldx; // activation operand
+  const float* ssq; int n_ssq; float inv_d, eps;
+  const float* resid;         // MM_RESID: [B][ldy]
+  float* y; int ldy;          // float32 output rows (not MM_GATEUP)
+  uint16_t* xo; int ldxo;     // next operand (MM_GATEUP; MM_RESID when gamma_next is set)
+  const uint16_t* gamma_next; // MM_RESID: gain of the next RMSNorm
+  float* ssq_out; int n_tiles_out;  // MM_RESID with gamma_next: [B][n_tiles_out], n_tiles_out = ceil(N/16)
+  int B;
+};
+hipError_t launch_mfma_gemv(MfmaMode mode, const MfmaArgs& a, hipStream_t s);
+// The first operand of a step from float32 input rows x [B][ldx]: x * gamma as hi/lo and the
+// sums of squares of x per 16 elements ([B][D/16]).
+hipError_t launch_mfma_prep(const float* x, int ldx, int D, const uint16_t* gamma, uint16_t* xo,
+                            int ldxo, float* ssq, int B, hipStream_t s);
 
 // ----------------------------------------------------------------- decode attention
 
@@ -71,6 +102,7 @@ struct AttnArgs {
   int pos, chunk, n_split;
   float* part;                     // [B][m_kv][n_split][8][dh + 4] when n_split > 1
   float* o; int ld_o;              // [B][ld_o] retained heads in ascending order
+  uint16_t* o_hl; int ld_ohl;      // when set: o as the hi/lo BF16 operand [16][ld_ohl] instead
   int B;
 };
 // Split-KV partial attention (writes o directly when n_split == 1), then, for n_split > 1, the

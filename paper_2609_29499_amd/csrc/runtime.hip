@@ -42,6 +42,7 @@ constexpr size_t kLdsLimit = 159 * 1024;
 
 size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 int round_up16(int v) { return (v + 15) / 16 * 16; }
+int round_up64(int v) { return (v + 63) / 64 * 64; }
 
 // ----------------------------------------------------------------------- closure on the host
 
@@ -56,6 +57,7 @@ tasp_status check_desc(const tasp_model_desc* d) {
       d->d_ffn < 1 || d->vocab < 0 || d->max_batch < 1 || d->max_seq < 1 || d->max_prefill < 0)
     return fail(TASP_ERR_SHAPE, "non-positive dimension in model desc");
   if (d->d_model % 16) return fail(TASP_ERR_SHAPE, "d_model %% 16 != 0 (%d)", d->d_model);
+  if (d->d_model > 16384) return fail(TASP_ERR_SHAPE, "d_model > 16384 (%d)", d->d_model);
   if (d->head_dim != 64 && d->head_dim != 128)
     return fail(TASP_ERR_SHAPE, "head_dim must be 64 or 128 (%d)", d->head_dim);
   if (d->n_q_heads % d->n_kv_heads)
@@ -74,10 +76,13 @@ tasp_status check_desc(const tasp_model_desc* d) {
   if (qkv_rows * D > big || double(d->d_ffn) * D > big || D * d->n_q_heads * d->head_dim > big ||
       double(d->vocab) * D * 2.0 > big)
     return fail(TASP_ERR_SHAPE, "a weight panel exceeds 2^31 bytes");
+  // the batched gate/up kernel addresses both panels from the gate panel with 32-bit offsets
+  if (2.0 * double(d->d_ffn) * D + 2.0 * kAlign > 4294967295.0)
+    return fail(TASP_ERR_SHAPE, "gate + up panels exceed 2^32 bytes");
+  // batch 1 stages every GEMV input vector in LDS (batches 2..8 run on the matrix cores)
   const int widest = std::max({d->d_model, d->n_q_heads * d->head_dim, d->d_ffn});
-  if (tasp::gemv_lds_bytes(d->max_batch, widest) > kLdsLimit)
-    return fail(TASP_ERR_UNSUPPORTED, "max_batch x widest GEMV input exceeds LDS (%d x %d)",
-                d->max_batch, widest);
+  if (tasp::gemv_lds_bytes(1, widest) > kLdsLimit)
+    return fail(TASP_ERR_UNSUPPORTED, "widest GEMV input exceeds LDS (%d)", widest);
   return TASP_OK;
 }
 
@@ -135,9 +140,10 @@ struct Layout {
   size_t idx_q, idx_kv, idx_slot, idx_slot_start, idx_ffn, counts;
   size_t final_norm, lm_head, rope_cos, rope_sin;
   size_t r_mid, r_io0, r_io1, qkv_buf, o_buf, h_buf, part;
+  size_t xd, xo, xh, ssq;            // batched path: hi/lo operands and sums of squares
   size_t zero_begin, zero_end;       // scratch cleared at compile
   size_t total;
-  int n_split_max, ld_qkv, ld_obuf, ld_h;
+  int n_split_max, ld_qkv, ld_obuf, ld_h, ld_xd, ld_xo, ld_xh;
 };
 
 Layout make_layout(const tasp_model_desc* d, const Closed& c) {
@@ -195,6 +201,14 @@ Layout make_layout(const tasp_model_desc* d, const Closed& c) {
   Y.o_buf = take(size_t(B) * Y.ld_obuf * 4);
   Y.h_buf = take(size_t(B) * Y.ld_h * 4);
   Y.part = take(size_t(B) * Hkv * Y.n_split_max * 8 * (dh + 4) * 4);
+  Y.ld_xd = round_up64(D);
+  Y.ld_xo = round_up64(Hq * dh);
+  Y.ld_xh = round_up64(F);
+  const bool batched = B > 1;
+  Y.xd = take(batched ? size_t(16) * Y.ld_xd * 2 : 0);
+  Y.xo = take(batched ? size_t(16) * Y.ld_xo * 2 : 0);
+  Y.xh = take(batched ? size_t(16) * Y.ld_xh * 2 : 0);
+  Y.ssq = take(batched ? size_t(B) * (D / 16) * 4 : 0);
   Y.zero_end = off;
   Y.total = off;
   return Y;
@@ -237,6 +251,9 @@ struct tasp_plan_s {
   float *rope_cos, *rope_sin;
   float *r_mid, *r_io[2], *qkv_buf, *o_buf, *h_buf, *part;
   int n_split_max, ld_qkv, ld_obuf, ld_h;
+  uint16_t *xd, *xo, *xh;            // batched path operands [16][ld_x*]
+  float* ssq;                        // [max_batch][d_model / 16]
+  int ld_xd, ld_xo, ld_xh;
 };
 
 namespace {
@@ -294,6 +311,121 @@ tasp::GemvArgs down_args(const tasp_plan_s* p, int l, int B, float* y) {
   return a;
 }
 
+// decode attention of layer l over the retained groups; hl: write o as the batched operand
+tasp::AttnArgs attn_args(const tasp_plan_s* p, int l, const tasp_kv_cache* cache, int pos, int B,
+                         bool hl) {
+  const LayerPlan& P = p->layers[l];
+  const tasp_model_desc& d = p->desc;
+  const size_t layer_cache = size_t(B) * d.n_kv_heads * cache->max_seq * d.head_dim;
+  const int total = pos + 1;
+  tasp::AttnArgs a{};
+  // rows per split: a multiple of the kernel's sub-block, large enough that about
+  // kAttnTargetBlocks workgroups run and that the split count stays within the merge's limit
+  const long sub = tasp::attn_min_chunk();
+  const long want = (long(total) * P.m_kv * B + kAttnTargetBlocks - 1) / kAttnTargetBlocks;
+  const long need = (long(total) + tasp::attn_max_split() - 1) / tasp::attn_max_split();
+  long chunk = std::max<long>(std::max(want, need), sub);
+  chunk = (chunk + sub - 1) / sub * sub;
+  a.qkv = p->qkv_buf; a.ld_qkv = p->ld_qkv; a.m_q = P.m_q; a.m_kv = P.m_kv; a.dh = d.head_dim;
+  for (int q = 0; q < P.m_kv; ++q) a.kv_idx[q] = P.kv_idx[q];
+  for (int q = 0; q <= P.m_kv; ++q) a.slot_start[q] = P.slot_start[q];
+  a.kc = static_cast<uint16_t*>(cache->k) + l * layer_cache;
+  a.vc = static_cast<uint16_t*>(cache->v) + l * layer_cache;
+  a.Hkv = d.n_kv_heads; a.S = cache->max_seq; a.rope_cos = p->rope_cos;
+  a.rope_sin = p->rope_sin; a.pos = pos; a.chunk = int(chunk);
+  a.n_split = int((total + chunk - 1) / chunk); a.part = p->part;
+  a.o = p->o_buf; a.ld_o = p->ld_obuf; a.B = B;
+  if (hl) { a.o_hl = p->xo; a.ld_ohl = p->ld_xo; }
+  return a;
+}
+
+// ---- batched path (2..8 sequences): projections on the matrix cores over hi/lo operands
+
+tasp::MfmaArgs mm_base(const tasp_plan_s* p, int B) {
+  tasp::MfmaArgs a{};
+  a.B = B;
+  a.inv_d = 1.0f / float(p->desc.d_model);
+  a.eps = p->desc.rms_eps;
+  a.n_ssq = p->desc.d_model / 16;
+  a.n_tiles_out = p->desc.d_model / 16;
+  return a;
+}
+
+// gate/up of layer l: operand xd (x_mid * gamma_ffn, inverse RMS from ssq) -> SwiGLU into xh
+tasp::MfmaArgs gateup_mm_args(const tasp_plan_s* p, int l, int B) {
+  const LayerPlan& P = p->layers[l];
+  tasp::MfmaArgs a = mm_base(p, B);
+  a.w = P.g; a.w2_off = uint32_t(reinterpret_cast<const char*>(P.u) - reinterpret_cast<const char*>(P.g));
+  a.scale = P.s_g; a.scale2 = P.s_u; a.N = P.c; a.K = p->desc.d_model; a.ld = p->desc.d_model;
+  a.x = p->xd; a.ldx = p->ld_xd; a.ssq = p->ssq; a.xo = p->xh; a.ldxo = p->ld_xh;
+  return a;
+}
+
+// down of layer l: y = x_mid + Wd h, and the next operand (gain of the next RMSNorm, if any)
+tasp::MfmaArgs down_mm_args(const tasp_plan_s* p, int l, int B, float* y) {
+  const LayerPlan& P = p->layers[l];
+  const tasp_model_desc& d = p->desc;
+  tasp::MfmaArgs a = mm_base(p, B);
+  a.w = P.dn; a.scale = P.s_d; a.N = d.d_model; a.K = P.c; a.ld = P.ld_d;
+  a.x = p->xh; a.ldx = p->ld_xh; a.resid = p->r_mid; a.y = y; a.ldy = d.d_model;
+  a.gamma_next = (l + 1 < d.n_layers) ? p->layers[l + 1].an : (d.vocab ? p->final_norm : nullptr);
+  a.xo = p->xd; a.ldxo = p->ld_xd; a.ssq_out = p->ssq;
+  return a;
+}
+
+tasp_status decode_batched(tasp_plan p, const float* x, tasp_kv_cache* cache, int pos, float* out,
+                           hipStream_t s, Timer* tm, int B) {
+  const tasp_model_desc& d = p->desc;
+  const int D = d.d_model, dh = d.head_dim, L = d.n_layers;
+  tasp_status st;
+  if ((st = run_kernel(tm, 6, s, [&] {
+         return tasp::launch_mfma_prep(x, D, D, p->layers[0].an, p->xd, p->ld_xd, p->ssq, B, s);
+       })))
+    return st;
+  for (int l = 0; l < L; ++l) {
+    const LayerPlan& P = p->layers[l];
+    const float* in = (l == 0) ? x : p->r_io[(l - 1) & 1];
+    float* lo = (l == L - 1 && d.vocab == 0) ? out : p->r_io[l & 1];
+    if (P.n_qkv > 0) {
+      tasp::MfmaArgs a = mm_base(p, B);
+      a.w = P.qkv; a.scale = P.s_qkv; a.N = P.n_qkv; a.K = D; a.ld = D;
+      a.x = p->xd; a.ldx = p->ld_xd; a.ssq = p->ssq; a.y = p->qkv_buf; a.ldy = p->ld_qkv;
+      if ((st = run_kernel(tm, 0, s, [&] { return tasp::launch_mfma_gemv(tasp::MM_QKV, a, s); })))
+        return st;
+    }
+    if (P.m_kv > 0) {
+      const tasp::AttnArgs a = attn_args(p, l, cache, pos, B, true);
+      if ((st = run_kernel(tm, 1, s, [&] { return tasp::launch_attn_decode(a, s); }))) return st;
+    }
+    {
+      tasp::MfmaArgs a = mm_base(p, B);
+      a.w = P.o; a.scale = P.s_o; a.N = D; a.K = P.m_q * dh; a.ld = P.ld_o;
+      a.x = p->xo; a.ldx = p->ld_xo; a.resid = in; a.y = p->r_mid; a.ldy = D;
+      a.gamma_next = P.fn; a.xo = p->xd; a.ldxo = p->ld_xd; a.ssq_out = p->ssq;
+      if ((st = run_kernel(tm, 2, s, [&] { return tasp::launch_mfma_gemv(tasp::MM_RESID, a, s); })))
+        return st;
+    }
+    if (P.c > 0) {
+      const tasp::MfmaArgs a = gateup_mm_args(p, l, B);
+      if ((st = run_kernel(tm, 3, s, [&] { return tasp::launch_mfma_gemv(tasp::MM_GATEUP, a, s); })))
+        return st;
+    }
+    {
+      const tasp::MfmaArgs a = down_mm_args(p, l, B, lo);
+      if ((st = run_kernel(tm, 4, s, [&] { return tasp::launch_mfma_gemv(tasp::MM_RESID, a, s); })))
+        return st;
+    }
+  }
+  if (d.vocab) {
+    tasp::MfmaArgs a = mm_base(p, B);
+    a.w = p->lm_head; a.N = d.vocab; a.K = D; a.ld = D; a.x = p->xd; a.ldx = p->ld_xd;
+    a.ssq = p->ssq; a.y = out; a.ldy = d.vocab;
+    if ((st = run_kernel(tm, 5, s, [&] { return tasp::launch_mfma_gemv(tasp::MM_LMHEAD, a, s); })))
+      return st;
+  }
+  return TASP_OK;
+}
+
 tasp_status decode_impl(tasp_plan p, const float* x, tasp_kv_cache* cache, int32_t pos,
                         float* out, void* stream, Timer* tm) {
   if (!p) return fail(TASP_ERR_INVALID_ARG, "plan is NULL");
@@ -313,8 +445,7 @@ tasp_status decode_impl(tasp_plan p, const float* x, tasp_kv_cache* cache, int32
   if (ob < xb + size_t(B) * D * 4 && xb < ob + out_elems * 4)
     return fail(TASP_ERR_INVALID_ARG, "x and out overlap");
   hipStream_t s = static_cast<hipStream_t>(stream);
-  const size_t layer_cache = size_t(B) * d.n_kv_heads * cache->max_seq * dh;
-  const int total = pos + 1;
+  if (B > 1) return decode_batched(p, x, cache, pos, out, s, tm, B);
 
   for (int l = 0; l < L; ++l) {
     const LayerPlan& P = p->layers[l];
@@ -329,23 +460,7 @@ tasp_status decode_impl(tasp_plan p, const float* x, tasp_kv_cache* cache, int32
         return st;
     }
     if (P.m_kv > 0) {
-      tasp::AttnArgs a{};
-      // rows per split: a multiple of the kernel's sub-block, large enough that about
-      // kAttnTargetBlocks workgroups run and that the split count stays within the merge's limit
-      const long sub = tasp::attn_min_chunk();
-      const long want = (long(total) * P.m_kv * B + kAttnTargetBlocks - 1) / kAttnTargetBlocks;
-      const long need = (long(total) + tasp::attn_max_split() - 1) / tasp::attn_max_split();
-      long chunk = std::max<long>(std::max(want, need), sub);
-      chunk = (chunk + sub - 1) / sub * sub;
-      a.qkv = p->qkv_buf; a.ld_qkv = p->ld_qkv; a.m_q = P.m_q; a.m_kv = P.m_kv; a.dh = dh;
-      for (int q = 0; q < P.m_kv; ++q) a.kv_idx[q] = P.kv_idx[q];
-      for (int q = 0; q <= P.m_kv; ++q) a.slot_start[q] = P.slot_start[q];
-      a.kc = static_cast<uint16_t*>(cache->k) + l * layer_cache;
-      a.vc = static_cast<uint16_t*>(cache->v) + l * layer_cache;
-      a.Hkv = d.n_kv_heads; a.S = cache->max_seq; a.rope_cos = p->rope_cos;
-      a.rope_sin = p->rope_sin; a.pos = pos; a.chunk = int(chunk);
-      a.n_split = int((total + chunk - 1) / chunk); a.part = p->part;
-      a.o = p->o_buf; a.ld_o = p->ld_obuf; a.B = B;
+      const tasp::AttnArgs a = attn_args(p, l, cache, pos, B, false);
       if ((st = run_kernel(tm, 1, s, [&] { return tasp::launch_attn_decode(a, s); }))) return st;
     }
     {
@@ -541,6 +656,11 @@ tasp_status tasp_compile_plan(const tasp_model_desc* desc, const tasp_store* sto
   p->h_buf = reinterpret_cast<float*>(at(Y.h_buf));
   p->part = reinterpret_cast<float*>(at(Y.part));
   p->n_split_max = Y.n_split_max; p->ld_qkv = Y.ld_qkv; p->ld_obuf = Y.ld_obuf; p->ld_h = Y.ld_h;
+  p->xd = reinterpret_cast<uint16_t*>(at(Y.xd));
+  p->xo = reinterpret_cast<uint16_t*>(at(Y.xo));
+  p->xh = reinterpret_cast<uint16_t*>(at(Y.xh));
+  p->ssq = reinterpret_cast<float*>(at(Y.ssq));
+  p->ld_xd = Y.ld_xd; p->ld_xo = Y.ld_xo; p->ld_xh = Y.ld_xh;
 
   // read the device index lists back (the one synchronisation) and check them
   std::vector<int> hq_idx(size_t(L) * Hq), hkv_idx(size_t(L) * Hkv), hslot(size_t(L) * Hq),
@@ -747,23 +867,30 @@ tasp_status tasp_profile_stage(const tasp_plan* plans, int32_t n_plans, int32_t 
     return fail(TASP_ERR_INVALID_ARG, "plans / n_plans / reps / ms_per_launch");
   if (kind != 3 && kind != 4) return fail(TASP_ERR_UNSUPPORTED, "stage kind %d is not profiled", kind);
   std::vector<tasp::GemvArgs> args(n_plans);
+  std::vector<tasp::MfmaArgs> margs(n_plans);
   for (int i = 0; i < n_plans; ++i) {
     const tasp_plan_s* p = plans[i];
     if (!p) return fail(TASP_ERR_INVALID_ARG, "plans[%d] is NULL", i);
     if (layer < 0 || layer >= p->desc.n_layers) return fail(TASP_ERR_INVALID_ARG, "bad layer %d", layer);
     if (batch < 1 || batch > p->desc.max_batch) return fail(TASP_ERR_SHAPE, "bad batch %d", batch);
     if (kind == 3 && p->layers[layer].c == 0) return fail(TASP_ERR_SHAPE, "layer has no FFN channels");
-    args[i] = (kind == 3) ? gateup_args(p, layer, batch)
-                          : down_args(p, layer, batch, p->r_io[layer & 1]);
+    if (batch == 1)
+      args[i] = (kind == 3) ? gateup_args(p, layer, batch)
+                            : down_args(p, layer, batch, p->r_io[layer & 1]);
+    else
+      margs[i] = (kind == 3) ? gateup_mm_args(p, layer, batch)
+                             : down_mm_args(p, layer, batch, p->r_io[layer & 1]);
   }
   const tasp::GemvMode mode = (kind == 3) ? tasp::GEMV_GATEUP : tasp::GEMV_RESID;
+  const tasp::MfmaMode mmode = (kind == 3) ? tasp::MM_GATEUP : tasp::MM_RESID;
   hipStream_t s = static_cast<hipStream_t>(stream);
   hipEvent_t e0, e1;
   HIP_TRY(hipEventCreate(&e0));
   HIP_TRY(hipEventCreate(&e1));
   hipError_t h = hipEventRecord(e0, s);
   for (int r = 0; r < reps && h == hipSuccess; ++r)
-    for (int i = 0; i < n_plans && h == hipSuccess; ++i) h = tasp::launch_gemv(mode, args[i], s);
+    for (int i = 0; i < n_plans && h == hipSuccess; ++i)
+      h = (batch == 1) ? tasp::launch_gemv(mode, args[i], s) : tasp::launch_mfma_gemv(mmode, margs[i], s);
   if (h == hipSuccess) h = hipEventRecord(e1, s);
   if (h == hipSuccess) h = hipEventSynchronize(e1);
   float ms = 0.0f;

@@ -58,13 +58,23 @@ def test_workspace_bytes_scales_with_mask():
     (dict(d_model=520), "TASP_ERR_SHAPE"),
     (dict(max_batch=9), "TASP_ERR_SHAPE"),
     (dict(n_layers=0), "TASP_ERR_SHAPE"),
-    (dict(d_ffn=8192, max_batch=8), "TASP_ERR_UNSUPPORTED"),
+    (dict(d_model=16400, n_q_heads=8, n_kv_heads=2), "TASP_ERR_SHAPE"),
+    (dict(d_ffn=49152), "TASP_ERR_UNSUPPORTED"),             # batch-1 input beyond LDS
 ])
 def test_bad_desc_rejected(kw, status):
     _lib()
     with pytest.raises(B.TaspError) as e:
         B.tasp_plan_workspace_bytes(_desc(**kw), None)
     assert B.STATUS[e.value.status] == status
+
+
+def test_batched_desc_accepted():
+    """Batches of 2..8 do not stage inputs in LDS: a wide FFN at batch 8 is a valid desc, and the
+    batched operands add workspace."""
+    _lib()
+    one = B.tasp_plan_workspace_bytes(_desc(d_ffn=14336), None)
+    eight = B.tasp_plan_workspace_bytes(_desc(d_ffn=14336, max_batch=8), None)
+    assert eight > one
 
 
 def test_bad_mask_byte_rejected():

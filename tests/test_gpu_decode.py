@@ -155,16 +155,17 @@ def test_head_dim_128_ragged_groups():
     _check_cache_rows(case)
 
 
+@pytest.mark.parametrize("batch", [1, 3])
 @pytest.mark.parametrize("what", ["no_heads", "no_ffn", "nothing"])
-def test_empty_modules(what):
-    _flush(f"case empty {what}")
+def test_empty_modules(what, batch):
+    _flush(f"case empty {what} batch={batch}")
     sh = SMALL.with_layers(2)
     q, kv, f = synth.all_kept_mask(sh)
     if what in ("no_heads", "nothing"):
         q[0] = 0
     if what in ("no_ffn", "nothing"):
         f[1] = 0
-    case, got, want = _decode_case(sh, (q, kv, f), 1, 9, max_seq=16)
+    case, got, want = _decode_case(sh, (q, kv, f), batch, 9, max_seq=16)
     assert_parity(got, want, what=what)
 
 
@@ -177,13 +178,47 @@ def test_positions_and_split_boundaries(pos):
     _check_cache_rows(case)
 
 
-def test_stack_with_lm_head_logits():
-    _flush("case stack + lm head")
+@pytest.mark.parametrize("batch", [1, 2, 7])
+def test_stack_with_lm_head_logits(batch):
+    _flush(f"case stack + lm head batch={batch}")
     sh = synth.tiny_shape(d=256, hq=8, hkv=2, dh=64, f=512, layers=3, vocab=3000)
-    case, got, want = _decode_case(sh, synth.raw_mask(sh, 6), 2, 40, max_seq=48)
+    case, got, want = _decode_case(sh, synth.raw_mask(sh, 6), batch, 40, max_seq=48)
     m, s = assert_parity(got, want, what="logits")
     assert (got.argmax(axis=1) == want.argmax(axis=1)).all()
     assert np.abs(got - want).max() < 2e-3 * max(1.0, np.abs(want).max())
+
+
+@pytest.mark.parametrize("batch", [2, 5, 8])
+def test_batched_tiny_layer(batch):
+    """Batches of 2..8 run every projection on the matrix cores over hi/lo BF16 operands."""
+    _flush(f"case batched tiny batch={batch}")
+    sh = synth.TINY
+    case, got, want = _decode_case(sh, synth.tiny_mask(sh), batch, 128)
+    m, s = assert_parity(got, want, what="batched tiny")
+    _flush(f"  max_rel={m:.2e} sum_rel={s:.2e}")
+    _check_cache_rows(case)
+
+
+@pytest.mark.parametrize("pos", [0, 1, 129, 511])
+def test_batched_positions(pos):
+    _flush(f"case batched pos={pos}")
+    sh = SMALL.with_layers(2)
+    case, got, want = _decode_case(sh, synth.raw_mask(sh, 9, p_q=0.6, p_kv=0.8), 8, pos,
+                                   max_seq=512)
+    assert_parity(got, want, what=f"batched pos {pos}")
+    _check_cache_rows(case)
+
+
+@pytest.mark.timeout(600)
+def test_llama3_8b_batch8_full_size():
+    """One Llama-3-8B-shaped layer under the seed-1 budget mask, 8 sequences at 8192 prior
+    positions each (batched decode)."""
+    _flush("case 8b layer batch 8 pos 8192")
+    sh = synth.LLAMA3_8B.with_layers(1, vocab=0)
+    case, got, want = _decode_case(sh, synth.budget_mask(sh, 1), 8, 8192)
+    m, s = assert_parity(got, want, what="8b batch 8")
+    _flush(f"  max_rel={m:.2e} sum_rel={s:.2e}")
+    _check_cache_rows(case)
 
 
 def test_llama3_8b_layer_full_size():
@@ -238,11 +273,12 @@ def test_llama3_8b_two_layer_stack_with_lm_head():
     assert np.abs(got - want).max() < 2e-3 * max(1.0, np.abs(want).max())
 
 
-def test_repeat_and_graph_replay_are_stable():
-    """Repeated decode (self-resetting counters) and HIP-graph replays give the eager result."""
-    _flush("case repeat + graph")
+@pytest.mark.parametrize("batch", [1, 4])
+def test_repeat_and_graph_replay_are_stable(batch):
+    """Repeated decode and HIP-graph replays give the eager result bit for bit."""
+    _flush(f"case repeat + graph batch={batch}")
     sh = SMALL
-    case = Case(sh, synth.raw_mask(sh, 7), 1, 200, max_seq=256)
+    case = Case(sh, synth.raw_mask(sh, 7), batch, 200, max_seq=256)
     first = case.run()
     for _ in range(3):
         assert np.array_equal(case.run(), first)
