@@ -29,6 +29,7 @@ sys.path.insert(0, ROOT)
 
 METRIC = "ms/token decode at batch 1 (sparse vs dense) + achieved HBM GB/s % of peak"
 PEAK_GBPS = 8000.0
+STAGE_KIND = {"attention": 1, "gateup_gemv": 3}
 ROTATE_BYTES = 2.5e9
 
 
@@ -63,7 +64,10 @@ def layer_bytes(sh, m_q, m_kv, c, pos, batch=1):
     s = 4 * ((m_q + 2 * m_kv) * dh + d + 2 * c + d)
     kv = batch * m_kv * (pos + 1) * dh * 2 * 2
     gateup = 2 * c * d + 2 * c * 4 + batch * (d * 4 + c * 4)
-    return {"weights": w, "scales": s, "kv": kv, "total": w + s + kv, "gateup": gateup}
+    # split-KV attention + merge: cache rows, q/k/v in, new k/v rows written, o out
+    attention = kv + batch * ((m_q + 2 * m_kv) * dh * 4 + 2 * m_kv * dh * 2 + m_q * dh * 4)
+    return {"weights": w, "scales": s, "kv": kv, "total": w + s + kv, "gateup": gateup,
+            "attention": attention}
 
 
 class Rotation:
@@ -71,9 +75,11 @@ class Rotation:
 
     def __init__(self, S, torch, sh, desc, dstore, mask, prior, x, pos, copies):
         self.plans, self.caches = [], []
+        batch = x.shape[0]
+        self.batch = batch
         for _ in range(copies):
             plan = S.Plan(desc, dstore, mask)
-            cache = S.KVCache(desc, 1, pos + 1)
+            cache = S.KVCache(desc, batch, pos + 1)
             cache.load_layer(0, *prior)
             plan.bind(cache)
             self.plans.append(plan)
@@ -118,8 +124,9 @@ class Rotation:
 
     def stage_ms(self, kind, reps=20):
         """Mean duration (ms) of one stage kernel over back-to-back launches across the copies."""
-        return self.S.B.tasp_profile_stage([p.handle for p in self.plans], 0, kind, 1, reps,
-                                           self.S.current_stream())
+        return self.S.B.tasp_profile_stage([p.handle for p in self.plans],
+                                           [c.struct for c in self.caches], 0, kind, self.pos,
+                                           reps, self.S.current_stream())
 
     def kernel_times(self, launches):
         """Per-kernel durations (ms) from HIP events around each launch, over the copies."""
@@ -288,15 +295,25 @@ def bench_stack(args, wl):
     print(json.dumps(line), flush=True)
 
 
-def load_traffic(kernel_hash):
-    """HBM traffic of the gate/up GEMV from the committed counter summary, if it was taken on the
-    current kernel source."""
-    p = os.path.join(ROOT, "profiles", "gateup_gemv_llama3_8b_layer_traffic.json")
-    if not os.path.exists(p):
+KERNEL_SOURCES = {
+    "gateup_gemv": ["paper_2609_29499_amd/csrc/gemv_kernels.hip",
+                    "paper_2609_29499_amd/csrc/device_common.hpp"],
+    "gateup_mfma": ["paper_2609_29499_amd/csrc/mfma_kernels.hip",
+                    "paper_2609_29499_amd/csrc/device_common.hpp"],
+    "attention": ["paper_2609_29499_amd/csrc/attn_kernels.hip",
+                  "paper_2609_29499_amd/csrc/device_common.hpp"],
+}
+
+
+def load_traffic(kernel, workload):
+    """HBM bytes per launch of a kernel from the committed counter summary of this workload, if
+    the counters were taken on the current kernel source; else None."""
+    p = os.path.join(ROOT, "profiles", f"{kernel}_{workload}_traffic.json")
+    if not os.path.exists(p) or kernel not in KERNEL_SOURCES:
         return None
     with open(p) as f:
         t = json.load(f)
-    if t.get("kernel_source_hash") != kernel_hash:
+    if t.get("kernel_source_hash") != source_hash(KERNEL_SOURCES[kernel]):
         return None
     return t.get("bytes_per_launch")
 
@@ -321,25 +338,30 @@ def main():
     if sh.n_layers > 1 and wl.batch == 1 and wl.prefill_tokens == 0:
         bench_stack(args, wl)
         return
-    if sh.n_layers != 1 or wl.batch != 1:
-        print(json.dumps({"error": f"workload {args.workload} is not a single-layer batch-1 decode"}))
+    if sh.n_layers != 1 or wl.prefill_tokens:
+        print(json.dumps({"error": f"workload {args.workload} is not a single-layer decode"}))
         sys.exit(2)
+    batch = wl.batch
     t_setup = time.time()
     print(f"[bench] generating {args.workload}", file=sys.stderr, flush=True)
     layer = synth.layer_weights(sh, 0)
     mask = synth.budget_mask(sh, args.mask_seed)
-    prior = synth.kv_prior(sh, 0, 1, pos, pos + 1)
-    x = synth.activations(1, sh.d_model)
-    desc = S.desc_from_shape(sh, max_batch=1, max_seq=pos + 1)
+    prior = synth.kv_prior(sh, 0, batch, pos, pos + 1)
+    x = synth.activations(batch, sh.d_model)
+    desc = S.desc_from_shape(sh, max_batch=batch, max_seq=pos + 1)
     dstore = S.DeviceStore([layer])
     results = {}
     plans = (("sparse", mask),) if args.sparse_only else (("sparse", mask), ("dense", None))
+    # the kernel that moves the most bytes: the gate/up panels at batch 1, the KV cache at batch 8
+    probe_counts = S.Plan(desc, dstore, mask).counts(0)
+    nb0 = layer_bytes(sh, *probe_counts, pos, batch)
+    dominant = "attention" if nb0["attention"] > nb0["gateup"] else "gateup_gemv"
     for name, m in plans:
         probe = S.Plan(desc, dstore, m)
         counts = probe.counts(0)
         ledger = probe.ledger()
         del probe
-        nb = layer_bytes(sh, *counts, pos)
+        nb = layer_bytes(sh, *counts, pos, batch)
         copies = max(2, math.ceil(ROTATE_BYTES / nb["total"]))
         print(f"[bench] {name}: counts={counts} bytes={nb['total']/1e6:.1f} MB copies={copies}",
               file=sys.stderr, flush=True)
@@ -349,10 +371,10 @@ def main():
         ms = rot.time_steps(args.steps)
         blocks = [rot.time_steps(200) for _ in range(args.blocks)]
         ktimes = rot.kernel_times(args.timed_launches)
-        gateup_ms = rot.stage_ms(3)
+        stage_ms = rot.stage_ms(STAGE_KIND[dominant])
         results[name] = {"counts": counts, "ledger": ledger, "bytes": nb, "ms": ms,
                          "blocks": blocks, "kernels": ktimes, "copies": copies,
-                         "gateup_ms": gateup_ms}
+                         "stage_ms": stage_ms}
         print(f"[bench] {name}: {ms*1e3:.2f} us/step  kernels(us)=" +
               " ".join(f"{k}={v*1e3:.2f}" for k, v in ktimes.items()), file=sys.stderr, flush=True)
         del rot
@@ -365,11 +387,11 @@ def main():
         return
     sp, dn = results["sparse"], results["dense"]
     gbps = sp["bytes"]["total"] / (sp["ms"] * 1e-3) / 1e9
-    gu_ms = sp["gateup_ms"]
-    gu_gbps = sp["bytes"]["gateup"] / (gu_ms * 1e-3) / 1e9
-    khash = source_hash(["paper_2609_29499_amd/csrc/gemv_kernels.hip",
-                         "paper_2609_29499_amd/csrc/device_common.hpp"])
-    traffic = load_traffic(khash)
+    st_ms = sp["stage_ms"]
+    st_bytes = sp["bytes"]["attention" if dominant == "attention" else "gateup"]
+    st_gbps = st_bytes / (st_ms * 1e-3) / 1e9
+    traffic = load_traffic("gateup_mfma" if dominant == "gateup_gemv" and batch > 1 else dominant,
+                           args.workload)
     line = {
         "metric": METRIC, "value": round(sp["ms"], 6), "unit": "ms/token", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(sp["ms"], 6),
@@ -377,7 +399,7 @@ def main():
         "data": "synthetic",
         "config": {"workload": args.workload, "d_model": sh.d_model, "n_q_heads": sh.n_q_heads,
                    "n_kv_heads": sh.n_kv_heads, "head_dim": sh.head_dim, "d_ffn": sh.d_ffn,
-                   "layers": 1, "batch": 1, "pos": pos, "mask_seed": args.mask_seed,
+                   "layers": 1, "batch": batch, "pos": pos, "mask_seed": args.mask_seed,
                    "active_flop_ratio": round(sp["ledger"]["active_flop_ratio"], 4),
                    "retained": {"q_heads": sp["counts"][0], "kv_groups": sp["counts"][1],
                                 "ffn_channels": sp["counts"][2]}},
@@ -394,10 +416,10 @@ def main():
                       "dense": [round(b, 6) for b in dn["blocks"]]},
         "kernels_us": {k: {n: round(v * 1e3, 3) for n, v in r["kernels"].items()}
                        for k, r in results.items()},
-        "roofline": {"bound": "hbm", "kernel": "gateup_gemv", "achieved": round(gu_gbps, 1),
-                     "peak": PEAK_GBPS, "unit": "GB/s", "frac": round(gu_gbps / PEAK_GBPS, 4),
-                     "traffic": traffic, "algorithmic_bytes": sp["bytes"]["gateup"],
-                     "avg_launch_us": round(gu_ms * 1e3, 3)},
+        "roofline": {"bound": "hbm", "kernel": dominant, "achieved": round(st_gbps, 1),
+                     "peak": PEAK_GBPS, "unit": "GB/s", "frac": round(st_gbps / PEAK_GBPS, 4),
+                     "traffic": traffic, "algorithmic_bytes": st_bytes,
+                     "avg_launch_us": round(st_ms * 1e3, 3)},
         "paper_context": "45.2 -> 31.3 ms/token dense vs compiled sparse, Llama-3-70B, INT8/BF16, one A100 80GB",
         "rotation_copies": {"sparse": sp["copies"], "dense": dn["copies"]},
     }

@@ -179,22 +179,25 @@ tasp_status tasp_prefill(tasp_plan plan, const float* x, int32_t T, tasp_kv_cach
 
 /* Profiling variant of tasp_decode_step: records a HIP event pair around every kernel it launches,
  * synchronises `stream`, and writes each kernel's duration in milliseconds to kernel_ms[i] and a
- * kernel-kind code to kinds[i] (0 QKV, 1 attention, 2 O, 3 gate/up, 4 down, 5 LM head) for up to
+ * kernel-kind code to kinds[i] (0 QKV, 1 attention, 2 O, 3 gate/up, 4 down, 5 LM head, 6 batched
+ * operand preparation) for up to
  * cap kernels; *n receives the number launched. Not capturable (it synchronises). */
 tasp_status tasp_decode_step_timed(tasp_plan plan, const float* x, tasp_kv_cache* cache,
                                    int32_t pos, float* out, void* stream, float* kernel_ms,
                                    int32_t* kinds, int32_t cap, int32_t* n);
 
-/* Profiling: average duration of one stage kernel, measured as n_plans * reps back-to-back launches
- * between two HIP events on `stream`. Stage `kind` 3 is the gate/up GEMV (RMSNorm + SwiGLU; reads
- * the plan's post-attention residual, writes its SwiGLU scratch) and 4 the down GEMV (writes the
- * plan's scratch, not a caller buffer) of layer `layer`. Launch i uses plans[i % n_plans], so
- * distinct plan copies keep every launch streaming its panel from HBM rather than from cache. Each
- * plan must have run a tasp_decode_step with batch `batch` (its scratch holds the stage's input).
- * Synchronises `stream`; writes the mean milliseconds per launch. Not capturable. */
-tasp_status tasp_profile_stage(const tasp_plan* plans, int32_t n_plans, int32_t layer,
-                               int32_t kind, int32_t batch, int32_t reps, void* stream,
-                               float* ms_per_launch);
+/* Profiling: average duration of one stage of layer `layer`, measured as n_plans * reps
+ * back-to-back launches between two HIP events on `stream`. Stage `kind`: 1 attention at `pos`
+ * (split-KV partials plus, when split, the merge kernel; rewrites cache row pos with the same
+ * values), 3 the gate/up projection (RMSNorm + SwiGLU), 4 the down projection (writes the plan's
+ * scratch, not a caller buffer). Launch i uses plans[i % n_plans] with caches[i % n_plans] (bound
+ * to that plan; its batch selects the batch-1 or the batched kernels), so distinct plan copies
+ * keep every launch streaming from HBM rather than from cache. Each plan must have run a
+ * tasp_decode_step with that cache at `pos` (its scratch holds the stage's input). Synchronises
+ * `stream`; writes the mean milliseconds per launch. Not capturable. */
+tasp_status tasp_profile_stage(const tasp_plan* plans, const tasp_kv_cache* caches,
+                               int32_t n_plans, int32_t layer, int32_t kind, int32_t pos,
+                               int32_t reps, void* stream, float* ms_per_launch);
 
 /* Plain streaming copy of `bytes` (multiple of 16) from src to dst (device): the reference kernel
  * whose counter readings calibrate memory-traffic measurements. */

@@ -94,7 +94,8 @@ def load(path: str = LIB_PATH):
         "tasp_prefill": [P, P, I32, C.POINTER(tasp_kv_cache), I32, P, P],
         "tasp_decode_step_timed": [P, P, C.POINTER(tasp_kv_cache), I32, P, P, C.POINTER(C.c_float),
                                    C.POINTER(I32), I32, C.POINTER(I32)],
-        "tasp_profile_stage": [C.POINTER(P), I32, I32, I32, I32, I32, P, C.POINTER(C.c_float)],
+        "tasp_profile_stage": [C.POINTER(P), C.POINTER(tasp_kv_cache), I32, I32, I32, I32, I32, P,
+                               C.POINTER(C.c_float)],
         "tasp_copy_probe": [P, P, SZ, P],
     }
     for name, args in sig.items():
@@ -183,10 +184,13 @@ def tasp_decode_step_timed(plan, x_ptr, cache, pos, out_ptr, stream, cap=4096):
     return [(KERNEL_KINDS[kinds[i]], ms[i]) for i in range(n.value)]
 
 
-def tasp_profile_stage(plans, layer, kind, batch, reps, stream):
+def tasp_profile_stage(plans, caches, layer, kind, pos, reps, stream):
+    """``caches``: tasp_kv_cache structs, one per plan."""
     arr = (C.c_void_p * len(plans))(*[p.value if isinstance(p, C.c_void_p) else p for p in plans])
+    carr = (tasp_kv_cache * len(caches))(*caches)
     ms = C.c_float()
-    _check(load().tasp_profile_stage(arr, len(plans), layer, kind, batch, reps, stream, C.byref(ms)))
+    _check(load().tasp_profile_stage(arr, carr, len(plans), layer, kind, pos, reps, stream,
+                                     C.byref(ms)))
     return ms.value
 
 

@@ -25,8 +25,10 @@ namespace {
 typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8;
 typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4;
 
-constexpr int kPF = 4;                 // steps per load batch (two batches in flight)
-constexpr int kMaxSsqPerLane = 16;     // sums-of-squares partials per lane: d_model <= 16384
+constexpr int kStepsPerBatch = 4;      // 16-row weight loads per lane and load batch
+constexpr int kNumCu = 256;
+constexpr int kMmTwoTileRows = 8192;   // panels at least this tall use two row tiles per wave
+constexpr int kSsqBatch = 8;           // sums-of-squares partials loaded per thread and round
 
 // Two float32 holding values exact in BF16 -> packed BF16 pair (lo in the low half).
 __device__ __forceinline__ uint32_t pack_exact(float lo, float hi) {
@@ -49,172 +51,218 @@ __device__ __forceinline__ void store_hilo(uint16_t* xo, int ldxo, int b, int co
   xo[size_t(2 * b + 1) * ldxo + col] = f32_to_bf16(v - bf16_to_f32(hi));
 }
 
+template <int RT>
 struct Frag {
-  int4 a;        // 16 weight bytes (INT8) or 8 BF16 weights
-  int4 x0, x1;   // activation fragments for the step's two MFMAs (x1 unused for BF16 weights)
+  int4 a[RT];    // 16 weight bytes (INT8) or 8 BF16 weights of each row tile
+  int4 x0, x1;   // activation fragments for the step's two k halves (x1 unused for BF16 weights)
 };
 
-template <int MODE, int WAVES>
+// Per-thread epilogue operands of one tile (thread -> (row, sequence) of the output tile).
+struct EpiOps {
+  float s1, s2, res, g;
+};
+
+// Persistent: workgroup w serves tiles w, w + grid, ... A tile is RT row tiles of 16 rows (gate/up:
+// 8 RT channels, gate rows then up rows); every wave computes all RT row tiles over its K run,
+// so each activation fragment it loads feeds RT MFMAs. The waves split each tile's K range into
+// equal runs of spw steps (a multiple of the batch; steps past K are skipped), so every wave reaches a
+// tile boundary at the same flattened step and the cross-wave reduction lines up. The load
+// stream runs across tile boundaries: the first steps of the next tile are in flight while the
+// current tile is reduced and stored.
+template <int MODE, int WAVES, int RT>
 __global__ __launch_bounds__(WAVES * kWave) void mfma_gemv_kernel(MfmaArgs a) {
+  constexpr int kPF = kStepsPerBatch / RT;             // steps per load batch (two batches in flight)
   constexpr bool BF = (MODE == MM_LMHEAD);
+  constexpr bool GU = (MODE == MM_GATEUP);
   constexpr int KS = BF ? 32 : 64;                      // k per wave step
-  __shared__ float red[WAVES][4][kWave];
-  __shared__ float tile_s[16][17];
+  constexpr int ROWS = 16 * RT;                         // tile rows
+  constexpr int RPT = GU ? 8 * RT : ROWS;               // output rows (channels) per tile
+  __shared__ float red[WAVES][4 * RT][kWave];
+  __shared__ float tile_s[ROWS][17];
   __shared__ float rs[8];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int r = lane & 15, q = lane >> 4;
-  const int tile = blockIdx.x;
   const int B = a.B, N = a.N, K = a.K;
+  const int n_tiles = (N + RPT - 1) / RPT;
+  const int grid = gridDim.x, wg = blockIdx.x;
+  const int my_tiles = wg < n_tiles ? (n_tiles - 1 - wg) / grid + 1 : 0;
+  const int n_steps = (K + KS - 1) / KS;
+  // at least one batch per tile, so that an empty input still writes its epilogue
+  const int spw = max(kPF, ((n_steps + WAVES - 1) / WAVES + kPF - 1) / kPF * kPF);
+  const int total = my_tiles * spw;
 
-  // ---- this lane's weight row and activation column
-  int row;
-  uint32_t row_base;
-  const uint32_t row_bytes = uint32_t(a.ld) * (BF ? 2u : 1u);
-  if (MODE == MM_GATEUP) {
-    row = tile * 8 + (r & 7);
-    row_base = (r < 8 ? 0u : a.w2_off) + uint32_t(row) * row_bytes;
-  } else {
-    row = tile * 16 + r;
-    row_base = uint32_t(row) * row_bytes;
-  }
-  const bool row_ok = row < N;
-  const uint32_t w_bytes = (MODE == MM_GATEUP) ? a.w2_off + uint32_t(N) * row_bytes
-                                               : uint32_t(N) * row_bytes;
+  const uint32_t esz = BF ? 2u : 1u;
+  const uint32_t row_bytes = uint32_t(a.ld) * esz;
+  const uint32_t w_bytes = GU ? a.w2_off + uint32_t(N) * row_bytes : uint32_t(N) * row_bytes;
   const __amdgpu_buffer_rsrc_t rw = make_rsrc(a.w, w_bytes);
   const __amdgpu_buffer_rsrc_t rx = make_rsrc(a.x, uint32_t(2 * B) * uint32_t(a.ldx) * 2u);
   const uint32_t x_base = uint32_t(r) * uint32_t(a.ldx) * 2u;   // >= the record count when r >= 2B
-
-  // ---- this wave's steps
-  const int n_steps = (K + KS - 1) / KS;
-  const int s0 = (wave * n_steps) / WAVES, s1 = ((wave + 1) * n_steps) / WAVES;
   const int lane_k = q * (BF ? 8 : 16);                 // first k of the lane inside a step
 
-  // RMS partials first (all loads issued before any use): they are L2 hits and retire ahead of
-  // the weight stream. Wave w reduces sequences w and w + WAVES; n_ssq <= 16 * 64.
-  float ssq_v[2][kMaxSsqPerLane];
-  const bool rms = a.ssq != nullptr;
-  if (rms) {
-    const __amdgpu_buffer_rsrc_t rq = make_rsrc(a.ssq, uint32_t(B) * uint32_t(a.n_ssq) * 4u);
-#pragma unroll
-    for (int u = 0; u < 2; ++u) {
-      const int b = wave + u * WAVES;
-#pragma unroll
-      for (int i = 0; i < kMaxSsqPerLane; ++i) {
-        const int j = i * kWave + lane;
-        const uint32_t off = (b < B && j < a.n_ssq) ? (uint32_t(b) * uint32_t(a.n_ssq) + uint32_t(j)) * 4u : kOOB;
-        ssq_v[u][i] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rq, int(off), 0, 0));
-      }
-    }
-  }
-  // epilogue operands of the threads that write outputs
-  float e_s1 = 1.0f, e_s2 = 1.0f, e_res = 0.0f, e_g = 0.0f;
-  {
-    if (MODE == MM_GATEUP) {
-      const int ch = tile * 8 + (tid & 7), b = tid >> 3;
-      if (b < B && ch < N) { e_s1 = a.scale[ch]; e_s2 = a.scale2[ch]; }
-    } else if (MODE != MM_LMHEAD) {
-      const int gr = tile * 16 + (tid & 15), b = tid >> 4;
-      if (b < B && gr < N) {
-        e_s1 = a.scale[gr];
-        if (MODE == MM_RESID) {
-          e_res = a.resid[size_t(b) * a.ldy + gr];
-          if (a.gamma_next) e_g = bf16_to_f32(a.gamma_next[gr]);
-        }
-      }
-    }
-  }
+  // row of this lane in row tile rt of a tile, and the byte offset of its panel
+  auto lane_row = [&](int tile, int rt) {
+    if (GU) return tile * RPT + (RT == 1 ? (r & 7) : r);
+    return tile * ROWS + 16 * rt + r;
+  };
+  auto lane_half = [&](int rt) -> uint32_t {
+    if (!GU) return 0u;
+    return (RT == 1 ? (r >= 8) : (rt == 1)) ? a.w2_off : 0u;
+  };
 
-  auto issue = [&](int t, Frag (&f)[kPF]) {
+  // epilogue thread roles and their operand resources (out-of-range offsets read zero)
+  const int e_b = tid / RPT, e_r = tid % RPT;           // gate/up: channel e_r, else row e_r
+  const __amdgpu_buffer_rsrc_t rs1 = make_rsrc(BF ? nullptr : a.scale, BF ? 0u : uint32_t(N) * 4u);
+  const __amdgpu_buffer_rsrc_t rs2 = make_rsrc(GU ? a.scale2 : nullptr, GU ? uint32_t(N) * 4u : 0u);
+  const bool resid_on = (MODE == MM_RESID);
+  const __amdgpu_buffer_rsrc_t rres =
+      make_rsrc(resid_on ? a.resid : nullptr, resid_on ? uint32_t(B) * uint32_t(a.ldy) * 4u : 0u);
+  const bool gam_on = resid_on && a.gamma_next != nullptr;
+  const __amdgpu_buffer_rsrc_t rgam = make_rsrc(gam_on ? a.gamma_next : nullptr, gam_on ? uint32_t(N) * 2u : 0u);
+
+  auto load_ops = [&](int tile, EpiOps& e) {
+    const int row = tile * RPT + e_r;
+    const bool ok = e_b < B && row < N;
+    const uint32_t o4 = ok ? uint32_t(row) * 4u : kOOB;
+    e.s1 = BF ? 1.0f : __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rs1, int(o4), 0, 0));
+    e.s2 = GU ? __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rs2, int(o4), 0, 0)) : 1.0f;
+    e.res = resid_on ? __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
+                           rres, int(ok ? (uint32_t(e_b) * uint32_t(a.ldy) + uint32_t(row)) * 4u : kOOB), 0, 0))
+                     : 0.0f;
+    e.g = gam_on ? bf16_to_f32(__builtin_amdgcn_raw_buffer_load_b16(rgam, int(ok ? uint32_t(row) * 2u : kOOB), 0, 0))
+                 : 0.0f;
+  };
+
+  EpiOps ops0{}, ops1{};
+  auto issue = [&](int g, Frag<RT> (&f)[kPF]) {
+    const int i = g / spw, jb = g - i * spw;
+    const int tile = wg + i * grid;
+    const bool ok_t = g < total;
+    if (ok_t && jb == 0) {
+      if (i & 1) load_ops(tile, ops1); else load_ops(tile, ops0);
+    }
 #pragma unroll
     for (int u = 0; u < kPF; ++u) {
-      const int step = t + u;
+      const int step = wave * spw + jb + u;
       const int k = step * KS + lane_k;
-      const bool ok = step < s1;
-      const uint32_t wo = (ok && row_ok && k < a.ld) ? row_base + uint32_t(k) * (BF ? 2u : 1u) : kOOB;
+      const bool ok = ok_t && step < n_steps;
+#pragma unroll
+      for (int rt = 0; rt < RT; ++rt) {
+        const int row = lane_row(tile, rt);
+        const uint32_t wo = (ok && row < N && k < a.ld)
+                                ? lane_half(rt) + uint32_t(row) * row_bytes + uint32_t(k) * esz : kOOB;
+        f[u].a[rt] = buf_load16(rw, wo);
+      }
       const uint32_t xo = ok ? x_base + uint32_t(k) * 2u : kOOB;
-      f[u].a = buf_load16(rw, wo);
       f[u].x0 = buf_load16(rx, xo);
       if (!BF) f[u].x1 = buf_load16(rx, xo + 16u);
     }
   };
 
-  f32x4 acc0 = {0.0f, 0.0f, 0.0f, 0.0f}, acc1 = {0.0f, 0.0f, 0.0f, 0.0f};
-  auto process = [&](const Frag (&f)[kPF], int t) {
+  f32x4 acc0[RT], acc1[RT];
+#pragma unroll
+  for (int rt = 0; rt < RT; ++rt) {
+    acc0[rt] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+    acc1[rt] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+  }
+
+  auto epilogue = [&](int tile, const EpiOps& e) {
+    // sum the waves' partial tiles: lane holds D[4q + i][r] of each row tile
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) red[wave][4 * rt + i][lane] = acc0[rt][i] + acc1[rt][i];
+      acc0[rt] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+      acc1[rt] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+    }
+    __syncthreads();
+    for (int idx = tid; idx < 256 * RT; idx += WAVES * kWave) {
+      const int ri = idx >> 6, l = idx & 63;            // ri = 4 rt + i
+      float v = 0.0f;
+#pragma unroll
+      for (int w = 0; w < WAVES; ++w) v += red[w][ri][l];
+      tile_s[16 * (ri >> 2) + 4 * (l >> 4) + (ri & 3)][l & 15] = v;
+    }
+    __syncthreads();
+    const int b = e_b;
+    if (b >= B) return;
+    const float rb = a.ssq ? rs[b] : 1.0f;
+    if (GU) {
+      const int ch = tile * RPT + e_r;
+      if (ch >= N) return;
+      const float gv = (tile_s[e_r][2 * b] + tile_s[e_r][2 * b + 1]) * e.s1 * rb;
+      const float uv = (tile_s[RPT + e_r][2 * b] + tile_s[RPT + e_r][2 * b + 1]) * e.s2 * rb;
+      store_hilo(a.xo, a.ldxo, b, ch, gv / (1.0f + exp2f(-gv * kLog2e)) * uv);
+      return;
+    }
+    const int gr = tile * RPT + e_r;
+    const float dot = tile_s[e_r][2 * b] + tile_s[e_r][2 * b + 1];
+    if (MODE == MM_RESID) {
+      const float v = gr < N ? e.res + dot * e.s1 * rb : 0.0f;
+      if (gr < N) a.y[size_t(b) * a.ldy + gr] = v;
+      if (gam_on) {                                     // each 16-lane row: one sequence, 16 rows
+        if (gr < N) store_hilo(a.xo, a.ldxo, b, gr, v * e.g);
+        const float ss = row16_sum(v * v);
+        if ((e_r & 15) == 0 && gr < N) a.ssq_out[size_t(b) * a.n_tiles_out + (gr >> 4)] = ss;
+      }
+      return;
+    }
+    if (gr < N) a.y[size_t(b) * a.ldy + gr] = dot * e.s1 * rb;
+  };
+
+  auto process = [&](const Frag<RT> (&f)[kPF], int g) {
+    if (g >= total) return;
+    const int i = g / spw, jb = g - i * spw;
 #pragma unroll
     for (int u = 0; u < kPF; ++u) {
-      if (t + u >= s1) break;
-      if (BF) {
-        acc0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, f[u].a),
-                                                       __builtin_bit_cast(bf16x8, f[u].x0), acc0, 0, 0, 0);
-      } else {
-        const bf16x8 w_lo = widen_i8(uint32_t(f[u].a.x), uint32_t(f[u].a.y));
-        const bf16x8 w_hi = widen_i8(uint32_t(f[u].a.z), uint32_t(f[u].a.w));
-        acc0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w_lo, __builtin_bit_cast(bf16x8, f[u].x0), acc0, 0, 0, 0);
-        acc1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w_hi, __builtin_bit_cast(bf16x8, f[u].x1), acc1, 0, 0, 0);
+      if (wave * spw + jb + u >= n_steps) break;
+#pragma unroll
+      for (int rt = 0; rt < RT; ++rt) {
+        if (BF) {
+          acc0[rt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, f[u].a[rt]),
+                                                             __builtin_bit_cast(bf16x8, f[u].x0), acc0[rt], 0, 0, 0);
+        } else {
+          const bf16x8 w_lo = widen_i8(uint32_t(f[u].a[rt].x), uint32_t(f[u].a[rt].y));
+          const bf16x8 w_hi = widen_i8(uint32_t(f[u].a[rt].z), uint32_t(f[u].a[rt].w));
+          acc0[rt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w_lo, __builtin_bit_cast(bf16x8, f[u].x0), acc0[rt], 0, 0, 0);
+          acc1[rt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w_hi, __builtin_bit_cast(bf16x8, f[u].x1), acc1[rt], 0, 0, 0);
+        }
       }
+    }
+    if (jb + kPF == spw) {
+      if (i & 1) epilogue(wg + i * grid, ops1); else epilogue(wg + i * grid, ops0);
     }
   };
 
-  Frag fa[kPF], fb[kPF];
-  issue(s0, fa);
-  if (rms) {
-#pragma unroll
-    for (int u = 0; u < 2; ++u) {
-      const int b = wave + u * WAVES;
-      float t = 0.0f;
-#pragma unroll
-      for (int i = 0; i < kMaxSsqPerLane; ++i) t += ssq_v[u][i];
-      t = wave_sum(t);
-      if (b < B && lane == 0) rs[b] = rsqrtf(t * a.inv_d + a.eps);
-    }
-  }
-  for (int t = s0; t < s1; t += 2 * kPF) {
-    issue(t + kPF, fb);
-    process(fa, t);
-    issue(t + 2 * kPF, fa);
-    process(fb, t + kPF);
-  }
-
-  // ---- sum the waves' partial tiles: lane holds D[4q + i][r]
-#pragma unroll
-  for (int i = 0; i < 4; ++i) red[wave][i][lane] = acc0[i] + acc1[i];
-  __syncthreads();
-  if (tid < 256) {
-    const int i = tid >> 6, l = tid & 63;
+  Frag<RT> fa[kPF], fb[kPF];
+  issue(0, fa);
+  // inverse RMS of every sequence, once per workgroup: thread t sums the partials
+  // ssq[t / 32][j], j = t % 32 (mod 32); visible after the first epilogue barrier
+  if (a.ssq && tid < 256) {
+    const int b = tid >> 5;
+    const __amdgpu_buffer_rsrc_t rq = make_rsrc(a.ssq, uint32_t(B) * uint32_t(a.n_ssq) * 4u);
     float v = 0.0f;
+    for (int j0 = 0; j0 < a.n_ssq; j0 += 32 * kSsqBatch) {
+      float t[kSsqBatch];
 #pragma unroll
-    for (int w = 0; w < WAVES; ++w) v += red[w][i][l];
-    tile_s[4 * (l >> 4) + i][l & 15] = v;
-  }
-  __syncthreads();
-
-  // ---- epilogue
-  if (MODE == MM_GATEUP) {
-    const int chl = tid & 7, b = tid >> 3, ch = tile * 8 + chl;
-    if (b >= B || ch >= N) return;
-    const float rb = rms ? rs[b] : 1.0f;
-    const float g = (tile_s[chl][2 * b] + tile_s[chl][2 * b + 1]) * e_s1 * rb;
-    const float u = (tile_s[8 + chl][2 * b] + tile_s[8 + chl][2 * b + 1]) * e_s2 * rb;
-    store_hilo(a.xo, a.ldxo, b, ch, g / (1.0f + exp2f(-g * kLog2e)) * u);
-    return;
-  }
-  const int rl = tid & 15, b = tid >> 4, gr = tile * 16 + rl;
-  if (b >= B) return;                                   // whole rows of 16 lanes stay together
-  const float rb = rms ? rs[b] : 1.0f;
-  const float dot = tile_s[rl][2 * b] + tile_s[rl][2 * b + 1];
-  if (MODE == MM_RESID) {
-    const float v = gr < N ? e_res + dot * e_s1 * rb : 0.0f;
-    if (gr < N) a.y[size_t(b) * a.ldy + gr] = v;
-    if (a.gamma_next) {
-      if (gr < N) store_hilo(a.xo, a.ldxo, b, gr, v * e_g);
-      const float ss = row16_sum(v * v);
-      if (rl == 0) a.ssq_out[size_t(b) * a.n_tiles_out + tile] = ss;
+      for (int u = 0; u < kSsqBatch; ++u) {
+        const int j = j0 + u * 32 + (tid & 31);
+        const uint32_t off = (b < B && j < a.n_ssq) ? (uint32_t(b) * uint32_t(a.n_ssq) + uint32_t(j)) * 4u : kOOB;
+        t[u] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rq, int(off), 0, 0));
+      }
+#pragma unroll
+      for (int u = 0; u < kSsqBatch; ++u) v += t[u];
     }
-    return;
+    v = row16_sum(v);
+    v += __shfl_xor(v, 16, kWave);
+    if ((tid & 31) == 0 && b < B) rs[b] = rsqrtf(v * a.inv_d + a.eps);
   }
-  if (gr >= N) return;
-  a.y[size_t(b) * a.ldy + gr] = (MODE == MM_LMHEAD) ? dot * rb : dot * e_s1 * rb;
+  for (int g = 0; g < total; g += 2 * kPF) {
+    issue(g + kPF, fb);
+    process(fa, g);
+    issue(g + 2 * kPF, fa);
+    process(fb, g + kPF);
+  }
 }
 
 // First operand of a step: u = x * gamma as hi/lo BF16 and per-16-element sums of squares of x.
@@ -229,25 +277,38 @@ __global__ __launch_bounds__(kBlock) void mfma_prep_kernel(const float* __restri
   if ((threadIdx.x & 15) == 0 && i < D) ssq[size_t(b) * n_tiles + (i >> 4)] = ss;
 }
 
-template <int MODE, int WAVES>
-hipError_t launch_mm(const MfmaArgs& a, int grid, hipStream_t s) {
-  hipLaunchKernelGGL((mfma_gemv_kernel<MODE, WAVES>), dim3(grid), dim3(WAVES * kWave), 0, s, a);
+template <int MODE, int WAVES, int RT>
+hipError_t launch_mm(const MfmaArgs& a, hipStream_t s) {
+  const int rpt = (MODE == MM_GATEUP) ? 8 * RT : 16 * RT;
+  const int tiles = (a.N + rpt - 1) / rpt;
+  if (tiles == 0) return hipSuccess;
+  // resident workgroups per CU at this kernel's register and LDS use, queried once
+  static int per_cu = [] {
+    int n = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, mfma_gemv_kernel<MODE, WAVES, RT>,
+                                                     WAVES * kWave, 0) != hipSuccess || n < 1)
+      n = 1;
+    return n;
+  }();
+  const int grid = tiles < per_cu * kNumCu ? tiles : per_cu * kNumCu;
+  hipLaunchKernelGGL((mfma_gemv_kernel<MODE, WAVES, RT>), dim3(grid), dim3(WAVES * kWave), 0, s, a);
   return hipGetLastError();
 }
 
 template <int MODE>
 hipError_t launch_mm_mode(const MfmaArgs& a, hipStream_t s) {
-  const int tiles = (MODE == MM_GATEUP) ? (a.N + 7) / 8 : (a.N + 15) / 16;
-  if (tiles == 0) return hipSuccess;
-  // small panels: more waves per tile so that enough loads are in flight
-  return tiles >= 1024 ? launch_mm<MODE, 4>(a, tiles, s) : launch_mm<MODE, 8>(a, tiles, s);
+  // two row tiles per wave halve the activation reads per weight byte; panels with few rows
+  // keep one so that every CU gets a tile, with more waves per tile so that enough loads fly
+  const int rows = (MODE == MM_GATEUP) ? 2 * a.N : a.N;
+  if (rows >= kMmTwoTileRows) return launch_mm<MODE, 4, 2>(a, s);
+  return launch_mm<MODE, 8, 1>(a, s);
 }
 
 }  // namespace
 
 hipError_t launch_mfma_gemv(MfmaMode mode, const MfmaArgs& a, hipStream_t s) {
   if (a.B < 1 || a.B > 8 || a.K < 0 || a.K > a.ld || a.ld % 16 != 0 || a.ldx % 64 != 0 ||
-      a.ldx < a.K || (a.ssq && a.n_ssq > kMaxSsqPerLane * kWave))
+      a.ldx < a.K)
     return hipErrorInvalidValue;
   switch (mode) {
     case MM_QKV: return launch_mm_mode<MM_QKV>(a, s);

@@ -860,21 +860,33 @@ tasp_status tasp_prefill(tasp_plan p, const float* x, int32_t T, tasp_kv_cache* 
   return fail(TASP_ERR_UNSUPPORTED, "prefill is not built yet");
 }
 
-tasp_status tasp_profile_stage(const tasp_plan* plans, int32_t n_plans, int32_t layer,
-                               int32_t kind, int32_t batch, int32_t reps, void* stream,
-                               float* ms_per_launch) {
-  if (!plans || n_plans < 1 || reps < 1 || !ms_per_launch)
-    return fail(TASP_ERR_INVALID_ARG, "plans / n_plans / reps / ms_per_launch");
-  if (kind != 3 && kind != 4) return fail(TASP_ERR_UNSUPPORTED, "stage kind %d is not profiled", kind);
+tasp_status tasp_profile_stage(const tasp_plan* plans, const tasp_kv_cache* caches,
+                               int32_t n_plans, int32_t layer, int32_t kind, int32_t pos,
+                               int32_t reps, void* stream, float* ms_per_launch) {
+  if (!plans || !caches || n_plans < 1 || reps < 1 || !ms_per_launch)
+    return fail(TASP_ERR_INVALID_ARG, "plans / caches / n_plans / reps / ms_per_launch");
+  if (kind != 1 && kind != 3 && kind != 4)
+    return fail(TASP_ERR_UNSUPPORTED, "stage kind %d is not profiled", kind);
   std::vector<tasp::GemvArgs> args(n_plans);
   std::vector<tasp::MfmaArgs> margs(n_plans);
+  std::vector<tasp::AttnArgs> aargs(n_plans);
+  int batch = 0;
   for (int i = 0; i < n_plans; ++i) {
     const tasp_plan_s* p = plans[i];
     if (!p) return fail(TASP_ERR_INVALID_ARG, "plans[%d] is NULL", i);
+    tasp_status st = check_cache(p, &caches[i]);
+    if (st != TASP_OK) return st;
+    if (caches[i].plan_sig != p->sig) return fail(TASP_ERR_CACHE_PLAN_MISMATCH, "caches[%d]", i);
+    if (i > 0 && caches[i].batch != batch) return fail(TASP_ERR_SHAPE, "caches differ in batch");
+    batch = caches[i].batch;
     if (layer < 0 || layer >= p->desc.n_layers) return fail(TASP_ERR_INVALID_ARG, "bad layer %d", layer);
-    if (batch < 1 || batch > p->desc.max_batch) return fail(TASP_ERR_SHAPE, "bad batch %d", batch);
-    if (kind == 3 && p->layers[layer].c == 0) return fail(TASP_ERR_SHAPE, "layer has no FFN channels");
-    if (batch == 1)
+    if (pos < 0 || pos >= caches[i].max_seq) return fail(TASP_ERR_POS_RANGE, "pos %d", pos);
+    const LayerPlan& P = p->layers[layer];
+    if (kind == 3 && P.c == 0) return fail(TASP_ERR_SHAPE, "layer has no FFN channels");
+    if (kind == 1 && P.m_kv == 0) return fail(TASP_ERR_SHAPE, "layer has no retained KV group");
+    if (kind == 1)
+      aargs[i] = attn_args(p, layer, &caches[i], pos, batch, batch > 1);
+    else if (batch == 1)
       args[i] = (kind == 3) ? gateup_args(p, layer, batch)
                             : down_args(p, layer, batch, p->r_io[layer & 1]);
     else
@@ -883,14 +895,17 @@ tasp_status tasp_profile_stage(const tasp_plan* plans, int32_t n_plans, int32_t 
   }
   const tasp::GemvMode mode = (kind == 3) ? tasp::GEMV_GATEUP : tasp::GEMV_RESID;
   const tasp::MfmaMode mmode = (kind == 3) ? tasp::MM_GATEUP : tasp::MM_RESID;
+  auto launch = [&](int i, hipStream_t s) {
+    if (kind == 1) return tasp::launch_attn_decode(aargs[i], s);
+    return (batch == 1) ? tasp::launch_gemv(mode, args[i], s) : tasp::launch_mfma_gemv(mmode, margs[i], s);
+  };
   hipStream_t s = static_cast<hipStream_t>(stream);
   hipEvent_t e0, e1;
   HIP_TRY(hipEventCreate(&e0));
   HIP_TRY(hipEventCreate(&e1));
   hipError_t h = hipEventRecord(e0, s);
   for (int r = 0; r < reps && h == hipSuccess; ++r)
-    for (int i = 0; i < n_plans && h == hipSuccess; ++i)
-      h = (batch == 1) ? tasp::launch_gemv(mode, args[i], s) : tasp::launch_mfma_gemv(mmode, margs[i], s);
+    for (int i = 0; i < n_plans && h == hipSuccess; ++i) h = launch(i, s);
   if (h == hipSuccess) h = hipEventRecord(e1, s);
   if (h == hipSuccess) h = hipEventSynchronize(e1);
   float ms = 0.0f;

@@ -209,6 +209,20 @@ def test_batched_positions(pos):
     _check_cache_rows(case)
 
 
+def test_batched_tall_panels():
+    """Hidden 8192 with 64 query heads: the QKV, O and down panels are tall enough for the
+    two-row-tile batched kernels (RMS partials, residual and next-operand epilogues)."""
+    _flush("case batched tall panels")
+    sh = synth.tiny_shape(d=8192, hq=64, hkv=8, dh=128, f=1024, theta=500000.0)
+    q, kv, f = synth.all_kept_mask(sh)
+    q[0, 5:9] = 0
+    f[0, 3::5] = 0
+    case, got, want = _decode_case(sh, (q, kv, f), 3, 100, max_seq=128)
+    m, s = assert_parity(got, want, what="tall panels")
+    _flush(f"  max_rel={m:.2e} sum_rel={s:.2e}")
+    _check_cache_rows(case)
+
+
 @pytest.mark.timeout(600)
 def test_llama3_8b_batch8_full_size():
     """One Llama-3-8B-shaped layer under the seed-1 budget mask, 8 sequences at 8192 prior
@@ -297,6 +311,29 @@ def test_repeat_and_graph_replay_are_stable(batch):
         g.replay()
         torch.cuda.synchronize()
         assert np.array_equal(case.out.cpu().numpy().astype(np.float64), first)
+
+
+@pytest.mark.parametrize("batch", [1, 3])
+def test_profile_stage(batch):
+    """The stage profiler times attention, gate/up and down over plan copies; it leaves the
+    decode result unchanged and rejects a cache of another plan."""
+    _flush(f"case profile stage batch={batch}")
+    sh = SMALL
+    case = Case(sh, synth.raw_mask(sh, 3), batch, 150, max_seq=160)
+    first = case.run()
+    for kind in (1, 3, 4):
+        ms = B.tasp_profile_stage([case.plan.handle], [case.cache.struct], 0, kind, case.pos, 3,
+                                  S.current_stream())
+        assert ms > 0.0
+    assert np.array_equal(case.run(), first)
+    other = S.Plan(case.desc, case.dstore, synth.raw_mask(sh, 4))
+    with pytest.raises(B.TaspError) as e:
+        B.tasp_profile_stage([other.handle], [case.cache.struct], 0, 3, case.pos, 1,
+                             S.current_stream())
+    assert e.value.status == -6
+    with pytest.raises(B.TaspError):
+        B.tasp_profile_stage([case.plan.handle], [case.cache.struct], 0, 2, case.pos, 1,
+                             S.current_stream())
 
 
 def test_cache_plan_binding_errors():
