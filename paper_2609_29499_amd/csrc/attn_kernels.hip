@@ -5,12 +5,12 @@
 // (1..8), so each K/V row is read from HBM once for every head that uses it. The slot -> group
 // and slot -> head-range tables of the layer travel inside the kernel arguments, so the cache
 // loads do not wait for an index load. The workgroup
-//   1. issues the K and V loads of its first 128-row sub-block, then rotates its heads' raw q
+//   1. issues the K and V loads of its first 64-row sub-block, then rotates its heads' raw q
 //      (RoPE at pos, table from the plan) into LDS, pre-scaled by log2(e)/sqrt(d_h) so the
 //      softmax works in base 2; if its range holds row pos it also rotates the new k, rounds k
 //      and v to BF16, appends them to the cache and keeps the rounded values in LDS (the values
 //      every later step reads);
-//   2. per sub-block: d_h/8 lanes share a cache row (16-byte loads; rows outside the range use an
+//   2. per sub-block (the next one's loads already in flight): d_h/8 lanes share a cache row (16-byte loads; rows outside the range use an
 //      out-of-range buffer offset, so no branch sits around a load); the per-row dot products are
 //      reduced across the row's lanes with DPP, and an online softmax (running max and sum per
 //      head, rescaled accumulators) folds the sub-block into P V. The head count is a template
@@ -18,6 +18,8 @@
 //   3. writes (max, sum, unnormalised output) per head when the range is split; a second, small
 //      kernel merges the ranges by log-sum-exp and writes o (a kernel boundary is the cheapest
 //      device-wide ordering here: an in-kernel fence + counter costs more than the merge itself).
+#include <algorithm>
+
 #include "device_common.hpp"
 #include "kernels.hpp"
 
@@ -25,7 +27,8 @@ namespace tasp {
 namespace {
 
 constexpr int kMaxHeads = 8;
-constexpr int kSub = 128;              // rows per sub-block
+constexpr int kSub = 64;               // rows per sub-block (two in flight per workgroup)
+constexpr int kMinChunk = 2 * kSub;    // rows per split are a multiple of this
 constexpr int kMaxSplit = 256;
 constexpr int kMergeBatch = 32;
 
@@ -101,12 +104,19 @@ __device__ __forceinline__ void attn_body(const AttnArgs& a, AttnSmem<DH>& sm, i
     return (t < t1 && t < a.pos) ? uint32_t(t) * (DH * 2u) + uint32_t(lr) * 16u : kOOB;
   };
 
-  int4 kw[U], vw[U];
+  // K and V of one sub-block: U rows per lane
+  struct KV {
+    int4 k[U], v[U];
+  };
+  auto issue = [&](int tb, KV& f) {
 #pragma unroll
-  for (int u = 0; u < U; ++u) {
-    kw[u] = buf_load16(rk, row_off(t0 + rb + u * RPB));
-    vw[u] = buf_load16(rv, row_off(t0 + rb + u * RPB));
-  }
+    for (int u = 0; u < U; ++u) {
+      f.k[u] = buf_load16(rk, row_off(tb + rb + u * RPB));
+      f.v[u] = buf_load16(rv, row_off(tb + rb + u * RPB));
+    }
+  };
+  KV fa, fb;
+  issue(t0, fa);
 
   // 1. RoPE of the queries (and of the new key): item (h, i4) rotates float4 i4 of the first half
   //    with its partner in the second half
@@ -170,21 +180,15 @@ __device__ __forceinline__ void attn_body(const AttnArgs& a, AttnSmem<DH>& sm, i
 #pragma unroll
     for (int i = 0; i < 8; ++i) acc[h][i] = 0.0f;
 
-  // 2. sub-blocks with an online softmax
-  for (int tb = t0; tb < t1; tb += kSub) {
-    if (tb != t0) {
-#pragma unroll
-      for (int u = 0; u < U; ++u) {
-        kw[u] = buf_load16(rk, row_off(tb + rb + u * RPB));
-        vw[u] = buf_load16(rv, row_off(tb + rb + u * RPB));
-      }
-    }
+  // 2. sub-blocks with an online softmax; the next sub-block's K and V are in flight while the
+  //    current one is scored and accumulated
+  auto process = [&](const KV& f, int tb) {
     float d[U][NH];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int t = tb + rb + u * RPB;
       float kf[8];
-      unpack_bf16x8(kw[u], kf);
+      unpack_bf16x8(f.k[u], kf);
       if (has_new && t == a.pos) {
 #pragma unroll
         for (int i = 0; i < 8; ++i) kf[i] = sm.knew[lr * 8 + i];
@@ -211,13 +215,12 @@ __device__ __forceinline__ void attn_body(const AttnArgs& a, AttnSmem<DH>& sm, i
     }
     __syncthreads();
     for (int h = wave; h < NH; h += 4) {
-      const float v0 = sm.sc[h][lane], v1 = sm.sc[h][lane + 64];
+      const float v0 = sm.sc[h][lane];
       const float mo = sm.m_s[h];
-      const float mn = fmaxf(mo, wave_max(fmaxf(v0, v1)));
-      const float p0 = exp2f(v0 - mn), p1 = exp2f(v1 - mn);
+      const float mn = fmaxf(mo, wave_max(v0));
+      const float p0 = exp2f(v0 - mn);
       sm.sc[h][lane] = p0;
-      sm.sc[h][lane + 64] = p1;
-      const float sum = wave_sum(p0 + p1);
+      const float sum = wave_sum(p0);
       if (lane == 0) {
         const float al = exp2f(mo - mn);
         sm.al_s[h] = al;
@@ -236,7 +239,7 @@ __device__ __forceinline__ void attn_body(const AttnArgs& a, AttnSmem<DH>& sm, i
     for (int u = 0; u < U; ++u) {
       const int t = tb + rb + u * RPB;
       float vf[8];
-      unpack_bf16x8(vw[u], vf);
+      unpack_bf16x8(f.v[u], vf);
       if (has_new && t == a.pos) {
 #pragma unroll
         for (int i = 0; i < 8; ++i) vf[i] = sm.vnew[lr * 8 + i];
@@ -249,6 +252,12 @@ __device__ __forceinline__ void attn_body(const AttnArgs& a, AttnSmem<DH>& sm, i
       }
     }
     __syncthreads();
+  };
+  for (int tb = t0; tb < t1; tb += 2 * kSub) {
+    issue(tb + kSub, fb);
+    process(fa, tb);
+    issue(tb + 2 * kSub, fa);
+    if (tb + kSub < t1) process(fb, tb + kSub);
   }
   // reduce over the rows of a wave (lanes that share lr), then over the 4 waves in LDS
 #pragma unroll
@@ -292,19 +301,28 @@ __device__ __forceinline__ void attn_body(const AttnArgs& a, AttnSmem<DH>& sm, i
         make_float2(sm.m_s[tid], sm.l_s[tid]);
 }
 
-template <int DH>
+// NHM bounds the retained heads of every group slot in the launch: the register budget is set by
+// the largest head count compiled into the kernel, so layers whose groups keep few heads run with
+// fewer registers and more resident workgroups.
+template <int DH, int NHM>
 __global__ __launch_bounds__(kBlock) void attn_decode_kernel(AttnArgs a) {
   __shared__ __attribute__((aligned(16))) AttnSmem<DH> sm;
   const int s = blockIdx.x, j = blockIdx.y, b = blockIdx.z;
-  switch (a.slot_start[j + 1] - a.slot_start[j]) {
-    case 1: attn_body<DH, 1>(a, sm, s, j, b); break;
-    case 2: attn_body<DH, 2>(a, sm, s, j, b); break;
+  const int nh = a.slot_start[j + 1] - a.slot_start[j];
+  if (NHM == 1 || nh == 1) { attn_body<DH, 1>(a, sm, s, j, b); return; }
+  if (NHM == 2 || nh == 2) { attn_body<DH, (NHM >= 2 ? 2 : 1)>(a, sm, s, j, b); return; }
+  if (NHM == 4) {
+    if (nh == 3) attn_body<DH, (NHM >= 3 ? 3 : 1)>(a, sm, s, j, b);
+    else attn_body<DH, (NHM >= 4 ? 4 : 1)>(a, sm, s, j, b);
+    return;
+  }
+  switch (nh) {
     case 3: attn_body<DH, 3>(a, sm, s, j, b); break;
     case 4: attn_body<DH, 4>(a, sm, s, j, b); break;
     case 5: attn_body<DH, 5>(a, sm, s, j, b); break;
     case 6: attn_body<DH, 6>(a, sm, s, j, b); break;
     case 7: attn_body<DH, 7>(a, sm, s, j, b); break;
-    case 8: attn_body<DH, 8>(a, sm, s, j, b); break;
+    default: attn_body<DH, 8>(a, sm, s, j, b); break;
   }
 }
 
@@ -363,16 +381,23 @@ __global__ __launch_bounds__(kBlock) void attn_merge_kernel(AttnArgs a) {
 
 }  // namespace
 
+template <int DH>
+hipError_t launch_partials(const AttnArgs& a, dim3 grid, int nhm, hipStream_t s) {
+  if (nhm <= 1) hipLaunchKernelGGL((attn_decode_kernel<DH, 1>), grid, dim3(kBlock), 0, s, a);
+  else if (nhm == 2) hipLaunchKernelGGL((attn_decode_kernel<DH, 2>), grid, dim3(kBlock), 0, s, a);
+  else if (nhm <= 4) hipLaunchKernelGGL((attn_decode_kernel<DH, 4>), grid, dim3(kBlock), 0, s, a);
+  else hipLaunchKernelGGL((attn_decode_kernel<DH, 8>), grid, dim3(kBlock), 0, s, a);
+  return hipGetLastError();
+}
+
 hipError_t launch_attn_decode(const AttnArgs& a, hipStream_t s) {
   if (a.m_kv == 0 || a.B == 0) return hipSuccess;
+  if (a.chunk % kMinChunk != 0 || a.dh != 64 && a.dh != 128) return hipErrorInvalidValue;
+  int nhm = 0;
+  for (int j = 0; j < a.m_kv; ++j) nhm = std::max(nhm, a.slot_start[j + 1] - a.slot_start[j]);
+  if (nhm < 1 || nhm > kMaxHeads) return hipErrorInvalidValue;
   const dim3 grid(a.n_split, a.m_kv, a.B);
-  if (a.dh == 128)
-    hipLaunchKernelGGL(attn_decode_kernel<128>, grid, dim3(kBlock), 0, s, a);
-  else if (a.dh == 64)
-    hipLaunchKernelGGL(attn_decode_kernel<64>, grid, dim3(kBlock), 0, s, a);
-  else
-    return hipErrorInvalidValue;
-  hipError_t e = hipGetLastError();
+  hipError_t e = (a.dh == 128) ? launch_partials<128>(a, grid, nhm, s) : launch_partials<64>(a, grid, nhm, s);
   if (e != hipSuccess || a.n_split == 1) return e;
   if (a.dh == 128)
     hipLaunchKernelGGL(attn_merge_kernel<128>, dim3(a.m_kv, a.B), dim3(kBlock), 0, s, a);
@@ -381,7 +406,7 @@ hipError_t launch_attn_decode(const AttnArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
-int attn_min_chunk() { return kSub; }
+int attn_min_chunk() { return kMinChunk; }
 int attn_max_split() { return kMaxSplit; }
 
 }  // namespace tasp
