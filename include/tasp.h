@@ -170,12 +170,23 @@ tasp_status tasp_kv_bind(tasp_plan plan, tasp_kv_cache* cache);
 tasp_status tasp_decode_step(tasp_plan plan, const float* x, tasp_kv_cache* cache, int32_t pos,
                              float* out, void* stream);
 
-/* Prefill of T tokens of one sequence (cache->batch must be 1) at positions pos0..pos0+T-1,
- * 1 <= T <= max_prefill, pos0 + T <= cache->max_seq. x (device) float32 [T][d_model]; out
- * (device) float32 [T][d_model], or logits [T][vocab] with an LM head. Token t attends causally
- * over rows 0..pos0+t. pos0 == 0 binds the cache to the plan; pos0 > 0 requires it bound. */
+/* Prefill of T tokens of one sequence (cache->batch must be 1) at positions pos0..pos0+T-1
+ * (paper, Sec. "Deployment": the plan fixed at the start of a turn serves the prompt and every
+ * later decode step). 1 <= T <= max_prefill (TASP_ERR_UNSUPPORTED for a plan compiled with
+ * max_prefill 0), pos0 + T <= cache->max_seq (else TASP_ERR_POS_RANGE). x (device) float32
+ * [T][d_model]; out (device, not overlapping x) float32 [T][d_model], or logits [T][vocab] with
+ * an LM head. Token t attends causally over rows 0..pos0+t; rows pos0..pos0+T-1 of every
+ * retained group receive the BF16 k and v of the tokens. pos0 == 0 binds the cache to the plan;
+ * pos0 > 0 requires it bound (else TASP_ERR_CACHE_PLAN_MISMATCH). Projections and attention run
+ * on the matrix cores with activations split into hi/lo BF16 pairs. Stream-ordered, capturable. */
 tasp_status tasp_prefill(tasp_plan plan, const float* x, int32_t T, tasp_kv_cache* cache,
                          int32_t pos0, float* out, void* stream);
+
+/* Profiling variant of tasp_prefill: an event pair around every kernel; kinds as for
+ * tasp_decode_step_timed, plus 7 for the RoPE / cache-append kernel. Synchronises `stream`. */
+tasp_status tasp_prefill_timed(tasp_plan plan, const float* x, int32_t T, tasp_kv_cache* cache,
+                               int32_t pos0, float* out, void* stream, float* kernel_ms,
+                               int32_t* kinds, int32_t cap, int32_t* n);
 
 /* Profiling variant of tasp_decode_step: records a HIP event pair around every kernel it launches,
  * synchronises `stream`, and writes each kernel's duration in milliseconds to kernel_ms[i] and a

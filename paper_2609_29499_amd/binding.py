@@ -20,11 +20,12 @@ STATUS = {0: "TASP_OK", -1: "TASP_ERR_INVALID_ARG", -2: "TASP_ERR_SHAPE", -3: "T
 IDX_Q, IDX_KV, IDX_QKVSLOT, IDX_FFN = 0, 1, 2, 3
 PANEL_QKV, PANEL_O, PANEL_GATE, PANEL_UP, PANEL_DOWN = 0, 1, 2, 3, 4
 KERNEL_KINDS = {0: "qkv_gemv", 1: "attention", 2: "o_gemv", 3: "gateup_gemv", 4: "down_gemv",
-                5: "lmhead_gemv", 6: "operand_prep"}
+                5: "lmhead_gemv", 6: "operand_prep", 7: "rope_append"}
 
 EXPORTS = ["tasp_plan_workspace_bytes", "tasp_compile_plan", "tasp_plan_counts",
            "tasp_plan_indices", "tasp_plan_panel", "tasp_plan_ledger", "tasp_plan_destroy",
-           "tasp_kv_bind", "tasp_decode_step", "tasp_prefill", "tasp_decode_step_timed",
+           "tasp_kv_bind", "tasp_decode_step", "tasp_prefill", "tasp_prefill_timed",
+           "tasp_decode_step_timed",
            "tasp_profile_stage", "tasp_copy_probe", "tasp_status_string", "tasp_last_error"]
 
 
@@ -92,6 +93,8 @@ def load(path: str = LIB_PATH):
         "tasp_kv_bind": [P, C.POINTER(tasp_kv_cache)],
         "tasp_decode_step": [P, P, C.POINTER(tasp_kv_cache), I32, P, P],
         "tasp_prefill": [P, P, I32, C.POINTER(tasp_kv_cache), I32, P, P],
+        "tasp_prefill_timed": [P, P, I32, C.POINTER(tasp_kv_cache), I32, P, P, C.POINTER(C.c_float),
+                               C.POINTER(I32), I32, C.POINTER(I32)],
         "tasp_decode_step_timed": [P, P, C.POINTER(tasp_kv_cache), I32, P, P, C.POINTER(C.c_float),
                                    C.POINTER(I32), I32, C.POINTER(I32)],
         "tasp_profile_stage": [C.POINTER(P), C.POINTER(tasp_kv_cache), I32, I32, I32, I32, I32, P,
@@ -173,6 +176,15 @@ def tasp_decode_step(plan, x_ptr, cache, pos, out_ptr, stream):
 
 def tasp_prefill(plan, x_ptr, T, cache, pos0, out_ptr, stream):
     _check(load().tasp_prefill(plan, x_ptr, T, C.byref(cache), pos0, out_ptr, stream))
+
+
+def tasp_prefill_timed(plan, x_ptr, T, cache, pos0, out_ptr, stream, cap=4096):
+    ms = (C.c_float * cap)()
+    kinds = (C.c_int32 * cap)()
+    n = C.c_int32()
+    _check(load().tasp_prefill_timed(plan, x_ptr, T, C.byref(cache), pos0, out_ptr, stream, ms,
+                                     kinds, cap, C.byref(n)))
+    return [(KERNEL_KINDS[kinds[i]], ms[i]) for i in range(n.value)]
 
 
 def tasp_decode_step_timed(plan, x_ptr, cache, pos, out_ptr, stream, cap=4096):

@@ -392,7 +392,7 @@ hipError_t launch_partials(const AttnArgs& a, dim3 grid, int nhm, hipStream_t s)
 
 hipError_t launch_attn_decode(const AttnArgs& a, hipStream_t s) {
   if (a.m_kv == 0 || a.B == 0) return hipSuccess;
-  if (a.chunk % kMinChunk != 0 || a.dh != 64 && a.dh != 128) return hipErrorInvalidValue;
+  if (a.chunk % kMinChunk != 0 || (a.dh != 64 && a.dh != 128)) return hipErrorInvalidValue;
   int nhm = 0;
   for (int j = 0; j < a.m_kv; ++j) nhm = std::max(nhm, a.slot_start[j + 1] - a.slot_start[j]);
   if (nhm < 1 || nhm > kMaxHeads) return hipErrorInvalidValue;

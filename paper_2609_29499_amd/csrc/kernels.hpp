@@ -89,6 +89,53 @@ hipError_t launch_mfma_gemv(MfmaMode mode, const MfmaArgs& a, hipStream_t s);
 hipError_t launch_mfma_prep(const float* x, int ldx, int D, const uint16_t* gamma, uint16_t* xo,
                             int ldxo, float* ssq, int B, hipStream_t s);
 
+// ----------------------------------------------------------------- prefill on MFMA
+
+// T tokens of one sequence. Activation operands are two BF16 planes (hi, lo) of [T][ldx] each,
+// `plane` elements apart; modes as for the batched decode. The inverse RMS of token t is
+// rsqrt(inv_d * sum(ssq[t][0..n_ssq)) + eps) when ssq is given (partials per 64 rows).
+struct PfArgs {
+  const void* w; uint32_t w2_off;     // panel rows [N][ld] (gate/up: gate rows; up at w2_off bytes)
+  const float* scale; const float* scale2;
+  int N, K, ld;
+  const uint16_t* x; int ldx; uint32_t plane;
+  const float* ssq; int n_ssq; float inv_d, eps;
+  const float* resid;                 // MM_RESID: [T][ldy]
+  float* y; int ldy;                  // float32 output [T][ldy] (not MM_GATEUP)
+  uint16_t* xo; int ldxo; uint32_t plane_o;   // next operand (MM_GATEUP; MM_RESID with gamma_next)
+  const uint16_t* gamma_next;
+  float* ssq_out; int n_ssq_out;      // MM_RESID with gamma_next: [T][ceil(N/64)]
+  int T;
+};
+hipError_t launch_pf_gemm(MfmaMode mode, const PfArgs& a, hipStream_t s);
+// x float32 [T][D] -> hi/lo planes of x * gamma and sums of squares per 64 elements [T][D/64].
+hipError_t launch_pf_prep(const float* x, int D, int T, const uint16_t* gamma, uint16_t* xo,
+                          size_t plane, int ldxo, float* ssq, hipStream_t s);
+int pf_ssq_block();
+
+struct PfRopeArgs {
+  const float* qkv; int ld_qkv;       // [T][ld_qkv]: raw q (m_q*dh), k (m_kv*dh), v (m_kv*dh)
+  int m_q, m_kv, dh;
+  int kv_idx[64];
+  uint16_t* kc; uint16_t* vc;         // this layer's cache of sequence 0, [Hkv][S][dh]
+  int S;
+  const float* rope_cos; const float* rope_sin;
+  int pos0, T;
+  uint16_t* q_out; uint32_t q_plane; int T_ld;   // [2][m_q][T_ld][dh] hi/lo, q * log2(e)/sqrt(dh)
+};
+hipError_t launch_pf_rope(const PfRopeArgs& a, hipStream_t s);
+
+struct PfAttnArgs {
+  const uint16_t* q; uint32_t q_plane; int T_ld;   // as PfRopeArgs::q_out
+  int m_kv, dh;
+  int kv_idx[64];
+  int slot_start[65];
+  const uint16_t* kc; const uint16_t* vc;         // [Hkv][S][dh]
+  int S, pos0, T;
+  uint16_t* o; int ldo; uint32_t o_plane;         // hi/lo operand [2][T][ldo]
+};
+hipError_t launch_pf_attn(const PfAttnArgs& a, hipStream_t s);
+
 // ----------------------------------------------------------------- decode attention
 
 struct AttnArgs {

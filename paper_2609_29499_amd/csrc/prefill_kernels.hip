@@ -1,0 +1,335 @@
+// Prefill projections on the matrix cores: C[t][n] = sum_k A[t][k] P[n][k] for the T tokens of a
+// prompt chunk, with v_mfma_f32_16x16x32_bf16 and float32 accumulation.
+//
+// Operands. The activation A is carried as two BF16 planes, hi = bf16(v) and lo = bf16(v - hi),
+// and every tile is multiplied twice (hi, then lo, into the same accumulator), so activations keep
+// 16 significant bits; INT8 panel rows are widened exactly to BF16 while they are staged in LDS
+// (the dense BF16 LM head is staged as is). The inverse RMS of an RMSNorm input is applied per
+// token in the epilogue (W (c x) = c (W x)); the producer of an operand writes x * gamma and
+// per-64-row sums of squares of x, which the consumer reduces once per workgroup.
+//
+// Tiling. A workgroup computes 128 tokens x 128 panel rows (gate/up: 64 channels, each wave's
+// 64 rows being 32 gate rows and the 32 up rows of the same channels, so SwiGLU stays in
+// registers). Four waves in a 2 x 2 arrangement own 64 x 64 each as 4 x 4 MFMA tiles. K advances
+// in chunks of 32: the next chunk's global loads are in flight while the current chunk's 32
+// MFMAs per wave run from LDS (double-buffered, one barrier per chunk). LDS rows are padded to
+// 40 BF16 so that the 16 lanes reading one fragment column hit distinct banks.
+#include "device_common.hpp"
+#include "kernels.hpp"
+
+namespace tasp {
+namespace {
+
+typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8;
+typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4;
+
+constexpr int kTM = 128;               // tokens per workgroup tile
+constexpr int kTN = 128;               // panel rows per workgroup tile
+constexpr int kKC = 32;                // k per chunk
+constexpr int kLdsRow = 40;            // BF16 per LDS row (32 + padding)
+constexpr int kSsqBlk = 64;            // rows per sum-of-squares partial
+
+struct PfSmem {
+  uint16_t a[2][2][kTM * kLdsRow];     // [buffer][hi/lo][token * 40 + k]
+  uint16_t b[2][kTN * kLdsRow];        // [buffer][row * 40 + k]
+  float rs[kTM];                       // inverse RMS of the tile's tokens
+};
+
+__device__ __forceinline__ uint32_t pack_exact(float lo, float hi) {
+  return __builtin_amdgcn_perm(__float_as_uint(hi), __float_as_uint(lo), 0x07060302u);
+}
+
+// 16 signed INT8 -> 16 BF16 (exact), as two 16-byte halves
+__device__ __forceinline__ void widen16(const int4& w, int4& lo, int4& hi) {
+  const uint32_t v[4] = {uint32_t(w.x), uint32_t(w.y), uint32_t(w.z), uint32_t(w.w)};
+  uint32_t o[8];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    o[2 * i] = pack_exact(float(int8_t(v[i] & 0xffu)), float(int8_t((v[i] >> 8) & 0xffu)));
+    o[2 * i + 1] = pack_exact(float(int8_t((v[i] >> 16) & 0xffu)), float(int8_t(v[i] >> 24)));
+  }
+  lo = make_int4(int(o[0]), int(o[1]), int(o[2]), int(o[3]));
+  hi = make_int4(int(o[4]), int(o[5]), int(o[6]), int(o[7]));
+}
+
+__device__ __forceinline__ void store_hilo_pf(uint16_t* xo, size_t plane, int ld, int t, int col, float v) {
+  const uint16_t hi = f32_to_bf16(v);
+  xo[size_t(t) * ld + col] = hi;
+  xo[plane + size_t(t) * ld + col] = f32_to_bf16(v - bf16_to_f32(hi));
+}
+
+template <int MODE>
+__global__ __launch_bounds__(kBlock) void pf_gemm_kernel(PfArgs a) {
+  constexpr bool BF = (MODE == MM_LMHEAD);
+  constexpr bool GU = (MODE == MM_GATEUP);
+  __shared__ __attribute__((aligned(16))) PfSmem sm;
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int r = lane & 15, q = lane >> 4;
+  const int wm = wave >> 1, wn = wave & 1;
+  const int T = a.T, N = a.N, K = a.K;
+  const int m0 = blockIdx.y * kTM;
+  const int n0 = blockIdx.x * (GU ? kTN / 2 : kTN);   // first row (gate/up: first channel)
+  const int nk = (K + kKC - 1) / kKC;
+
+  // ---- global -> register staging of one chunk
+  const __amdgpu_buffer_rsrc_t ra = make_rsrc(a.x, uint32_t(2 * a.plane) * 2u);
+  const uint32_t esz = BF ? 2u : 1u;
+  const uint32_t row_bytes = uint32_t(a.ld) * esz;
+  const uint32_t w_bytes = GU ? a.w2_off + uint32_t(N) * row_bytes : uint32_t(N) * row_bytes;
+  const __amdgpu_buffer_rsrc_t rw = make_rsrc(a.w, w_bytes);
+  // A pieces: thread t loads pieces t + 256 i (i < 4): plane i / 2, token row, 16-byte quarter
+  auto a_off = [&](int i, int k0) -> uint32_t {
+    const int p = tid + kBlock * i;
+    const int plane = p >> 9, row = (p >> 2) & (kTM - 1), qu = p & 3;
+    const int t = m0 + row;
+    const int k = k0 + 8 * qu;
+    return (t < T && k < a.ldx) ? uint32_t(plane) * uint32_t(a.plane) * 2u + (uint32_t(t) * uint32_t(a.ldx) + uint32_t(k)) * 2u
+                                : kOOB;
+  };
+  // B rows of this thread: INT8 row t / 2, half t % 2 (16 bytes); BF16 rows p / 4, quarter p % 4
+  auto w_row = [&](int lr) -> int {                     // panel row of LDS row lr
+    if (!GU) return n0 + lr;
+    return n0 + 32 * (lr >> 6) + (lr & 31);             // channel
+  };
+  auto w_off = [&](int lr, int kbyte) -> uint32_t {
+    const int row = w_row(lr);
+    const bool up = GU && ((lr & 63) >= 32);
+    const bool ok = (GU ? row < N : row < N) && kbyte < int(row_bytes);
+    return ok ? (up ? a.w2_off : 0u) + uint32_t(row) * row_bytes + uint32_t(kbyte) : kOOB;
+  };
+  struct Stage {
+    int4 av[4];
+    int4 bv[2];
+  };
+  auto load = [&](int kc, Stage& st) {
+    const int k0 = kc * kKC;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) st.av[i] = buf_load16(ra, kc < nk ? a_off(i, k0) : kOOB);
+    if (BF) {
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        const int p = tid + kBlock * i;
+        st.bv[i] = buf_load16(rw, kc < nk ? w_off(p >> 2, (k0 + 8 * (p & 3)) * 2) : kOOB);
+      }
+    } else {
+      st.bv[0] = buf_load16(rw, kc < nk ? w_off(tid >> 1, k0 + 16 * (tid & 1)) : kOOB);
+    }
+  };
+  auto commit = [&](int buf, const Stage& st) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int p = tid + kBlock * i;
+      const int plane = p >> 9, row = (p >> 2) & (kTM - 1), qu = p & 3;
+      *reinterpret_cast<int4*>(&sm.a[buf][plane][row * kLdsRow + 8 * qu]) = st.av[i];
+    }
+    if (BF) {
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        const int p = tid + kBlock * i;
+        *reinterpret_cast<int4*>(&sm.b[buf][(p >> 2) * kLdsRow + 8 * (p & 3)]) = st.bv[i];
+      }
+    } else {
+      int4 lo, hi;
+      widen16(st.bv[0], lo, hi);
+      uint16_t* dst = &sm.b[buf][(tid >> 1) * kLdsRow + 16 * (tid & 1)];
+      *reinterpret_cast<int4*>(dst) = lo;
+      *reinterpret_cast<int4*>(dst + 8) = hi;
+    }
+  };
+
+  Stage st;
+  load(0, st);
+
+  // ---- inverse RMS of the tile's tokens (RMSNorm inputs): thread t sums half of token t / 2
+  if (a.ssq) {
+    const int row = tid >> 1, half = tid & 1, t = m0 + row;
+    const __amdgpu_buffer_rsrc_t rq = make_rsrc(a.ssq, uint32_t(T) * uint32_t(a.n_ssq) * 4u);
+    float v = 0.0f;
+    for (int j0 = 0; j0 < a.n_ssq; j0 += 16) {
+      float tv[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int j = j0 + 2 * u + half;
+        tv[u] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
+                                              rq, int((t < T && j < a.n_ssq) ? (uint32_t(t) * uint32_t(a.n_ssq) + uint32_t(j)) * 4u : kOOB), 0, 0));
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) v += tv[u];
+    }
+    v += __shfl_xor(v, 1, kWave);
+    if (half == 0) sm.rs[row] = rsqrtf(v * a.inv_d + a.eps);
+  }
+
+  commit(0, st);
+  __syncthreads();
+
+  f32x4 acc[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+
+  for (int kc = 0; kc < nk; ++kc) {
+    const int buf = kc & 1;
+    load(kc + 1, st);                                   // next chunk in flight
+    bf16x8 bw[4];
+#pragma unroll
+    for (int nt = 0; nt < 4; ++nt)
+      bw[nt] = *reinterpret_cast<const bf16x8*>(&sm.b[buf][(wn * 64 + nt * 16 + r) * kLdsRow + 8 * q]);
+#pragma unroll
+    for (int mt = 0; mt < 4; ++mt) {
+      const int ar = (wm * 64 + mt * 16 + r) * kLdsRow + 8 * q;
+      const bf16x8 ahi = *reinterpret_cast<const bf16x8*>(&sm.a[buf][0][ar]);
+      const bf16x8 alo = *reinterpret_cast<const bf16x8*>(&sm.a[buf][1][ar]);
+#pragma unroll
+      for (int nt = 0; nt < 4; ++nt) {
+        acc[mt][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ahi, bw[nt], acc[mt][nt], 0, 0, 0);
+        acc[mt][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(alo, bw[nt], acc[mt][nt], 0, 0, 0);
+      }
+    }
+    if (kc + 1 < nk) commit(buf ^ 1, st);
+    __syncthreads();
+  }
+
+  // ---- epilogue: lane holds tokens 4q + i of each token tile, panel row r of each row tile
+  const bool resid_on = (MODE == MM_RESID);
+#pragma unroll
+  for (int mt = 0; mt < 4; ++mt) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int tl = wm * 64 + mt * 16 + 4 * q + i;
+      const int t = m0 + tl;
+      const bool t_ok = t < T;
+      const float rb = a.ssq ? sm.rs[tl] : 1.0f;
+      if (GU) {
+#pragma unroll
+        for (int nt = 0; nt < 2; ++nt) {
+          const int ch = n0 + 32 * wn + 16 * nt + r;
+          if (t_ok && ch < N) {
+            const float gv = acc[mt][nt][i] * a.scale[ch] * rb;
+            const float uv = acc[mt][nt + 2][i] * a.scale2[ch] * rb;
+            store_hilo_pf(a.xo, a.plane_o, a.ldxo, t, ch, gv / (1.0f + exp2f(-gv * kLog2e)) * uv);
+          }
+        }
+        continue;
+      }
+      float ss = 0.0f;
+#pragma unroll
+      for (int nt = 0; nt < 4; ++nt) {
+        const int n = n0 + wn * 64 + nt * 16 + r;
+        const bool ok = t_ok && n < N;
+        float v = 0.0f;
+        if (MODE == MM_LMHEAD) {
+          v = acc[mt][nt][i] * rb;
+        } else if (resid_on) {
+          v = ok ? a.resid[size_t(t) * a.ldy + n] + acc[mt][nt][i] * a.scale[n] : 0.0f;
+          if (ok && a.gamma_next) store_hilo_pf(a.xo, a.plane_o, a.ldxo, t, n, v * bf16_to_f32(a.gamma_next[n]));
+          ss = fmaf(v, v, ss);
+        } else {
+          v = ok ? acc[mt][nt][i] * a.scale[n] * rb : 0.0f;
+        }
+        if (ok) a.y[size_t(t) * a.ldy + n] = v;
+      }
+      if (resid_on && a.gamma_next) {
+        ss = row16_sum(ss);                             // the 16 lanes of this token
+        if (r == 0 && t_ok && n0 + wn * 64 < N) a.ssq_out[size_t(t) * a.n_ssq_out + (n0 + wn * 64) / kSsqBlk] = ss;
+      }
+    }
+  }
+}
+
+// First operand of a prefill: x * gamma as hi/lo planes and per-64-element sums of squares of x.
+__global__ __launch_bounds__(kBlock) void pf_prep_kernel(const float* __restrict__ x, int D,
+                                                         const uint16_t* __restrict__ gamma,
+                                                         uint16_t* xo, size_t plane, int ldxo,
+                                                         float* ssq, int n_ssq) {
+  const int t = blockIdx.y, i = blockIdx.x * kBlock + threadIdx.x;
+  const float v = i < D ? x[size_t(t) * D + i] : 0.0f;
+  if (i < D) store_hilo_pf(xo, plane, ldxo, t, i, v * bf16_to_f32(gamma[i]));
+  const float ss = wave_sum(v * v);
+  if ((threadIdx.x & 63) == 0 && i < D) ssq[size_t(t) * n_ssq + i / kSsqBlk] = ss;
+}
+
+// RoPE of the T tokens' q and k at positions pos0 + t. q (scaled by log2(e) / sqrt(d_h)) goes to
+// the attention operand as hi/lo planes [2][m_q][T][d_h]; k and v are rounded to BF16 and
+// written to the cache rows pos0 + t of their retained groups.
+__global__ __launch_bounds__(kBlock) void pf_rope_kernel(PfRopeArgs a) {
+  const int t = blockIdx.x;
+  const int dh = a.dh, half = dh / 2;
+  const float* row = a.qkv + size_t(t) * a.ld_qkv;
+  const int pos = a.pos0 + t;
+  const float* cs = a.rope_cos + size_t(pos) * half;
+  const float* sn = a.rope_sin + size_t(pos) * half;
+  const float qscale = kLog2e * rsqrtf(float(dh));
+  const int nq = a.m_q * half, nk = a.m_kv * half, nv = a.m_kv * dh;
+  for (int it = threadIdx.x; it < nq + nk + nv; it += kBlock) {
+    if (it < nq + nk) {
+      const bool is_q = it < nq;
+      const int u = is_q ? it : it - nq;
+      const int h = u / half, i = u % half;
+      const float* src = row + (is_q ? h * dh : (a.m_q + h) * dh);
+      const float x1 = src[i], x2 = src[i + half];
+      const float y1 = x1 * cs[i] - x2 * sn[i];
+      const float y2 = x2 * cs[i] + x1 * sn[i];
+      if (is_q) {
+        uint16_t* qo = a.q_out + (size_t(h) * a.T_ld + t) * dh;
+        const float v1 = y1 * qscale, v2 = y2 * qscale;
+        const uint16_t h1 = f32_to_bf16(v1), h2 = f32_to_bf16(v2);
+        qo[i] = h1;
+        qo[i + half] = h2;
+        qo[a.q_plane + i] = f32_to_bf16(v1 - bf16_to_f32(h1));
+        qo[a.q_plane + i + half] = f32_to_bf16(v2 - bf16_to_f32(h2));
+      } else {
+        uint16_t* kc = a.kc + (size_t(a.kv_idx[h]) * a.S + pos) * dh;
+        kc[i] = f32_to_bf16(y1);
+        kc[i + half] = f32_to_bf16(y2);
+      }
+    } else {
+      const int u = it - nq - nk;
+      const int j = u / dh, e = u % dh;
+      a.vc[(size_t(a.kv_idx[j]) * a.S + pos) * dh + e] = f32_to_bf16(row[(a.m_q + a.m_kv + j) * dh + e]);
+    }
+  }
+}
+
+template <int MODE>
+hipError_t launch_pf(const PfArgs& a, hipStream_t s) {
+  const int rows_per_tile = (MODE == MM_GATEUP) ? kTN / 2 : kTN;
+  const dim3 grid((a.N + rows_per_tile - 1) / rows_per_tile, (a.T + kTM - 1) / kTM);
+  if (grid.x == 0 || grid.y == 0) return hipSuccess;
+  hipLaunchKernelGGL(pf_gemm_kernel<MODE>, grid, dim3(kBlock), 0, s, a);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_pf_gemm(MfmaMode mode, const PfArgs& a, hipStream_t s) {
+  if (a.T < 1 || a.K < 0 || a.K > a.ld || a.ld % 16 != 0 || a.ldx % 64 != 0 || a.ldx < a.K)
+    return hipErrorInvalidValue;
+  switch (mode) {
+    case MM_QKV: return launch_pf<MM_QKV>(a, s);
+    case MM_RESID: return launch_pf<MM_RESID>(a, s);
+    case MM_GATEUP: return launch_pf<MM_GATEUP>(a, s);
+    case MM_LMHEAD: return launch_pf<MM_LMHEAD>(a, s);
+  }
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_pf_prep(const float* x, int D, int T, const uint16_t* gamma, uint16_t* xo,
+                          size_t plane, int ldxo, float* ssq, hipStream_t s) {
+  if (D % 16 != 0 || T < 1) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(pf_prep_kernel, dim3((D + kBlock - 1) / kBlock, T), dim3(kBlock), 0, s, x, D,
+                     gamma, xo, plane, ldxo, ssq, (D + kSsqBlk - 1) / kSsqBlk);
+  return hipGetLastError();
+}
+
+hipError_t launch_pf_rope(const PfRopeArgs& a, hipStream_t s) {
+  if (a.T < 1) return hipSuccess;
+  hipLaunchKernelGGL(pf_rope_kernel, dim3(a.T), dim3(kBlock), 0, s, a);
+  return hipGetLastError();
+}
+
+int pf_ssq_block() { return kSsqBlk; }
+
+}  // namespace tasp

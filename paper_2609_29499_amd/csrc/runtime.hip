@@ -68,6 +68,7 @@ tasp_status check_desc(const tasp_model_desc* d) {
     return fail(TASP_ERR_SHAPE, "at most 256 query heads and 64 KV heads");
   if (d->d_ffn % 16) return fail(TASP_ERR_SHAPE, "d_ffn %% 16 != 0 (%d)", d->d_ffn);
   if (d->max_batch > 8) return fail(TASP_ERR_SHAPE, "max_batch > 8");
+  if (d->max_prefill > 4096) return fail(TASP_ERR_SHAPE, "max_prefill > 4096");
   if (!(d->rms_eps > 0.0f) || !(d->rope_theta > 0.0))
     return fail(TASP_ERR_SHAPE, "rms_eps and rope_theta must be positive");
   // every panel (and the BF16 LM head) must be addressable by a 31-bit buffer offset
@@ -141,9 +142,10 @@ struct Layout {
   size_t final_norm, lm_head, rope_cos, rope_sin;
   size_t r_mid, r_io0, r_io1, qkv_buf, o_buf, h_buf, part;
   size_t xd, xo, xh, ssq;            // batched path: hi/lo operands and sums of squares
+  size_t pxd, pxw, pq, pqkv, pr_mid, pr_io0, pr_io1, pssq;   // prefill scratch
   size_t zero_begin, zero_end;       // scratch cleared at compile
   size_t total;
-  int n_split_max, ld_qkv, ld_obuf, ld_h, ld_xd, ld_xo, ld_xh;
+  int n_split_max, ld_qkv, ld_obuf, ld_h, ld_xd, ld_xo, ld_xh, ld_xw;
 };
 
 Layout make_layout(const tasp_model_desc* d, const Closed& c) {
@@ -209,6 +211,17 @@ Layout make_layout(const tasp_model_desc* d, const Closed& c) {
   Y.xo = take(batched ? size_t(16) * Y.ld_xo * 2 : 0);
   Y.xh = take(batched ? size_t(16) * Y.ld_xh * 2 : 0);
   Y.ssq = take(batched ? size_t(B) * (D / 16) * 4 : 0);
+  // prefill of up to P tokens: hi/lo operand planes, q planes, q/k/v, residuals, RMS partials
+  const size_t P = size_t(d->max_prefill);
+  Y.ld_xw = round_up64(std::max(Hq * dh, F));
+  Y.pxd = take(2 * P * Y.ld_xd * 2);
+  Y.pxw = take(2 * P * Y.ld_xw * 2);
+  Y.pq = take(2 * size_t(Hq) * P * dh * 2);
+  Y.pqkv = take(P * Y.ld_qkv * 4);
+  Y.pr_mid = take(P * D * 4);
+  Y.pr_io0 = take(P * D * 4);
+  Y.pr_io1 = take(P * D * 4);
+  Y.pssq = take(P * ((D + 63) / 64) * 4);
   Y.zero_end = off;
   Y.total = off;
   return Y;
@@ -254,6 +267,9 @@ struct tasp_plan_s {
   uint16_t *xd, *xo, *xh;            // batched path operands [16][ld_x*]
   float* ssq;                        // [max_batch][d_model / 16]
   int ld_xd, ld_xo, ld_xh;
+  uint16_t *pxd, *pxw, *pq;          // prefill operands: [2][max_prefill][ld_xd | ld_xw], q planes
+  float *pqkv, *pr_mid, *pr_io[2], *pssq;
+  int ld_xw;
 };
 
 namespace {
@@ -277,6 +293,26 @@ tasp_status run_kernel(Timer* tm, int kind, hipStream_t s, F&& launch) {
   const hipError_t e = launch();
   if (e != hipSuccess) return fail(TASP_ERR_HIP, "kernel launch (kind %d): %s", kind, hipGetErrorString(e));
   if (tm) HIP_TRY(hipEventRecord(e1, s));
+  return TASP_OK;
+}
+
+// waits for the timed launches, reads their event pairs and releases the events
+tasp_status finish_timed(tasp_status st, Timer* tm, hipStream_t s, float* kernel_ms, int32_t* kinds,
+                         int32_t cap, int32_t* n, const char* what) {
+  hipError_t h = hipStreamSynchronize(s);
+  const int k = int(tm->kinds.size());
+  if (st == TASP_OK && h == hipSuccess) {
+    for (int i = 0; i < k && i < cap; ++i) {
+      float ms = 0.0f;
+      if (h == hipSuccess) h = hipEventElapsedTime(&ms, tm->ev[2 * i], tm->ev[2 * i + 1]);
+      kernel_ms[i] = ms;
+      kinds[i] = tm->kinds[i];
+    }
+    *n = k;
+  }
+  for (hipEvent_t e : tm->ev) (void)hipEventDestroy(e);
+  if (st != TASP_OK) return st;
+  if (h != hipSuccess) return fail(TASP_ERR_HIP, "%s: %s", what, hipGetErrorString(h));
   return TASP_OK;
 }
 
@@ -424,6 +460,119 @@ tasp_status decode_batched(tasp_plan p, const float* x, tasp_kv_cache* cache, in
       return st;
   }
   return TASP_OK;
+}
+
+// ---- prefill (T tokens of one sequence): projections and attention on the matrix cores
+
+tasp::PfArgs pf_base(const tasp_plan_s* p, int T) {
+  tasp::PfArgs a{};
+  a.T = T;
+  a.inv_d = 1.0f / float(p->desc.d_model);
+  a.eps = p->desc.rms_eps;
+  a.n_ssq = (p->desc.d_model + tasp::pf_ssq_block() - 1) / tasp::pf_ssq_block();
+  a.n_ssq_out = a.n_ssq;
+  return a;
+}
+
+tasp_status prefill_impl(tasp_plan p, const float* x, int T, tasp_kv_cache* cache, int pos0,
+                         float* out, hipStream_t s, Timer* tm) {
+  const tasp_model_desc& d = p->desc;
+  const int D = d.d_model, dh = d.head_dim, L = d.n_layers, Pm = d.max_prefill;
+  const uint32_t plane_d = uint32_t(size_t(Pm) * p->ld_xd);
+  const uint32_t plane_w = uint32_t(size_t(Pm) * p->ld_xw);
+  const uint32_t plane_q = uint32_t(size_t(d.n_q_heads) * Pm * dh);
+  const size_t layer_cache = size_t(cache->batch) * d.n_kv_heads * cache->max_seq * dh;
+  tasp_status st;
+  if ((st = run_kernel(tm, 6, s, [&] {
+         return tasp::launch_pf_prep(x, D, T, p->layers[0].an, p->pxd, plane_d, p->ld_xd, p->pssq, s);
+       })))
+    return st;
+  for (int l = 0; l < L; ++l) {
+    const LayerPlan& P = p->layers[l];
+    const float* in = (l == 0) ? x : p->pr_io[(l - 1) & 1];
+    float* lo = (l == L - 1 && d.vocab == 0) ? out : p->pr_io[l & 1];
+    uint16_t* kc = static_cast<uint16_t*>(cache->k) + l * layer_cache;
+    uint16_t* vc = static_cast<uint16_t*>(cache->v) + l * layer_cache;
+    if (P.n_qkv > 0) {
+      tasp::PfArgs a = pf_base(p, T);
+      a.w = P.qkv; a.scale = P.s_qkv; a.N = P.n_qkv; a.K = D; a.ld = D;
+      a.x = p->pxd; a.ldx = p->ld_xd; a.plane = plane_d; a.ssq = p->pssq;
+      a.y = p->pqkv; a.ldy = p->ld_qkv;
+      if ((st = run_kernel(tm, 0, s, [&] { return tasp::launch_pf_gemm(tasp::MM_QKV, a, s); })))
+        return st;
+    }
+    if (P.m_kv > 0) {
+      tasp::PfRopeArgs r{};
+      r.qkv = p->pqkv; r.ld_qkv = p->ld_qkv; r.m_q = P.m_q; r.m_kv = P.m_kv; r.dh = dh;
+      for (int q = 0; q < P.m_kv; ++q) r.kv_idx[q] = P.kv_idx[q];
+      r.kc = kc; r.vc = vc; r.S = cache->max_seq; r.rope_cos = p->rope_cos; r.rope_sin = p->rope_sin;
+      r.pos0 = pos0; r.T = T; r.q_out = p->pq; r.q_plane = plane_q; r.T_ld = Pm;
+      if ((st = run_kernel(tm, 7, s, [&] { return tasp::launch_pf_rope(r, s); }))) return st;
+      tasp::PfAttnArgs a{};
+      a.q = p->pq; a.q_plane = plane_q; a.T_ld = Pm; a.m_kv = P.m_kv; a.dh = dh;
+      for (int q = 0; q < P.m_kv; ++q) a.kv_idx[q] = P.kv_idx[q];
+      for (int q = 0; q <= P.m_kv; ++q) a.slot_start[q] = P.slot_start[q];
+      a.kc = kc; a.vc = vc; a.S = cache->max_seq; a.pos0 = pos0; a.T = T;
+      a.o = p->pxw; a.ldo = p->ld_xw; a.o_plane = plane_w;
+      if ((st = run_kernel(tm, 1, s, [&] { return tasp::launch_pf_attn(a, s); }))) return st;
+    }
+    {
+      tasp::PfArgs a = pf_base(p, T);
+      a.w = P.o; a.scale = P.s_o; a.N = D; a.K = P.m_q * dh; a.ld = P.ld_o;
+      a.x = p->pxw; a.ldx = p->ld_xw; a.plane = plane_w; a.resid = in; a.y = p->pr_mid; a.ldy = D;
+      a.gamma_next = P.fn; a.xo = p->pxd; a.ldxo = p->ld_xd; a.plane_o = plane_d; a.ssq_out = p->pssq;
+      if ((st = run_kernel(tm, 2, s, [&] { return tasp::launch_pf_gemm(tasp::MM_RESID, a, s); })))
+        return st;
+    }
+    if (P.c > 0) {
+      tasp::PfArgs a = pf_base(p, T);
+      a.w = P.g; a.w2_off = uint32_t(reinterpret_cast<const char*>(P.u) - reinterpret_cast<const char*>(P.g));
+      a.scale = P.s_g; a.scale2 = P.s_u; a.N = P.c; a.K = D; a.ld = D;
+      a.x = p->pxd; a.ldx = p->ld_xd; a.plane = plane_d; a.ssq = p->pssq;
+      a.xo = p->pxw; a.ldxo = p->ld_xw; a.plane_o = plane_w;
+      if ((st = run_kernel(tm, 3, s, [&] { return tasp::launch_pf_gemm(tasp::MM_GATEUP, a, s); })))
+        return st;
+    }
+    {
+      tasp::PfArgs a = pf_base(p, T);
+      a.w = P.dn; a.scale = P.s_d; a.N = D; a.K = P.c; a.ld = P.ld_d;
+      a.x = p->pxw; a.ldx = p->ld_xw; a.plane = plane_w; a.resid = p->pr_mid; a.y = lo; a.ldy = D;
+      a.gamma_next = (l + 1 < L) ? p->layers[l + 1].an : (d.vocab ? p->final_norm : nullptr);
+      a.xo = p->pxd; a.ldxo = p->ld_xd; a.plane_o = plane_d; a.ssq_out = p->pssq;
+      if ((st = run_kernel(tm, 4, s, [&] { return tasp::launch_pf_gemm(tasp::MM_RESID, a, s); })))
+        return st;
+    }
+  }
+  if (d.vocab) {
+    tasp::PfArgs a = pf_base(p, T);
+    a.w = p->lm_head; a.N = d.vocab; a.K = D; a.ld = D; a.x = p->pxd; a.ldx = p->ld_xd;
+    a.plane = plane_d; a.ssq = p->pssq; a.y = out; a.ldy = d.vocab;
+    if ((st = run_kernel(tm, 5, s, [&] { return tasp::launch_pf_gemm(tasp::MM_LMHEAD, a, s); })))
+      return st;
+  }
+  return TASP_OK;
+}
+
+tasp_status prefill_checked(tasp_plan p, const float* x, int32_t T, tasp_kv_cache* cache,
+                            int32_t pos0, float* out, void* stream, Timer* tm) {
+  if (!p) return fail(TASP_ERR_INVALID_ARG, "plan is NULL");
+  if (!x || !out) return fail(TASP_ERR_INVALID_ARG, "x / out is NULL");
+  tasp_status st = check_cache(p, cache);
+  if (st != TASP_OK) return st;
+  if (p->desc.max_prefill < 1) return fail(TASP_ERR_UNSUPPORTED, "plan compiled with max_prefill 0");
+  if (cache->batch != 1) return fail(TASP_ERR_SHAPE, "prefill takes one sequence (cache batch %d)", cache->batch);
+  if (T < 1 || T > p->desc.max_prefill) return fail(TASP_ERR_SHAPE, "T %d outside 1..%d", T, p->desc.max_prefill);
+  if (pos0 < 0 || pos0 + T > cache->max_seq) return fail(TASP_ERR_POS_RANGE, "pos0 + T beyond the cache");
+  if (pos0 > 0 && cache->plan_sig != p->sig)
+    return fail(TASP_ERR_CACHE_PLAN_MISMATCH, "cache belongs to plan %016llx, not %016llx",
+                (unsigned long long)cache->plan_sig, (unsigned long long)p->sig);
+  const size_t out_elems = size_t(T) * (p->desc.vocab ? p->desc.vocab : p->desc.d_model);
+  const char* xb = reinterpret_cast<const char*>(x);
+  const char* ob = reinterpret_cast<const char*>(out);
+  if (ob < xb + size_t(T) * p->desc.d_model * 4 && xb < ob + out_elems * 4)
+    return fail(TASP_ERR_INVALID_ARG, "x and out overlap");
+  if (pos0 == 0) cache->plan_sig = p->sig;             // a fresh sequence binds the cache
+  return prefill_impl(p, x, T, cache, pos0, out, static_cast<hipStream_t>(stream), tm);
 }
 
 tasp_status decode_impl(tasp_plan p, const float* x, tasp_kv_cache* cache, int32_t pos,
@@ -661,6 +810,15 @@ tasp_status tasp_compile_plan(const tasp_model_desc* desc, const tasp_store* sto
   p->xh = reinterpret_cast<uint16_t*>(at(Y.xh));
   p->ssq = reinterpret_cast<float*>(at(Y.ssq));
   p->ld_xd = Y.ld_xd; p->ld_xo = Y.ld_xo; p->ld_xh = Y.ld_xh;
+  p->pxd = reinterpret_cast<uint16_t*>(at(Y.pxd));
+  p->pxw = reinterpret_cast<uint16_t*>(at(Y.pxw));
+  p->pq = reinterpret_cast<uint16_t*>(at(Y.pq));
+  p->pqkv = reinterpret_cast<float*>(at(Y.pqkv));
+  p->pr_mid = reinterpret_cast<float*>(at(Y.pr_mid));
+  p->pr_io[0] = reinterpret_cast<float*>(at(Y.pr_io0));
+  p->pr_io[1] = reinterpret_cast<float*>(at(Y.pr_io1));
+  p->pssq = reinterpret_cast<float*>(at(Y.pssq));
+  p->ld_xw = Y.ld_xw;
 
   // read the device index lists back (the one synchronisation) and check them
   std::vector<int> hq_idx(size_t(L) * Hq), hkv_idx(size_t(L) * Hkv), hslot(size_t(L) * Hq),
@@ -831,33 +989,21 @@ tasp_status tasp_decode_step_timed(tasp_plan p, const float* x, tasp_kv_cache* c
   if (!kernel_ms || !kinds || !n) return fail(TASP_ERR_INVALID_ARG, "timing outputs are NULL");
   Timer tm;
   tasp_status st = decode_impl(p, x, cache, pos, out, stream, &tm);
-  hipError_t h = hipStreamSynchronize(static_cast<hipStream_t>(stream));
-  const int k = int(tm.kinds.size());
-  if (st == TASP_OK && h == hipSuccess) {
-    for (int i = 0; i < k && i < cap; ++i) {
-      float ms = 0.0f;
-      if (h == hipSuccess) h = hipEventElapsedTime(&ms, tm.ev[2 * i], tm.ev[2 * i + 1]);
-      kernel_ms[i] = ms;
-      kinds[i] = tm.kinds[i];
-    }
-    *n = k;
-  }
-  for (hipEvent_t e : tm.ev) (void)hipEventDestroy(e);
-  if (st != TASP_OK) return st;
-  if (h != hipSuccess) return fail(TASP_ERR_HIP, "timed decode: %s", hipGetErrorString(h));
-  return TASP_OK;
+  return finish_timed(st, &tm, static_cast<hipStream_t>(stream), kernel_ms, kinds, cap, n, "timed decode");
 }
 
 tasp_status tasp_prefill(tasp_plan p, const float* x, int32_t T, tasp_kv_cache* cache,
                          int32_t pos0, float* out, void* stream) {
-  (void)stream;
-  if (!p) return fail(TASP_ERR_INVALID_ARG, "plan is NULL");
-  if (!x || !out) return fail(TASP_ERR_INVALID_ARG, "x / out is NULL");
-  tasp_status st = check_cache(p, cache);
-  if (st != TASP_OK) return st;
-  if (T < 1 || T > p->desc.max_prefill) return fail(TASP_ERR_SHAPE, "T %d outside 1..%d", T, p->desc.max_prefill);
-  if (pos0 < 0 || pos0 + T > cache->max_seq) return fail(TASP_ERR_POS_RANGE, "pos0 + T beyond the cache");
-  return fail(TASP_ERR_UNSUPPORTED, "prefill is not built yet");
+  return prefill_checked(p, x, T, cache, pos0, out, stream, nullptr);
+}
+
+tasp_status tasp_prefill_timed(tasp_plan p, const float* x, int32_t T, tasp_kv_cache* cache,
+                               int32_t pos0, float* out, void* stream, float* kernel_ms,
+                               int32_t* kinds, int32_t cap, int32_t* n) {
+  if (!kernel_ms || !kinds || !n) return fail(TASP_ERR_INVALID_ARG, "timing outputs are NULL");
+  Timer tm;
+  tasp_status st = prefill_checked(p, x, T, cache, pos0, out, stream, &tm);
+  return finish_timed(st, &tm, static_cast<hipStream_t>(stream), kernel_ms, kinds, cap, n, "timed prefill");
 }
 
 tasp_status tasp_profile_stage(const tasp_plan* plans, const tasp_kv_cache* caches,

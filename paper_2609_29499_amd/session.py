@@ -154,3 +154,7 @@ class Plan:
     def prefill(self, x, T, cache, pos0, out, stream=None):
         B.tasp_prefill(self.handle, x.data_ptr(), T, cache.struct, pos0, out.data_ptr(),
                        stream if stream is not None else current_stream())
+
+    def prefill_timed(self, x, T, cache, pos0, out, stream=None):
+        return B.tasp_prefill_timed(self.handle, x.data_ptr(), T, cache.struct, pos0, out.data_ptr(),
+                                    stream if stream is not None else current_stream())

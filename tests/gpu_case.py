@@ -63,3 +63,53 @@ class Case:
                                self.sh, self.final_norm, self.lm_head)
         self.oracle_caches = caches
         return res
+
+
+class PrefillCase:
+    """A prefill of T tokens of one sequence at pos0 (prior rows 0..pos0-1 from the synthetic
+    cache, everything else NaN until the prefill writes it), with the oracle's result."""
+
+    def __init__(self, sh, mask, T, pos0, max_seq=None, max_prefill=None, seed_w=0, seed_x=3,
+                 seed_kv=2, store=None, device="cuda"):
+        self.sh, self.T, self.pos0 = sh, T, pos0
+        self.max_seq = max_seq or pos0 + T
+        self.mask = mask
+        self.store = store if store is not None else [synth.layer_weights(sh, l, seed_w)
+                                                      for l in range(sh.n_layers)]
+        lm = sh.vocab > 0
+        self.final_norm = synth.final_norm(sh, seed_w) if lm else None
+        self.lm_head = synth.lm_head(sh, seed_w) if lm else None
+        self.closed = ref.close_mask(*(mask if mask is not None else synth.all_kept_mask(sh)),
+                                     sh.group_size)
+        self.x = synth.activations(T, sh.d_model, seed_x)
+        self.desc = S.desc_from_shape(sh, max_batch=1, max_seq=self.max_seq,
+                                      max_prefill=max_prefill or T)
+        self.dstore = S.DeviceStore(self.store, self.final_norm, self.lm_head, device)
+        self.plan = S.Plan(self.desc, self.dstore, mask)
+        torch.cuda.synchronize()
+        self.priors = [synth.kv_prior(sh, l, 1, pos0, self.max_seq, seed_kv)
+                       for l in range(sh.n_layers)]
+        self.cache = S.KVCache(self.desc, 1, self.max_seq, device)
+        for l, (k, v) in enumerate(self.priors):
+            b = k.copy(), v.copy()
+            for a in b:
+                a[:, :, pos0:] = NAN_BF16
+                a[:, ~self.closed[1][l]] = NAN_BF16
+            self.cache.load_layer(l, *b)
+        if pos0 > 0:
+            self.plan.bind(self.cache)
+        self.xd = torch.from_numpy(self.x).to(device)
+        self.out = torch.full((T, sh.vocab if lm else sh.d_model), float("nan"), device=device)
+
+    def run(self):
+        self.plan.prefill(self.xd, self.T, self.cache, self.pos0, self.out)
+        torch.cuda.synchronize()
+        return self.out.cpu().numpy().astype(np.float64)
+
+    def oracle(self):
+        caches = [(synth.bf16_bits_to_f32(k[0]).astype(np.float64),
+                   synth.bf16_bits_to_f32(v[0]).astype(np.float64)) for k, v in self.priors]
+        res = ref.prefill_stack(lambda l: self.store[l], self.closed, self.x, caches, self.pos0,
+                                self.sh, self.final_norm, self.lm_head)
+        self.oracle_caches = caches
+        return res
