@@ -305,6 +305,138 @@ KERNEL_SOURCES = {
 }
 
 
+def prefill_flops(sh, counts, T, pos0=0):
+    """Algorithmic FLOPs of one prefill of T tokens of one layer: every retained panel weight is
+    one multiply-add per token; causal attention is 2 d_h multiply-adds per (query, visible row)
+    per retained head (scores and P V)."""
+    m_q, m_kv, c = counts
+    d, dh = sh.d_model, sh.head_dim
+    proj = 2 * T * ((m_q + 2 * m_kv) * dh * d + d * m_q * dh + 3 * d * c)
+    visible = sum(pos0 + t + 1 for t in range(T))
+    attn = 4 * dh * m_q * visible
+    gateup = 2 * T * 2 * c * d
+    return {"projections": proj, "attention": attn, "total": proj + attn, "gateup": gateup}
+
+
+def bench_prefill(args, wl):
+    """Prefill of wl.prefill_tokens tokens of one sequence into an empty cache through one layer:
+    ms per prefill for the sparse and the dense plan, MFMA throughput on algorithmic FLOPs."""
+    import torch
+    import synth
+    from paper_2609_29499_amd import session as S
+    sh, T = wl.shape, wl.prefill_tokens
+    t_setup = time.time()
+    layer = synth.layer_weights(sh, 0)
+    mask = synth.budget_mask(sh, args.mask_seed)
+    x = synth.activations(T, sh.d_model, 1)
+    desc = S.desc_from_shape(sh, max_batch=1, max_seq=T, max_prefill=T)
+    dstore = S.DeviceStore([layer])
+    xd = torch.from_numpy(x).cuda()
+    out = torch.empty_like(xd)
+    results = {}
+    for name, m in (("sparse", mask), ("dense", None)):
+        probe = S.Plan(desc, dstore, m)
+        counts = probe.counts(0)
+        del probe
+        nb = layer_bytes(sh, *counts, 0)
+        copies = max(2, math.ceil(ROTATE_BYTES / nb["weights"]))
+        plans = [S.Plan(desc, dstore, m) for _ in range(copies)]
+        caches = [S.KVCache(desc, 1, T) for _ in range(copies)]
+        for p, c in zip(plans, caches):
+            p.prefill(xd, T, c, 0, out)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        st = torch.cuda.Stream()
+        st.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(st):
+            for p, c in zip(plans, caches):
+                p.prefill(xd, T, c, 0, out, stream=S.current_stream())
+        torch.cuda.current_stream().wait_stream(st)
+        torch.cuda.synchronize()
+        with torch.cuda.graph(g):
+            for p, c in zip(plans, caches):
+                p.prefill(xd, T, c, 0, out, stream=S.current_stream())
+        reps = max(1, args.steps // copies)
+        for _ in range(max(1, args.warmup // copies)):
+            g.replay()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            g.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / (reps * copies)
+        kt = {}
+        for i in range(2 * copies):
+            for kname, kms in plans[i % copies].prefill_timed(xd, T, caches[i % copies], 0, out):
+                kt.setdefault(kname, []).append(kms)
+        kt = {k: float(np.mean(v)) for k, v in kt.items()}
+        fl = prefill_flops(sh, counts, T)
+        results[name] = {"counts": counts, "ms": ms, "kernels": kt, "flops": fl, "copies": copies,
+                         "steps": reps * copies}
+        print(f"[bench] prefill {name}: {ms:.3f} ms, {fl['total'] / (ms * 1e-3) / 1e12:.1f} TFLOP/s, "
+              f"kernels(us)=" + " ".join(f"{k}={v*1e3:.1f}" for k, v in kt.items()),
+              file=sys.stderr, flush=True)
+        del g, plans, caches
+        torch.cuda.empty_cache()
+    sp, dn = results["sparse"], results["dense"]
+    gu_ms = sp["kernels"]["gateup_gemv"]
+    gu_tf = sp["flops"]["gateup"] / (gu_ms * 1e-3) / 1e12
+    line = {
+        "metric": METRIC, "value": round(sp["ms"], 5), "unit": "ms/prefill", "n_gpus": 1,
+        "steps": sp["steps"], "warmup": args.warmup, "ms_per_step": round(sp["ms"], 5),
+        "higher_is_better": False, "scaling": "weak", "vs_baseline": None, "dtype": "bf16x2-mfma",
+        "data": "synthetic",
+        "config": {"workload": wl.name, "d_model": sh.d_model, "n_q_heads": sh.n_q_heads,
+                   "n_kv_heads": sh.n_kv_heads, "head_dim": sh.head_dim, "d_ffn": sh.d_ffn,
+                   "layers": 1, "tokens": T, "pos0": 0, "mask_seed": args.mask_seed,
+                   "retained": {"q_heads": sp["counts"][0], "kv_groups": sp["counts"][1],
+                                "ffn_channels": sp["counts"][2]}},
+        "tokens_per_s": round(T / (sp["ms"] * 1e-3), 1),
+        "algorithmic_TFLOPs": round(sp["flops"]["total"] / (sp["ms"] * 1e-3) / 1e12, 2),
+        "dense_ms_per_prefill": round(dn["ms"], 5),
+        "speedup_vs_dense": round(dn["ms"] / sp["ms"], 4),
+        "flop_ratio_sparse_over_dense": round(sp["flops"]["total"] / dn["flops"]["total"], 4),
+        "kernels_us": {k: {n: round(v * 1e3, 2) for n, v in r["kernels"].items()} for k, r in results.items()},
+        "roofline": {"bound": "mfma", "kernel": "gateup_gemm", "achieved": round(gu_tf, 1),
+                     "peak": 2500.0, "unit": "TFLOP/s", "frac": round(gu_tf / 2500.0, 4),
+                     "issued_frac": round(2 * gu_tf / 2500.0, 4), "traffic": None,
+                     "algorithmic_flops": sp["flops"]["gateup"], "avg_launch_us": round(gu_ms * 1e3, 2),
+                     "note": "activations as hi/lo BF16 pairs: every algorithmic MFMA is issued twice"},
+        "paper_context": "prefill 1814 -> 1326 ms (2048 tokens, 80 layers, dense vs sparse, A100)",
+    }
+    print(f"[bench] setup+timing {time.time() - t_setup:.1f}s", file=sys.stderr, flush=True)
+    if not args.no_cpu:
+        line["cpu_baseline"] = cpu_prefill_baseline(sh, layer, mask, x, args.cpu_seconds)
+    else:
+        line["cpu_baseline"] = None
+    print(json.dumps(line), flush=True)
+
+
+def cpu_prefill_baseline(sh, store_layer, mask, x, budget_s):
+    import threadpoolctl
+    from oracle import reference as ref
+    closed = ref.close_mask(*mask, sh.group_size)
+    W = ref.masked_layer(store_layer, closed[0][0], closed[1][0], closed[2][0], sh.head_dim)
+    T = x.shape[0]
+    times = []
+    t_start = time.perf_counter()
+    while time.perf_counter() - t_start < budget_s or len(times) < 1:
+        K = np.zeros((sh.n_kv_heads, T, sh.head_dim))
+        V = np.zeros_like(K)
+        t0 = time.perf_counter()
+        ref.prefill_layer(W, x, K, V, 0, sh)
+        times.append(time.perf_counter() - t0)
+    info = threadpoolctl.threadpool_info()
+    threads = max([i.get("num_threads", 1) for i in info] or [1])
+    return {"value": float(np.median(times) * 1e3), "unit": "ms/prefill", "cores": int(threads),
+            "kind": "oracle",
+            "sample": f"{len(times)} oracle prefills of the same layer and {T} tokens (float64 numpy, "
+                      f"zero-masked dequantised weights resident), median",
+            "host_cpus": len(os.sched_getaffinity(0))}
+
+
 def load_traffic(kernel, workload):
     """HBM bytes per launch of a kernel from the committed counter summary of this workload, if
     the counters were taken on the current kernel source; else None."""
@@ -337,6 +469,9 @@ def main():
     sh, pos = wl.shape, wl.pos
     if sh.n_layers > 1 and wl.batch == 1 and wl.prefill_tokens == 0:
         bench_stack(args, wl)
+        return
+    if wl.prefill_tokens:
+        bench_prefill(args, wl)
         return
     if sh.n_layers != 1 or wl.prefill_tokens:
         print(json.dumps({"error": f"workload {args.workload} is not a single-layer decode"}))

@@ -23,16 +23,18 @@ namespace {
 typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8;
 typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4;
 
-constexpr int kTM = 128;               // tokens per workgroup tile
+constexpr int kTMax = 128;             // tokens per workgroup tile (largest)
 constexpr int kTN = 128;               // panel rows per workgroup tile
 constexpr int kKC = 32;                // k per chunk
 constexpr int kLdsRow = 40;            // BF16 per LDS row (32 + padding)
 constexpr int kSsqBlk = 64;            // rows per sum-of-squares partial
+constexpr long kPfMinTiles = 384;      // fewer 128-token tiles than this: use 64-token tiles
 
+template <int TM>
 struct PfSmem {
-  uint16_t a[2][2][kTM * kLdsRow];     // [buffer][hi/lo][token * 40 + k]
+  uint16_t a[2][2][TM * kLdsRow];      // [buffer][hi/lo][token * 40 + k]
   uint16_t b[2][kTN * kLdsRow];        // [buffer][row * 40 + k]
-  float rs[kTM];                       // inverse RMS of the tile's tokens
+  float rs[TM];                        // inverse RMS of the tile's tokens
 };
 
 __device__ __forceinline__ uint32_t pack_exact(float lo, float hi) {
@@ -58,17 +60,19 @@ __device__ __forceinline__ void store_hilo_pf(uint16_t* xo, size_t plane, int ld
   xo[plane + size_t(t) * ld + col] = f32_to_bf16(v - bf16_to_f32(hi));
 }
 
-template <int MODE>
+template <int MODE, int TM>
 __global__ __launch_bounds__(kBlock) void pf_gemm_kernel(PfArgs a) {
   constexpr bool BF = (MODE == MM_LMHEAD);
   constexpr bool GU = (MODE == MM_GATEUP);
-  __shared__ __attribute__((aligned(16))) PfSmem sm;
+  constexpr int MT = TM / 32;                           // token tiles of 16 per wave
+  constexpr int APT = TM / 32;                          // A pieces per thread and chunk
+  __shared__ __attribute__((aligned(16))) PfSmem<TM> sm;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int r = lane & 15, q = lane >> 4;
   const int wm = wave >> 1, wn = wave & 1;
   const int T = a.T, N = a.N, K = a.K;
-  const int m0 = blockIdx.y * kTM;
+  const int m0 = blockIdx.y * TM;
   const int n0 = blockIdx.x * (GU ? kTN / 2 : kTN);   // first row (gate/up: first channel)
   const int nk = (K + kKC - 1) / kKC;
 
@@ -78,10 +82,10 @@ __global__ __launch_bounds__(kBlock) void pf_gemm_kernel(PfArgs a) {
   const uint32_t row_bytes = uint32_t(a.ld) * esz;
   const uint32_t w_bytes = GU ? a.w2_off + uint32_t(N) * row_bytes : uint32_t(N) * row_bytes;
   const __amdgpu_buffer_rsrc_t rw = make_rsrc(a.w, w_bytes);
-  // A pieces: thread t loads pieces t + 256 i (i < 4): plane i / 2, token row, 16-byte quarter
+  // A pieces: thread t loads pieces t + 256 i (i < APT): plane, token row, 16-byte quarter
   auto a_off = [&](int i, int k0) -> uint32_t {
     const int p = tid + kBlock * i;
-    const int plane = p >> 9, row = (p >> 2) & (kTM - 1), qu = p & 3;
+    const int plane = p / (4 * TM), row = (p >> 2) & (TM - 1), qu = p & 3;
     const int t = m0 + row;
     const int k = k0 + 8 * qu;
     return (t < T && k < a.ldx) ? uint32_t(plane) * uint32_t(a.plane) * 2u + (uint32_t(t) * uint32_t(a.ldx) + uint32_t(k)) * 2u
@@ -99,13 +103,13 @@ __global__ __launch_bounds__(kBlock) void pf_gemm_kernel(PfArgs a) {
     return ok ? (up ? a.w2_off : 0u) + uint32_t(row) * row_bytes + uint32_t(kbyte) : kOOB;
   };
   struct Stage {
-    int4 av[4];
+    int4 av[APT];
     int4 bv[2];
   };
   auto load = [&](int kc, Stage& st) {
     const int k0 = kc * kKC;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) st.av[i] = buf_load16(ra, kc < nk ? a_off(i, k0) : kOOB);
+    for (int i = 0; i < APT; ++i) st.av[i] = buf_load16(ra, kc < nk ? a_off(i, k0) : kOOB);
     if (BF) {
 #pragma unroll
       for (int i = 0; i < 2; ++i) {
@@ -118,9 +122,9 @@ __global__ __launch_bounds__(kBlock) void pf_gemm_kernel(PfArgs a) {
   };
   auto commit = [&](int buf, const Stage& st) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
+    for (int i = 0; i < APT; ++i) {
       const int p = tid + kBlock * i;
-      const int plane = p >> 9, row = (p >> 2) & (kTM - 1), qu = p & 3;
+      const int plane = p / (4 * TM), row = (p >> 2) & (TM - 1), qu = p & 3;
       *reinterpret_cast<int4*>(&sm.a[buf][plane][row * kLdsRow + 8 * qu]) = st.av[i];
     }
     if (BF) {
@@ -164,9 +168,9 @@ __global__ __launch_bounds__(kBlock) void pf_gemm_kernel(PfArgs a) {
   commit(0, st);
   __syncthreads();
 
-  f32x4 acc[4][4];
+  f32x4 acc[MT][4];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < MT; ++i)
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
 
@@ -178,8 +182,8 @@ __global__ __launch_bounds__(kBlock) void pf_gemm_kernel(PfArgs a) {
     for (int nt = 0; nt < 4; ++nt)
       bw[nt] = *reinterpret_cast<const bf16x8*>(&sm.b[buf][(wn * 64 + nt * 16 + r) * kLdsRow + 8 * q]);
 #pragma unroll
-    for (int mt = 0; mt < 4; ++mt) {
-      const int ar = (wm * 64 + mt * 16 + r) * kLdsRow + 8 * q;
+    for (int mt = 0; mt < MT; ++mt) {
+      const int ar = (wm * (TM / 2) + mt * 16 + r) * kLdsRow + 8 * q;
       const bf16x8 ahi = *reinterpret_cast<const bf16x8*>(&sm.a[buf][0][ar]);
       const bf16x8 alo = *reinterpret_cast<const bf16x8*>(&sm.a[buf][1][ar]);
 #pragma unroll
@@ -195,10 +199,10 @@ __global__ __launch_bounds__(kBlock) void pf_gemm_kernel(PfArgs a) {
   // ---- epilogue: lane holds tokens 4q + i of each token tile, panel row r of each row tile
   const bool resid_on = (MODE == MM_RESID);
 #pragma unroll
-  for (int mt = 0; mt < 4; ++mt) {
+  for (int mt = 0; mt < MT; ++mt) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const int tl = wm * 64 + mt * 16 + 4 * q + i;
+      const int tl = wm * (TM / 2) + mt * 16 + 4 * q + i;
       const int t = m0 + tl;
       const bool t_ok = t < T;
       const float rb = a.ssq ? sm.rs[tl] : 1.0f;
@@ -293,13 +297,22 @@ __global__ __launch_bounds__(kBlock) void pf_rope_kernel(PfRopeArgs a) {
   }
 }
 
+template <int MODE, int TM>
+hipError_t launch_pf_tm(const PfArgs& a, hipStream_t s) {
+  const int rows_per_tile = (MODE == MM_GATEUP) ? kTN / 2 : kTN;
+  const dim3 grid((a.N + rows_per_tile - 1) / rows_per_tile, (a.T + TM - 1) / TM);
+  if (grid.x == 0 || grid.y == 0) return hipSuccess;
+  hipLaunchKernelGGL((pf_gemm_kernel<MODE, TM>), grid, dim3(kBlock), 0, s, a);
+  return hipGetLastError();
+}
+
 template <int MODE>
 hipError_t launch_pf(const PfArgs& a, hipStream_t s) {
+  // 128-token tiles halve the panel re-reads; smaller ones when that leaves CUs idle
   const int rows_per_tile = (MODE == MM_GATEUP) ? kTN / 2 : kTN;
-  const dim3 grid((a.N + rows_per_tile - 1) / rows_per_tile, (a.T + kTM - 1) / kTM);
-  if (grid.x == 0 || grid.y == 0) return hipSuccess;
-  hipLaunchKernelGGL(pf_gemm_kernel<MODE>, grid, dim3(kBlock), 0, s, a);
-  return hipGetLastError();
+  const long tiles = long((a.N + rows_per_tile - 1) / rows_per_tile) * ((a.T + kTMax - 1) / kTMax);
+  if (tiles >= kPfMinTiles) return launch_pf_tm<MODE, kTMax>(a, s);
+  return launch_pf_tm<MODE, kTMax / 2>(a, s);
 }
 
 }  // namespace
