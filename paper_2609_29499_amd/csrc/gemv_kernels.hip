@@ -1,12 +1,14 @@
 // Decode-time GEMVs over compacted panels: y = s * (P x), float32 x and float32 accumulation,
-// INT8 panels for the projections and the dense BF16 LM head. All of them are bound by the panel
-// stream from HBM.
+// INT8 panels for the projections and the dense BF16 LM head, for one sequence. They stream the
+// panel from HBM; at the 8B layer shape each launch is short enough that its fixed costs (launch,
+// first-byte latency, the last wave's work) weigh as much as the stream.
 //
 // Work decomposition: rows are taken in groups of 4 (for gate/up: 2 SwiGLU channels = 2 gate + 2
-// up rows). A tile is one group x 4 KiB of each of its rows (4 chunks of 1 KiB; a wave reads
-// whole contiguous KiB, 16 bytes per lane). Each wave owns a contiguous range of whole groups and
-// walks its tiles with two register buffers in ping-pong: the next tile's 16 buffer loads are in
-// flight while the current tile is dequantised and accumulated, so arithmetic overlaps the stream.
+// up rows). A tile is one group x 2 KiB of each of its rows (2 chunks of 1 KiB; a wave reads
+// whole contiguous KiB, 16 bytes per lane). Four workgroups per CU and small tiles keep the
+// slowest wave's share short. Each wave owns a contiguous range of whole groups and walks its
+// tiles with two register buffers in ping-pong: the next tile's 8 buffer loads are in flight
+// while the current tile is dequantised and accumulated, so arithmetic overlaps the stream.
 // Loads are branch-free: lanes past a row end and tiles past the wave's range use an
 // out-of-range buffer offset, which returns zeros without memory traffic. The first tile is
 // issued before the prologue stages the input vector in LDS (RMS-normalised when a gain is
@@ -24,8 +26,8 @@ namespace tasp {
 namespace {
 
 constexpr int kR = 4;             // rows per group
-constexpr int kC = 4;             // 1 KiB chunks per tile
-constexpr int kWgPerCu = 2;
+constexpr int kC = 2;             // 1 KiB chunks per tile
+constexpr int kWgPerCu = 4;
 constexpr int kNumCu = 256;
 constexpr size_t kMaxGemvLds = 159 * 1024;     // gfx950: 160 KiB of LDS per workgroup, minus statics
 

@@ -1,0 +1,29 @@
+#!/bin/bash
+# rocprofv3 runs behind the committed summaries in profiles/ (run from the repository root on
+# a GPU host; raw results go to gpurun_out/).
+#   decode_b1:  kernel trace of the default benchmark (8B layer, batch 1), then FETCH_SIZE and
+#               WRITE_SIZE passes of its sparse plan
+#   decode_b8:  kernel trace and FETCH_SIZE / WRITE_SIZE passes of the batch-8 benchmark
+#   prefill:    kernel trace and MFMA counter pass of the 512-token prefill benchmark
+set -o pipefail
+export TMPDIR=/tmp
+R=$(pwd)
+O=$R/gpurun_out
+mkdir -p $O
+which=${1:-decode_b1}
+case $which in
+decode_b1)
+  echo "[prof] b1 kernel trace" && timeout -k 10 400 rocprofv3 --kernel-trace --stats -d $O/b1_trace -o trace -- python3 -u bench.py --cpu-seconds 3 > $O/b1_trace.json 2> $O/b1_trace.err &&
+  echo "[prof] b1 FETCH_SIZE" && timeout -s KILL 300 rocprofv3 --pmc FETCH_SIZE -d $O/b1_fetch -o fetch -- python3 -u bench.py --sparse-only --no-cpu --steps 200 --warmup 20 --blocks 1 --timed-launches 8 > $O/b1_fetch.json 2> $O/b1_fetch.err &&
+  echo "[prof] b1 WRITE_SIZE" && timeout -s KILL 300 rocprofv3 --pmc WRITE_SIZE -d $O/b1_write -o write -- python3 -u bench.py --sparse-only --no-cpu --steps 200 --warmup 20 --blocks 1 --timed-launches 8 > $O/b1_write.json 2> $O/b1_write.err
+  ;;
+decode_b8)
+  echo "[prof] b8 kernel trace" && timeout -k 10 400 rocprofv3 --kernel-trace --stats -d $O/b8_trace -o trace -- python3 -u bench.py --workload llama3_8b_batch8 --steps 200 --warmup 20 --cpu-seconds 3 > $O/b8_trace.json 2> $O/b8_trace.err &&
+  echo "[prof] b8 FETCH_SIZE" && timeout -s KILL 300 rocprofv3 --pmc FETCH_SIZE -d $O/b8_fetch -o fetch -- python3 -u bench.py --workload llama3_8b_batch8 --sparse-only --no-cpu --steps 100 --warmup 10 --blocks 1 --timed-launches 8 > $O/b8_fetch.json 2> $O/b8_fetch.err &&
+  echo "[prof] b8 WRITE_SIZE" && timeout -s KILL 300 rocprofv3 --pmc WRITE_SIZE -d $O/b8_write -o write -- python3 -u bench.py --workload llama3_8b_batch8 --sparse-only --no-cpu --steps 100 --warmup 10 --blocks 1 --timed-launches 8 > $O/b8_write.json 2> $O/b8_write.err
+  ;;
+prefill)
+  echo "[prof] prefill kernel trace" && timeout -k 10 400 rocprofv3 --kernel-trace --stats -d $O/pf_trace -o trace -- python3 -u bench.py --workload llama3_8b_prefill512 --steps 200 --warmup 20 --cpu-seconds 3 > $O/pf_trace.json 2> $O/pf_trace.err &&
+  echo "[prof] prefill MFMA counters" && timeout -s KILL 300 rocprofv3 --pmc SQ_VALU_MFMA_BUSY_CYCLES SQ_BUSY_CU_CYCLES GRBM_GUI_ACTIVE -d $O/pf_mfma -o mfma -- python3 -u bench.py --workload llama3_8b_prefill512 --no-cpu --steps 40 --warmup 4 > $O/pf_mfma.json 2> $O/pf_mfma.err
+  ;;
+esac
