@@ -24,6 +24,6 @@ decode_b8)
   ;;
 prefill)
   echo "[prof] prefill kernel trace" && timeout -k 10 400 rocprofv3 --kernel-trace --stats -d $O/pf_trace -o trace -- python3 -u bench.py --workload llama3_8b_prefill512 --steps 200 --warmup 20 --cpu-seconds 3 > $O/pf_trace.json 2> $O/pf_trace.err &&
-  echo "[prof] prefill MFMA counters" && timeout -s KILL 300 rocprofv3 --pmc SQ_VALU_MFMA_BUSY_CYCLES SQ_BUSY_CU_CYCLES GRBM_GUI_ACTIVE -d $O/pf_mfma -o mfma -- python3 -u bench.py --workload llama3_8b_prefill512 --no-cpu --steps 40 --warmup 4 > $O/pf_mfma.json 2> $O/pf_mfma.err
+  echo "[prof] prefill MFMA counters" && timeout -s KILL 300 rocprofv3 --pmc MfmaUtil SQ_INSTS_VALU_MFMA_MOPS_BF16 SQ_BUSY_CU_CYCLES -d $O/pf_mfma -o mfma -- python3 -u bench.py --workload llama3_8b_prefill512 --no-cpu --steps 40 --warmup 4 > $O/pf_mfma.json 2> $O/pf_mfma.err
   ;;
 esac

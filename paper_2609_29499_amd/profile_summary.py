@@ -7,8 +7,8 @@
     python -m paper_2609_29499_amd.profile_summary traffic FETCH_DB WRITE_DB KIND
         HBM bytes per dispatch of KIND from a FETCH_SIZE and a WRITE_SIZE run, each scaled by what
         the same counter reads for the library's 1 GiB streaming copy in the same run
-    python -m paper_2609_29499_amd.profile_summary pmc DB KIND
-        mean of every collected counter per dispatch of KIND
+    python -m paper_2609_29499_amd.profile_summary pmc DB KIND [--grid G]
+        mean of every collected counter per dispatch of KIND (of grid size G work-items)
 
 Kernel kinds are read from the demangled names; GEMVs that share a template (O and down) are told
 apart by their order inside a step (down follows gate/up).
@@ -125,11 +125,11 @@ def traffic(fetch_db, write_db, kind):
     return out
 
 
-def pmc(db, kind):
+def pmc(db, kind, grid=None):
     per = _per_dispatch(db)
     acc = collections.defaultdict(list)
     for k, g, c in per:
-        if k == kind:
+        if k == kind and (grid is None or g == grid):
             for n, v in c.items():
                 acc[n].append(v)
     return {n: {"dispatches": len(v), "mean": statistics.mean(v)} for n, v in acc.items()}
@@ -148,6 +148,7 @@ def main():
     p = sub.add_parser("pmc")
     p.add_argument("db")
     p.add_argument("kind")
+    p.add_argument("--grid", type=int, help="only dispatches of this grid size (work-items)")
     a = ap.parse_args()
     if a.cmd == "trace":
         trace(a.db, a.split)
@@ -156,7 +157,7 @@ def main():
         print(json.dumps(traffic(a.fetch_db, a.write_db, a.kind), indent=1))
     else:
         import json
-        print(json.dumps(pmc(a.db, a.kind), indent=1))
+        print(json.dumps(pmc(a.db, a.kind, a.grid), indent=1))
 
 
 if __name__ == "__main__":
