@@ -11,9 +11,9 @@
 // Tiling. A workgroup computes 128 tokens x 128 panel rows (gate/up: 64 channels, each wave's
 // 64 rows being 32 gate rows and the 32 up rows of the same channels, so SwiGLU stays in
 // registers). Four waves in a 2 x 2 arrangement own 64 x 64 each as 4 x 4 MFMA tiles. K advances
-// in chunks of 32: the next chunk's global loads are in flight while the current chunk's 32
-// MFMAs per wave run from LDS (double-buffered, one barrier per chunk). LDS rows are padded to
-// 40 BF16 so that the 16 lanes reading one fragment column hit distinct banks.
+// in chunks of 32: the global loads of the next three chunks are in flight (in registers) while
+// the current chunk's MFMAs run from LDS (double-buffered, one barrier per chunk). LDS rows are
+// padded to 40 BF16 so that the 16 lanes reading one fragment column hit distinct banks.
 #include "device_common.hpp"
 #include "kernels.hpp"
 
@@ -142,8 +142,12 @@ __global__ __launch_bounds__(kBlock) void pf_gemm_kernel(PfArgs a) {
     }
   };
 
-  Stage st;
-  load(0, st);
+  // three chunks in flight in registers: chunk c is loaded while chunk c - 3 is computed and
+  // committed to LDS after chunk c - 1 has been computed
+  Stage s0, s1, s2;
+  load(0, s0);
+  load(1, s1);
+  load(2, s2);
 
   // ---- inverse RMS of the tile's tokens (RMSNorm inputs): thread t sums half of token t / 2
   if (a.ssq) {
@@ -165,7 +169,7 @@ __global__ __launch_bounds__(kBlock) void pf_gemm_kernel(PfArgs a) {
     if (half == 0) sm.rs[row] = rsqrtf(v * a.inv_d + a.eps);
   }
 
-  commit(0, st);
+  commit(0, s0);
   __syncthreads();
 
   f32x4 acc[MT][4];
@@ -174,9 +178,9 @@ __global__ __launch_bounds__(kBlock) void pf_gemm_kernel(PfArgs a) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
 
-  for (int kc = 0; kc < nk; ++kc) {
+  auto step = [&](int kc, Stage& mine, const Stage& next) {
     const int buf = kc & 1;
-    load(kc + 1, st);                                   // next chunk in flight
+    load(kc + 3, mine);                                 // chunk kc was committed already
     bf16x8 bw[4];
 #pragma unroll
     for (int nt = 0; nt < 4; ++nt)
@@ -192,8 +196,13 @@ __global__ __launch_bounds__(kBlock) void pf_gemm_kernel(PfArgs a) {
         acc[mt][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(alo, bw[nt], acc[mt][nt], 0, 0, 0);
       }
     }
-    if (kc + 1 < nk) commit(buf ^ 1, st);
+    if (kc + 1 < nk) commit(buf ^ 1, next);
     __syncthreads();
+  };
+  for (int kc = 0; kc < nk; kc += 3) {
+    step(kc, s0, s1);
+    if (kc + 1 < nk) step(kc + 1, s1, s2);
+    if (kc + 2 < nk) step(kc + 2, s2, s0);
   }
 
   // ---- epilogue: lane holds tokens 4q + i of each token tile, panel row r of each row tile
