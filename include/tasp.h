@@ -210,6 +210,28 @@ tasp_status tasp_profile_stage(const tasp_plan* plans, const tasp_kv_cache* cach
                                int32_t n_plans, int32_t layer, int32_t kind, int32_t pos,
                                int32_t reps, void* stream, float* ms_per_launch);
 
+/* Greedy dependency-closed mask construction (paper, Sec. "Dependency-Closed Masks and
+ * Cache-Consistent Routing"; costs from Eqs. flop-attn and flop-mlp). Candidates are every query
+ * head and every SwiGLU group of `granule` consecutive channels (gate row, up row and down column
+ * jointly). They are ranked by score / active FLOPs in float64 (a head: 4 d d_h plus 1/r of its
+ * KV group's 4 d d_h; a channel group: 6 d granule), equal keys by ascending candidate index
+ * (layer-major, a layer's heads before its channel groups), and accepted in that order when the
+ * marginal cost (a head whose KV group is not open yet also pays the group) fits the budget
+ * floor(target x full-width decoder FLOPs); a candidate that does not fit is skipped. Outputs are
+ * dependency-closed by construction.
+ *   head_scores (device) float32 [n_layers][n_q_heads]; chan_scores (device) float32
+ *   [n_layers][d_ffn / granule]; all finite (else TASP_ERR_INVALID_ARG).
+ *   q_keep [L][Hq], kv_keep [L][Hkv], ffn_keep [L][d_ffn] (device, caller-owned) receive 0/1.
+ *   granule must divide d_ffn (else TASP_ERR_SHAPE); 0 <= target <= 1.
+ *   workspace: device, 256-byte aligned, at least tasp_mask_workspace_bytes.
+ * Synchronises `stream` (it reads back the status and the FLOPs spent, *flops_spent if given). */
+tasp_status tasp_mask_workspace_bytes(const tasp_model_desc* desc, int32_t granule, size_t* bytes);
+tasp_status tasp_build_mask(const tasp_model_desc* desc, const float* head_scores,
+                            const float* chan_scores, int32_t granule, double target,
+                            void* workspace, size_t workspace_bytes, uint8_t* q_keep,
+                            uint8_t* kv_keep, uint8_t* ffn_keep, uint64_t* flops_spent,
+                            void* stream);
+
 /* Plain streaming copy of `bytes` (multiple of 16) from src to dst (device): the reference kernel
  * whose counter readings calibrate memory-traffic measurements. */
 tasp_status tasp_copy_probe(void* dst, const void* src, size_t bytes, void* stream);

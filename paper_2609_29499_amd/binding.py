@@ -26,7 +26,8 @@ EXPORTS = ["tasp_plan_workspace_bytes", "tasp_compile_plan", "tasp_plan_counts",
            "tasp_plan_indices", "tasp_plan_panel", "tasp_plan_ledger", "tasp_plan_destroy",
            "tasp_kv_bind", "tasp_decode_step", "tasp_prefill", "tasp_prefill_timed",
            "tasp_decode_step_timed",
-           "tasp_profile_stage", "tasp_copy_probe", "tasp_status_string", "tasp_last_error"]
+           "tasp_profile_stage", "tasp_mask_workspace_bytes", "tasp_build_mask", "tasp_copy_probe",
+           "tasp_status_string", "tasp_last_error"]
 
 
 class TaspError(RuntimeError):
@@ -99,6 +100,9 @@ def load(path: str = LIB_PATH):
                                    C.POINTER(I32), I32, C.POINTER(I32)],
         "tasp_profile_stage": [C.POINTER(P), C.POINTER(tasp_kv_cache), I32, I32, I32, I32, I32, P,
                                C.POINTER(C.c_float)],
+        "tasp_mask_workspace_bytes": [C.POINTER(tasp_model_desc), I32, C.POINTER(SZ)],
+        "tasp_build_mask": [C.POINTER(tasp_model_desc), P, P, I32, C.c_double, P, SZ, P, P, P,
+                            C.POINTER(U64), P],
         "tasp_copy_probe": [P, P, SZ, P],
     }
     for name, args in sig.items():
@@ -204,6 +208,20 @@ def tasp_profile_stage(plans, caches, layer, kind, pos, reps, stream):
     _check(load().tasp_profile_stage(arr, carr, len(plans), layer, kind, pos, reps, stream,
                                      C.byref(ms)))
     return ms.value
+
+
+def tasp_mask_workspace_bytes(desc, granule):
+    n = C.c_size_t()
+    _check(load().tasp_mask_workspace_bytes(C.byref(desc), granule, C.byref(n)))
+    return n.value
+
+
+def tasp_build_mask(desc, head_scores_ptr, chan_scores_ptr, granule, target, ws_ptr, ws_bytes,
+                    q_ptr, kv_ptr, f_ptr, stream):
+    spent = C.c_uint64()
+    _check(load().tasp_build_mask(C.byref(desc), head_scores_ptr, chan_scores_ptr, granule, target,
+                                  ws_ptr, ws_bytes, q_ptr, kv_ptr, f_ptr, C.byref(spent), stream))
+    return spent.value
 
 
 def tasp_copy_probe(dst_ptr, src_ptr, nbytes, stream):

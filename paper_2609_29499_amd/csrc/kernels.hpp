@@ -136,6 +136,23 @@ struct PfAttnArgs {
 };
 hipError_t launch_pf_attn(const PfAttnArgs& a, hipStream_t s);
 
+// ----------------------------------------------------------------- mask construction
+
+struct MaskArgs {
+  const float* head_scores;           // device [L][Hq]
+  const float* chan_scores;           // device [L][nG]
+  int L, Hq, Hkv, nG, granule, n_cand;
+  double head_rank_cost;              // own + group / r, the ranking denominator of a head
+  unsigned long long head_cost, group_cost, chan_cost, budget;
+  uint8_t* q_keep; uint8_t* kv_keep; uint8_t* ffn_keep;   // device outputs
+  unsigned* status;                   // bit 0: a non-finite score
+  unsigned long long* spent;          // FLOPs of the accepted set
+};
+size_t mask_scan_lds_bytes(int L, int Hq, int Hkv, int nG);
+hipError_t mask_sort_temp_bytes(int n, size_t* bytes);
+hipError_t launch_build_mask(const MaskArgs& a, void* temp, size_t temp_bytes, double* keys_in,
+                             double* keys_out, int* idx_in, int* idx_out, hipStream_t s);
+
 // ----------------------------------------------------------------- decode attention
 
 struct AttnArgs {

@@ -1063,6 +1063,100 @@ tasp_status tasp_profile_stage(const tasp_plan* plans, const tasp_kv_cache* cach
   return TASP_OK;
 }
 
+// ---- greedy mask construction
+
+namespace {
+
+struct MaskLayout {
+  size_t status, keys_in, keys_out, idx_in, idx_out, temp, temp_bytes, total;
+};
+
+tasp_status mask_layout(const tasp_model_desc* d, int granule, MaskLayout* y) {
+  tasp_status st = check_desc(d);
+  if (st != TASP_OK) return st;
+  if (granule < 1 || d->d_ffn % granule)
+    return fail(TASP_ERR_SHAPE, "granule %d does not divide d_ffn %d", granule, d->d_ffn);
+  const int nG = d->d_ffn / granule;
+  const long n = long(d->n_layers) * (d->n_q_heads + nG);
+  if (n > (1L << 30)) return fail(TASP_ERR_SHAPE, "too many candidates");
+  if (tasp::mask_scan_lds_bytes(d->n_layers, d->n_q_heads, d->n_kv_heads, nG) > kLdsLimit)
+    return fail(TASP_ERR_UNSUPPORTED, "candidate flags exceed LDS");
+  size_t off = 0;
+  auto take = [&](size_t bytes) { const size_t at = off; off = align_up(off + bytes, kAlign); return at; };
+  y->status = take(16);
+  y->keys_in = take(size_t(n) * 8);
+  y->keys_out = take(size_t(n) * 8);
+  y->idx_in = take(size_t(n) * 4);
+  y->idx_out = take(size_t(n) * 4);
+  size_t tb = 0;
+  const hipError_t e = tasp::mask_sort_temp_bytes(int(n), &tb);
+  if (e != hipSuccess) return fail(TASP_ERR_HIP, "sort size query: %s", hipGetErrorString(e));
+  y->temp_bytes = tb;
+  y->temp = take(tb);
+  y->total = off;
+  return TASP_OK;
+}
+
+}  // namespace
+
+tasp_status tasp_mask_workspace_bytes(const tasp_model_desc* desc, int32_t granule, size_t* bytes) {
+  if (!bytes) return fail(TASP_ERR_INVALID_ARG, "bytes is NULL");
+  MaskLayout y;
+  tasp_status st = mask_layout(desc, granule, &y);
+  if (st != TASP_OK) return st;
+  *bytes = y.total;
+  return TASP_OK;
+}
+
+tasp_status tasp_build_mask(const tasp_model_desc* desc, const float* head_scores,
+                            const float* chan_scores, int32_t granule, double target,
+                            void* workspace, size_t workspace_bytes, uint8_t* q_keep,
+                            uint8_t* kv_keep, uint8_t* ffn_keep, uint64_t* flops_spent,
+                            void* stream) {
+  MaskLayout y;
+  tasp_status st = mask_layout(desc, granule, &y);
+  if (st != TASP_OK) return st;
+  if (!head_scores || !chan_scores || !q_keep || !kv_keep || !ffn_keep)
+    return fail(TASP_ERR_INVALID_ARG, "scores / outputs are NULL");
+  if (!(target >= 0.0 && target <= 1.0)) return fail(TASP_ERR_INVALID_ARG, "target outside [0, 1]");
+  if (!workspace) return fail(TASP_ERR_INVALID_ARG, "workspace is NULL");
+  if (reinterpret_cast<uintptr_t>(workspace) % kAlign)
+    return fail(TASP_ERR_WORKSPACE, "workspace not %zu-byte aligned", kAlign);
+  if (workspace_bytes < y.total)
+    return fail(TASP_ERR_WORKSPACE, "workspace %zu bytes, need %zu", workspace_bytes, y.total);
+  const tasp_model_desc& d = *desc;
+  char* base = static_cast<char*>(workspace);
+  tasp::MaskArgs a{};
+  a.head_scores = head_scores; a.chan_scores = chan_scores;
+  a.L = d.n_layers; a.Hq = d.n_q_heads; a.Hkv = d.n_kv_heads; a.nG = d.d_ffn / granule;
+  a.granule = granule; a.n_cand = a.L * (a.Hq + a.nG);
+  const unsigned long long D = d.d_model, dh = d.head_dim;
+  a.head_cost = 2 * D * dh + 2 * dh * D;
+  a.group_cost = 2 * D * dh * 2;
+  a.chan_cost = 6 * D * (unsigned long long)granule;
+  a.head_rank_cost = double(a.head_cost) + double(a.group_cost) / double(a.Hq / a.Hkv);
+  const unsigned long long full = (unsigned long long)d.n_layers *
+      (2 * D * dh * (unsigned long long)(d.n_q_heads + 2 * d.n_kv_heads) +
+       2 * dh * (unsigned long long)d.n_q_heads * D + 6 * D * (unsigned long long)d.d_ffn);
+  a.budget = (unsigned long long)std::floor(target * double(full));
+  a.q_keep = q_keep; a.kv_keep = kv_keep; a.ffn_keep = ffn_keep;
+  a.status = reinterpret_cast<unsigned*>(base + y.status);
+  a.spent = reinterpret_cast<unsigned long long*>(base + y.status + 8);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  HIP_TRY(hipMemsetAsync(base + y.status, 0, 16, s));
+  HIP_TRY(tasp::launch_build_mask(a, base + y.temp, y.temp_bytes,
+                                  reinterpret_cast<double*>(base + y.keys_in),
+                                  reinterpret_cast<double*>(base + y.keys_out),
+                                  reinterpret_cast<int*>(base + y.idx_in),
+                                  reinterpret_cast<int*>(base + y.idx_out), s));
+  uint64_t word[2] = {0, 0};
+  HIP_TRY(hipMemcpyAsync(word, base + y.status, 16, hipMemcpyDeviceToHost, s));
+  HIP_TRY(hipStreamSynchronize(s));
+  if (word[0] & 1u) return fail(TASP_ERR_INVALID_ARG, "non-finite score");
+  if (flops_spent) *flops_spent = word[1];
+  return TASP_OK;
+}
+
 tasp_status tasp_copy_probe(void* dst, const void* src, size_t bytes, void* stream) {
   if (!dst || !src) return fail(TASP_ERR_INVALID_ARG, "dst / src is NULL");
   if (bytes % 16) return fail(TASP_ERR_INVALID_ARG, "bytes %% 16 != 0");

@@ -158,3 +158,19 @@ class Plan:
     def prefill_timed(self, x, T, cache, pos0, out, stream=None):
         return B.tasp_prefill_timed(self.handle, x.data_ptr(), T, cache.struct, pos0, out.data_ptr(),
                                     stream if stream is not None else current_stream())
+
+
+def build_mask(desc, head_scores, chan_scores, granule, target, stream=None):
+    """Greedy dependency-closed mask from device float32 scores ([L][Hq], [L][d_ffn/granule]).
+    Returns (q_keep, kv_keep, ffn_keep) as device uint8 tensors and the FLOPs spent."""
+    dev = head_scores.device
+    n = B.tasp_mask_workspace_bytes(desc, granule)
+    ws = torch.empty(n + 256, dtype=torch.uint8, device=dev)
+    base = ws.data_ptr() + (-ws.data_ptr()) % 256
+    q = torch.empty((desc.n_layers, desc.n_q_heads), dtype=torch.uint8, device=dev)
+    kv = torch.empty((desc.n_layers, desc.n_kv_heads), dtype=torch.uint8, device=dev)
+    f = torch.empty((desc.n_layers, desc.d_ffn), dtype=torch.uint8, device=dev)
+    spent = B.tasp_build_mask(desc, head_scores.data_ptr(), chan_scores.data_ptr(), granule, target,
+                              base, n, q.data_ptr(), kv.data_ptr(), f.data_ptr(),
+                              stream if stream is not None else current_stream())
+    return q, kv, f, spent

@@ -53,6 +53,8 @@ class Workload:
     prefill_tokens: int = 0
     mask_seeds: tuple = (1,)
     include_dense: bool = True
+    kind: str = "decode"    # "decode" (decode / prefill steps) or "mask" (mask construction)
+    granule: int = 1024     # SwiGLU channels per candidate group (mask construction)
 
 
 WORKLOADS = {
@@ -70,6 +72,10 @@ WORKLOADS = {
     # one 8B-shaped layer: 512-token prefill from an empty cache
     "llama3_8b_prefill512": Workload("llama3_8b_prefill512", LLAMA3_8B.with_layers(1, vocab=0),
                                      batch=1, pos=0, prefill_tokens=512, mask_seeds=(1,)),
+    # greedy mask construction over the 80-layer 70B candidate set (64 heads + 28 groups of
+    # 1024 channels per layer, 7360 candidates) at the 0.57 active-FLOP target
+    "llama3_70b_mask": Workload("llama3_70b_mask", LLAMA3_70B, batch=0, pos=0, kind="mask",
+                                granule=1024),
     # one 8B-shaped layer: batch-8 decode, every sequence at 8192 prior positions
     "llama3_8b_batch8": Workload("llama3_8b_batch8", LLAMA3_8B.with_layers(1, vocab=0),
                                  batch=8, pos=8192, mask_seeds=(1,)),

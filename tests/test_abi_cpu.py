@@ -117,3 +117,17 @@ def test_calls_on_null_plan_fail_cleanly():
     assert lib.tasp_plan_ledger(None, None, None, None, None) == -1
     assert lib.tasp_copy_probe(None, None, 16, None) == -1
     assert lib.tasp_status_string(-6) == b"KV cache belongs to another plan"
+
+
+def test_mask_workspace_and_granule_checks():
+    _lib()
+    d = _desc(n_layers=3, d_ffn=2048)
+    small = B.tasp_mask_workspace_bytes(d, 1024)
+    big = B.tasp_mask_workspace_bytes(d, 128)
+    assert big > small > 0                                   # more candidates, more workspace
+    with pytest.raises(B.TaspError) as e:
+        B.tasp_mask_workspace_bytes(d, 1000)                 # does not divide d_ffn
+    assert B.STATUS[e.value.status] == "TASP_ERR_SHAPE"
+    with pytest.raises(B.TaspError) as e:
+        B.tasp_mask_workspace_bytes(d, 0)
+    assert B.STATUS[e.value.status] == "TASP_ERR_SHAPE"
