@@ -292,3 +292,36 @@ def decode_bytes(sh, counts, batch, pos, lm_head=False):
     kv = int(sum(batch * b * (pos + 1) * dh * 2 * 2 for b in m_kv))
     lm = 2 * sh.vocab * d if lm_head else 0
     return {"weights": int(w), "scales": s, "kv": kv, "lm_head": lm, "total": int(w) + s + kv + lm}
+
+
+# ------------------------------------------------------------------------ request loop
+
+def embed_rows(table, scales, ids):
+    """Token embedding: row id of the INT8 table times its float32 scale (the INT8 store keeps the
+    embedding dense, Sec. "Dependency-Closed Masks and Cache-Consistent Routing")."""
+    ids = np.asarray(ids)
+    return table[ids].astype(np.float64) * scales[ids].astype(np.float64)[:, None]
+
+
+def greedy_token(logits_row):
+    """Greedy decoding: the highest logit, the lowest id among equal ones."""
+    return int(np.argmax(logits_row))
+
+
+def generate(layer_source, closed_mask, table, scales, prompt, n_new, caches, sh,
+             final_norm_bits, lm_head_bits, kv_store=bf16_store):
+    """A request under one fixed plan (Sec. "Dependency-Closed Masks and Cache-Consistent
+    Routing"; the timed request of Table "configuration"): prefill the prompt, take the greedy
+    token of its last position, then n_new decode steps, each feeding the previous token at the
+    next position. Returns the n_new + 1 generated ids and the logits they were taken from."""
+    T = len(prompt)
+    logits = prefill_stack(layer_source, closed_mask, embed_rows(table, scales, prompt), caches, 0,
+                           sh, final_norm_bits, lm_head_bits, kv_store)
+    toks, rows = [greedy_token(logits[-1])], [logits[-1]]
+    for s_ in range(n_new):
+        lg = decode_stack(layer_source, closed_mask, embed_rows(table, scales, [toks[-1]]),
+                          [(K[None], V[None]) for K, V in caches], T + s_, sh, final_norm_bits,
+                          lm_head_bits, kv_store)
+        toks.append(greedy_token(lg[0]))
+        rows.append(lg[0])
+    return np.array(toks), np.array(rows)

@@ -21,7 +21,7 @@ from .configs import Shape
 __all__ = [
     "WEIGHT_NAMES", "to_bf16_bits", "bf16_bits_to_f32", "bf16_round", "quantize_rows",
     "layer_weights", "final_norm", "lm_head", "activations", "kv_prior", "tiny_mask",
-    "budget_mask", "raw_mask", "all_kept_mask", "mask_counts",
+    "budget_mask", "raw_mask", "all_kept_mask", "mask_counts", "embedding", "prompt_ids",
 ]
 
 WEIGHT_NAMES = ("wq", "wk", "wv", "wo", "wg", "wu", "wd")
@@ -100,6 +100,18 @@ def lm_head(sh: Shape, seed_w: int = 0, std: float = 0.02) -> np.ndarray:
     w = rng.standard_normal((sh.vocab, sh.d_model), dtype=np.float32)
     w *= np.float32(std)
     return to_bf16_bits(w)
+
+
+def embedding(sh: Shape, seed_w: int = 0):
+    """INT8 token embedding ``(int8 [V][d], float32 [V])``: N(0, 1) rows quantised per row."""
+    rng = np.random.default_rng([seed_w, sh.n_layers, 2])
+    w = rng.standard_normal((sh.vocab, sh.d_model), dtype=np.float32)
+    return quantize_rows(w)
+
+
+def prompt_ids(n: int, vocab: int, seed: int = 4) -> np.ndarray:
+    """Seeded prompt token ids, int32 [n], uniform over the vocabulary."""
+    return np.random.default_rng([seed]).integers(0, vocab, n).astype(np.int32)
 
 
 def activations(n_rows: int, d: int, seed_x: int = 1) -> np.ndarray:
