@@ -182,6 +182,22 @@ tasp_status tasp_decode_step(tasp_plan plan, const float* x, tasp_kv_cache* cach
 tasp_status tasp_prefill(tasp_plan plan, const float* x, int32_t T, tasp_kv_cache* cache,
                          int32_t pos0, float* out, void* stream);
 
+/* One request under the plan (paper, Sec. "Dependency-Closed Masks and Cache-Consistent Routing":
+ * the plan stays fixed through prefill and every decode step; Table "configuration": the timed
+ * request is a prefill followed by greedy decoding). The prompt's ids (device int32 [T]) are
+ * embedded from the dense INT8 table (device int8 [vocab][d_model] with float32 row scales
+ * [vocab]), prefilled at positions 0..T-1 (binding the cache), and the greedy id of the last
+ * position goes to out_ids[0]; then n_new decode steps feed out_ids[i] at position T + i and
+ * write the greedy id of its logits to out_ids[i + 1]. Greedy = highest logit, lowest id on ties;
+ * ids stay on the device, so nothing waits for the host between tokens.
+ *   Requires an LM head (else TASP_ERR_UNSUPPORTED), cache batch 1, 1 <= T <= max_prefill and
+ *   T + n_new <= cache->max_seq (else TASP_ERR_POS_RANGE).
+ *   out_ids: device int32 [n_new + 1]; x_scratch: device float32 [T][d_model]; logits: device
+ *   float32 [T][vocab] (holds the last step's logits afterwards). Stream-ordered. */
+tasp_status tasp_generate(tasp_plan plan, const int8_t* embed, const float* embed_scale,
+                          const int32_t* prompt, int32_t T, int32_t n_new, tasp_kv_cache* cache,
+                          int32_t* out_ids, float* x_scratch, float* logits, void* stream);
+
 /* Profiling variant of tasp_prefill: an event pair around every kernel; kinds as for
  * tasp_decode_step_timed, plus 7 for the RoPE / cache-append kernel. Synchronises `stream`. */
 tasp_status tasp_prefill_timed(tasp_plan plan, const float* x, int32_t T, tasp_kv_cache* cache,

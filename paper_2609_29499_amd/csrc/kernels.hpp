@@ -136,6 +136,14 @@ struct PfAttnArgs {
 };
 hipError_t launch_pf_attn(const PfAttnArgs& a, hipStream_t s);
 
+// ----------------------------------------------------------------- request loop
+
+// x[t] = scale[ids[t]] * table[ids[t]] for t < n (NaN rows for ids outside [0, V)); d % 4 == 0
+hipError_t launch_embed(const int8_t* table, const float* scale, int V, int d, const int* ids,
+                        int n, float* x, hipStream_t s);
+// ids_out[r] = argmax of logits row r of n rows of V (lowest id among equal maxima)
+hipError_t launch_argmax(const float* logits, int n, int V, int* ids_out, hipStream_t s);
+
 // ----------------------------------------------------------------- mask construction
 
 struct MaskArgs {

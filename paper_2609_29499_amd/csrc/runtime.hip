@@ -1063,6 +1063,31 @@ tasp_status tasp_profile_stage(const tasp_plan* plans, const tasp_kv_cache* cach
   return TASP_OK;
 }
 
+tasp_status tasp_generate(tasp_plan p, const int8_t* embed, const float* embed_scale,
+                          const int32_t* prompt, int32_t T, int32_t n_new, tasp_kv_cache* cache,
+                          int32_t* out_ids, float* x_scratch, float* logits, void* stream) {
+  if (!p) return fail(TASP_ERR_INVALID_ARG, "plan is NULL");
+  const tasp_model_desc& d = p->desc;
+  if (d.vocab < 1) return fail(TASP_ERR_UNSUPPORTED, "plan has no LM head");
+  if (!embed || !embed_scale || !prompt || !out_ids || !x_scratch || !logits)
+    return fail(TASP_ERR_INVALID_ARG, "embedding / prompt / outputs / scratch is NULL");
+  if (n_new < 0) return fail(TASP_ERR_INVALID_ARG, "n_new < 0");
+  tasp_status st = check_cache(p, cache);
+  if (st != TASP_OK) return st;
+  if (long(T) + n_new > cache->max_seq)
+    return fail(TASP_ERR_POS_RANGE, "prompt + new tokens (%d + %d) beyond the cache", T, n_new);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  HIP_TRY(tasp::launch_embed(embed, embed_scale, d.vocab, d.d_model, prompt, T, x_scratch, s));
+  if ((st = prefill_checked(p, x_scratch, T, cache, 0, logits, stream, nullptr)) != TASP_OK) return st;
+  HIP_TRY(tasp::launch_argmax(logits + size_t(T - 1) * d.vocab, 1, d.vocab, out_ids, s));
+  for (int i = 0; i < n_new; ++i) {
+    HIP_TRY(tasp::launch_embed(embed, embed_scale, d.vocab, d.d_model, out_ids + i, 1, x_scratch, s));
+    if ((st = decode_impl(p, x_scratch, cache, T + i, logits, stream, nullptr)) != TASP_OK) return st;
+    HIP_TRY(tasp::launch_argmax(logits, 1, d.vocab, out_ids + i + 1, s));
+  }
+  return TASP_OK;
+}
+
 // ---- greedy mask construction
 
 namespace {

@@ -155,6 +155,20 @@ class Plan:
         B.tasp_prefill(self.handle, x.data_ptr(), T, cache.struct, pos0, out.data_ptr(),
                        stream if stream is not None else current_stream())
 
+    def generate(self, embed, embed_scale, prompt, n_new, cache, stream=None, scratch=None):
+        """Prompt ids (device int32 [T]) -> n_new + 1 greedy ids (device int32). ``scratch`` may
+        pass (x [T][d], logits [T][vocab]) float32 device tensors to reuse."""
+        T = int(prompt.numel())
+        dev = prompt.device
+        if scratch is None:
+            scratch = (torch.empty((T, self.desc.d_model), device=dev),
+                       torch.empty((T, self.desc.vocab), device=dev))
+        out = torch.empty(n_new + 1, dtype=torch.int32, device=dev)
+        B.tasp_generate(self.handle, embed.data_ptr(), embed_scale.data_ptr(), prompt.data_ptr(), T,
+                        n_new, cache.struct, out.data_ptr(), scratch[0].data_ptr(),
+                        scratch[1].data_ptr(), stream if stream is not None else current_stream())
+        return out
+
     def prefill_timed(self, x, T, cache, pos0, out, stream=None):
         return B.tasp_prefill_timed(self.handle, x.data_ptr(), T, cache.struct, pos0, out.data_ptr(),
                                     stream if stream is not None else current_stream())

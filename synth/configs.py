@@ -53,7 +53,9 @@ class Workload:
     prefill_tokens: int = 0
     mask_seeds: tuple = (1,)
     include_dense: bool = True
-    kind: str = "decode"    # "decode" (decode / prefill steps) or "mask" (mask construction)
+    kind: str = "decode"    # "decode" (decode / prefill steps), "mask" (mask construction),
+                            # "request" (prefill of prefill_tokens, then n_new greedy decode steps)
+    n_new: int = 0
     granule: int = 1024     # SwiGLU channels per candidate group (mask construction)
 
 
@@ -72,6 +74,11 @@ WORKLOADS = {
     # one 8B-shaped layer: 512-token prefill from an empty cache
     "llama3_8b_prefill512": Workload("llama3_8b_prefill512", LLAMA3_8B.with_layers(1, vocab=0),
                                      batch=1, pos=0, prefill_tokens=512, mask_seeds=(1,)),
+    # the paper's timed request: 2048-token prompt, then 256 greedy decode steps, one plan
+    "llama3_8b_request": Workload("llama3_8b_request", LLAMA3_8B, batch=1, pos=0,
+                                  prefill_tokens=2048, kind="request", n_new=256),
+    "llama3_70b_request": Workload("llama3_70b_request", LLAMA3_70B, batch=1, pos=0,
+                                   prefill_tokens=2048, kind="request", n_new=256),
     # greedy mask construction over the 80-layer 70B candidate set (64 heads + 28 groups of
     # 1024 channels per layer, 7360 candidates) at the 0.57 active-FLOP target
     "llama3_70b_mask": Workload("llama3_70b_mask", LLAMA3_70B, batch=0, pos=0, kind="mask",
