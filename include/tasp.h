@@ -248,6 +248,90 @@ tasp_status tasp_build_mask(const tasp_model_desc* desc, const float* head_score
                             uint8_t* kv_keep, uint8_t* ffn_keep, uint64_t* flops_spent,
                             void* stream);
 
+/* ---- routing (paper, Sec. "Dependency-Closed Masks and Cache-Consistent Routing": a three-layer
+ * MLP router picks one task plan per user turn, or the dense plan when its temperature-scaled
+ * confidence is below tau; appendix "Router feature specification": the feature vector).
+ *
+ * Feature vector of a prompt (float32, proj_dim + 11 entries, in this order):
+ *   [0, proj_dim)  proj x tf, tf[bin] = (number of the prompt's byte trigrams, ASCII letters
+ *                  case-folded, whose 32-bit FNV-1a hash is bin modulo n_bins) / max(1, bytes - 2);
+ *   then ln(1 + bytes), the proxy-LM mean token log-probability (an input), ln(1 + count) of
+ *   digits, of operators (+ - * / = < > % ^), of code punctuation ({ } [ ] ( ) ; _ # ` \ | &) and
+ *   of question marks, and five 0/1 descriptors: numbered list (a line opening with 1-3 digits,
+ *   '.' or ')', a space), code fence (three backticks), translate cue ("translat", case-folded),
+ *   multiple-choice pattern (lines opening with option labels A and B, as "X.", "X)" or "(X)"
+ *   then a space), retrieval cue (case-folded who / when / where / which at a word start and
+ *   not followed by a letter).
+ * MLP: h1 = ReLU(w1 f + b1), h2 = ReLU(w2 h1 + b2), z = w3 h2 + b3; p = softmax(z / temperature);
+ * choice = the lowest task index of max p, or -1 (dense plan) when max p < tau. float32
+ * arithmetic; the text scan is integer. */
+#define TASP_ROUTER_SCALARS 11
+#define TASP_ROUTER_MAX_TASKS 16
+#define TASP_ROUTER_MAX_BINS 16384
+
+typedef struct {
+  int32_t n_bins;       /* hashed trigram bins (paper: 2,048), 1..16384 */
+  int32_t proj_dim;     /* width of the frozen random projection (paper: 256), >= 1 */
+  int32_t hidden1;      /* MLP hidden widths (paper: 512 and 256), >= 1 */
+  int32_t hidden2;
+  int32_t n_tasks;      /* task plans (paper: 5), 1..16 */
+  float temperature;    /* > 0; divides the logits */
+  float tau;            /* confidence threshold of the dense fallback (paper: 0.85) */
+  const float* proj;    /* device float32 [proj_dim][n_bins] */
+  const float* w1;      /* device float32 [hidden1][proj_dim + 11] */
+  const float* b1;      /* [hidden1] */
+  const float* w2;      /* [hidden2][hidden1] */
+  const float* b2;      /* [hidden2] */
+  const float* w3;      /* [n_tasks][hidden2] */
+  const float* b3;      /* [n_tasks] */
+} tasp_router;
+
+/* Device workspace bytes for routing n_prompts prompts (also covers tasp_serve_turn with
+ * n_prompts = 1). */
+tasp_status tasp_router_workspace_bytes(const tasp_router* router, int32_t n_prompts,
+                                        size_t* bytes);
+
+/* Route n_prompts prompts. text (device bytes, n_text of them) holds the prompts back to back;
+ * offsets (device int32 [n_prompts + 1]) bounds prompt i as [offsets[i], offsets[i + 1]), each
+ * bound clamped to [0, n_text] on the device (a decreasing pair is an empty prompt); offsets NULL
+ * means one prompt, the whole text (n_prompts must be 1). proxy_logprob: device float32
+ * [n_prompts]. Outputs (device): features float32 [n_prompts][proj_dim + 11] (may be NULL),
+ * probs float32 [n_prompts][n_tasks], choice int32 [n_prompts]. workspace: device, 256-byte
+ * aligned, at least tasp_router_workspace_bytes. Stream-ordered and asynchronous (five kernels,
+ * no allocation), so it may be captured into a HIP graph. Errors: TASP_ERR_INVALID_ARG for NULL
+ * pointers, sizes out of range (n_prompts 1..65535, n_text >= 0) or a temperature <= 0;
+ * TASP_ERR_WORKSPACE for a short workspace. */
+tasp_status tasp_route(const tasp_router* router, const uint8_t* text, int32_t n_text,
+                       const int32_t* offsets, int32_t n_prompts, const float* proxy_logprob,
+                       void* workspace, size_t workspace_bytes, float* features, float* probs,
+                       int32_t* choice, void* stream);
+
+/* One user turn with routing and dispatch (paper, Sec. "Dependency-Closed Masks and
+ * Cache-Consistent Routing": the decision is made once per turn, the chosen plan serves the
+ * turn's prefill and every decode step, and a KV cache is never reused across different masks).
+ *   1. routes the turn's text (device bytes [n_text], one prompt) with proxy_logprob (device
+ *      float32 [1]) and waits for the decision (this synchronises `stream`);
+ *   2. takes task_plans[choice], or dense_plan for choice -1 (all n_tasks + 1 plans must share
+ *      one model shape with an LM head);
+ *   3. if 0 < n_cached < T and the cache is bound to the chosen plan, its rows 0..n_cached-1 (the
+ *      conversation so far, written under that plan) are kept and prompt ids n_cached..T-1 are
+ *      prefilled at those positions (*reused = 1); otherwise the cache is invalidated: all T ids
+ *      are prefilled from position 0 and the cache is bound to the chosen plan (*reused = 0);
+ *   4. decodes greedily as tasp_generate: out_ids[0] from the last prompt position, then n_new
+ *      steps. After the turn the cache holds T + n_new valid rows (the last id is not fed).
+ *   prompt: device int32 [T] (the whole conversation's ids); x_scratch: device float32
+ *   [T][d_model]; logits: device float32 [T][vocab]; out_ids: device int32 [n_new + 1];
+ *   workspace: tasp_router_workspace_bytes(router, 1). *chosen receives the choice (-1 dense).
+ *   Errors as tasp_route and tasp_generate; T - prefilled start must fit the plan's max_prefill. */
+tasp_status tasp_serve_turn(const tasp_router* router, const tasp_plan* task_plans,
+                            tasp_plan dense_plan, const uint8_t* text, int32_t n_text,
+                            const float* proxy_logprob, const int8_t* embed,
+                            const float* embed_scale, const int32_t* prompt, int32_t T,
+                            int32_t n_cached, int32_t n_new, tasp_kv_cache* cache,
+                            int32_t* out_ids, float* x_scratch, float* logits, void* workspace,
+                            size_t workspace_bytes, int32_t* chosen, int32_t* reused,
+                            void* stream);
+
 /* Plain streaming copy of `bytes` (multiple of 16) from src to dst (device): the reference kernel
  * whose counter readings calibrate memory-traffic measurements. */
 tasp_status tasp_copy_probe(void* dst, const void* src, size_t bytes, void* stream);

@@ -26,7 +26,8 @@ EXPORTS = ["tasp_plan_workspace_bytes", "tasp_compile_plan", "tasp_plan_counts",
            "tasp_plan_indices", "tasp_plan_panel", "tasp_plan_ledger", "tasp_plan_destroy",
            "tasp_kv_bind", "tasp_decode_step", "tasp_prefill", "tasp_prefill_timed", "tasp_generate",
            "tasp_decode_step_timed",
-           "tasp_profile_stage", "tasp_mask_workspace_bytes", "tasp_build_mask", "tasp_copy_probe",
+           "tasp_profile_stage", "tasp_mask_workspace_bytes", "tasp_build_mask",
+           "tasp_router_workspace_bytes", "tasp_route", "tasp_serve_turn", "tasp_copy_probe",
            "tasp_status_string", "tasp_last_error"]
 
 
@@ -68,6 +69,15 @@ class tasp_kv_cache(C.Structure):
                 ("max_seq", C.c_int32), ("plan_sig", C.c_uint64)]
 
 
+class tasp_router(C.Structure):
+    _fields_ = [("n_bins", C.c_int32), ("proj_dim", C.c_int32), ("hidden1", C.c_int32),
+                ("hidden2", C.c_int32), ("n_tasks", C.c_int32), ("temperature", C.c_float),
+                ("tau", C.c_float), ("proj", C.c_void_p), ("w1", C.c_void_p), ("b1", C.c_void_p),
+                ("w2", C.c_void_p), ("b2", C.c_void_p), ("w3", C.c_void_p), ("b3", C.c_void_p)]
+
+
+ROUTER_SCALARS = 11
+
 _lib = None
 
 
@@ -104,6 +114,11 @@ def load(path: str = LIB_PATH):
         "tasp_mask_workspace_bytes": [C.POINTER(tasp_model_desc), I32, C.POINTER(SZ)],
         "tasp_build_mask": [C.POINTER(tasp_model_desc), P, P, I32, C.c_double, P, SZ, P, P, P,
                             C.POINTER(U64), P],
+        "tasp_router_workspace_bytes": [C.POINTER(tasp_router), I32, C.POINTER(SZ)],
+        "tasp_route": [C.POINTER(tasp_router), P, I32, P, I32, P, P, SZ, P, P, P, P],
+        "tasp_serve_turn": [C.POINTER(tasp_router), C.POINTER(P), P, P, I32, P, P, P, P, I32, I32,
+                            I32, C.POINTER(tasp_kv_cache), P, P, P, P, SZ, C.POINTER(I32),
+                            C.POINTER(I32), P],
         "tasp_copy_probe": [P, P, SZ, P],
     }
     for name, args in sig.items():
@@ -229,6 +244,33 @@ def tasp_build_mask(desc, head_scores_ptr, chan_scores_ptr, granule, target, ws_
     _check(load().tasp_build_mask(C.byref(desc), head_scores_ptr, chan_scores_ptr, granule, target,
                                   ws_ptr, ws_bytes, q_ptr, kv_ptr, f_ptr, C.byref(spent), stream))
     return spent.value
+
+
+def tasp_router_workspace_bytes(router, n_prompts):
+    n = C.c_size_t()
+    _check(load().tasp_router_workspace_bytes(C.byref(router), n_prompts, C.byref(n)))
+    return n.value
+
+
+def tasp_route(router, text_ptr, n_text, offsets_ptr, n_prompts, logprob_ptr, ws_ptr, ws_bytes,
+               feats_ptr, probs_ptr, choice_ptr, stream):
+    _check(load().tasp_route(C.byref(router), text_ptr, n_text, offsets_ptr, n_prompts,
+                             logprob_ptr, ws_ptr, ws_bytes, feats_ptr, probs_ptr, choice_ptr,
+                             stream))
+
+
+def tasp_serve_turn(router, task_plans, dense_plan, text_ptr, n_text, logprob_ptr, embed_ptr,
+                    scale_ptr, prompt_ptr, T, n_cached, n_new, cache, out_ids_ptr, x_ptr,
+                    logits_ptr, ws_ptr, ws_bytes, stream):
+    """Returns (choice, reused)."""
+    arr = (C.c_void_p * len(task_plans))(
+        *[p.value if isinstance(p, C.c_void_p) else p for p in task_plans])
+    chosen, reused = C.c_int32(), C.c_int32()
+    _check(load().tasp_serve_turn(C.byref(router), arr, dense_plan, text_ptr, n_text, logprob_ptr,
+                                  embed_ptr, scale_ptr, prompt_ptr, T, n_cached, n_new,
+                                  C.byref(cache), out_ids_ptr, x_ptr, logits_ptr, ws_ptr, ws_bytes,
+                                  C.byref(chosen), C.byref(reused), stream))
+    return chosen.value, reused.value
 
 
 def tasp_copy_probe(dst_ptr, src_ptr, nbytes, stream):

@@ -183,4 +183,38 @@ hipError_t launch_attn_decode(const AttnArgs& a, hipStream_t s);
 int attn_min_chunk();   // rows per split are a multiple of this
 int attn_max_split();
 
+// ----------------------------------------------------------------- router
+
+constexpr int kMaxRouterTasks = 16;
+constexpr int kMaxRouterBins = 16384;
+constexpr int kRouterScalars = 11;     // length, log-prob, 4 character counts, 5 descriptors
+
+struct RouterFeatArgs {
+  const uint8_t* text; int n_text;     // all prompts' bytes
+  const int* offsets;                  // [n + 1] prompt bounds, clamped to [0, n_text]; null: one
+                                       // prompt spanning the whole text
+  const float* logprob;                // [n] proxy-LM mean token log-probabilities
+  int n_bins, proj_dim;
+  float* tf;                           // [n][n_bins] trigram term frequencies
+  float* feats; int ld_feats;          // [n][ld_feats]; the scalars go to columns proj_dim ..
+};
+// y[b][j] = act(w[j] . x[b] + bias[j]) for j < N, b < B; w [N][K], bias [N] or null, act ReLU
+// when relu != 0
+struct RouterDenseArgs {
+  const float* w; const float* bias; int N, K;
+  const float* x; int ldx;
+  float* y; int ldy;
+  int B, relu;
+};
+struct RouterHeadArgs {
+  const float* w; const float* bias; int n_tasks, K;   // w [n_tasks][K]
+  const float* h;                                      // [n][K]
+  float temperature, tau;
+  float* probs; int* choice;                           // [n][n_tasks], [n]
+};
+size_t router_features_lds_bytes(int n_bins);
+hipError_t launch_router_features(const RouterFeatArgs& a, int n_prompts, hipStream_t s);
+hipError_t launch_router_dense(const RouterDenseArgs& a, hipStream_t s);
+hipError_t launch_router_head(const RouterHeadArgs& a, int n_prompts, hipStream_t s);
+
 }  // namespace tasp

@@ -1063,29 +1063,177 @@ tasp_status tasp_profile_stage(const tasp_plan* plans, const tasp_kv_cache* cach
   return TASP_OK;
 }
 
-tasp_status tasp_generate(tasp_plan p, const int8_t* embed, const float* embed_scale,
-                          const int32_t* prompt, int32_t T, int32_t n_new, tasp_kv_cache* cache,
-                          int32_t* out_ids, float* x_scratch, float* logits, void* stream) {
+namespace {
+
+// prompt ids pos0..T-1 are embedded and prefilled at those positions (pos0 == 0 binds the
+// cache), then n_new greedy decode steps
+tasp_status generate_impl(tasp_plan p, const int8_t* embed, const float* embed_scale,
+                          const int32_t* prompt, int32_t T, int32_t pos0, int32_t n_new,
+                          tasp_kv_cache* cache, int32_t* out_ids, float* x_scratch, float* logits,
+                          void* stream) {
   if (!p) return fail(TASP_ERR_INVALID_ARG, "plan is NULL");
   const tasp_model_desc& d = p->desc;
   if (d.vocab < 1) return fail(TASP_ERR_UNSUPPORTED, "plan has no LM head");
   if (!embed || !embed_scale || !prompt || !out_ids || !x_scratch || !logits)
     return fail(TASP_ERR_INVALID_ARG, "embedding / prompt / outputs / scratch is NULL");
   if (n_new < 0) return fail(TASP_ERR_INVALID_ARG, "n_new < 0");
+  if (pos0 < 0 || (pos0 > 0 && pos0 >= T))
+    return fail(TASP_ERR_INVALID_ARG, "prefill start %d outside [0, %d)", pos0, T);
   tasp_status st = check_cache(p, cache);
   if (st != TASP_OK) return st;
   if (long(T) + n_new > cache->max_seq)
     return fail(TASP_ERR_POS_RANGE, "prompt + new tokens (%d + %d) beyond the cache", T, n_new);
   hipStream_t s = static_cast<hipStream_t>(stream);
-  HIP_TRY(tasp::launch_embed(embed, embed_scale, d.vocab, d.d_model, prompt, T, x_scratch, s));
-  if ((st = prefill_checked(p, x_scratch, T, cache, 0, logits, stream, nullptr)) != TASP_OK) return st;
-  HIP_TRY(tasp::launch_argmax(logits + size_t(T - 1) * d.vocab, 1, d.vocab, out_ids, s));
+  const int n = T - pos0;
+  HIP_TRY(tasp::launch_embed(embed, embed_scale, d.vocab, d.d_model, prompt + pos0, n, x_scratch, s));
+  if ((st = prefill_checked(p, x_scratch, n, cache, pos0, logits, stream, nullptr)) != TASP_OK) return st;
+  HIP_TRY(tasp::launch_argmax(logits + size_t(n - 1) * d.vocab, 1, d.vocab, out_ids, s));
   for (int i = 0; i < n_new; ++i) {
     HIP_TRY(tasp::launch_embed(embed, embed_scale, d.vocab, d.d_model, out_ids + i, 1, x_scratch, s));
     if ((st = decode_impl(p, x_scratch, cache, T + i, logits, stream, nullptr)) != TASP_OK) return st;
     HIP_TRY(tasp::launch_argmax(logits, 1, d.vocab, out_ids + i + 1, s));
   }
   return TASP_OK;
+}
+
+}  // namespace
+
+tasp_status tasp_generate(tasp_plan p, const int8_t* embed, const float* embed_scale,
+                          const int32_t* prompt, int32_t T, int32_t n_new, tasp_kv_cache* cache,
+                          int32_t* out_ids, float* x_scratch, float* logits, void* stream) {
+  return generate_impl(p, embed, embed_scale, prompt, T, 0, n_new, cache, out_ids, x_scratch,
+                       logits, stream);
+}
+
+// ---- routing
+
+namespace {
+
+struct RouterLayout {
+  size_t tf, feats, h1, h2, probs1, choice1, total;
+  int feat_dim;
+};
+
+tasp_status router_layout(const tasp_router* r, int n, RouterLayout* y) {
+  if (!r) return fail(TASP_ERR_INVALID_ARG, "router is NULL");
+  if (r->n_bins < 1 || r->n_bins > tasp::kMaxRouterBins)
+    return fail(TASP_ERR_INVALID_ARG, "n_bins %d outside 1..%d", r->n_bins, tasp::kMaxRouterBins);
+  if (r->n_tasks < 1 || r->n_tasks > tasp::kMaxRouterTasks)
+    return fail(TASP_ERR_INVALID_ARG, "n_tasks %d outside 1..%d", r->n_tasks, tasp::kMaxRouterTasks);
+  if (r->proj_dim < 1 || r->hidden1 < 1 || r->hidden2 < 1 || r->proj_dim > (1 << 20) ||
+      r->hidden1 > (1 << 20) || r->hidden2 > (1 << 20))
+    return fail(TASP_ERR_INVALID_ARG, "router widths outside 1..2^20");
+  if (!(r->temperature > 0.0f) || !std::isfinite(r->temperature))
+    return fail(TASP_ERR_INVALID_ARG, "temperature must be finite and > 0");
+  if (!std::isfinite(r->tau)) return fail(TASP_ERR_INVALID_ARG, "tau is not finite");
+  if (!r->proj || !r->w1 || !r->b1 || !r->w2 || !r->b2 || !r->w3 || !r->b3)
+    return fail(TASP_ERR_INVALID_ARG, "router weight pointer is NULL");
+  if (n < 1 || n > 65535) return fail(TASP_ERR_INVALID_ARG, "n_prompts %d outside 1..65535", n);
+  y->feat_dim = r->proj_dim + tasp::kRouterScalars;
+  size_t off = 0;
+  auto take = [&](size_t bytes) { const size_t at = off; off = align_up(off + bytes, kAlign); return at; };
+  y->tf = take(size_t(n) * r->n_bins * 4);
+  y->feats = take(size_t(n) * y->feat_dim * 4);
+  y->h1 = take(size_t(n) * r->hidden1 * 4);
+  y->h2 = take(size_t(n) * r->hidden2 * 4);
+  y->probs1 = take(size_t(tasp::kMaxRouterTasks) * 4);
+  y->choice1 = take(4);
+  y->total = off;
+  return TASP_OK;
+}
+
+}  // namespace
+
+tasp_status tasp_router_workspace_bytes(const tasp_router* r, int32_t n, size_t* bytes) {
+  if (!bytes) return fail(TASP_ERR_INVALID_ARG, "bytes is NULL");
+  RouterLayout y;
+  tasp_status st = router_layout(r, n, &y);
+  if (st != TASP_OK) return st;
+  *bytes = y.total;
+  return TASP_OK;
+}
+
+tasp_status tasp_route(const tasp_router* r, const uint8_t* text, int32_t n_text,
+                       const int32_t* offsets, int32_t n, const float* proxy_logprob,
+                       void* workspace, size_t workspace_bytes, float* features, float* probs,
+                       int32_t* choice, void* stream) {
+  RouterLayout y;
+  tasp_status st = router_layout(r, n, &y);
+  if (st != TASP_OK) return st;
+  if (n_text < 0) return fail(TASP_ERR_INVALID_ARG, "n_text < 0");
+  if ((!text && n_text > 0) || !proxy_logprob || !probs || !choice || !workspace)
+    return fail(TASP_ERR_INVALID_ARG, "text / proxy_logprob / probs / choice / workspace is NULL");
+  if (!offsets && n != 1) return fail(TASP_ERR_INVALID_ARG, "offsets NULL with %d prompts", n);
+  if (reinterpret_cast<uintptr_t>(workspace) % kAlign)
+    return fail(TASP_ERR_WORKSPACE, "workspace is not 256-byte aligned");
+  if (workspace_bytes < y.total)
+    return fail(TASP_ERR_WORKSPACE, "workspace %zu < %zu bytes", workspace_bytes, y.total);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  char* ws = static_cast<char*>(workspace);
+  float* tf = reinterpret_cast<float*>(ws + y.tf);
+  float* feats = features ? features : reinterpret_cast<float*>(ws + y.feats);
+  float* h1 = reinterpret_cast<float*>(ws + y.h1);
+  float* h2 = reinterpret_cast<float*>(ws + y.h2);
+  tasp::RouterFeatArgs fa{};
+  fa.text = text; fa.n_text = n_text; fa.offsets = offsets; fa.logprob = proxy_logprob;
+  fa.n_bins = r->n_bins; fa.proj_dim = r->proj_dim; fa.tf = tf; fa.feats = feats;
+  fa.ld_feats = y.feat_dim;
+  HIP_TRY(tasp::launch_router_features(fa, n, s));
+  tasp::RouterDenseArgs pa{r->proj, nullptr, r->proj_dim, r->n_bins, tf, r->n_bins, feats,
+                           y.feat_dim, n, 0};
+  HIP_TRY(tasp::launch_router_dense(pa, s));
+  tasp::RouterDenseArgs l1{r->w1, r->b1, r->hidden1, y.feat_dim, feats, y.feat_dim, h1, r->hidden1, n, 1};
+  HIP_TRY(tasp::launch_router_dense(l1, s));
+  tasp::RouterDenseArgs l2{r->w2, r->b2, r->hidden2, r->hidden1, h1, r->hidden1, h2, r->hidden2, n, 1};
+  HIP_TRY(tasp::launch_router_dense(l2, s));
+  tasp::RouterHeadArgs ha{r->w3, r->b3, r->n_tasks, r->hidden2, h2, r->temperature, r->tau, probs, choice};
+  HIP_TRY(tasp::launch_router_head(ha, n, s));
+  return TASP_OK;
+}
+
+tasp_status tasp_serve_turn(const tasp_router* r, const tasp_plan* task_plans,
+                            tasp_plan dense_plan, const uint8_t* text, int32_t n_text,
+                            const float* proxy_logprob, const int8_t* embed,
+                            const float* embed_scale, const int32_t* prompt, int32_t T,
+                            int32_t n_cached, int32_t n_new, tasp_kv_cache* cache,
+                            int32_t* out_ids, float* x_scratch, float* logits, void* workspace,
+                            size_t workspace_bytes, int32_t* chosen, int32_t* reused,
+                            void* stream) {
+  RouterLayout y;
+  tasp_status st = router_layout(r, 1, &y);
+  if (st != TASP_OK) return st;
+  if (!task_plans || !dense_plan || !chosen || !reused)
+    return fail(TASP_ERR_INVALID_ARG, "plans / chosen / reused is NULL");
+  const tasp_model_desc& d0 = dense_plan->desc;
+  for (int t = 0; t < r->n_tasks; ++t) {
+    const tasp_plan q = task_plans[t];
+    if (!q) return fail(TASP_ERR_INVALID_ARG, "task plan %d is NULL", t);
+    const tasp_model_desc& d = q->desc;
+    if (d.n_layers != d0.n_layers || d.d_model != d0.d_model || d.n_q_heads != d0.n_q_heads ||
+        d.n_kv_heads != d0.n_kv_heads || d.head_dim != d0.head_dim || d.d_ffn != d0.d_ffn ||
+        d.vocab != d0.vocab)
+      return fail(TASP_ERR_SHAPE, "task plan %d has another model shape than the dense plan", t);
+  }
+  if (n_cached < 0) return fail(TASP_ERR_INVALID_ARG, "n_cached < 0");
+  if (!cache) return fail(TASP_ERR_INVALID_ARG, "cache is NULL");
+  char* ws = static_cast<char*>(workspace);
+  if (!ws) return fail(TASP_ERR_INVALID_ARG, "workspace is NULL");
+  float* probs = reinterpret_cast<float*>(ws + y.probs1);
+  int32_t* dchoice = reinterpret_cast<int32_t*>(ws + y.choice1);
+  if ((st = tasp_route(r, text, n_text, nullptr, 1, proxy_logprob, workspace, workspace_bytes,
+                       nullptr, probs, dchoice, stream)) != TASP_OK)
+    return st;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  int32_t c = 0;
+  HIP_TRY(hipMemcpyAsync(&c, dchoice, sizeof c, hipMemcpyDeviceToHost, s));
+  HIP_TRY(hipStreamSynchronize(s));
+  if (c < -1 || c >= r->n_tasks) return fail(TASP_ERR_INTERNAL, "router choice %d out of range", c);
+  const tasp_plan p = (c >= 0) ? task_plans[c] : dense_plan;
+  const bool keep = n_cached > 0 && n_cached < T && cache->plan_sig == p->sig;
+  *chosen = c;
+  *reused = keep ? 1 : 0;
+  return generate_impl(p, embed, embed_scale, prompt, T, keep ? n_cached : 0, n_new, cache,
+                       out_ids, x_scratch, logits, stream);
 }
 
 // ---- greedy mask construction

@@ -1,6 +1,6 @@
 """Summaries of rocprofv3 result databases for the library's kernels.
 
-    python -m paper_2609_29499_amd.profile_summary trace DB [--split KIND:GRID_X]
+    python -m paper_2609_29499_amd.profile_summary trace DB [--split KIND:GRID_X] [--by-grid]
         per-kernel dispatch count / mean / median / min duration (us); with --split the run is cut
         at the first dispatch of KIND with that grid size in work-items (the benchmark times the
         sparse plan first, then the dense one)
@@ -43,6 +43,11 @@ def kind_of(name: str) -> str | None:
         (r"pf_gemm_kernel<2,", "gateup_gemm"),
         (r"pf_gemm_kernel<1,", "resid_gemm"),
         (r"pf_gemm_kernel<3,", "lmhead_gemm"),
+        (r"router_features_kernel", "router_features"),
+        (r"router_dense_kernel", "router_dense"),
+        (r"router_head_kernel", "router_head"),
+        (r"embed_kernel", "embed"),
+        (r"argmax_kernel", "argmax"),
         (r"copy_kernel", "copy_probe"),
     ]
     for pat, k in rules:
@@ -64,7 +69,7 @@ def _named(kinds):
     return out
 
 
-def trace(db, split=None):
+def trace(db, split=None, by_grid=False):
     con = sqlite3.connect(db)
     rows = con.execute("select name, grid_x, start, end from kernels order by start").fetchall()
     kinds = _named([kind_of(r[0]) for r in rows])
@@ -78,11 +83,11 @@ def trace(db, split=None):
         if not k or k == "copy_probe":
             continue
         phase = "all" if t_split is None else ("second" if r[2] >= t_split else "first")
-        stats[(phase, k)].append((r[3] - r[2]) / 1000.0)
-    print("| phase | kernel | dispatches | mean us | median us | min us |")
-    print("|---|---|---|---|---|---|")
-    for (ph, k), v in stats.items():
-        print(f"| {ph} | {k} | {len(v)} | {statistics.mean(v):.2f} | {statistics.median(v):.2f} | {min(v):.2f} |")
+        stats[(phase, k, r[1] if by_grid else "")].append((r[3] - r[2]) / 1000.0)
+    print("| phase | kernel | grid | dispatches | mean us | median us | min us |")
+    print("|---|---|---|---|---|---|---|")
+    for (ph, k, g), v in stats.items():
+        print(f"| {ph} | {k} | {g} | {len(v)} | {statistics.mean(v):.2f} | {statistics.median(v):.2f} | {min(v):.2f} |")
 
 
 def _counter_rows(db):
@@ -141,6 +146,7 @@ def main():
     t = sub.add_parser("trace")
     t.add_argument("db")
     t.add_argument("--split")
+    t.add_argument("--by-grid", action="store_true", help="one row per (kernel, grid size)")
     f = sub.add_parser("traffic")
     f.add_argument("fetch_db")
     f.add_argument("write_db")
@@ -151,7 +157,7 @@ def main():
     p.add_argument("--grid", type=int, help="only dispatches of this grid size (work-items)")
     a = ap.parse_args()
     if a.cmd == "trace":
-        trace(a.db, a.split)
+        trace(a.db, a.split, a.by_grid)
     elif a.cmd == "traffic":
         import json
         print(json.dumps(traffic(a.fetch_db, a.write_db, a.kind), indent=1))

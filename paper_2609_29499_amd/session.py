@@ -188,3 +188,62 @@ def build_mask(desc, head_scores, chan_scores, granule, target, stream=None):
                               base, n, q.data_ptr(), kv.data_ptr(), f.data_ptr(),
                               stream if stream is not None else current_stream())
     return q, kv, f, spent
+
+
+class Router:
+    """Router weights on the device (float32 tensors keyed proj, w1, b1, w2, b2, w3, b3, row-major
+    [out][in]) and the ABI struct over them."""
+
+    def __init__(self, weights, temperature=1.0, tau=0.85, device="cuda"):
+        self.t = {k: torch.as_tensor(np.ascontiguousarray(v, np.float32)).to(device)
+                  for k, v in weights.items()}
+        proj_dim, n_bins = self.t["proj"].shape
+        self.struct = B.tasp_router(int(n_bins), int(proj_dim), int(self.t["w1"].shape[0]),
+                                    int(self.t["w2"].shape[0]), int(self.t["w3"].shape[0]),
+                                    float(temperature), float(tau),
+                                    *[self.t[k].data_ptr() for k in ("proj", "w1", "b1", "w2",
+                                                                      "b2", "w3", "b3")])
+        self.feat_dim = int(proj_dim) + B.ROUTER_SCALARS
+        self.n_tasks = int(self.t["w3"].shape[0])
+        self._ws = {}
+
+    def workspace(self, n, device):
+        """A 256-byte aligned workspace for n prompts: (tensor, base pointer, bytes)."""
+        if n not in self._ws:
+            nb = B.tasp_router_workspace_bytes(self.struct, n)
+            t = torch.empty(nb + 256, dtype=torch.uint8, device=device)
+            self._ws[n] = (t, t.data_ptr() + (-t.data_ptr()) % 256, nb)
+        return self._ws[n]
+
+    def route(self, text, offsets, logprob, stream=None, features=True):
+        """text: device uint8 [n_text]; offsets: device int32 [n + 1] (None: one prompt);
+        logprob: device float32 [n]. Returns (features or None, probs, choice) device tensors."""
+        n = int(logprob.numel())
+        dev = logprob.device
+        _, base, nb = self.workspace(n, dev)
+        feats = torch.empty((n, self.feat_dim), device=dev) if features else None
+        probs = torch.empty((n, self.n_tasks), device=dev)
+        choice = torch.empty(n, dtype=torch.int32, device=dev)
+        B.tasp_route(self.struct, text.data_ptr() if text.numel() else None, int(text.numel()),
+                     offsets.data_ptr() if offsets is not None else None, n, logprob.data_ptr(),
+                     base, nb, feats.data_ptr() if feats is not None else None, probs.data_ptr(),
+                     choice.data_ptr(), stream if stream is not None else current_stream())
+        return feats, probs, choice
+
+    def serve_turn(self, task_plans, dense_plan, text, logprob, embed, embed_scale, prompt,
+                   n_cached, n_new, cache, stream=None, scratch=None):
+        """One routed turn. Returns (choice, reused, out ids device int32 [n_new + 1])."""
+        T = int(prompt.numel())
+        dev = prompt.device
+        d = dense_plan.desc
+        if scratch is None:
+            scratch = (torch.empty((T, d.d_model), device=dev), torch.empty((T, d.vocab), device=dev))
+        out = torch.empty(n_new + 1, dtype=torch.int32, device=dev)
+        _, base, nb = self.workspace(1, dev)
+        c, reused = B.tasp_serve_turn(
+            self.struct, [p.handle for p in task_plans], dense_plan.handle,
+            text.data_ptr() if text.numel() else None, int(text.numel()), logprob.data_ptr(),
+            embed.data_ptr(), embed_scale.data_ptr(), prompt.data_ptr(), T, n_cached, n_new,
+            cache.struct, out.data_ptr(), scratch[0].data_ptr(), scratch[1].data_ptr(), base, nb,
+            stream if stream is not None else current_stream())
+        return c, reused, out

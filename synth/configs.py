@@ -54,7 +54,8 @@ class Workload:
     mask_seeds: tuple = (1,)
     include_dense: bool = True
     kind: str = "decode"    # "decode" (decode / prefill steps), "mask" (mask construction),
-                            # "request" (prefill of prefill_tokens, then n_new greedy decode steps)
+                            # "request" (prefill of prefill_tokens, then n_new greedy decode steps),
+                            # "router" (routing of user turns; the stack gives the path latencies)
     n_new: int = 0
     granule: int = 1024     # SwiGLU channels per candidate group (mask construction)
 
@@ -83,6 +84,11 @@ WORKLOADS = {
     # 1024 channels per layer, 7360 candidates) at the 0.57 active-FLOP target
     "llama3_70b_mask": Workload("llama3_70b_mask", LLAMA3_70B, batch=0, pos=0, kind="mask",
                                 granule=1024),
+    # the router (2048 hashed bins -> 256, MLP 512 / 256, 5 tasks) on 2048-token-sized prompts
+    # and a mix of the five task families; the mixture latency uses the sparse and dense decode
+    # of the 32-layer 8B stack at 4096 prior positions
+    "router_llama3_8b": Workload("router_llama3_8b", LLAMA3_8B, batch=1, pos=4096,
+                                 mask_seeds=(1,), kind="router"),
     # one 8B-shaped layer: batch-8 decode, every sequence at 8192 prior positions
     "llama3_8b_batch8": Workload("llama3_8b_batch8", LLAMA3_8B.with_layers(1, vocab=0),
                                  batch=8, pos=8192, mask_seeds=(1,)),

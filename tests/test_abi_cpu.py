@@ -131,3 +131,50 @@ def test_mask_workspace_and_granule_checks():
     with pytest.raises(B.TaspError) as e:
         B.tasp_mask_workspace_bytes(d, 0)
     assert B.STATUS[e.value.status] == "TASP_ERR_SHAPE"
+
+
+def _router(**kw):
+    base = dict(n_bins=2048, proj_dim=256, hidden1=512, hidden2=256, n_tasks=5, temperature=1.0,
+                tau=0.85)
+    base.update(kw)
+    fake = 4096                        # never dereferenced: every check runs before a launch
+    return B.tasp_router(base["n_bins"], base["proj_dim"], base["hidden1"], base["hidden2"],
+                         base["n_tasks"], base["temperature"], base["tau"], *([fake] * 7))
+
+
+def test_router_workspace_and_argument_checks():
+    _lib()
+    one = B.tasp_router_workspace_bytes(_router(), 1)
+    many = B.tasp_router_workspace_bytes(_router(), 64)
+    # term frequencies, features and both hidden layers per prompt, plus one prompt's decision
+    per = 4 * (2048 + 267 + 512 + 256)
+    assert one >= per and many >= 64 * per and many > one
+    for bad in (dict(n_bins=0), dict(n_bins=16385), dict(n_tasks=0), dict(n_tasks=17),
+                dict(temperature=0.0), dict(temperature=float("nan")), dict(hidden1=0),
+                dict(tau=float("inf"))):
+        with pytest.raises(B.TaspError) as e:
+            B.tasp_router_workspace_bytes(_router(**bad), 1)
+        assert B.STATUS[e.value.status] == "TASP_ERR_INVALID_ARG", bad
+    for n in (0, 65536):
+        with pytest.raises(B.TaspError):
+            B.tasp_router_workspace_bytes(_router(), n)
+    r = _router()
+    r.w2 = None
+    with pytest.raises(B.TaspError):
+        B.tasp_router_workspace_bytes(r, 1)
+    # tasp_route rejects before launching: short or misaligned workspace, missing offsets
+    r = _router()
+    nb = B.tasp_router_workspace_bytes(r, 2)
+    ws = 1 << 20
+    with pytest.raises(B.TaspError) as e:
+        B.tasp_route(r, 4096, 10, 4096, 2, 4096, ws, nb - 1, None, 4096, 4096, None)
+    assert B.STATUS[e.value.status] == "TASP_ERR_WORKSPACE"
+    with pytest.raises(B.TaspError) as e:
+        B.tasp_route(r, 4096, 10, 4096, 2, 4096, ws + 8, nb, None, 4096, 4096, None)
+    assert B.STATUS[e.value.status] == "TASP_ERR_WORKSPACE"
+    with pytest.raises(B.TaspError) as e:
+        B.tasp_route(r, 4096, 10, None, 2, 4096, ws, nb, None, 4096, 4096, None)
+    assert B.STATUS[e.value.status] == "TASP_ERR_INVALID_ARG"
+    with pytest.raises(B.TaspError) as e:
+        B.tasp_route(r, 4096, -1, None, 1, 4096, ws, nb, None, 4096, 4096, None)
+    assert B.STATUS[e.value.status] == "TASP_ERR_INVALID_ARG"
