@@ -632,8 +632,10 @@ def bench_router(args, wl):
     fitted = S.Router(w, temperature=temp, tau=0.85)
     _, probs, choice = fitted.route(btb, bto, blp, features=False)
     pmax = probs.max(dim=1).values.cpu().numpy()
-    usage = {f"{t:.2f}": round(float((pmax >= np.float32(t)).mean()), 4) for t in ROUTER_TAUS}
-    assert abs(usage["0.85"] - float((choice.cpu().numpy() >= 0).mean())) < 1e-9
+    used = {t: float((pmax >= np.float32(t)).mean()) for t in ROUTER_TAUS}
+    # the kernel's own decisions at tau = 0.85 agree with its probabilities
+    assert used[0.85] == float((choice.cpu().numpy() >= 0).mean())
+    usage = {f"{t:.2f}": round(u, 4) for t, u in used.items()}
     # the two path latencies the mixture is formed from
     rows = measure_stack(args, wl.shape, wl.pos, wl.mask_seeds)
     l_dense, l_sparse = rows[0]["ms_per_token"], rows[1]["ms_per_token"]

@@ -4,9 +4,10 @@
 // counts and five task descriptors; a three-layer MLP over it; temperature-scaled softmax; the
 // dense plan when the top probability is below tau.
 //
-//   1. router_features_kernel, one workgroup per prompt. The prompt is staged through LDS in
-//      chunks with a small halo on both sides (bytes outside the prompt read as zero, which no
-//      pattern byte equals). Every position is examined by one thread: its case-folded trigram's
+//   1. router_features_kernel, one workgroup of 1024 threads per prompt. The prompt is staged
+//      through LDS in chunks with a small halo on both sides (bytes outside the prompt read as
+//      zero, which no pattern byte equals; all byte loads of a chunk are in flight together).
+//      Every position is examined by one thread: its case-folded trigram's
 //      32-bit FNV-1a hash goes into an LDS histogram by an LDS atomic increment (integer, so the
 //      histogram does not depend on the order of the increments), its byte is classified, and
 //      the descriptor patterns that can start there are matched. Counts and descriptor bits are
@@ -25,8 +26,11 @@
 namespace tasp {
 namespace {
 
+constexpr int kFeatBlock = 1024;      // threads of the features kernel (one workgroup per prompt)
 constexpr int kChunk = 8192;          // prompt bytes staged per round
 constexpr int kHalo = 16;             // bytes kept on either side of a chunk (patterns need <= 9)
+constexpr int kStaged = kChunk + 2 * kHalo;
+constexpr int kStage = (kStaged + kFeatBlock - 1) / kFeatBlock;   // byte loads per thread
 constexpr int kDenseRows = kBlock / kWave;   // output rows per workgroup
 constexpr int kDensePrompts = 8;             // prompts per workgroup
 
@@ -86,9 +90,9 @@ __device__ __forceinline__ unsigned patterns_at(const uint8_t* t, bool line_star
   return f;
 }
 
-__global__ __launch_bounds__(kBlock) void router_features_kernel(RouterFeatArgs a) {
+__global__ __launch_bounds__(kFeatBlock) void router_features_kernel(RouterFeatArgs a) {
   extern __shared__ __attribute__((aligned(16))) uint32_t hist[];     // [n_bins]
-  __shared__ uint8_t tb[kChunk + 2 * kHalo];
+  __shared__ uint8_t tb[kStaged];
   __shared__ int cnt[4];
   __shared__ unsigned flags;
   const int b = blockIdx.x, tid = threadIdx.x;
@@ -98,8 +102,9 @@ __global__ __launch_bounds__(kBlock) void router_features_kernel(RouterFeatArgs 
     end = min(max(long(a.offsets[b + 1]), start), long(a.n_text));
   }
   const int n = int(end - start);
-  const uint8_t* text = a.text + start;
-  for (int i = tid; i < a.n_bins; i += kBlock) hist[i] = 0u;
+  // this prompt's bytes; loads at an offset past them return zero without touching memory
+  const __amdgpu_buffer_rsrc_t rt = make_rsrc(a.text + start, uint32_t(n));
+  for (int i = tid; i < a.n_bins; i += kFeatBlock) hist[i] = 0u;
   if (tid < 4) cnt[tid] = 0;
   if (tid == 0) flags = 0u;
   __syncthreads();
@@ -107,14 +112,23 @@ __global__ __launch_bounds__(kBlock) void router_features_kernel(RouterFeatArgs 
   unsigned fl = 0;
   const uint32_t nb = uint32_t(a.n_bins);
   for (int c0 = 0; c0 < n; c0 += kChunk) {
-    __syncthreads();                                   // the previous chunk is consumed
-    for (int i = tid; i < kChunk + 2 * kHalo; i += kBlock) {
+    uint8_t v[kStage];
+#pragma unroll
+    for (int u = 0; u < kStage; ++u) {
+      const int i = u * kFeatBlock + tid;
       const long q = long(c0) - kHalo + i;
-      tb[i] = (q >= 0 && q < n) ? text[q] : uint8_t(0);
+      v[u] = __builtin_amdgcn_raw_buffer_load_b8(
+          rt, (i < kStaged && q >= 0 && q < n) ? int(q) : int(kOOB), 0, 0);
+    }
+    __syncthreads();                                   // the previous chunk is consumed
+#pragma unroll
+    for (int u = 0; u < kStage; ++u) {
+      const int i = u * kFeatBlock + tid;
+      if (i < kStaged) tb[i] = v[u];
     }
     __syncthreads();
     const int lim = min(kChunk, n - c0);
-    for (int i = tid; i < lim; i += kBlock) {
+    for (int i = tid; i < lim; i += kFeatBlock) {
       const int p = c0 + i;
       const uint8_t* t = tb + kHalo + i;
       const unsigned c = t[0];
@@ -135,7 +149,7 @@ __global__ __launch_bounds__(kBlock) void router_features_kernel(RouterFeatArgs 
   __syncthreads();
   const float inv_n = float(max(1, n - 2));
   float* tf = a.tf + size_t(b) * a.n_bins;
-  for (int i = tid; i < a.n_bins; i += kBlock) tf[i] = float(hist[i]) / inv_n;
+  for (int i = tid; i < a.n_bins; i += kFeatBlock) tf[i] = float(hist[i]) / inv_n;
   if (tid == 0) {
     float* f = a.feats + size_t(b) * a.ld_feats + a.proj_dim;
     const unsigned g = flags;
@@ -226,7 +240,7 @@ hipError_t launch_router_features(const RouterFeatArgs& a, int n_prompts, hipStr
       reinterpret_cast<const void*>(&router_features_kernel),
       hipFuncAttributeMaxDynamicSharedMemorySize, int(router_features_lds_bytes(kMaxRouterBins)));
   if (attr != hipSuccess) return attr;
-  hipLaunchKernelGGL(router_features_kernel, dim3(n_prompts), dim3(kBlock), lds, s, a);
+  hipLaunchKernelGGL(router_features_kernel, dim3(n_prompts), dim3(kFeatBlock), lds, s, a);
   return hipGetLastError();
 }
 
