@@ -13,7 +13,8 @@ m^q, m^kv, c the retained query heads, KV groups and SwiGLU channels of a layer.
 
 Readings of points the paper leaves open (each is listed in the design notes):
 * quantisation is symmetric INT8 with one float32 scale per output row; a layer's weight is
-  W = q * s (q int8, s per row), and scales are never recomputed after masking;
+  W = q * s (q int8, s per row), and scales are never recomputed after masking; the groupwise
+  store keeps one BF16 scale per output row and run of 128 input columns instead;
 * query head h belongs to KV group g(h) = floor(h / r), r = H_q / H_kv (contiguous groups);
 * closure: a head whose KV group is dropped is dropped; a KV group is kept iff any of its
   query heads is kept; FFN channels are kept as given (gate row, up row and down column move
@@ -75,8 +76,18 @@ def index_lists(qc_l, kvc_l, ffnc_l, group_size):
 # ------------------------------------------------------------------------ weights
 
 def dequantize(qw, scale):
-    """W = q * s in float64 (products of an int8 and a float32 are exact in float64)."""
-    return np.asarray(qw, dtype=np.float64) * np.asarray(scale, dtype=np.float64)[:, None]
+    """W = q * s in float64 (products of an int8 and a float32 or BF16 value are exact in float64).
+
+    ``scale`` is either one float32 value per output row, or BF16 bit patterns (uint16)
+    [out][in / G] for the groupwise store: W[o][i] = q[o][i] * s[o][i // G] (paper, Table
+    "configuration": symmetric groupwise INT8, group size 128, BF16 scales)."""
+    q = np.asarray(qw, dtype=np.float64)
+    s = np.asarray(scale)
+    if s.ndim == 1:
+        return q * s.astype(np.float64)[:, None]
+    g = q.shape[1] // s.shape[1]
+    assert g * s.shape[1] == q.shape[1]
+    return q * np.repeat(bf16_bits_to_f64(s), g, axis=1)
 
 
 def bf16_bits_to_f64(bits):

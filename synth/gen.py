@@ -22,7 +22,10 @@ __all__ = [
     "WEIGHT_NAMES", "to_bf16_bits", "bf16_bits_to_f32", "bf16_round", "quantize_rows",
     "layer_weights", "final_norm", "lm_head", "activations", "kv_prior", "tiny_mask",
     "budget_mask", "raw_mask", "all_kept_mask", "mask_counts", "embedding", "prompt_ids",
+    "quantize_groups", "quantize_rows_bf16", "GROUP",
 ]
+
+GROUP = 128     # columns per scale group of the groupwise store
 
 WEIGHT_NAMES = ("wq", "wk", "wv", "wo", "wg", "wu", "wd")
 
@@ -61,6 +64,37 @@ def quantize_rows(w: np.ndarray):
     return q.astype(np.int8), s
 
 
+def quantize_rows_bf16(w: np.ndarray):
+    """Per-output-row INT8 whose scales are BF16 values: s_r = BF16(max_k |w_rk| / 127) (1 for an
+    all-zero row), q = clip(rint(w / s_r), -127, 127). Returns (int8 [out][in], float32 [out]);
+    the same bytes with every group scale equal to s_r form a groupwise store of identical
+    quantisation."""
+    w = np.asarray(w, dtype=np.float32)
+    amax = np.abs(w).max(axis=1)
+    s = bf16_round((amax / np.float32(127.0)).astype(np.float32))
+    s[amax == 0] = np.float32(1.0)
+    q = np.rint(w / s[:, None])
+    np.clip(q, -127, 127, out=q)
+    return q.astype(np.int8), s
+
+
+def quantize_groups(w: np.ndarray, group: int = GROUP):
+    """Symmetric groupwise INT8 with BF16 scales: for row r and each run g of ``group``
+    consecutive columns, s = BF16(max |w| / 127) (1 for an all-zero run) and q = clip(rint(w / s),
+    -127, 127), ties to even (a scale rounded below max/127 clips the largest entries at 127).
+    Returns (int8 [out][in], uint16 BF16 bits [out][in / group])."""
+    w = np.asarray(w, dtype=np.float32)
+    o, i = w.shape
+    assert i % group == 0, (i, group)
+    wg = w.reshape(o, i // group, group)
+    amax = np.abs(wg).max(axis=2)
+    s = bf16_round((amax / np.float32(127.0)).astype(np.float32))
+    s[amax == 0] = np.float32(1.0)
+    q = np.rint(wg / s[:, :, None])
+    np.clip(q, -127, 127, out=q)
+    return q.reshape(o, i).astype(np.int8), to_bf16_bits(s)
+
+
 def _weight_shapes(sh: Shape):
     qd, kd = sh.n_q_heads * sh.head_dim, sh.n_kv_heads * sh.head_dim
     d, f = sh.d_model, sh.d_ffn
@@ -72,18 +106,22 @@ def _gain(rng, n):
     return to_bf16_bits(np.float32(1.0) + np.float32(0.1) * rng.standard_normal(n, dtype=np.float32))
 
 
-def layer_weights(sh: Shape, layer: int, seed_w: int = 0, std: float = 0.02) -> dict:
+def layer_weights(sh: Shape, layer: int, seed_w: int = 0, std: float = 0.02,
+                  quant: str = "row") -> dict:
     """One decoder layer of the INT8 store.
 
-    Returns ``{name: (int8 [out][in], float32 scale [out])}`` for the seven projections plus
-    ``attn_norm`` / ``ffn_norm`` as BF16 bit patterns ``uint16 [d]``.
+    Returns ``{name: (int8 [out][in], scales)}`` for the seven projections plus ``attn_norm`` /
+    ``ffn_norm`` as BF16 bit patterns ``uint16 [d]``. ``quant``: "row" (float32 scale per row),
+    "row_bf16" (per row, BF16-valued float32 scales) or "group" (BF16 bits [out][in / 128]). The
+    float weights drawn are the same for every ``quant``.
     """
+    qz = {"row": quantize_rows, "row_bf16": quantize_rows_bf16, "group": quantize_groups}[quant]
     out = {}
     for m, (name, shp) in enumerate(_weight_shapes(sh).items()):
         rng = np.random.default_rng([seed_w, layer, m])
         w = rng.standard_normal(shp, dtype=np.float32)
         w *= np.float32(std)
-        out[name] = quantize_rows(w)
+        out[name] = qz(w)
         del w
     out["attn_norm"] = _gain(np.random.default_rng([seed_w, layer, 7]), sh.d_model)
     out["ffn_norm"] = _gain(np.random.default_rng([seed_w, layer, 8]), sh.d_model)
