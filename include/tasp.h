@@ -135,6 +135,52 @@ tasp_status tasp_compile_plan(const tasp_model_desc* desc, const tasp_store* sto
                               const tasp_mask* mask, void* workspace, size_t workspace_bytes,
                               void* stream, tasp_plan* out);
 
+/* ---- shared-store plans (paper, appendix "Backing-store semantics": every mask indexes one
+ * immutable packed store and owns no weight bytes, so memory grows only by plan metadata; Table
+ * "configuration": symmetric groupwise INT8, group size 128, BF16 scales).
+ *
+ * Groupwise matrix: w int8 [out][in] row-major (16-byte aligned), scale BF16 bits
+ * [out][in / 128] (2-byte aligned); W[o][i] = w[o][i] * scale[o][i / 128]. */
+typedef struct {
+  const int8_t* w;
+  const uint16_t* scale;
+} tasp_gqmat;
+
+/* One layer of the packed groupwise store: wqkv [(n_q_heads + 2 n_kv_heads) head_dim][d] holds
+ * every query head's rows, then every K row, then every V row; wo [d][n_q_heads head_dim];
+ * wg / wu [d_ffn][d]; wd [d][d_ffn]; gains BF16 [d] (device). */
+typedef struct {
+  tasp_gqmat wqkv, wo, wg, wu, wd;
+  const uint16_t* attn_norm;
+  const uint16_t* ffn_norm;
+} tasp_glayer;
+
+/* The packed store (host array of n_layers layers; final BF16 gain and dense BF16 LM head
+ * [vocab][d] on the device for vocab > 0). Plans keep pointers into it: it must outlive them. */
+typedef struct {
+  const tasp_glayer* layers;
+  const uint16_t* final_norm;
+  const uint16_t* lm_head;
+} tasp_gstore;
+
+/* Workspace bytes of a shared-store plan: masks, index lists, the maps into the store, the RoPE
+ * table and batch-1 decode scratch; the same for every mask. The desc must have max_batch 1 and
+ * max_prefill 0, and d_model, n_q_heads * head_dim and d_ffn divisible by 128. */
+tasp_status tasp_shared_plan_workspace_bytes(const tasp_model_desc* desc, size_t* bytes);
+
+/* Compile a plan over the shared store: closes the mask (as tasp_compile_plan), builds on the
+ * device the maps from plan rows / column pieces to store rows / columns (QKV rows of the
+ * retained heads and groups, W_o columns of the retained heads, gate / up rows and W_down column
+ * blocks of the retained channels) and checks them on the host; copies no weights. The retained
+ * channels of every layer must come in aligned blocks of 16 (else TASP_ERR_UNSUPPORTED; the
+ * paper's channel groups are 1,024 wide). Such a plan serves tasp_decode_step at batch 1
+ * (and tasp_decode_step_timed, tasp_profile_stage); tasp_prefill and tasp_plan_panel return
+ * TASP_ERR_UNSUPPORTED. Its signature differs from a per-row plan of the same mask, so caches
+ * are not shared between the two formats. Synchronises `stream`. */
+tasp_status tasp_compile_shared_plan(const tasp_model_desc* desc, const tasp_gstore* store,
+                                     const tasp_mask* mask, void* workspace,
+                                     size_t workspace_bytes, void* stream, tasp_plan* out);
+
 /* Retained counts of one layer after closure: query heads, KV groups, SwiGLU channels. */
 tasp_status tasp_plan_counts(tasp_plan plan, int32_t layer, int32_t* m_q, int32_t* m_kv,
                              int32_t* n_ffn);

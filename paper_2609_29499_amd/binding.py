@@ -24,6 +24,7 @@ KERNEL_KINDS = {0: "qkv_gemv", 1: "attention", 2: "o_gemv", 3: "gateup_gemv", 4:
 
 EXPORTS = ["tasp_plan_workspace_bytes", "tasp_compile_plan", "tasp_plan_counts",
            "tasp_plan_indices", "tasp_plan_panel", "tasp_plan_ledger", "tasp_plan_destroy",
+           "tasp_shared_plan_workspace_bytes", "tasp_compile_shared_plan",
            "tasp_kv_bind", "tasp_decode_step", "tasp_prefill", "tasp_prefill_timed", "tasp_generate",
            "tasp_decode_step_timed",
            "tasp_profile_stage", "tasp_mask_workspace_bytes", "tasp_build_mask",
@@ -57,6 +58,20 @@ class tasp_layer(C.Structure):
 
 class tasp_store(C.Structure):
     _fields_ = [("layers", C.POINTER(tasp_layer)), ("final_norm", C.c_void_p),
+                ("lm_head", C.c_void_p)]
+
+
+class tasp_gqmat(C.Structure):
+    _fields_ = [("w", C.c_void_p), ("scale", C.c_void_p)]
+
+
+class tasp_glayer(C.Structure):
+    _fields_ = [("wqkv", tasp_gqmat), ("wo", tasp_gqmat), ("wg", tasp_gqmat), ("wu", tasp_gqmat),
+                ("wd", tasp_gqmat), ("attn_norm", C.c_void_p), ("ffn_norm", C.c_void_p)]
+
+
+class tasp_gstore(C.Structure):
+    _fields_ = [("layers", C.POINTER(tasp_glayer)), ("final_norm", C.c_void_p),
                 ("lm_head", C.c_void_p)]
 
 
@@ -95,6 +110,9 @@ def load(path: str = LIB_PATH):
         "tasp_plan_workspace_bytes": [C.POINTER(tasp_model_desc), C.POINTER(tasp_mask), C.POINTER(SZ)],
         "tasp_compile_plan": [C.POINTER(tasp_model_desc), C.POINTER(tasp_store), C.POINTER(tasp_mask),
                               P, SZ, P, C.POINTER(P)],
+        "tasp_shared_plan_workspace_bytes": [C.POINTER(tasp_model_desc), C.POINTER(SZ)],
+        "tasp_compile_shared_plan": [C.POINTER(tasp_model_desc), C.POINTER(tasp_gstore),
+                                     C.POINTER(tasp_mask), P, SZ, P, C.POINTER(P)],
         "tasp_plan_counts": [P, I32, C.POINTER(I32), C.POINTER(I32), C.POINTER(I32)],
         "tasp_plan_indices": [P, I32, I32, C.POINTER(I32), I32, C.POINTER(I32)],
         "tasp_plan_panel": [P, I32, I32, C.POINTER(P), C.POINTER(P), C.POINTER(C.c_int64),
@@ -152,6 +170,19 @@ def tasp_compile_plan(desc, store, mask, workspace_ptr, workspace_bytes, stream)
     _check(load().tasp_compile_plan(C.byref(desc), C.byref(store), mask, workspace_ptr,
                                     workspace_bytes, stream, C.byref(plan)))
     return plan
+
+
+def tasp_shared_plan_workspace_bytes(desc):
+    n = C.c_size_t()
+    _check(load().tasp_shared_plan_workspace_bytes(C.byref(desc), C.byref(n)))
+    return n.value
+
+
+def tasp_compile_shared_plan(desc, store, mask, workspace_ptr, workspace_bytes, stream):
+    out = C.c_void_p()
+    _check(load().tasp_compile_shared_plan(C.byref(desc), C.byref(store), mask, workspace_ptr,
+                                           workspace_bytes, stream, C.byref(out)))
+    return out
 
 
 def tasp_plan_counts(plan, layer):

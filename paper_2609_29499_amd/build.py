@@ -19,7 +19,7 @@ HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 SOURCES = ["plan_kernels.hip", "gemv_kernels.hip", "mfma_kernels.hip", "attn_kernels.hip",
            "prefill_kernels.hip", "prefill_attn.hip", "mask_kernels.hip", "token_kernels.hip",
-           "router_kernels.hip", "runtime.hip"]
+           "router_kernels.hip", "shared_kernels.hip", "runtime.hip"]
 FLAGS = [
     "--offload-arch=gfx950", "-O3", "-fPIC", "-std=c++17", "-Wall", "-Wno-unused-function",
     # packed FP32 instructions stay off: ordinary float code only

@@ -58,6 +58,39 @@ struct GemvArgs {
 hipError_t launch_gemv(GemvMode mode, const GemvArgs& a, hipStream_t s);
 size_t gemv_lds_bytes(int B, int K);
 
+// ----------------------------------------------------------------- shared-store decode GEMVs
+
+// Batch-1 GEMVs over the groupwise store (INT8 [store_rows][ld], BF16 scales
+// [store_rows][ld / 128]) through a plan's maps: plan row i reads store row rows[i] (null:
+// i), plan columns 16 p .. 16 p + 15 read store columns cols[p] .. cols[p] + 15 (null: 16 p).
+// Modes as for launch_gemv except the LM head. K % 16 == 0, ld % 128 == 0.
+constexpr size_t kMaxSharedGemvLds = 159 * 1024;
+struct SharedGemvArgs {
+  const int8_t* w; const int8_t* w2;       // store matrix (gate/up: gate, up)
+  const uint16_t* s; const uint16_t* s2;   // their scales
+  int ld, store_rows;
+  const int* rows; const int* cols;        // device maps (nullable)
+  int N, K;                                // plan rows (gate/up: channels), plan columns
+  const float* x;                          // input [K]
+  const uint16_t* gamma; float eps;        // RMSNorm gain (QKV, gate/up)
+  const float* resid;                      // GEMV_RESID: [N]
+  float* y;                                // [N]
+};
+hipError_t launch_shared_gemv(GemvMode mode, const SharedGemvArgs& a, hipStream_t s);
+size_t shared_gemv_lds_bytes(int K);
+
+// Maps of every layer from the closure's index lists and counts: qkv_rows [L][(Hq + 2Hkv) dh]
+// (store rows of the retained q heads, then K and V rows of the retained groups, for a store
+// whose QKV matrix holds all q rows, then all K rows, then all V rows), o_cols [L][Hq dh / 16]
+// (store columns of the retained heads' pieces), down_cols [L][F / 16] (first store column of
+// each block of 16 retained channels; the retained channels must come in such blocks).
+struct SharedMapsArgs {
+  int Hq, Hkv, dh, F;
+  const int* q_idx; const int* kv_idx; const int* ffn_idx; const int* counts;
+  int* qkv_rows; int* o_cols; int* down_cols;
+};
+hipError_t launch_shared_maps(const SharedMapsArgs& a, int n_layers, hipStream_t s);
+
 // ----------------------------------------------------------------- batched decode on MFMA
 
 // Batch 2..8. Activations are a [16][ldx] BF16 operand: row 2b = bf16(v), row 2b+1 =

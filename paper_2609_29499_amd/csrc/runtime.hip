@@ -143,6 +143,7 @@ struct Layout {
   size_t r_mid, r_io0, r_io1, qkv_buf, o_buf, h_buf, part;
   size_t xd, xo, xh, ssq;            // batched path: hi/lo operands and sums of squares
   size_t pxd, pxw, pq, pqkv, pr_mid, pr_io0, pr_io1, pssq;   // prefill scratch
+  size_t qkv_rows, o_cols, down_cols;                        // shared-store plans: maps
   size_t zero_begin, zero_end;       // scratch cleared at compile
   size_t total;
   int n_split_max, ld_qkv, ld_obuf, ld_h, ld_xd, ld_xo, ld_xh, ld_xw;
@@ -227,6 +228,50 @@ Layout make_layout(const tasp_model_desc* d, const Closed& c) {
   return Y;
 }
 
+// A shared-store plan holds no weights: masks and index lists, the maps into the store, the
+// RoPE table and the batch-1 decode scratch. Its size does not depend on the mask.
+Layout make_shared_layout(const tasp_model_desc* d) {
+  Layout Y{};
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = off;
+    off = align_up(off + bytes, kAlign);
+    return at;
+  };
+  const int L = d->n_layers, D = d->d_model, Hq = d->n_q_heads, Hkv = d->n_kv_heads;
+  const int dh = d->head_dim, F = d->d_ffn;
+  Y.mask_q = take(size_t(L) * Hq);
+  Y.mask_kv = take(size_t(L) * Hkv);
+  Y.mask_f = take(size_t(L) * F);
+  Y.idx_q = take(size_t(L) * Hq * 4);
+  Y.idx_kv = take(size_t(L) * Hkv * 4);
+  Y.idx_slot = take(size_t(L) * Hq * 4);
+  Y.idx_slot_start = take(size_t(L) * (Hkv + 1) * 4);
+  Y.idx_ffn = take(size_t(L) * F * 4);
+  Y.counts = take(size_t(L) * 4 * 4);
+  Y.qkv_rows = take(size_t(L) * (Hq + 2 * Hkv) * dh * 4);
+  Y.o_cols = take(size_t(L) * (Hq * dh / 16) * 4);
+  Y.down_cols = take(size_t(L) * (F / 16) * 4);
+  Y.rope_cos = take(size_t(d->max_seq) * (dh / 2) * 4);
+  Y.rope_sin = take(size_t(d->max_seq) * (dh / 2) * 4);
+  Y.n_split_max = std::min((d->max_seq + tasp::attn_min_chunk() - 1) / tasp::attn_min_chunk(),
+                           tasp::attn_max_split());
+  Y.ld_qkv = (Hq + 2 * Hkv) * dh;
+  Y.ld_obuf = Hq * dh;
+  Y.ld_h = round_up16(F);
+  Y.zero_begin = off;
+  Y.r_mid = take(size_t(D) * 4);
+  Y.r_io0 = take(size_t(D) * 4);
+  Y.r_io1 = take(size_t(D) * 4);
+  Y.qkv_buf = take(size_t(Y.ld_qkv) * 4);
+  Y.o_buf = take(size_t(Y.ld_obuf) * 4);
+  Y.h_buf = take(size_t(Y.ld_h) * 4);
+  Y.part = take(size_t(Hkv) * Y.n_split_max * 8 * (dh + 4) * 4);
+  Y.zero_end = off;
+  Y.total = off;
+  return Y;
+}
+
 uint64_t fnv1a(uint64_t h, const void* p, size_t n) {
   const uint8_t* b = static_cast<const uint8_t*>(p);
   for (size_t i = 0; i < n; ++i) {
@@ -254,8 +299,17 @@ struct LayerPlan {
   std::vector<int> q_idx, kv_idx, q_kvslot, ffn_idx, slot_start;
 };
 
+// a shared-store plan's view of one store layer and its maps (device pointers)
+struct SharedLayer {
+  const int8_t *qkv, *o, *g, *u, *d;
+  const uint16_t *s_qkv, *s_o, *s_g, *s_u, *s_d;
+  const int *qkv_rows, *o_cols, *ffn_rows, *down_cols;
+};
+
 struct tasp_plan_s {
   tasp_model_desc desc;
+  bool shared = false;               // indexes a groupwise store instead of owning panels
+  std::vector<SharedLayer> sl;
   uint64_t sig;
   double ratio;
   uint64_t weight_bytes, scale_bytes;
@@ -344,6 +398,53 @@ tasp::GemvArgs down_args(const tasp_plan_s* p, int l, int B, float* y) {
   tasp::GemvArgs a{};
   a.w = P.dn; a.scale = P.s_d; a.N = D; a.K = P.c; a.ld = P.ld_d; a.x = p->h_buf;
   a.ldx = p->ld_h; a.resid = p->r_mid; a.y = y; a.ldy = D; a.B = B;
+  return a;
+}
+
+// ---- shared-store plans (batch 1): the four projections through the plan's maps
+
+tasp::SharedGemvArgs shared_qkv_args(const tasp_plan_s* p, int l, const float* in) {
+  const LayerPlan& P = p->layers[l];
+  const SharedLayer& Q = p->sl[l];
+  const tasp_model_desc& d = p->desc;
+  tasp::SharedGemvArgs a{};
+  a.w = Q.qkv; a.s = Q.s_qkv; a.ld = d.d_model;
+  a.store_rows = (d.n_q_heads + 2 * d.n_kv_heads) * d.head_dim;
+  a.rows = Q.qkv_rows; a.N = P.n_qkv; a.K = d.d_model;
+  a.x = in; a.gamma = P.an; a.eps = d.rms_eps; a.y = p->qkv_buf;
+  return a;
+}
+
+tasp::SharedGemvArgs shared_o_args(const tasp_plan_s* p, int l, const float* in) {
+  const LayerPlan& P = p->layers[l];
+  const SharedLayer& Q = p->sl[l];
+  const tasp_model_desc& d = p->desc;
+  tasp::SharedGemvArgs a{};
+  a.w = Q.o; a.s = Q.s_o; a.ld = d.n_q_heads * d.head_dim; a.store_rows = d.d_model;
+  a.cols = Q.o_cols; a.N = d.d_model; a.K = P.m_q * d.head_dim;
+  a.x = p->o_buf; a.resid = in; a.y = p->r_mid;
+  return a;
+}
+
+tasp::SharedGemvArgs shared_gateup_args(const tasp_plan_s* p, int l) {
+  const LayerPlan& P = p->layers[l];
+  const SharedLayer& Q = p->sl[l];
+  const tasp_model_desc& d = p->desc;
+  tasp::SharedGemvArgs a{};
+  a.w = Q.g; a.w2 = Q.u; a.s = Q.s_g; a.s2 = Q.s_u; a.ld = d.d_model; a.store_rows = d.d_ffn;
+  a.rows = Q.ffn_rows; a.N = P.c; a.K = d.d_model;
+  a.x = p->r_mid; a.gamma = P.fn; a.eps = d.rms_eps; a.y = p->h_buf;
+  return a;
+}
+
+tasp::SharedGemvArgs shared_down_args(const tasp_plan_s* p, int l, float* y) {
+  const LayerPlan& P = p->layers[l];
+  const SharedLayer& Q = p->sl[l];
+  const tasp_model_desc& d = p->desc;
+  tasp::SharedGemvArgs a{};
+  a.w = Q.d; a.s = Q.s_d; a.ld = d.d_ffn; a.store_rows = d.d_model;
+  a.cols = Q.down_cols; a.N = d.d_model; a.K = P.c;
+  a.x = p->h_buf; a.resid = p->r_mid; a.y = y;
   return a;
 }
 
@@ -575,6 +676,52 @@ tasp_status prefill_checked(tasp_plan p, const float* x, int32_t T, tasp_kv_cach
   return prefill_impl(p, x, T, cache, pos0, out, static_cast<hipStream_t>(stream), tm);
 }
 
+// one decode step of a shared-store plan (batch 1): the per-row kernels' sequence with the
+// projections read from the store through the plan's maps; the LM head is the store's
+tasp_status decode_shared(tasp_plan p, const float* x, tasp_kv_cache* cache, int pos, float* out,
+                          hipStream_t s, Timer* tm) {
+  const tasp_model_desc& d = p->desc;
+  const int D = d.d_model, L = d.n_layers;
+  tasp_status st = TASP_OK;
+  for (int l = 0; l < L; ++l) {
+    const LayerPlan& P = p->layers[l];
+    const float* in = (l == 0) ? x : p->r_io[(l - 1) & 1];
+    float* lo = (l == L - 1 && d.vocab == 0) ? out : p->r_io[l & 1];
+    if (P.n_qkv > 0) {
+      const tasp::SharedGemvArgs a = shared_qkv_args(p, l, in);
+      if ((st = run_kernel(tm, 0, s, [&] { return tasp::launch_shared_gemv(tasp::GEMV_QKV, a, s); })))
+        return st;
+    }
+    if (P.m_kv > 0) {
+      const tasp::AttnArgs a = attn_args(p, l, cache, pos, 1, false);
+      if ((st = run_kernel(tm, 1, s, [&] { return tasp::launch_attn_decode(a, s); }))) return st;
+    }
+    {
+      const tasp::SharedGemvArgs a = shared_o_args(p, l, in);
+      if ((st = run_kernel(tm, 2, s, [&] { return tasp::launch_shared_gemv(tasp::GEMV_RESID, a, s); })))
+        return st;
+    }
+    if (P.c > 0) {
+      const tasp::SharedGemvArgs a = shared_gateup_args(p, l);
+      if ((st = run_kernel(tm, 3, s, [&] { return tasp::launch_shared_gemv(tasp::GEMV_GATEUP, a, s); })))
+        return st;
+    }
+    {
+      const tasp::SharedGemvArgs a = shared_down_args(p, l, lo);
+      if ((st = run_kernel(tm, 4, s, [&] { return tasp::launch_shared_gemv(tasp::GEMV_RESID, a, s); })))
+        return st;
+    }
+  }
+  if (d.vocab) {
+    tasp::GemvArgs a{};
+    a.w = p->lm_head; a.N = d.vocab; a.K = D; a.ld = 2 * D; a.x = p->r_io[(L - 1) & 1];
+    a.ldx = D; a.gamma = p->final_norm; a.eps = d.rms_eps; a.y = out; a.ldy = d.vocab; a.B = 1;
+    if ((st = run_kernel(tm, 5, s, [&] { return tasp::launch_gemv(tasp::GEMV_LMHEAD, a, s); })))
+      return st;
+  }
+  return TASP_OK;
+}
+
 tasp_status decode_impl(tasp_plan p, const float* x, tasp_kv_cache* cache, int32_t pos,
                         float* out, void* stream, Timer* tm) {
   if (!p) return fail(TASP_ERR_INVALID_ARG, "plan is NULL");
@@ -595,6 +742,7 @@ tasp_status decode_impl(tasp_plan p, const float* x, tasp_kv_cache* cache, int32
     return fail(TASP_ERR_INVALID_ARG, "x and out overlap");
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (B > 1) return decode_batched(p, x, cache, pos, out, s, tm, B);
+  if (p->shared) return decode_shared(p, x, cache, pos, out, s, tm);
 
   for (int l = 0; l < L; ++l) {
     const LayerPlan& P = p->layers[l];
@@ -643,8 +791,8 @@ tasp_status decode_impl(tasp_plan p, const float* x, tasp_kv_cache* cache, int32
 }  // namespace
 
 // ------------------------------------------------------------------------------- C ABI
-
-extern "C" {
+// (every entry point below is declared extern "C" in tasp.h; helpers between them sit in
+// anonymous namespaces and stay internal)
 
 const char* tasp_status_string(tasp_status s) {
   switch (s) {
@@ -674,6 +822,106 @@ tasp_status tasp_plan_workspace_bytes(const tasp_model_desc* desc, const tasp_ma
   *bytes = make_layout(desc, c).total;
   return TASP_OK;
 }
+
+namespace {
+
+// Signature of a plan: the model shape, the closed mask and the store format (0 per-row panels,
+// 1 groupwise shared store); equal signatures mean interchangeable cache contents.
+uint64_t plan_signature(const tasp_model_desc& d, const Closed& c, int32_t format) {
+  uint64_t sig = 1469598103934665603ull;
+  const int32_t shape[7] = {d.n_layers, d.d_model, d.n_q_heads, d.n_kv_heads, d.head_dim, d.d_ffn, d.vocab};
+  sig = fnv1a(sig, shape, sizeof shape);
+  sig = fnv1a(sig, c.q.data(), c.q.size());
+  sig = fnv1a(sig, c.kv.data(), c.kv.size());
+  sig = fnv1a(sig, c.f.data(), c.f.size());
+  if (format) sig = fnv1a(sig, &format, sizeof format);
+  return sig ? sig : 1;
+}
+
+// A shared-store plan decodes one sequence: its scale groups of 128 must tile every input
+// dimension, and its widest GEMV input (with the piece sums and the column map) must fit LDS.
+tasp_status check_shared_desc(const tasp_model_desc* d) {
+  tasp_status st = check_desc(d);
+  if (st != TASP_OK) return st;
+  if (d->max_batch != 1 || d->max_prefill != 0)
+    return fail(TASP_ERR_UNSUPPORTED, "shared-store plans decode one sequence (max_batch 1, "
+                "max_prefill 0)");
+  if (d->d_model % 128 || (d->n_q_heads * d->head_dim) % 128 || d->d_ffn % 128)
+    return fail(TASP_ERR_SHAPE, "the groupwise store needs d_model, n_q_heads*head_dim and d_ffn "
+                "divisible by 128");
+  const int widest = std::max({d->d_model, d->n_q_heads * d->head_dim, d->d_ffn});
+  if (tasp::shared_gemv_lds_bytes(widest) > tasp::kMaxSharedGemvLds)
+    return fail(TASP_ERR_UNSUPPORTED, "widest GEMV input exceeds LDS (%d)", widest);
+  return TASP_OK;
+}
+
+// Reads the device index lists back (the compile's one synchronisation; `h` carries the status of
+// the work enqueued before it), checks them against the host closure and keeps them in the plan.
+tasp_status read_back_indices(tasp_plan_s* p, const Closed& c, const Layout& Y, char* ws,
+                              hipStream_t s, hipError_t h) {
+  const tasp_model_desc& d = p->desc;
+  const int L = d.n_layers, Hq = d.n_q_heads, Hkv = d.n_kv_heads, F = d.d_ffn;
+  auto at = [&](size_t off) { return ws + off; };
+  int* dq = reinterpret_cast<int*>(at(Y.idx_q));
+  int* dkv = reinterpret_cast<int*>(at(Y.idx_kv));
+  int* dslot = reinterpret_cast<int*>(at(Y.idx_slot));
+  int* dss = reinterpret_cast<int*>(at(Y.idx_slot_start));
+  int* dffn = reinterpret_cast<int*>(at(Y.idx_ffn));
+  int* dcnt = reinterpret_cast<int*>(at(Y.counts));
+  // read the device index lists back (the one synchronisation) and check them
+  std::vector<int> hq_idx(size_t(L) * Hq), hkv_idx(size_t(L) * Hkv), hslot(size_t(L) * Hq),
+      hffn(size_t(L) * F), hcnt(size_t(L) * 4);
+  if (h == hipSuccess) h = hipMemcpyAsync(hq_idx.data(), dq, hq_idx.size() * 4, hipMemcpyDeviceToHost, s);
+  if (h == hipSuccess) h = hipMemcpyAsync(hkv_idx.data(), dkv, hkv_idx.size() * 4, hipMemcpyDeviceToHost, s);
+  if (h == hipSuccess) h = hipMemcpyAsync(hslot.data(), dslot, hslot.size() * 4, hipMemcpyDeviceToHost, s);
+  if (h == hipSuccess) h = hipMemcpyAsync(hffn.data(), dffn, hffn.size() * 4, hipMemcpyDeviceToHost, s);
+  if (h == hipSuccess) h = hipMemcpyAsync(hcnt.data(), dcnt, hcnt.size() * 4, hipMemcpyDeviceToHost, s);
+  if (h == hipSuccess) h = hipStreamSynchronize(s);
+  if (h != hipSuccess) {
+    (void)hipStreamSynchronize(s);
+    return fail(TASP_ERR_HIP, "compile: %s", hipGetErrorString(h));
+  }
+  const int r = Hq / Hkv;
+  for (int l = 0; l < L; ++l) {
+    LayerPlan& P = p->layers[l];
+    if (hcnt[l * 4] != P.m_q || hcnt[l * 4 + 1] != P.m_kv || hcnt[l * 4 + 2] != P.c) {
+      return fail(TASP_ERR_INTERNAL, "layer %d: device counts (%d,%d,%d) != host (%d,%d,%d)", l,
+                  hcnt[l * 4], hcnt[l * 4 + 1], hcnt[l * 4 + 2], P.m_q, P.m_kv, P.c);
+    }
+    P.q_idx.assign(hq_idx.begin() + size_t(l) * Hq, hq_idx.begin() + size_t(l) * Hq + P.m_q);
+    P.q_kvslot.assign(hslot.begin() + size_t(l) * Hq, hslot.begin() + size_t(l) * Hq + P.m_q);
+    P.kv_idx.assign(hkv_idx.begin() + size_t(l) * Hkv, hkv_idx.begin() + size_t(l) * Hkv + P.m_kv);
+    P.ffn_idx.assign(hffn.begin() + size_t(l) * F, hffn.begin() + size_t(l) * F + P.c);
+    bool ok = true;
+    int k = 0;
+    for (int hh = 0; hh < Hq; ++hh)
+      if (c.q[size_t(l) * Hq + hh]) ok &= (k < P.m_q && P.q_idx[k++] == hh);
+    k = 0;
+    for (int g = 0; g < Hkv; ++g)
+      if (c.kv[size_t(l) * Hkv + g]) ok &= (k < P.m_kv && P.kv_idx[k++] == g);
+    k = 0;
+    for (int j = 0; j < F; ++j)
+      if (c.f[size_t(l) * F + j]) ok &= (k < P.c && P.ffn_idx[k++] == j);
+    for (int i = 0; i < P.m_q && ok; ++i)
+      ok &= P.q_kvslot[i] >= 0 && P.q_kvslot[i] < P.m_kv && P.kv_idx[P.q_kvslot[i]] == P.q_idx[i] / r;
+    // slot j's heads are the run of the ascending head list whose slot is j
+    P.slot_start.assign(size_t(P.m_kv) + 1, 0);
+    for (int jj = 0; jj <= P.m_kv; ++jj)
+      for (int i = 0; i < P.m_q; ++i) P.slot_start[jj] += (P.q_kvslot[i] < jj);
+    for (int jj = 0; jj < P.m_kv && ok; ++jj) ok &= P.slot_start[jj + 1] > P.slot_start[jj];
+    std::vector<int> dev_ss(size_t(Hkv) + 1);
+    if (ok && hipMemcpy(dev_ss.data(), dss + size_t(l) * (Hkv + 1), (P.m_kv + 1) * sizeof(int),
+                        hipMemcpyDeviceToHost) == hipSuccess) {
+      for (int jj = 0; jj <= P.m_kv; ++jj) ok &= dev_ss[jj] == P.slot_start[jj];
+    } else {
+      ok = false;
+    }
+    if (!ok) return fail(TASP_ERR_INTERNAL, "layer %d: device index lists differ from the host closure", l);
+  }
+  return TASP_OK;
+}
+
+}  // namespace
 
 tasp_status tasp_compile_plan(const tasp_model_desc* desc, const tasp_store* store,
                               const tasp_mask* mask, void* workspace, size_t workspace_bytes,
@@ -820,59 +1068,11 @@ tasp_status tasp_compile_plan(const tasp_model_desc* desc, const tasp_store* sto
   p->pssq = reinterpret_cast<float*>(at(Y.pssq));
   p->ld_xw = Y.ld_xw;
 
-  // read the device index lists back (the one synchronisation) and check them
-  std::vector<int> hq_idx(size_t(L) * Hq), hkv_idx(size_t(L) * Hkv), hslot(size_t(L) * Hq),
-      hffn(size_t(L) * F), hcnt(size_t(L) * 4);
-  if (h == hipSuccess) h = hipMemcpyAsync(hq_idx.data(), dq, hq_idx.size() * 4, hipMemcpyDeviceToHost, s);
-  if (h == hipSuccess) h = hipMemcpyAsync(hkv_idx.data(), dkv, hkv_idx.size() * 4, hipMemcpyDeviceToHost, s);
-  if (h == hipSuccess) h = hipMemcpyAsync(hslot.data(), dslot, hslot.size() * 4, hipMemcpyDeviceToHost, s);
-  if (h == hipSuccess) h = hipMemcpyAsync(hffn.data(), dffn, hffn.size() * 4, hipMemcpyDeviceToHost, s);
-  if (h == hipSuccess) h = hipMemcpyAsync(hcnt.data(), dcnt, hcnt.size() * 4, hipMemcpyDeviceToHost, s);
-  if (h == hipSuccess) h = hipStreamSynchronize(s);
-  if (h != hipSuccess) {
-    (void)hipStreamSynchronize(s);
-    delete p;
-    return fail(TASP_ERR_HIP, "compile: %s", hipGetErrorString(h));
-  }
-  const int r = Hq / Hkv;
-  for (int l = 0; l < L; ++l) {
-    LayerPlan& P = p->layers[l];
-    if (hcnt[l * 4] != P.m_q || hcnt[l * 4 + 1] != P.m_kv || hcnt[l * 4 + 2] != P.c) {
+  {
+    const tasp_status rb = read_back_indices(p, c, Y, ws, s, h);
+    if (rb != TASP_OK) {
       delete p;
-      return fail(TASP_ERR_INTERNAL, "layer %d: device counts (%d,%d,%d) != host (%d,%d,%d)", l,
-                  hcnt[l * 4], hcnt[l * 4 + 1], hcnt[l * 4 + 2], P.m_q, P.m_kv, P.c);
-    }
-    P.q_idx.assign(hq_idx.begin() + size_t(l) * Hq, hq_idx.begin() + size_t(l) * Hq + P.m_q);
-    P.q_kvslot.assign(hslot.begin() + size_t(l) * Hq, hslot.begin() + size_t(l) * Hq + P.m_q);
-    P.kv_idx.assign(hkv_idx.begin() + size_t(l) * Hkv, hkv_idx.begin() + size_t(l) * Hkv + P.m_kv);
-    P.ffn_idx.assign(hffn.begin() + size_t(l) * F, hffn.begin() + size_t(l) * F + P.c);
-    bool ok = true;
-    int k = 0;
-    for (int hh = 0; hh < Hq; ++hh)
-      if (c.q[size_t(l) * Hq + hh]) ok &= (k < P.m_q && P.q_idx[k++] == hh);
-    k = 0;
-    for (int g = 0; g < Hkv; ++g)
-      if (c.kv[size_t(l) * Hkv + g]) ok &= (k < P.m_kv && P.kv_idx[k++] == g);
-    k = 0;
-    for (int j = 0; j < F; ++j)
-      if (c.f[size_t(l) * F + j]) ok &= (k < P.c && P.ffn_idx[k++] == j);
-    for (int i = 0; i < P.m_q && ok; ++i)
-      ok &= P.q_kvslot[i] >= 0 && P.q_kvslot[i] < P.m_kv && P.kv_idx[P.q_kvslot[i]] == P.q_idx[i] / r;
-    // slot j's heads are the run of the ascending head list whose slot is j
-    P.slot_start.assign(size_t(P.m_kv) + 1, 0);
-    for (int jj = 0; jj <= P.m_kv; ++jj)
-      for (int i = 0; i < P.m_q; ++i) P.slot_start[jj] += (P.q_kvslot[i] < jj);
-    for (int jj = 0; jj < P.m_kv && ok; ++jj) ok &= P.slot_start[jj + 1] > P.slot_start[jj];
-    std::vector<int> dev_ss(size_t(Hkv) + 1);
-    if (ok && hipMemcpy(dev_ss.data(), dss + size_t(l) * (Hkv + 1), (P.m_kv + 1) * sizeof(int),
-                        hipMemcpyDeviceToHost) == hipSuccess) {
-      for (int jj = 0; jj <= P.m_kv; ++jj) ok &= dev_ss[jj] == P.slot_start[jj];
-    } else {
-      ok = false;
-    }
-    if (!ok) {
-      delete p;
-      return fail(TASP_ERR_INTERNAL, "layer %d: device index lists differ from the host closure", l);
+      return rb;
     }
   }
   // ledger and signature
@@ -888,13 +1088,184 @@ tasp_status tasp_compile_plan(const tasp_model_desc* desc, const tasp_store* sto
   p->ratio = num / den;
   p->weight_bytes = wb;
   p->scale_bytes = sb;
-  uint64_t sig = 1469598103934665603ull;
-  const int32_t shape[7] = {d.n_layers, d.d_model, d.n_q_heads, d.n_kv_heads, d.head_dim, d.d_ffn, d.vocab};
-  sig = fnv1a(sig, shape, sizeof shape);
-  sig = fnv1a(sig, c.q.data(), c.q.size());
-  sig = fnv1a(sig, c.kv.data(), c.kv.size());
-  sig = fnv1a(sig, c.f.data(), c.f.size());
-  p->sig = sig ? sig : 1;
+  p->sig = plan_signature(d, c, 0);
+  *out = p;
+  return TASP_OK;
+}
+
+tasp_status tasp_shared_plan_workspace_bytes(const tasp_model_desc* desc, size_t* bytes) {
+  if (!bytes) return fail(TASP_ERR_INVALID_ARG, "bytes is NULL");
+  tasp_status st = check_shared_desc(desc);
+  if (st != TASP_OK) return st;
+  *bytes = make_shared_layout(desc).total;
+  return TASP_OK;
+}
+
+tasp_status tasp_compile_shared_plan(const tasp_model_desc* desc, const tasp_gstore* store,
+                                     const tasp_mask* mask, void* workspace,
+                                     size_t workspace_bytes, void* stream, tasp_plan* out) {
+  tasp_status st = check_shared_desc(desc);
+  if (st != TASP_OK) return st;
+  if (!store || !store->layers || !out) return fail(TASP_ERR_INVALID_ARG, "store / out is NULL");
+  if (!workspace) return fail(TASP_ERR_INVALID_ARG, "workspace is NULL");
+  if (reinterpret_cast<uintptr_t>(workspace) % kAlign)
+    return fail(TASP_ERR_WORKSPACE, "workspace not %zu-byte aligned", kAlign);
+  const tasp_model_desc& d = *desc;
+  for (int l = 0; l < d.n_layers; ++l) {
+    const tasp_glayer& S = store->layers[l];
+    const tasp_gqmat* mats[5] = {&S.wqkv, &S.wo, &S.wg, &S.wu, &S.wd};
+    for (const tasp_gqmat* m : mats) {
+      if (!m->w || !m->scale) return fail(TASP_ERR_INVALID_ARG, "layer %d: NULL weight", l);
+      if (reinterpret_cast<uintptr_t>(m->w) % 16 || reinterpret_cast<uintptr_t>(m->scale) % 2)
+        return fail(TASP_ERR_INVALID_ARG, "layer %d: weight not 16-byte / scale not 2-byte aligned", l);
+    }
+    if (!S.attn_norm || !S.ffn_norm) return fail(TASP_ERR_INVALID_ARG, "layer %d: NULL gain", l);
+  }
+  if (d.vocab && (!store->final_norm || !store->lm_head))
+    return fail(TASP_ERR_INVALID_ARG, "vocab > 0 but final_norm / lm_head is NULL");
+  Closed c;
+  if ((st = host_close(desc, mask, &c)) != TASP_OK) return st;
+  const int L = d.n_layers, Hq = d.n_q_heads, Hkv = d.n_kv_heads, dh = d.head_dim, F = d.d_ffn;
+  // W_down columns are read 16 at a time: retained channels must come in aligned blocks of 16
+  for (int l = 0; l < L; ++l)
+    for (int j0 = 0; j0 < F; j0 += 16)
+      for (int j = j0 + 1; j < j0 + 16; ++j)
+        if (c.f[size_t(l) * F + j] != c.f[size_t(l) * F + j0])
+          return fail(TASP_ERR_UNSUPPORTED,
+                      "layer %d: channels %d..%d are partly retained (shared-store plans keep "
+                      "channels in aligned blocks of 16)", l, j0, j0 + 15);
+  const Layout Y = make_shared_layout(desc);
+  if (workspace_bytes < Y.total)
+    return fail(TASP_ERR_WORKSPACE, "workspace %zu < %zu bytes", workspace_bytes, Y.total);
+  char* ws = static_cast<char*>(workspace);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  auto at = [&](size_t off) { return ws + off; };
+
+  std::vector<uint8_t> ones_q, ones_f;
+  const uint8_t* hq = mask ? mask->q_keep : nullptr;
+  const uint8_t* hf = mask ? mask->ffn_keep : nullptr;
+  if (!hq) { ones_q.assign(size_t(L) * Hq, 1); hq = ones_q.data(); }
+  if (!hf) { ones_f.assign(size_t(L) * F, 1); hf = ones_f.data(); }
+  const bool has_kv = mask && mask->kv_keep;
+  HIP_TRY(hipMemcpyAsync(at(Y.mask_q), hq, size_t(L) * Hq, hipMemcpyHostToDevice, s));
+  if (has_kv)
+    HIP_TRY(hipMemcpyAsync(at(Y.mask_kv), mask->kv_keep, size_t(L) * Hkv, hipMemcpyHostToDevice, s));
+  HIP_TRY(hipMemcpyAsync(at(Y.mask_f), hf, size_t(L) * F, hipMemcpyHostToDevice, s));
+  int* dq = reinterpret_cast<int*>(at(Y.idx_q));
+  int* dkv = reinterpret_cast<int*>(at(Y.idx_kv));
+  int* dffn = reinterpret_cast<int*>(at(Y.idx_ffn));
+  int* dcnt = reinterpret_cast<int*>(at(Y.counts));
+  HIP_TRY(tasp::launch_closure(reinterpret_cast<uint8_t*>(at(Y.mask_q)),
+                               has_kv ? reinterpret_cast<uint8_t*>(at(Y.mask_kv)) : nullptr,
+                               reinterpret_cast<uint8_t*>(at(Y.mask_f)), L, Hq, Hkv, F, dq, dkv,
+                               reinterpret_cast<int*>(at(Y.idx_slot)),
+                               reinterpret_cast<int*>(at(Y.idx_slot_start)), dffn, dcnt, s));
+  tasp::SharedMapsArgs ma{Hq, Hkv, dh, F, dq, dkv, dffn, dcnt,
+                          reinterpret_cast<int*>(at(Y.qkv_rows)), reinterpret_cast<int*>(at(Y.o_cols)),
+                          reinterpret_cast<int*>(at(Y.down_cols))};
+  HIP_TRY(tasp::launch_shared_maps(ma, L, s));
+
+  tasp_plan_s* p = new (std::nothrow) tasp_plan_s();
+  if (!p) return fail(TASP_ERR_INTERNAL, "out of host memory");
+  p->desc = d;
+  p->shared = true;
+  p->layers.resize(L);
+  p->sl.resize(L);
+  for (int l = 0; l < L; ++l) {
+    const tasp_glayer& S = store->layers[l];
+    LayerPlan& P = p->layers[l];
+    P.m_q = c.m_q[l]; P.m_kv = c.m_kv[l]; P.c = c.c[l];
+    P.n_qkv = (P.m_q + 2 * P.m_kv) * dh; P.ld_o = P.m_q * dh; P.ld_d = P.c;
+    P.qkv = P.o = P.g = P.u = P.dn = nullptr;
+    P.s_qkv = P.s_o = P.s_g = P.s_u = P.s_d = nullptr;
+    P.an = const_cast<uint16_t*>(S.attn_norm);
+    P.fn = const_cast<uint16_t*>(S.ffn_norm);
+    SharedLayer& Q = p->sl[l];
+    Q.qkv = S.wqkv.w; Q.o = S.wo.w; Q.g = S.wg.w; Q.u = S.wu.w; Q.d = S.wd.w;
+    Q.s_qkv = S.wqkv.scale; Q.s_o = S.wo.scale; Q.s_g = S.wg.scale; Q.s_u = S.wu.scale;
+    Q.s_d = S.wd.scale;
+    Q.qkv_rows = reinterpret_cast<int*>(at(Y.qkv_rows)) + size_t(l) * (Hq + 2 * Hkv) * dh;
+    Q.o_cols = reinterpret_cast<int*>(at(Y.o_cols)) + size_t(l) * (Hq * dh / 16);
+    Q.ffn_rows = dffn + size_t(l) * F;
+    Q.down_cols = reinterpret_cast<int*>(at(Y.down_cols)) + size_t(l) * (F / 16);
+  }
+  p->final_norm = d.vocab ? const_cast<uint16_t*>(store->final_norm) : nullptr;
+  p->lm_head = d.vocab ? const_cast<uint16_t*>(store->lm_head) : nullptr;
+  const int half = dh / 2;
+  std::vector<float> tc(size_t(d.max_seq) * half), ts(size_t(d.max_seq) * half);
+  for (int t = 0; t < d.max_seq; ++t)
+    for (int i = 0; i < half; ++i) {
+      const double ang = double(t) * std::pow(d.rope_theta, -2.0 * i / dh);
+      tc[size_t(t) * half + i] = float(std::cos(ang));
+      ts[size_t(t) * half + i] = float(std::sin(ang));
+    }
+  p->rope_cos = reinterpret_cast<float*>(at(Y.rope_cos));
+  p->rope_sin = reinterpret_cast<float*>(at(Y.rope_sin));
+  hipError_t h = hipMemcpyAsync(p->rope_cos, tc.data(), tc.size() * 4, hipMemcpyHostToDevice, s);
+  if (h == hipSuccess) h = hipMemcpyAsync(p->rope_sin, ts.data(), ts.size() * 4, hipMemcpyHostToDevice, s);
+  if (h == hipSuccess) h = tasp::launch_fill_zero(at(Y.zero_begin), Y.zero_end - Y.zero_begin, s);
+  p->r_mid = reinterpret_cast<float*>(at(Y.r_mid));
+  p->r_io[0] = reinterpret_cast<float*>(at(Y.r_io0));
+  p->r_io[1] = reinterpret_cast<float*>(at(Y.r_io1));
+  p->qkv_buf = reinterpret_cast<float*>(at(Y.qkv_buf));
+  p->o_buf = reinterpret_cast<float*>(at(Y.o_buf));
+  p->h_buf = reinterpret_cast<float*>(at(Y.h_buf));
+  p->part = reinterpret_cast<float*>(at(Y.part));
+  p->n_split_max = Y.n_split_max; p->ld_qkv = Y.ld_qkv; p->ld_obuf = Y.ld_obuf; p->ld_h = Y.ld_h;
+  p->xd = p->xo = p->xh = p->pxd = p->pxw = p->pq = nullptr;
+  p->ssq = p->pqkv = p->pr_mid = p->pr_io[0] = p->pr_io[1] = p->pssq = nullptr;
+  p->ld_xd = p->ld_xo = p->ld_xh = p->ld_xw = 0;
+  if ((st = read_back_indices(p, c, Y, ws, s, h)) != TASP_OK) {
+    delete p;
+    return st;
+  }
+  // the maps, checked against the host's reading of the index lists
+  {
+    std::vector<int> qr(size_t(L) * (Hq + 2 * Hkv) * dh), oc(size_t(L) * (Hq * dh / 16)),
+        dc(size_t(L) * (F / 16));
+    h = hipMemcpy(qr.data(), at(Y.qkv_rows), qr.size() * 4, hipMemcpyDeviceToHost);
+    if (h == hipSuccess) h = hipMemcpy(oc.data(), at(Y.o_cols), oc.size() * 4, hipMemcpyDeviceToHost);
+    if (h == hipSuccess) h = hipMemcpy(dc.data(), at(Y.down_cols), dc.size() * 4, hipMemcpyDeviceToHost);
+    if (h != hipSuccess) {
+      delete p;
+      return fail(TASP_ERR_HIP, "compile: %s", hipGetErrorString(h));
+    }
+    for (int l = 0; l < L; ++l) {
+      const LayerPlan& P = p->layers[l];
+      bool ok = true;
+      const int* lq = qr.data() + size_t(l) * (Hq + 2 * Hkv) * dh;
+      for (int i = 0; i < P.m_q; ++i)
+        for (int e = 0; e < dh; ++e) ok &= lq[i * dh + e] == P.q_idx[i] * dh + e;
+      for (int j = 0; j < P.m_kv; ++j)
+        for (int e = 0; e < dh; ++e) {
+          ok &= lq[(P.m_q + j) * dh + e] == (Hq + P.kv_idx[j]) * dh + e;
+          ok &= lq[(P.m_q + P.m_kv + j) * dh + e] == (Hq + Hkv + P.kv_idx[j]) * dh + e;
+        }
+      const int* lo = oc.data() + size_t(l) * (Hq * dh / 16);
+      for (int q = 0; q < P.m_q * dh / 16; ++q) ok &= lo[q] == P.q_idx[q * 16 / dh] * dh + (q * 16) % dh;
+      const int* ld = dc.data() + size_t(l) * (F / 16);
+      for (int q = 0; q < P.c / 16; ++q) ok &= ld[q] == P.ffn_idx[q * 16];
+      if (!ok) {
+        delete p;
+        return fail(TASP_ERR_INTERNAL, "layer %d: device maps differ from the index lists", l);
+      }
+    }
+  }
+  double num = 0.0, den = 0.0;
+  uint64_t wb = 0, sb = 0;
+  const int D = d.d_model;
+  for (int l = 0; l < L; ++l) {
+    const LayerPlan& P = p->layers[l];
+    num += layer_flops(desc, P.m_q, P.m_kv, P.c);
+    den += layer_flops(desc, Hq, Hkv, F);
+    wb += uint64_t(P.n_qkv) * D + uint64_t(D) * P.m_q * dh + 3ull * D * P.c;
+    // one BF16 scale per 128 weights read
+    sb += 2ull * ((uint64_t(P.n_qkv) * D + uint64_t(D) * P.m_q * dh + 3ull * D * P.c) / 128);
+  }
+  p->ratio = num / den;
+  p->weight_bytes = wb;
+  p->scale_bytes = sb;
+  p->sig = plan_signature(d, c, 1);
   *out = p;
   return TASP_OK;
 }
@@ -934,6 +1305,7 @@ tasp_status tasp_plan_panel(tasp_plan p, int32_t layer, int32_t which, const int
                             const float** scale, int64_t* rows, int64_t* cols, int64_t* ld) {
   if (!p) return fail(TASP_ERR_INVALID_ARG, "plan is NULL");
   if (layer < 0 || layer >= p->desc.n_layers) return fail(TASP_ERR_INVALID_ARG, "bad layer %d", layer);
+  if (p->shared) return fail(TASP_ERR_UNSUPPORTED, "a shared-store plan owns no panels");
   const LayerPlan& P = p->layers[layer];
   const int D = p->desc.d_model;
   const int8_t* pw;
@@ -1016,6 +1388,8 @@ tasp_status tasp_profile_stage(const tasp_plan* plans, const tasp_kv_cache* cach
   std::vector<tasp::GemvArgs> args(n_plans);
   std::vector<tasp::MfmaArgs> margs(n_plans);
   std::vector<tasp::AttnArgs> aargs(n_plans);
+  std::vector<tasp::SharedGemvArgs> sargs(n_plans);
+  std::vector<char> shared(n_plans, 0);
   int batch = 0;
   for (int i = 0; i < n_plans; ++i) {
     const tasp_plan_s* p = plans[i];
@@ -1030,8 +1404,11 @@ tasp_status tasp_profile_stage(const tasp_plan* plans, const tasp_kv_cache* cach
     const LayerPlan& P = p->layers[layer];
     if (kind == 3 && P.c == 0) return fail(TASP_ERR_SHAPE, "layer has no FFN channels");
     if (kind == 1 && P.m_kv == 0) return fail(TASP_ERR_SHAPE, "layer has no retained KV group");
+    shared[i] = p->shared;
     if (kind == 1)
       aargs[i] = attn_args(p, layer, &caches[i], pos, batch, batch > 1);
+    else if (p->shared)
+      sargs[i] = (kind == 3) ? shared_gateup_args(p, layer) : shared_down_args(p, layer, p->r_io[layer & 1]);
     else if (batch == 1)
       args[i] = (kind == 3) ? gateup_args(p, layer, batch)
                             : down_args(p, layer, batch, p->r_io[layer & 1]);
@@ -1043,6 +1420,7 @@ tasp_status tasp_profile_stage(const tasp_plan* plans, const tasp_kv_cache* cach
   const tasp::MfmaMode mmode = (kind == 3) ? tasp::MM_GATEUP : tasp::MM_RESID;
   auto launch = [&](int i, hipStream_t s) {
     if (kind == 1) return tasp::launch_attn_decode(aargs[i], s);
+    if (shared[i]) return tasp::launch_shared_gemv(mode, sargs[i], s);
     return (batch == 1) ? tasp::launch_gemv(mode, args[i], s) : tasp::launch_mfma_gemv(mmode, margs[i], s);
   };
   hipStream_t s = static_cast<hipStream_t>(stream);
@@ -1336,5 +1714,3 @@ tasp_status tasp_copy_probe(void* dst, const void* src, size_t bytes, void* stre
   HIP_TRY(tasp::launch_copy(dst, src, bytes, static_cast<hipStream_t>(stream)));
   return TASP_OK;
 }
-
-}  // extern "C"

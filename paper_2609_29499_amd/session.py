@@ -65,6 +65,43 @@ class DeviceStore:
                                    self.lm_head.data_ptr() if self.lm_head is not None else None)
 
 
+class GroupStore:
+    """The packed groupwise store on the device. ``layers`` is a list of dicts ``name: (int8
+    [out][in], BF16 scale bits uint16 [out][in / 128])`` for wq, wk, wv, wo, wg, wu, wd plus the
+    two gains; wq, wk and wv are stacked into the store's QKV matrix (layout only)."""
+
+    def __init__(self, layers, final_norm=None, lm_head=None, device="cuda"):
+        self.tensors = []
+        arr = (B.tasp_glayer * len(layers))()
+        for i, lay in enumerate(layers):
+            keep = {}
+            qkv = (np.concatenate([lay["wq"][0], lay["wk"][0], lay["wv"][0]]),
+                   np.concatenate([lay["wq"][1], lay["wk"][1], lay["wv"][1]]))
+            for n, (w, sc) in (("wqkv", qkv), ("wo", lay["wo"]), ("wg", lay["wg"]),
+                               ("wu", lay["wu"]), ("wd", lay["wd"])):
+                w, sc = _dev(w, device), _dev(np.ascontiguousarray(sc, np.uint16).view(np.int16), device)
+                keep[n] = (w, sc)
+                setattr(arr[i], n, B.tasp_gqmat(w.data_ptr(), sc.data_ptr()))
+            for n in ("attn_norm", "ffn_norm"):
+                g = _dev(lay[n], device)
+                keep[n] = g
+                setattr(arr[i], n, g.data_ptr())
+            self.tensors.append(keep)
+        self.final_norm = None if final_norm is None else _dev(final_norm, device)
+        self.lm_head = None if lm_head is None else _dev(lm_head, device)
+        self._layers = arr
+        self.struct = B.tasp_gstore(arr, self.final_norm.data_ptr() if self.final_norm is not None else None,
+                                    self.lm_head.data_ptr() if self.lm_head is not None else None)
+
+    def nbytes(self):
+        n = sum(t.numel() * t.element_size() for lay in self.tensors for v in lay.values()
+                for t in (v if isinstance(v, tuple) else (v,)))
+        for t in (self.final_norm, self.lm_head):
+            if t is not None:
+                n += t.numel() * t.element_size()
+        return n
+
+
 def mask_struct(mask):
     """(q_keep, kv_keep or None, ffn_keep) uint8 numpy arrays -> (tasp_mask, keepalive)."""
     if mask is None:
@@ -116,6 +153,23 @@ class Plan:
             except Exception:
                 pass
             self.handle = None
+
+    @classmethod
+    def shared(cls, desc, gstore, mask=None, stream=None, device="cuda"):
+        """A plan over the shared groupwise store (no weight copies)."""
+        self = cls.__new__(cls)
+        self.desc = desc
+        self.store = gstore
+        mptr, self._mask_keep = mask_struct(mask)
+        self.ws_bytes = B.tasp_shared_plan_workspace_bytes(desc)
+        self.ws = torch.empty(self.ws_bytes + 256, dtype=torch.uint8, device=device)
+        off = (-self.ws.data_ptr()) % 256
+        self.ws_base = self.ws.data_ptr() + off
+        self.ws_off = off
+        self.handle = B.tasp_compile_shared_plan(desc, gstore.struct, mptr, self.ws_base,
+                                                 self.ws_bytes,
+                                                 stream if stream is not None else current_stream())
+        return self
 
     def counts(self, layer):
         return B.tasp_plan_counts(self.handle, layer)

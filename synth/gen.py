@@ -200,14 +200,18 @@ def tiny_mask(sh: Shape, seed: int = 1):
     return q, kv, f
 
 
-def raw_mask(sh: Shape, seed: int, p_q=0.7, p_kv=0.8, p_f=0.6):
+def raw_mask(sh: Shape, seed: int, p_q=0.7, p_kv=0.8, p_f=0.6, block: int = 1):
     """Independent Bernoulli keep bits per query head, KV group and FFN channel. The result is
     generally not dependency-closed (a kept head may sit in a dropped group, a kept group may
-    have no kept head), which exercises the closure."""
+    have no kept head), which exercises the closure. With ``block`` > 1 the FFN bits are drawn
+    per aligned block of that many channels."""
     rng = np.random.default_rng([seed, 77])
     L = sh.n_layers
     q = (rng.uniform(size=(L, sh.n_q_heads)) < p_q).astype(np.uint8)
     kv = (rng.uniform(size=(L, sh.n_kv_heads)) < p_kv).astype(np.uint8)
+    if block > 1:
+        fb = (rng.uniform(size=(L, sh.d_ffn // block)) < p_f).astype(np.uint8)
+        return q, kv, np.repeat(fb, block, axis=1)
     f = (rng.uniform(size=(L, sh.d_ffn)) < p_f).astype(np.uint8)
     return q, kv, f
 

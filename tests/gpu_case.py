@@ -19,11 +19,13 @@ NAN_BF16 = np.uint16(0x7FC0)
 
 class Case:
     def __init__(self, sh, mask, batch, pos, max_seq=None, seed_w=0, seed_x=1, seed_kv=2,
-                 with_lm_head=None, store=None, device="cuda"):
+                 with_lm_head=None, store=None, device="cuda", shared=False):
+        """shared: a groupwise store (BF16 scales per 128 inputs) and a shared-store plan."""
         self.sh, self.batch, self.pos = sh, batch, pos
         self.max_seq = max_seq or pos + 1
         self.mask = mask
-        self.store = store if store is not None else [synth.layer_weights(sh, l, seed_w)
+        quant = "group" if shared else "row"
+        self.store = store if store is not None else [synth.layer_weights(sh, l, seed_w, quant=quant)
                                                       for l in range(sh.n_layers)]
         lm = sh.vocab > 0 if with_lm_head is None else with_lm_head
         self.final_norm = synth.final_norm(sh, seed_w) if lm else None
@@ -32,8 +34,12 @@ class Case:
                                      sh.group_size)
         self.x = synth.activations(batch, sh.d_model, seed_x)
         self.desc = S.desc_from_shape(sh, max_batch=batch, max_seq=self.max_seq)
-        self.dstore = S.DeviceStore(self.store, self.final_norm, self.lm_head, device)
-        self.plan = S.Plan(self.desc, self.dstore, mask)
+        if shared:
+            self.dstore = S.GroupStore(self.store, self.final_norm, self.lm_head, device)
+            self.plan = S.Plan.shared(self.desc, self.dstore, mask)
+        else:
+            self.dstore = S.DeviceStore(self.store, self.final_norm, self.lm_head, device)
+            self.plan = S.Plan(self.desc, self.dstore, mask)
         torch.cuda.synchronize()
         self.priors = [synth.kv_prior(sh, l, batch, pos, self.max_seq, seed_kv)
                        for l in range(sh.n_layers)]

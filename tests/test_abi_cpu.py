@@ -3,6 +3,8 @@ bad arguments on the host before enqueuing any GPU work (no GPU needed)."""
 import ctypes as C
 import os
 import re
+import shutil
+import subprocess
 
 import numpy as np
 import pytest
@@ -26,6 +28,14 @@ def test_every_declared_symbol_is_exported():
     assert declared == set(B.EXPORTS)
     for name in declared:
         assert hasattr(lib, name), name
+    # and nothing else: internal helpers keep internal linkage
+    nm = shutil.which("nm")
+    if nm:
+        out = subprocess.run([nm, "-D", "--defined-only", B.LIB_PATH], capture_output=True,
+                             text=True, check=True).stdout
+        c_names = {l.split()[-1] for l in out.splitlines()
+                   if l.split()[1:2] == ["T"] and not l.split()[-1].startswith("_Z")}
+        assert c_names == declared, c_names ^ declared
 
 
 def _desc(**kw):
@@ -178,3 +188,33 @@ def test_router_workspace_and_argument_checks():
     with pytest.raises(B.TaspError) as e:
         B.tasp_route(r, 4096, -1, None, 1, 4096, ws, nb, None, 4096, 4096, None)
     assert B.STATUS[e.value.status] == "TASP_ERR_INVALID_ARG"
+
+
+def test_shared_plan_host_checks():
+    """Shared-store plans: mask-independent workspace, one-sequence descs, 128-divisible widths,
+    and retained channels in aligned blocks of 16; all rejected before any GPU work."""
+    _lib()
+    d = _desc(d_model=512, d_ffn=1536, max_batch=1)
+    n = B.tasp_shared_plan_workspace_bytes(d)
+    assert n > 0 and n < B.tasp_plan_workspace_bytes(d, None)
+    for bad, status in ((dict(max_batch=2), "TASP_ERR_UNSUPPORTED"),
+                        (dict(max_prefill=16), "TASP_ERR_UNSUPPORTED"),
+                        (dict(d_model=528), "TASP_ERR_SHAPE"),
+                        (dict(d_ffn=1552), "TASP_ERR_SHAPE")):
+        with pytest.raises(B.TaspError) as e:
+            B.tasp_shared_plan_workspace_bytes(_desc(**{**dict(d_model=512, d_ffn=1536, max_batch=1), **bad}))
+        assert B.STATUS[e.value.status] == status, bad
+    fake = 1 << 20                          # never dereferenced: the checks run on the host
+    lay = B.tasp_glayer(*([B.tasp_gqmat(fake, fake)] * 5), fake, fake)
+    layers = (B.tasp_glayer * 1)(lay)
+    store = B.tasp_gstore(layers, None, None)
+    q = np.ones((1, 8), np.uint8)
+    f = np.ones((1, 1536), np.uint8)
+    f[0, 5] = 0                             # breaks the block of channels 0..15
+    m = B.tasp_mask(q.ctypes.data, None, f.ctypes.data)
+    with pytest.raises(B.TaspError) as e:
+        B.tasp_compile_shared_plan(d, store, C.pointer(m), 1 << 30, n, None)
+    assert B.STATUS[e.value.status] == "TASP_ERR_UNSUPPORTED"
+    with pytest.raises(B.TaspError) as e:
+        B.tasp_compile_shared_plan(d, store, None, (1 << 30) + 8, n, None)
+    assert B.STATUS[e.value.status] == "TASP_ERR_WORKSPACE"

@@ -1,0 +1,201 @@
+"""GPU parity of shared-store plans (groupwise INT8 with BF16 scales per 128 inputs; plans are
+maps into one store and copy no weights) against the oracle, and the one-store validation: a
+shared-store plan against a separately materialised plan at identical quantisation scales (max
+absolute logit difference below 2e-3 and at least 99.98% greedy-token agreement, the targets
+the paper states for its one-store check)."""
+import numpy as np
+import pytest
+import torch
+
+import synth
+from paper_2609_29499_amd import binding as B
+from paper_2609_29499_amd import session as S
+from tests.gpu_case import Case
+from tests.helpers import assert_parity
+
+pytestmark = pytest.mark.gpu
+
+
+def _flush(msg):
+    print(msg, flush=True)
+
+
+def _check(case):
+    got = case.run()
+    want = case.oracle()
+    return assert_parity(got, want, what="shared decode")
+
+
+TINY = dict(d=256, hq=8, hkv=2, dh=64, f=512)
+
+
+@pytest.mark.parametrize("seed,pos", [(1, 0), (2, 1), (3, 77), (4, 300)])
+def test_tiny_layer_block_masks(seed, pos):
+    _flush(f"case shared tiny seed={seed} pos={pos}")
+    sh = synth.tiny_shape(layers=1, **TINY)
+    _check(Case(sh, synth.raw_mask(sh, seed, block=16), 1, pos, shared=True))
+
+
+def test_tiny_layer_dense_and_head_dim_128():
+    _flush("case shared dense / dh128")
+    sh = synth.tiny_shape(layers=1, **TINY)
+    _check(Case(sh, None, 1, 64, shared=True))
+    sh = synth.tiny_shape(d=512, hq=8, hkv=2, dh=128, f=1024, layers=1)
+    _check(Case(sh, synth.raw_mask(sh, 5, block=16), 1, 129, shared=True))
+
+
+def test_empty_modules():
+    """A layer with no retained head and no channel: both branches add zero."""
+    _flush("case shared empty modules")
+    sh = synth.tiny_shape(layers=2, **TINY)
+    q, kv, f = synth.all_kept_mask(sh)
+    q[0, :] = 0
+    f[1, :] = 0
+    f[0, 64:128] = 0
+    _check(Case(sh, (q, kv, f), 1, 33, shared=True))
+
+
+def test_stack_with_lm_head():
+    _flush("case shared stack + LM head")
+    sh = synth.tiny_shape(layers=3, vocab=3000, **TINY)
+    case = Case(sh, synth.raw_mask(sh, 6, block=16), 1, 40, shared=True)
+    got = case.run()
+    want = case.oracle()
+    assert_parity(got, want, what="logits")
+    margin = np.sort(want[0])[-2:]
+    if margin[1] - margin[0] > 1e-2 * np.abs(want).max():
+        assert int(np.argmax(got[0])) == int(np.argmax(want[0]))
+
+
+def test_llama3_8b_layer_budget_mask():
+    """Full Llama-3-8B layer, seed-1 budget mask (128-channel granules), 2048 prior positions."""
+    _flush("case shared 8B layer")
+    sh = synth.LLAMA3_8B.with_layers(1, vocab=0)
+    _check(Case(sh, synth.budget_mask(sh, 1), 1, 2048, shared=True))
+
+
+def test_graph_replay_and_timed_kernels():
+    _flush("case shared graph replay")
+    sh = synth.tiny_shape(layers=2, **TINY)
+    case = Case(sh, synth.raw_mask(sh, 7, block=16), 1, 50, shared=True)
+    eager = case.run().copy()
+    g = torch.cuda.CUDAGraph()
+    st = torch.cuda.Stream()
+    st.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(st):
+        case.plan.decode(case.xd, case.cache, case.pos, case.out, stream=S.current_stream())
+    torch.cuda.current_stream().wait_stream(st)
+    torch.cuda.synchronize()
+    with torch.cuda.graph(g):
+        case.plan.decode(case.xd, case.cache, case.pos, case.out, stream=S.current_stream())
+    for rep in range(3):
+        case.out.fill_(float("nan"))
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert np.array_equal(case.out.cpu().numpy().astype(np.float64), eager), rep
+    kinds = [k for k, _ in case.plan.decode_timed(case.xd, case.cache, case.pos, case.out)]
+    assert kinds == ["qkv_gemv", "attention", "o_gemv", "gateup_gemv", "down_gemv"] * 2
+
+
+def test_shared_plans_own_no_weights():
+    """Five masks over one store: every plan's workspace has the same small size (metadata and
+    scratch), no weights are copied, and the device allocation grows by the workspaces only."""
+    _flush("case shared memory ledger")
+    sh = synth.tiny_shape(layers=2, vocab=1000, **TINY)
+    layers = [synth.layer_weights(sh, l, quant="group") for l in range(sh.n_layers)]
+    desc = S.desc_from_shape(sh, max_batch=1, max_seq=256)
+    store = S.GroupStore(layers, synth.final_norm(sh), synth.lm_head(sh))
+    torch.cuda.synchronize()
+    before = torch.cuda.memory_allocated()
+    plans = [S.Plan.shared(desc, store, synth.raw_mask(sh, 10 + i, block=16)) for i in range(5)]
+    torch.cuda.synchronize()
+    grown = torch.cuda.memory_allocated() - before
+    ws = {p.ws_bytes for p in plans}
+    assert len(ws) == 1
+    assert grown <= 5 * (ws.pop() + 1024)
+    # a materialised plan of the same mask holds its panels
+    mat = S.Plan(S.desc_from_shape(sh, max_batch=1, max_seq=256),
+                 S.DeviceStore([synth.layer_weights(sh, l) for l in range(2)], synth.final_norm(sh),
+                               synth.lm_head(sh)), synth.raw_mask(sh, 10, block=16))
+    assert mat.ws_bytes > plans[0].ws_bytes + plans[0].ledger()["weight_bytes"]
+    # equal masks: equal signatures within a format, different across formats
+    again = S.Plan.shared(desc, store, synth.raw_mask(sh, 10, block=16))
+    assert again.ledger()["signature"] == plans[0].ledger()["signature"]
+    assert mat.ledger()["signature"] != plans[0].ledger()["signature"]
+
+
+def test_shared_plan_rejections():
+    _flush("case shared rejections")
+    sh = synth.tiny_shape(layers=1, **TINY)
+    layers = [synth.layer_weights(sh, 0, quant="group")]
+    store = S.GroupStore(layers)
+    desc = S.desc_from_shape(sh, max_batch=1, max_seq=64)
+    with pytest.raises(B.TaspError, match="UNSUPPORTED"):
+        S.Plan.shared(desc, store, synth.raw_mask(sh, 1))          # per-channel FFN bits
+    plan = S.Plan.shared(desc, store, synth.raw_mask(sh, 1, block=16))
+    with pytest.raises(B.TaspError, match="UNSUPPORTED"):
+        plan.panel(0, B.PANEL_QKV)
+    cache = S.KVCache(desc, 1, 64)
+    x = torch.zeros((4, sh.d_model), device="cuda")
+    with pytest.raises(B.TaspError, match="UNSUPPORTED"):
+        plan.prefill(x, 4, cache, 0, torch.empty((4, sh.d_model), device="cuda"))
+    # a cache filled under the per-row plan of the same mask is refused
+    mat = S.Plan(desc, S.DeviceStore([synth.layer_weights(sh, 0)]), synth.raw_mask(sh, 1, block=16))
+    mat.bind(cache)
+    with pytest.raises(B.TaspError, match="CACHE_PLAN_MISMATCH"):
+        plan.decode(torch.zeros((1, sh.d_model), device="cuda"), cache, 3,
+                    torch.empty((1, sh.d_model), device="cuda"))
+
+
+def _equal_scale_stores(sh):
+    """The same INT8 bytes as a per-row store (BF16-valued float32 scales) and as a groupwise
+    store whose group scales all equal the row's: identical quantisation in the two formats."""
+    rows, groups = [], []
+    for l in range(sh.n_layers):
+        lw = synth.layer_weights(sh, l, quant="row_bf16")
+        gw = dict(lw)
+        for n in synth.WEIGHT_NAMES:
+            q, s = lw[n]
+            gw[n] = (q, np.repeat(synth.to_bf16_bits(s)[:, None], q.shape[1] // 128, axis=1))
+        rows.append(lw)
+        groups.append(gw)
+    return rows, groups
+
+
+def test_one_store_validation_greedy_decode():
+    """Shared-store vs materialised plans of three masks, 48 greedy steps each from the same
+    start: max |logit difference| < 2e-3 and >= 99.98% token agreement (teacher-forced on the
+    materialised plan's tokens so every step compares the same history)."""
+    _flush("case one-store validation")
+    sh = synth.tiny_shape(layers=4, vocab=4000, **TINY)
+    rows, groups = _equal_scale_stores(sh)
+    fn, lm = synth.final_norm(sh), synth.lm_head(sh)
+    table, scales = synth.embedding(sh)
+    steps = 48
+    desc = S.desc_from_shape(sh, max_batch=1, max_seq=steps + 1)
+    mstore = S.DeviceStore(rows, fn, lm)
+    gstore = S.GroupStore(groups, fn, lm)
+    worst, agree, total = 0.0, 0, 0
+    for seed in (21, 22, 23):
+        mask = synth.raw_mask(sh, seed, block=16)
+        pm, ps = S.Plan(desc, mstore, mask), S.Plan.shared(desc, gstore, mask)
+        cm, cs = S.KVCache(desc, 1, steps + 1), S.KVCache(desc, 1, steps + 1)
+        pm.bind(cm)
+        ps.bind(cs)
+        tok = 7
+        lm_out = torch.empty((1, sh.vocab), device="cuda")
+        ls_out = torch.empty((1, sh.vocab), device="cuda")
+        for pos in range(steps):
+            x = torch.from_numpy((table[tok].astype(np.float32) * scales[tok])[None, :]).cuda()
+            pm.decode(x, cm, pos, lm_out)
+            ps.decode(x, cs, pos, ls_out)
+            torch.cuda.synchronize()
+            a, b = lm_out.cpu().numpy()[0], ls_out.cpu().numpy()[0]
+            assert np.all(np.isfinite(b))
+            worst = max(worst, float(np.abs(a - b).max()))
+            agree += int(np.argmax(a) == np.argmax(b))
+            total += 1
+            tok = int(np.argmax(a))
+    assert worst < 2e-3, worst
+    assert agree / total >= 0.9998, (agree, total)
