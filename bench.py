@@ -73,12 +73,13 @@ def layer_bytes(sh, m_q, m_kv, c, pos, batch=1):
 class Rotation:
     """R compiled copies of one plan with their own KV caches, and HIP graphs of one step each."""
 
-    def __init__(self, S, torch, sh, desc, dstore, mask, prior, x, pos, copies):
+    def __init__(self, S, torch, sh, desc, dstore, mask, prior, x, pos, copies, make_plan=None):
+        """make_plan(i): the plan of copy i (default: a plan of `mask` compiled from dstore)."""
         self.plans, self.caches = [], []
         batch = x.shape[0]
         self.batch = batch
-        for _ in range(copies):
-            plan = S.Plan(desc, dstore, mask)
+        for i in range(copies):
+            plan = make_plan(i) if make_plan else S.Plan(desc, dstore, mask)
             cache = S.KVCache(desc, batch, pos + 1)
             cache.load_layer(0, *prior)
             plan.bind(cache)
@@ -556,6 +557,129 @@ def bench_mask(args, wl):
     print(json.dumps(line), flush=True)
 
 
+def shared_ledger(S, B, sh, seeds):
+    """Device bytes of the store and of 1 .. len(seeds) plans in both formats, from the
+    library's workspace queries (no allocation): a shared-store plan adds its fixed metadata
+    and scratch; a materialised plan holds its own panels (its store can be freed)."""
+    import synth
+    d, dh, F = sh.d_model, sh.head_dim, sh.d_ffn
+    per_layer = ((sh.n_q_heads + 2 * sh.n_kv_heads) * dh * d + d * sh.n_q_heads * dh + 3 * F * d)
+    weights = sh.n_layers * per_layer
+    scales = weights // 128 * 2
+    gains = sh.n_layers * 2 * d * 2 + (d * 2 + sh.vocab * d * 2 if sh.vocab else 0)
+    desc = S.desc_from_shape(sh, max_batch=1, max_seq=4096)
+    ws_shared = B.tasp_shared_plan_workspace_bytes(desc)
+    mats = []
+    for sd in seeds:
+        mptr, keep = S.mask_struct(synth.budget_mask(sh, sd))
+        mats.append(B.tasp_plan_workspace_bytes(desc, mptr))
+    rows = []
+    for n in (1, 3, len(seeds)):
+        rows.append({"masks": n, "shared_GB": round((weights + scales + gains + n * ws_shared) / 1e9, 3),
+                     "shared_metadata_GB": round(n * ws_shared / 1e9, 4),
+                     "materialised_GB": round(sum(mats[:n]) / 1e9, 3)})
+    return {"store_weight_GB": round(weights / 1e9, 3), "store_scale_GB": round(scales / 1e9, 3),
+            "plan_workspace_MB": round(ws_shared / 1e6, 2), "by_masks": rows,
+            "note": "workspaces include the RoPE table and decode scratch at max_seq 4096"}
+
+
+def bench_shared(args, wl):
+    """Batch-1 decode of one layer from shared-store plans (groupwise INT8, BF16 scales per 128
+    inputs; plans are maps into the store) against the materialised per-row plan of the same
+    mask, with every timed step reading its weights from HBM (rotation over store copies), the
+    shared gate/up kernel's roofline, and the memory ledger at the 8B and 70B shapes."""
+    import torch
+    import synth
+    from paper_2609_29499_amd import binding as B
+    from paper_2609_29499_amd import session as S
+    sh, pos = wl.shape, wl.pos
+    t0 = time.time()
+    layer_g = synth.layer_weights(sh, 0, quant="group")
+    mask = synth.budget_mask(sh, args.mask_seed)
+    prior = synth.kv_prior(sh, 0, 1, pos, pos + 1)
+    x = synth.activations(1, sh.d_model)
+    desc = S.desc_from_shape(sh, max_batch=1, max_seq=pos + 1)
+    first = S.GroupStore([layer_g])
+    store_bytes = first.nbytes()
+    copies = max(2, math.ceil(ROTATE_BYTES / store_bytes))
+    stores = [first]
+    for _ in range(copies - 1):
+        stores.append(S.GroupStore([{k: v for k, v in layer_g.items()}]))
+    torch.cuda.synchronize()
+    print(f"[bench] {wl.name}: {copies} store copies of {store_bytes / 1e6:.1f} MB in "
+          f"{time.time() - t0:.1f}s", file=sys.stderr, flush=True)
+    results = {}
+    for name, m in (("shared_sparse", mask), ("shared_dense", None)):
+        rot = Rotation(S, torch, sh, desc, None, m, prior, x, pos, copies,
+                       make_plan=lambda i, m=m: S.Plan.shared(desc, stores[i], m))
+        rot.run_steps(args.warmup)
+        ms = rot.time_steps(args.steps)
+        kt = rot.kernel_times(args.timed_launches)
+        st_ms = rot.stage_ms(STAGE_KIND["gateup_gemv"]) if name == "shared_sparse" else None
+        counts = rot.plans[0].counts(0)
+        results[name] = {"ms": ms, "kernels": kt, "stage_ms": st_ms, "counts": counts,
+                         "ledger": rot.plans[0].ledger()}
+        print(f"[bench] {name}: {ms * 1e3:.2f} us/step kernels(us)=" +
+              " ".join(f"{k}={v * 1e3:.2f}" for k, v in kt.items()), file=sys.stderr, flush=True)
+        del rot
+        torch.cuda.empty_cache()
+    del stores, first
+    torch.cuda.empty_cache()
+    # the materialised per-row plan of the same mask (the default benchmark's sparse plan)
+    layer_r = synth.layer_weights(sh, 0)
+    dstore = S.DeviceStore([layer_r])
+    probe = S.Plan(desc, dstore, mask)
+    nb = layer_bytes(sh, *probe.counts(0), pos, 1)
+    mat_ws = probe.ws_bytes
+    del probe
+    mcopies = max(2, math.ceil(ROTATE_BYTES / nb["total"]))
+    rot = Rotation(S, torch, sh, desc, dstore, mask, prior, x, pos, mcopies)
+    rot.run_steps(args.warmup)
+    mat_ms = rot.time_steps(args.steps)
+    del rot
+    torch.cuda.empty_cache()
+    print(f"[bench] materialised per-row: {mat_ms * 1e3:.2f} us/step", file=sys.stderr, flush=True)
+    sp = results["shared_sparse"]
+    c = sp["counts"][2]
+    d = sh.d_model
+    gu_bytes = 2 * c * d + 2 * c * (d // 128) * 2 + d * 4 + c * 4
+    gu_gbps = gu_bytes / (sp["stage_ms"] * 1e-3) / 1e9
+    line = {
+        "metric": METRIC, "value": round(sp["ms"], 6), "unit": "ms/token", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(sp["ms"], 6),
+        "higher_is_better": False, "scaling": "weak", "vs_baseline": None, "dtype": "int8w-g128-f32",
+        "data": "synthetic",
+        "config": {"workload": wl.name, "d_model": d, "layers": 1, "batch": 1, "pos": pos,
+                   "mask_seed": args.mask_seed, "scales": "BF16 per 128 inputs",
+                   "retained": {"q_heads": sp["counts"][0], "kv_groups": sp["counts"][1],
+                                "ffn_channels": c}},
+        "us_per_layer": {"shared_sparse": round(sp["ms"] * 1e3, 3),
+                         "shared_dense": round(results["shared_dense"]["ms"] * 1e3, 3),
+                         "materialised_per_row_sparse": round(mat_ms * 1e3, 3)},
+        "speedup_vs_shared_dense": round(results["shared_dense"]["ms"] / sp["ms"], 4),
+        "kernels_us": {k: {n: round(v * 1e3, 3) for n, v in r["kernels"].items()}
+                       for k, r in results.items()},
+        "roofline": {"bound": "hbm", "kernel": "shared_gateup_gemv", "achieved": round(gu_gbps, 1),
+                     "peak": PEAK_GBPS, "unit": "GB/s", "frac": round(gu_gbps / PEAK_GBPS, 4),
+                     "traffic": None, "algorithmic_bytes": gu_bytes,
+                     "avg_launch_us": round(sp["stage_ms"] * 1e3, 3)},
+        "memory": {"layer_store_MB": round(store_bytes / 1e6, 1),
+                   "shared_plan_workspace_MB": round(B.tasp_shared_plan_workspace_bytes(desc) / 1e6, 3),
+                   "materialised_plan_workspace_MB": round(mat_ws / 1e6, 1),
+                   "llama3_8b": shared_ledger(S, B, synth.LLAMA3_8B, (1, 2, 3, 4, 5)),
+                   "llama3_70b": shared_ledger(S, B, synth.LLAMA3_70B, (1, 2, 3, 4, 5))},
+        "rotation_copies": {"shared": copies, "materialised": mcopies},
+        "paper_context": "one packed store for five 70B masks: 76.9 / 77.1 / 77.3 GB peak for 1 / 3 / 5 "
+                         "masks, plan metadata 0.14 / 0.34 / 0.54 GB (A100 runtime)",
+    }
+    if not args.no_cpu:
+        print("[bench] timing the CPU oracle", file=sys.stderr, flush=True)
+        line["cpu_baseline"] = cpu_baseline(sh, layer_g, mask, prior, x, pos, args.cpu_seconds)
+    else:
+        line["cpu_baseline"] = None
+    print(json.dumps(line), flush=True)
+
+
 ROUTER_TAUS = (0.50, 0.70, 0.85, 0.95)
 PAPER_USAGE_085 = 0.76       # sparse-path share at tau = 0.85 in the paper's threshold sweep
 
@@ -715,6 +839,9 @@ def main():
         return
     if wl.kind == "router":
         bench_router(args, wl)
+        return
+    if wl.kind == "shared":
+        bench_shared(args, wl)
         return
     if sh.n_layers > 1 and wl.batch == 1 and wl.prefill_tokens == 0:
         bench_stack(args, wl)

@@ -6,6 +6,7 @@
 #   decode_b8:  kernel trace and FETCH_SIZE / WRITE_SIZE passes of the batch-8 benchmark
 #   prefill:    kernel trace and MFMA counter pass of the 512-token prefill benchmark
 #   router:     kernel trace of the router benchmark (one 7 KiB turn, then 512-prompt batches)
+#   shared:     kernel trace of the shared-store benchmark (8B layer, batch 1)
 set -o pipefail
 export TMPDIR=/tmp
 R=$(pwd)
@@ -29,5 +30,8 @@ prefill)
   ;;
 router)
   echo "[prof] router kernel trace" && timeout -k 10 400 rocprofv3 --kernel-trace --stats -d $O/rt_trace -o trace -- python3 -u bench.py --workload router_llama3_8b --steps 200 --warmup 20 --cpu-seconds 3 > $O/rt_trace.json 2> $O/rt_trace.err
+  ;;
+shared)
+  echo "[prof] shared kernel trace" && timeout -k 10 400 rocprofv3 --kernel-trace --stats -d $O/sh_trace -o trace -- python3 -u bench.py --workload llama3_8b_layer_shared --steps 200 --warmup 20 --cpu-seconds 3 > $O/sh_trace.json 2> $O/sh_trace.err
   ;;
 esac

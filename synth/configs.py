@@ -55,7 +55,8 @@ class Workload:
     include_dense: bool = True
     kind: str = "decode"    # "decode" (decode / prefill steps), "mask" (mask construction),
                             # "request" (prefill of prefill_tokens, then n_new greedy decode steps),
-                            # "router" (routing of user turns; the stack gives the path latencies)
+                            # "router" (routing of user turns; the stack gives the path latencies),
+                            # "shared" (batch-1 decode from the shared groupwise store)
     n_new: int = 0
     granule: int = 1024     # SwiGLU channels per candidate group (mask construction)
 
@@ -89,6 +90,10 @@ WORKLOADS = {
     # of the 32-layer 8B stack at 4096 prior positions
     "router_llama3_8b": Workload("router_llama3_8b", LLAMA3_8B, batch=1, pos=4096,
                                  mask_seeds=(1,), kind="router"),
+    # one 8B-shaped layer from the shared groupwise store (BF16 scales per 128 inputs), batch 1,
+    # 2048 prior positions, seed-1 mask
+    "llama3_8b_layer_shared": Workload("llama3_8b_layer_shared", LLAMA3_8B.with_layers(1, vocab=0),
+                                       batch=1, pos=2048, mask_seeds=(1,), kind="shared"),
     # one 8B-shaped layer: batch-8 decode, every sequence at 8192 prior positions
     "llama3_8b_batch8": Workload("llama3_8b_batch8", LLAMA3_8B.with_layers(1, vocab=0),
                                  batch=8, pos=8192, mask_seeds=(1,)),
