@@ -12,8 +12,8 @@
 // 64 rows being 32 gate rows and the 32 up rows of the same channels, so SwiGLU stays in
 // registers). Four waves in a 2 x 2 arrangement own 64 x 64 each as 4 x 4 MFMA tiles. K advances
 // in chunks of 32: the global loads of the next three chunks are in flight (in registers) while
-// the current chunk's MFMAs run from LDS (double-buffered, one barrier per chunk). LDS rows are
-// padded to 40 BF16 so that the 16 lanes reading one fragment column hit distinct banks.
+// the current chunk's MFMAs run from LDS (double-buffered, one barrier per chunk). LDS rows hold
+// one chunk (32 BF16) with their 16-byte quarters XOR-swizzled by row (bank-conflict free).
 #include "device_common.hpp"
 #include "kernels.hpp"
 
@@ -26,16 +26,24 @@ typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4;
 constexpr int kTMax = 128;             // tokens per workgroup tile (largest)
 constexpr int kTN = 128;               // panel rows per workgroup tile
 constexpr int kKC = 32;                // k per chunk
-constexpr int kLdsRow = 40;            // BF16 per LDS row (32 + padding)
+constexpr int kLdsRow = 32;            // BF16 per LDS row (one chunk of k)
 constexpr int kSsqBlk = 64;            // rows per sum-of-squares partial
 constexpr long kPfMinTiles = 384;      // fewer 128-token tiles than this: use 64-token tiles
 
 template <int TM>
 struct PfSmem {
-  uint16_t a[2][2][TM * kLdsRow];      // [buffer][hi/lo][token * 40 + k]
-  uint16_t b[2][kTN * kLdsRow];        // [buffer][row * 40 + k]
+  uint16_t a[2][2][TM * kLdsRow];      // [buffer][hi/lo][swizzled token row]
+  uint16_t b[2][kTN * kLdsRow];        // [buffer][swizzled panel row]
   float rs[TM];                        // inverse RMS of the tile's tokens
 };
+
+// LDS offset (BF16 elements) of 16-byte quarter qu of LDS row `row`. Quarters are XOR-swizzled
+// with bits 1-4 of the row: the 8 or 16 lanes served together by a 16-byte read (one fragment
+// column: 16 consecutive rows, one quarter) or write (4 consecutive rows, all quarters) then
+// touch distinct banks.
+__device__ __forceinline__ int lds_q(int row, int qu) {
+  return row * kLdsRow + 8 * (qu ^ (((row >> 1) ^ (row >> 3)) & 3));
+}
 
 __device__ __forceinline__ uint32_t pack_exact(float lo, float hi) {
   return __builtin_amdgcn_perm(__float_as_uint(hi), __float_as_uint(lo), 0x07060302u);
@@ -125,20 +133,20 @@ __global__ __launch_bounds__(kBlock) void pf_gemm_kernel(PfArgs a) {
     for (int i = 0; i < APT; ++i) {
       const int p = tid + kBlock * i;
       const int plane = p / (4 * TM), row = (p >> 2) & (TM - 1), qu = p & 3;
-      *reinterpret_cast<int4*>(&sm.a[buf][plane][row * kLdsRow + 8 * qu]) = st.av[i];
+      *reinterpret_cast<int4*>(&sm.a[buf][plane][lds_q(row, qu)]) = st.av[i];
     }
     if (BF) {
 #pragma unroll
       for (int i = 0; i < 2; ++i) {
         const int p = tid + kBlock * i;
-        *reinterpret_cast<int4*>(&sm.b[buf][(p >> 2) * kLdsRow + 8 * (p & 3)]) = st.bv[i];
+        *reinterpret_cast<int4*>(&sm.b[buf][lds_q(p >> 2, p & 3)]) = st.bv[i];
       }
     } else {
       int4 lo, hi;
       widen16(st.bv[0], lo, hi);
-      uint16_t* dst = &sm.b[buf][(tid >> 1) * kLdsRow + 16 * (tid & 1)];
-      *reinterpret_cast<int4*>(dst) = lo;
-      *reinterpret_cast<int4*>(dst + 8) = hi;
+      const int row = tid >> 1, h = tid & 1;
+      *reinterpret_cast<int4*>(&sm.b[buf][lds_q(row, 2 * h)]) = lo;
+      *reinterpret_cast<int4*>(&sm.b[buf][lds_q(row, 2 * h + 1)]) = hi;
     }
   };
 
@@ -184,10 +192,10 @@ __global__ __launch_bounds__(kBlock) void pf_gemm_kernel(PfArgs a) {
     bf16x8 bw[4];
 #pragma unroll
     for (int nt = 0; nt < 4; ++nt)
-      bw[nt] = *reinterpret_cast<const bf16x8*>(&sm.b[buf][(wn * 64 + nt * 16 + r) * kLdsRow + 8 * q]);
+      bw[nt] = *reinterpret_cast<const bf16x8*>(&sm.b[buf][lds_q(wn * 64 + nt * 16 + r, q)]);
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
-      const int ar = (wm * (TM / 2) + mt * 16 + r) * kLdsRow + 8 * q;
+      const int ar = lds_q(wm * (TM / 2) + mt * 16 + r, q);
       const bf16x8 ahi = *reinterpret_cast<const bf16x8*>(&sm.a[buf][0][ar]);
       const bf16x8 alo = *reinterpret_cast<const bf16x8*>(&sm.a[buf][1][ar]);
 #pragma unroll
