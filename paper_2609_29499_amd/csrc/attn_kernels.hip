@@ -111,8 +111,8 @@ __device__ __forceinline__ void attn_body(const AttnArgs& a, AttnSmem<DH>& sm, i
   auto issue = [&](int tb, KV& f) {
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      f.k[u] = buf_load16(rk, row_off(tb + rb + u * RPB));
-      f.v[u] = buf_load16(rv, row_off(tb + rb + u * RPB));
+      f.k[u] = buf_load16_stream(rk, row_off(tb + rb + u * RPB));
+      f.v[u] = buf_load16_stream(rv, row_off(tb + rb + u * RPB));
     }
   };
   KV fa, fb;

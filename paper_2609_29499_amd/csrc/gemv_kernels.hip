@@ -158,7 +158,7 @@ __global__ __launch_bounds__(kBlock) void gemv_kernel(GemvArgs a) {
         const int row = row_of(gi, r);
         const bool ok = ok_t && (row < N) && (k < K);
         const uint32_t off = ok ? uint32_t(row) * row_bytes + uint32_t(k) * (BF ? 2u : 1u) : kOOB;
-        w[u][r] = buf_load16((MODE == GEMV_GATEUP && r >= 2) ? rw2 : rw, off);
+        w[u][r] = buf_load16_stream((MODE == GEMV_GATEUP && r >= 2) ? rw2 : rw, off);
       }
     }
   };

@@ -151,7 +151,7 @@ __global__ __launch_bounds__(WAVES * kWave) void mfma_gemv_kernel(MfmaArgs a) {
         const int row = lane_row(tile, rt);
         const uint32_t wo = (ok && row < N && k < a.ld)
                                 ? lane_half(rt) + uint32_t(row) * row_bytes + uint32_t(k) * esz : kOOB;
-        f[u].a[rt] = buf_load16(rw, wo);
+        f[u].a[rt] = buf_load16_stream(rw, wo);
       }
       const uint32_t xo = ok ? x_base + uint32_t(k) * 2u : kOOB;
       f[u].x0 = buf_load16(rx, xo);

@@ -88,7 +88,7 @@ __global__ __launch_bounds__(kBlock) void shared_gemv_kernel(SharedGemvArgs a) {
         const uint32_t soff =
             ok ? (uint32_t(srow[r]) * lds_groups + uint32_t(scol) / kScaleGroup) * 2u : kOOB;
         const bool second = (MODE == GEMV_GATEUP && r >= 2);
-        w[u][r] = buf_load16(second ? rw2 : rw, off);
+        w[u][r] = buf_load16_stream(second ? rw2 : rw, off);
         sv[u][r] = __builtin_amdgcn_raw_buffer_load_b16(second ? rs2 : rs, int(soff), 0, 0);
       }
     }
