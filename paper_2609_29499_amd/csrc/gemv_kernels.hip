@@ -10,10 +10,11 @@
 // tiles with two register buffers in ping-pong: the next tile's 8 buffer loads are in flight
 // while the current tile is dequantised and accumulated, so arithmetic overlaps the stream.
 // Loads are branch-free: lanes past a row end and tiles past the wave's range use an
-// out-of-range buffer offset, which returns zeros without memory traffic. The first tile is
-// issued before the prologue stages the input vector in LDS (RMS-normalised when a gain is
-// given, the inverse RMS being applied in the epilogue), and the epilogue's per-row operands
-// (scales, residual) are wave-uniform scalar loads, which do not queue behind the vector loads.
+// out-of-range buffer offset, which returns zeros without memory traffic. The prologue stages
+// the input vector in LDS (RMS-normalised when a gain is given, the inverse RMS being applied in
+// the epilogue); the first tiles are issued around it (see the kernel), and the epilogue's
+// per-row operands (scales, residual) are wave-uniform scalar loads, which do not queue behind
+// the vector loads.
 //
 // INT8 dequantisation happens in registers: each byte b is XOR-ed with 0x80 so that
 // v_cvt_f32_ubyte gives b + 128 exactly; the bias is removed once per row as 128 * sum(x); the
@@ -48,14 +49,20 @@ __device__ __forceinline__ void fma_bf16x4(float& acc, uint32_t w0, uint32_t w1,
 
 // Stage B input rows of K floats into LDS (swizzled, zero padded to KP).
 // Thread t owns the float4 at columns 1024 i + 4 t (i < KP / 1024); loads are issued in
-// batches of 4 before any use. With a gain the LDS holds x * gamma and the row's inverse RMS is
-// returned in xscale (applied after the dot product: W (c x) = c (W x)); without, xscale = 1.
+// batches of 8 (4 for BF16 rows) before any use. With a gain the LDS holds x * gamma and the
+// row's inverse RMS is returned in xscale (applied after the dot product: W (c x) = c (W x));
+// without, xscale = 1.
 // For INT8 rows bias = 128 * sum of the staged values (removes the +128 of the byte conversion).
-template <int B, bool NORM, bool I8>
+// `after_first` runs right after the first batch of input loads is issued: the caller may issue
+// its first weight tile there. Vector loads retire in issue order, so waiting for the input
+// batch then does not wait for the weights, and the weight stream starts before the input
+// arrives.
+template <int B, bool NORM, bool I8, class F>
 __device__ __forceinline__ void stage_inputs(const float* __restrict__ x, int ldx, int K, int KP,
                                              const uint16_t* __restrict__ gamma, float eps,
-                                             float* xs, float* red2, float* xscale, float* bias) {
-  constexpr int kBatch = 4;
+                                             float* xs, float* red2, float* xscale, float* bias,
+                                             F&& after_first) {
+  constexpr int kBatch = I8 ? 8 : 4;                    // BF16 rows: fewer registers in flight
   const int tid = threadIdx.x;
   const int n4 = (K + 3) >> 2;                          // float4 slots holding valid columns
   const int npass = KP >> 10;
@@ -64,9 +71,9 @@ __device__ __forceinline__ void stage_inputs(const float* __restrict__ x, int ld
   for (int b = 0; b < B; ++b) {
     const __amdgpu_buffer_rsrc_t rx = make_rsrc(x + size_t(b) * ldx, uint32_t(n4) * 16u);
     float ss = 0.0f, sx = 0.0f;
-    for (int i0 = 0; i0 < npass; i0 += kBatch) {
-      int4 xv[kBatch];
-      int2 gv[kBatch];
+    int4 xv[kBatch];
+    int2 gv[kBatch];
+    auto load_batch = [&](int i0) {
 #pragma unroll
       for (int u = 0; u < kBatch; ++u) {
         const int c4 = ((i0 + u) << 8) + tid;           // float4 index
@@ -75,6 +82,8 @@ __device__ __forceinline__ void stage_inputs(const float* __restrict__ x, int ld
           gv[u] = __builtin_bit_cast(int2, __builtin_amdgcn_raw_buffer_load_b64(
                                                rg, c4 < n4 ? int(uint32_t(c4) * 8u) : int(kOOB), 0, 0));
       }
+    };
+    auto store_batch = [&](int i0) {
 #pragma unroll
       for (int u = 0; u < kBatch; ++u) {
         const int i = i0 + u;
@@ -96,6 +105,15 @@ __device__ __forceinline__ void stage_inputs(const float* __restrict__ x, int ld
         sx += (v.x + v.y) + (v.z + v.w);
         *reinterpret_cast<float4*>(xs + size_t(b) * KP + (I8 ? xs_slot_i8(k) : xs_slot_bf16(k))) = v;
       }
+    };
+    // the first batch is peeled so that the caller's loads sit between its issue and its use
+    // without a branch around them
+    load_batch(0);
+    if (b == 0) after_first();
+    store_batch(0);
+    for (int i0 = kBatch; i0 < npass; i0 += kBatch) {
+      load_batch(i0);
+      store_batch(i0);
     }
     // one block reduction for both sums
     ss = wave_sum(ss);
@@ -114,8 +132,9 @@ __device__ __forceinline__ void stage_inputs(const float* __restrict__ x, int ld
   __syncthreads();
 }
 
+// At most 128 VGPRs, so that four waves share each SIMD (the grid is sized for that).
 template <int B, int MODE>
-__global__ __launch_bounds__(kBlock) void gemv_kernel(GemvArgs a) {
+__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) void gemv_kernel(GemvArgs a) {
   constexpr bool BF = (MODE == GEMV_LMHEAD);
   constexpr bool NORM = (MODE != GEMV_RESID);
   constexpr int CPC = BF ? 512 : 1024;                 // columns per 1 KiB chunk
@@ -163,11 +182,20 @@ __global__ __launch_bounds__(kBlock) void gemv_kernel(GemvArgs a) {
     }
   };
 
+  // Order of the first loads (measured per projection at the 8B shapes): the gate/up panel, the
+  // largest, is fastest with the input staged before any weight load (its input loads would
+  // otherwise queue behind the whole launch's weight stream); the smaller panels put their first
+  // tile in flight between the input loads and their use.
   int4 wa[kC][kR], wb[kC][kR];
-  issue(t_begin, wa);                                   // in flight during the prologue
-
   float xscale[B], bias[B];
-  stage_inputs<B, NORM, !BF>(a.x, a.ldx, K, KP, a.gamma, a.eps, xs, red2, xscale, bias);
+  if (MODE == GEMV_GATEUP) {
+    stage_inputs<B, NORM, !BF>(a.x, a.ldx, K, KP, a.gamma, a.eps, xs, red2, xscale, bias, [] {});
+    issue(t_begin, wa);
+  } else {
+    stage_inputs<B, NORM, !BF>(a.x, a.ldx, K, KP, a.gamma, a.eps, xs, red2, xscale, bias,
+                               [&] { issue(t_begin, wa); });
+  }
+  issue(t_begin + 1, wb);
 
   float acc[B][kR];
   float s1[kR], s2[2], res[B][kR];
@@ -249,10 +277,10 @@ __global__ __launch_bounds__(kBlock) void gemv_kernel(GemvArgs a) {
   };
 
   for (int t = t_begin; t < t_end; t += 2) {
-    issue(t + 1, wb);
     process(wa, t);
     issue(t + 2, wa);
     if (t + 1 < t_end) process(wb, t + 1);
+    issue(t + 3, wb);
   }
 }
 
