@@ -15,9 +15,13 @@
 //      reduced across the row's lanes with DPP, and an online softmax (running max and sum per
 //      head, rescaled accumulators) folds the sub-block into P V. The head count is a template
 //      parameter, so every per-head loop is unrolled and independent chains interleave;
-//   3. writes (max, sum, unnormalised output) per head when the range is split; a second, small
-//      kernel merges the ranges by log-sum-exp and writes o (a kernel boundary is the cheapest
-//      device-wide ordering here: an in-kernel fence + counter costs more than the merge itself).
+//   3. when the range is split, writes (max, sum, unnormalised output) per head with
+//      device-coherent stores, waits for them to complete and counts itself done on the
+//      (group slot, sequence) counter; the workgroup that brings the count to n_split reads every
+//      split's record back with device-coherent loads, merges them by log-sum-exp, writes o and
+//      resets the counter for the next launch. Nothing waits on another workgroup, and no L2
+//      write-back is needed (an earlier version fenced every workgroup, which serialised on the
+//      write-backs; a second merge kernel cost a launch and a round trip through memory).
 #include <algorithm>
 
 #include "device_common.hpp"
@@ -30,7 +34,7 @@ constexpr int kMaxHeads = 8;
 constexpr int kSub = 64;               // rows per sub-block (two in flight per workgroup)
 constexpr int kMinChunk = 2 * kSub;    // rows per split are a multiple of this
 constexpr int kMaxSplit = 256;
-constexpr int kMergeBatch = 32;
+constexpr int kMergeBatch = 16;        // split records in flight per thread while merging
 
 __device__ __forceinline__ void unpack_bf16x8(const int4& w, float (&f)[8]) {
   f[0] = bf16_lo(uint32_t(w.x)); f[1] = bf16_hi(uint32_t(w.x));
@@ -55,6 +59,7 @@ struct AttnSmem {
   float knew[DH];
   float vnew[DH];
   float m_s[kMaxHeads], l_s[kMaxHeads], al_s[kMaxHeads];
+  int last;                            // this workgroup merges the splits
 };
 
 template <int LPR>
@@ -285,8 +290,11 @@ __device__ __forceinline__ void attn_body(const AttnArgs& a, AttnSmem<DH>& sm, i
     }
     return;
   }
-  // 3. partial results: record per (split, head) = [max, sum, 0, 0, acc[DH]] (float4-aligned)
-  float* part = a.part + (size_t(b) * a.m_kv + j) * size_t(a.n_split) * kMaxHeads * PS;
+  // 3. partial results: record per (split, head) = [max, sum, 0, 0, acc[DH]] (float4-aligned),
+  //    written device-coherent; the last split of (j, b) to finish merges all of them
+  const size_t rec0 = (size_t(b) * a.m_kv + j) * size_t(a.n_split) * kMaxHeads * PS;
+  const __amdgpu_buffer_rsrc_t rp =
+      make_rsrc(a.part + rec0, uint32_t(a.n_split) * kMaxHeads * PS * 4u);
   for (int i = tid; i < NH * Q4; i += kBlock) {
     const int h = i / Q4, e4 = i % Q4;
     float4 v;
@@ -294,11 +302,63 @@ __device__ __forceinline__ void attn_body(const AttnArgs& a, AttnSmem<DH>& sm, i
     v.y = sm.red[0][h][4 * e4 + 1] + sm.red[1][h][4 * e4 + 1] + sm.red[2][h][4 * e4 + 1] + sm.red[3][h][4 * e4 + 1];
     v.z = sm.red[0][h][4 * e4 + 2] + sm.red[1][h][4 * e4 + 2] + sm.red[2][h][4 * e4 + 2] + sm.red[3][h][4 * e4 + 2];
     v.w = sm.red[0][h][4 * e4 + 3] + sm.red[1][h][4 * e4 + 3] + sm.red[2][h][4 * e4 + 3] + sm.red[3][h][4 * e4 + 3];
-    reinterpret_cast<float4*>(part + (size_t(s) * kMaxHeads + h) * PS + 4)[e4] = v;
+    buf_store16_device(__builtin_bit_cast(int4, v), rp,
+                       uint32_t(((s * kMaxHeads + h) * PS + 4) * 4 + e4 * 16));
   }
   if (tid < NH)
-    *reinterpret_cast<float2*>(part + (size_t(s) * kMaxHeads + tid) * PS) =
-        make_float2(sm.m_s[tid], sm.l_s[tid]);
+    buf_store8_device(__builtin_bit_cast(int2, make_float2(sm.m_s[tid], sm.l_s[tid])), rp,
+                      uint32_t((s * kMaxHeads + tid) * PS * 4));
+  __builtin_amdgcn_s_waitcnt(0);        // this thread's records have reached the coherence point
+  __syncthreads();                      // ... and every thread's
+  int* cnt = a.cnt + size_t(b) * a.m_kv + j;
+  if (tid == 0) {
+    const int done = __hip_atomic_fetch_add(cnt, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    sm.last = (done == a.n_split - 1);
+  }
+  __syncthreads();
+  if (!sm.last) return;
+  if (tid == 0) __hip_atomic_store(cnt, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  // merge: thread (h, e4) combines 4 output dims of one head over all splits, kMergeBatch records
+  // in flight at once, with a running log-sum-exp across batches
+  if (tid >= NH * Q4) return;
+  const int h = tid / Q4, e4 = tid % Q4;
+  float M = -INFINITY, L = 0.0f;
+  float4 A = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+  for (int k0 = 0; k0 < a.n_split; k0 += kMergeBatch) {
+    float2 ml[kMergeBatch];
+    float4 av[kMergeBatch];
+#pragma unroll
+    for (int q = 0; q < kMergeBatch; ++q) {
+      const uint32_t rec = uint32_t((min(k0 + q, a.n_split - 1) * kMaxHeads + h) * PS * 4);
+      ml[q] = __builtin_bit_cast(float2, buf_load8_device(rp, rec));
+      av[q] = __builtin_bit_cast(float4, buf_load16_device(rp, rec + 16u + uint32_t(e4) * 16u));
+    }
+    float bm = M;
+#pragma unroll
+    for (int q = 0; q < kMergeBatch; ++q) bm = fmaxf(bm, ml[q].x);
+    const float rs = exp2f(M - bm);             // rescale what was merged so far
+    L *= rs;
+    A.x *= rs; A.y *= rs; A.z *= rs; A.w *= rs;
+#pragma unroll
+    for (int q = 0; q < kMergeBatch; ++q) {
+      const float w = (k0 + q < a.n_split) ? exp2f(ml[q].x - bm) : 0.0f;
+      L = fmaf(ml[q].y, w, L);
+      A.x = fmaf(av[q].x, w, A.x); A.y = fmaf(av[q].y, w, A.y);
+      A.z = fmaf(av[q].z, w, A.z); A.w = fmaf(av[q].w, w, A.w);
+    }
+    M = bm;
+  }
+  const float inv = 1.0f / L;
+  const int col = (h0 + h) * DH + 4 * e4;
+  if (a.o_hl) {
+    store_o(a, b, col + 0, A.x * inv);
+    store_o(a, b, col + 1, A.y * inv);
+    store_o(a, b, col + 2, A.z * inv);
+    store_o(a, b, col + 3, A.w * inv);
+  } else {
+    *reinterpret_cast<float4*>(a.o + size_t(b) * a.ld_o + col) =
+        make_float4(A.x * inv, A.y * inv, A.z * inv, A.w * inv);
+  }
 }
 
 // NHM bounds the retained heads of every group slot in the launch: the register budget is set by
@@ -326,59 +386,6 @@ __global__ __launch_bounds__(kBlock) void attn_decode_kernel(AttnArgs a) {
   }
 }
 
-// Merge of the split partials of one (group slot, sequence): thread (h, e4) combines 4 output dims
-// of one head over all splits, kMergeBatch records in flight at once, with a running
-// log-sum-exp across batches. The kernel boundary makes the partials visible.
-template <int DH>
-__global__ __launch_bounds__(kBlock) void attn_merge_kernel(AttnArgs a) {
-  constexpr int Q4 = DH / 4;
-  constexpr int PS = DH + 4;
-  const int j = blockIdx.x, b = blockIdx.y, tid = threadIdx.x;
-  const int h0 = a.slot_start[j];
-  const int nh = a.slot_start[j + 1] - h0;
-  if (tid >= nh * Q4) return;
-  const int h = tid / Q4, e4 = tid % Q4;
-  const float* part = a.part + (size_t(b) * a.m_kv + j) * size_t(a.n_split) * kMaxHeads * PS;
-  float M = -INFINITY, L = 0.0f;
-  float4 A = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-  for (int k0 = 0; k0 < a.n_split; k0 += kMergeBatch) {
-    float2 ml[kMergeBatch];
-    float4 av[kMergeBatch];
-#pragma unroll
-    for (int q = 0; q < kMergeBatch; ++q) {
-      const float* rec = part + (size_t(min(k0 + q, a.n_split - 1)) * kMaxHeads + h) * PS;
-      ml[q] = *reinterpret_cast<const float2*>(rec);
-      av[q] = reinterpret_cast<const float4*>(rec + 4)[e4];
-    }
-    float bm = M;
-#pragma unroll
-    for (int q = 0; q < kMergeBatch; ++q) bm = fmaxf(bm, ml[q].x);
-    const float rs = exp2f(M - bm);             // rescale what was merged so far
-    L *= rs;
-    A.x *= rs; A.y *= rs; A.z *= rs; A.w *= rs;
-#pragma unroll
-    for (int q = 0; q < kMergeBatch; ++q) {
-      const float w = (k0 + q < a.n_split) ? exp2f(ml[q].x - bm) : 0.0f;
-      L = fmaf(ml[q].y, w, L);
-      A.x = fmaf(av[q].x, w, A.x); A.y = fmaf(av[q].y, w, A.y);
-      A.z = fmaf(av[q].z, w, A.z); A.w = fmaf(av[q].w, w, A.w);
-    }
-    M = bm;
-  }
-  const float inv = 1.0f / L;
-  if (a.o_hl) {
-    const int col = (h0 + h) * DH + 4 * e4;
-    store_o(a, b, col + 0, A.x * inv);
-    store_o(a, b, col + 1, A.y * inv);
-    store_o(a, b, col + 2, A.z * inv);
-    store_o(a, b, col + 3, A.w * inv);
-    return;
-  }
-  float* ob = a.o + size_t(b) * a.ld_o;
-  reinterpret_cast<float4*>(ob + size_t(h0 + h) * DH)[e4] =
-      make_float4(A.x * inv, A.y * inv, A.z * inv, A.w * inv);
-}
-
 }  // namespace
 
 template <int DH>
@@ -396,14 +403,9 @@ hipError_t launch_attn_decode(const AttnArgs& a, hipStream_t s) {
   int nhm = 0;
   for (int j = 0; j < a.m_kv; ++j) nhm = std::max(nhm, a.slot_start[j + 1] - a.slot_start[j]);
   if (nhm < 1 || nhm > kMaxHeads) return hipErrorInvalidValue;
+  if (a.n_split > 1 && (!a.part || !a.cnt)) return hipErrorInvalidValue;
   const dim3 grid(a.n_split, a.m_kv, a.B);
-  hipError_t e = (a.dh == 128) ? launch_partials<128>(a, grid, nhm, s) : launch_partials<64>(a, grid, nhm, s);
-  if (e != hipSuccess || a.n_split == 1) return e;
-  if (a.dh == 128)
-    hipLaunchKernelGGL(attn_merge_kernel<128>, dim3(a.m_kv, a.B), dim3(kBlock), 0, s, a);
-  else
-    hipLaunchKernelGGL(attn_merge_kernel<64>, dim3(a.m_kv, a.B), dim3(kBlock), 0, s, a);
-  return hipGetLastError();
+  return (a.dh == 128) ? launch_partials<128>(a, grid, nhm, s) : launch_partials<64>(a, grid, nhm, s);
 }
 
 int attn_min_chunk() { return kMinChunk; }

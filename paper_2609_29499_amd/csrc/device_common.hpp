@@ -108,4 +108,24 @@ __device__ __forceinline__ int4 buf_load16_stream(__amdgpu_buffer_rsrc_t r, uint
   return __builtin_bit_cast(int4, __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, kCpolStream));
 }
 
+// Device-coherent accesses for data that workgroups exchange inside one launch: cache-policy bit
+// sc1, the bit the compiler sets on agent-scope atomic loads and stores. Such stores are written
+// through to the device-wide coherence point (complete once the wave's vmcnt drains) and such
+// loads read from it, so no L2 write-back or invalidate is needed between the two sides.
+constexpr int kCpolDevice = 16;
+__device__ __forceinline__ int4 buf_load16_device(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  return __builtin_bit_cast(int4, __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, kCpolDevice));
+}
+__device__ __forceinline__ int2 buf_load8_device(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  return __builtin_bit_cast(int2, __builtin_amdgcn_raw_buffer_load_b64(r, (int)off, 0, kCpolDevice));
+}
+__device__ __forceinline__ void buf_store16_device(const int4& v, __amdgpu_buffer_rsrc_t r, uint32_t off) {
+  __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(__attribute__((ext_vector_type(4))) unsigned, v),
+                                         r, (int)off, 0, kCpolDevice);
+}
+__device__ __forceinline__ void buf_store8_device(const int2& v, __amdgpu_buffer_rsrc_t r, uint32_t off) {
+  __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(__attribute__((ext_vector_type(2))) unsigned, v),
+                                        r, (int)off, 0, kCpolDevice);
+}
+
 }  // namespace tasp

@@ -206,12 +206,13 @@ struct AttnArgs {
   const float* rope_cos; const float* rope_sin;  // [max_seq][dh/2]
   int pos, chunk, n_split;
   float* part;                     // [B][m_kv][n_split][8][dh + 4] when n_split > 1
+  int* cnt;                        // [B][m_kv] split counters, zero before and after a launch
   float* o; int ld_o;              // [B][ld_o] retained heads in ascending order
   uint16_t* o_hl; int ld_ohl;      // when set: o as the hi/lo BF16 operand [16][ld_ohl] instead
   int B;
 };
-// Split-KV partial attention (writes o directly when n_split == 1), then, for n_split > 1, the
-// log-sum-exp merge of the partials into o.
+// Split-KV partial attention; for n_split > 1 the last split of each (group slot, sequence) to
+// finish merges the partials into o by log-sum-exp (n_split == 1 writes o directly).
 hipError_t launch_attn_decode(const AttnArgs& a, hipStream_t s);
 int attn_min_chunk();   // rows per split are a multiple of this
 int attn_max_split();

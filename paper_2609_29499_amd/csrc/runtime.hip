@@ -140,7 +140,7 @@ struct Layout {
   size_t mask_q, mask_kv, mask_f;
   size_t idx_q, idx_kv, idx_slot, idx_slot_start, idx_ffn, counts;
   size_t final_norm, lm_head, rope_cos, rope_sin;
-  size_t r_mid, r_io0, r_io1, qkv_buf, o_buf, h_buf, part;
+  size_t r_mid, r_io0, r_io1, qkv_buf, o_buf, h_buf, part, acnt;
   size_t xd, xo, xh, ssq;            // batched path: hi/lo operands and sums of squares
   size_t pxd, pxw, pq, pqkv, pr_mid, pr_io0, pr_io1, pssq;   // prefill scratch
   size_t qkv_rows, o_cols, down_cols;                        // shared-store plans: maps
@@ -204,6 +204,7 @@ Layout make_layout(const tasp_model_desc* d, const Closed& c) {
   Y.o_buf = take(size_t(B) * Y.ld_obuf * 4);
   Y.h_buf = take(size_t(B) * Y.ld_h * 4);
   Y.part = take(size_t(B) * Hkv * Y.n_split_max * 8 * (dh + 4) * 4);
+  Y.acnt = take(size_t(B) * Hkv * 4);
   Y.ld_xd = round_up64(D);
   Y.ld_xo = round_up64(Hq * dh);
   Y.ld_xh = round_up64(F);
@@ -267,6 +268,7 @@ Layout make_shared_layout(const tasp_model_desc* d) {
   Y.o_buf = take(size_t(Y.ld_obuf) * 4);
   Y.h_buf = take(size_t(Y.ld_h) * 4);
   Y.part = take(size_t(Hkv) * Y.n_split_max * 8 * (dh + 4) * 4);
+  Y.acnt = take(size_t(Hkv) * 4);
   Y.zero_end = off;
   Y.total = off;
   return Y;
@@ -317,6 +319,7 @@ struct tasp_plan_s {
   uint16_t *final_norm, *lm_head;
   float *rope_cos, *rope_sin;
   float *r_mid, *r_io[2], *qkv_buf, *o_buf, *h_buf, *part;
+  int* acnt;                       // attention split counters [B][H_kv], zero between launches
   int n_split_max, ld_qkv, ld_obuf, ld_h;
   uint16_t *xd, *xo, *xh;            // batched path operands [16][ld_x*]
   float* ssq;                        // [max_batch][d_model / 16]
@@ -470,7 +473,7 @@ tasp::AttnArgs attn_args(const tasp_plan_s* p, int l, const tasp_kv_cache* cache
   a.vc = static_cast<uint16_t*>(cache->v) + l * layer_cache;
   a.Hkv = d.n_kv_heads; a.S = cache->max_seq; a.rope_cos = p->rope_cos;
   a.rope_sin = p->rope_sin; a.pos = pos; a.chunk = int(chunk);
-  a.n_split = int((total + chunk - 1) / chunk); a.part = p->part;
+  a.n_split = int((total + chunk - 1) / chunk); a.part = p->part; a.cnt = p->acnt;
   a.o = p->o_buf; a.ld_o = p->ld_obuf; a.B = B;
   if (hl) { a.o_hl = p->xo; a.ld_ohl = p->ld_xo; }
   return a;
@@ -1052,6 +1055,7 @@ tasp_status tasp_compile_plan(const tasp_model_desc* desc, const tasp_store* sto
   p->o_buf = reinterpret_cast<float*>(at(Y.o_buf));
   p->h_buf = reinterpret_cast<float*>(at(Y.h_buf));
   p->part = reinterpret_cast<float*>(at(Y.part));
+  p->acnt = reinterpret_cast<int*>(at(Y.acnt));
   p->n_split_max = Y.n_split_max; p->ld_qkv = Y.ld_qkv; p->ld_obuf = Y.ld_obuf; p->ld_h = Y.ld_h;
   p->xd = reinterpret_cast<uint16_t*>(at(Y.xd));
   p->xo = reinterpret_cast<uint16_t*>(at(Y.xo));
@@ -1211,6 +1215,7 @@ tasp_status tasp_compile_shared_plan(const tasp_model_desc* desc, const tasp_gst
   p->o_buf = reinterpret_cast<float*>(at(Y.o_buf));
   p->h_buf = reinterpret_cast<float*>(at(Y.h_buf));
   p->part = reinterpret_cast<float*>(at(Y.part));
+  p->acnt = reinterpret_cast<int*>(at(Y.acnt));
   p->n_split_max = Y.n_split_max; p->ld_qkv = Y.ld_qkv; p->ld_obuf = Y.ld_obuf; p->ld_h = Y.ld_h;
   p->xd = p->xo = p->xh = p->pxd = p->pxw = p->pq = nullptr;
   p->ssq = p->pqkv = p->pr_mid = p->pr_io[0] = p->pr_io[1] = p->pssq = nullptr;
