@@ -4,7 +4,7 @@
 // first-byte latency, the last wave's work) weigh as much as the stream.
 //
 // Work decomposition: rows are taken in groups (2 rows for QKV, O and down; 4 for the LM head;
-// for gate/up 2 SwiGLU channels = 2 gate + 2 up rows). A tile is one group x 2 KiB of each of its
+// for gate/up one SwiGLU channel = its gate and up rows). A tile is one group x 2 KiB of each of its
 // rows (2 chunks of 1 KiB; a wave reads whole contiguous KiB, 16 bytes per lane). Several
 // workgroups per CU and small tiles keep the slowest wave's share short. Each wave owns a
 // contiguous range of whole groups and walks its tiles with two register buffers in ping-pong:
@@ -27,10 +27,10 @@
 namespace tasp {
 namespace {
 
-// Rows per group: 2 for the QKV, O and down projections (at the 8B shapes twice the waves of
-// 4-row groups, measured 4-8 % faster per launch), 4 for gate/up (2 channels x {gate, up}) and the
-// LM head.
-constexpr int rows_per_group(int mode) { return (mode == GEMV_QKV || mode == GEMV_RESID) ? 2 : 4; }
+// Rows per group: 2 for the INT8 projections (gate/up: one channel = its gate and up rows), 4 for
+// the BF16 LM head. At the 8B shapes 2-row groups measured 4-8 % faster per launch than 4-row
+// groups (twice the waves, half the bytes in flight per wave).
+constexpr int rows_per_group(int mode) { return mode == GEMV_LMHEAD ? 4 : 2; }
 constexpr int kC = 2;             // 1 KiB chunks per tile
 constexpr int kWgPerCu = 4;
 constexpr int kNumCu = 256;
@@ -158,7 +158,8 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) voi
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(blockIdx.x * (kBlock / kWave) + (threadIdx.x >> 6));
   const int nwaves = gridDim.x * (kBlock / kWave);
-  const int per_group = (MODE == GEMV_GATEUP) ? 2 : kR;
+  constexpr int CH = kR / 2;                           // gate/up: channels per group
+  const int per_group = (MODE == GEMV_GATEUP) ? CH : kR;
   const int G = (N + per_group - 1) / per_group;
   const int g0 = int((long(wave) * G) / nwaves), g1 = int((long(wave + 1) * G) / nwaves);
   const int t_begin = g0 * KB, t_end = g1 * KB;
@@ -168,7 +169,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) voi
       make_rsrc(MODE == GEMV_GATEUP ? a.w2 : a.w, uint32_t(N) * row_bytes);
 
   auto row_of = [&](int gi, int r) {
-    return (MODE == GEMV_GATEUP) ? gi * 2 + (r & 1) : gi * kR + r;
+    return (MODE == GEMV_GATEUP) ? gi * CH + (r % CH) : gi * kR + r;
   };
   auto issue = [&](int t, int4 (&w)[kC][kR]) {
     const bool ok_t = t < t_end;
@@ -182,7 +183,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) voi
         const int row = row_of(gi, r);
         const bool ok = ok_t && (row < N) && (k < K);
         const uint32_t off = ok ? uint32_t(row) * row_bytes + uint32_t(k) * (BF ? 2u : 1u) : kOOB;
-        w[u][r] = buf_load16_stream((MODE == GEMV_GATEUP && r >= 2) ? rw2 : rw, off);
+        w[u][r] = buf_load16_stream((MODE == GEMV_GATEUP && r >= CH) ? rw2 : rw, off);
       }
     }
   };
@@ -203,7 +204,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) voi
   issue(t_begin + 1, wb);
 
   float acc[B][kR];
-  float s1[kR], s2[2], res[B][kR];
+  float s1[kR], s2[CH], res[B][kR];
   auto process = [&](const int4 (&w)[kC][kR], int t) {
     const int gi = t / KB;
     const int kb = t - gi * KB;
@@ -216,9 +217,9 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) voi
       // epilogue operands: wave-uniform addresses -> scalar loads
 #pragma unroll
       for (int r = 0; r < kR; ++r) {
-        const int row = min(MODE == GEMV_GATEUP ? row0 + (r & 1) : row0 + r, N - 1);
+        const int row = min(MODE == GEMV_GATEUP ? row0 + (r % CH) : row0 + r, N - 1);
         s1[r] = BF ? 1.0f : scale[row];
-        if (MODE == GEMV_GATEUP && r < 2) s2[r] = scale2[row];
+        if (MODE == GEMV_GATEUP && r < CH) s2[r] = scale2[row];
 #pragma unroll
         for (int b = 0; b < B; ++b)
           res[b][r] = (MODE == GEMV_RESID) ? resid[size_t(b) * a.ldy + row] : 0.0f;
@@ -263,11 +264,11 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) voi
       float* yb = a.y + size_t(b) * a.ldy;
       if (MODE == GEMV_GATEUP) {
 #pragma unroll
-        for (int r = 0; r < 2; ++r) {
+        for (int r = 0; r < CH; ++r) {
           const int ch = row0 + r;
           if (ch >= N) continue;
           const float g = s1[r] * xscale[b] * (tot[b][r] - bias[b]);
-          const float u = s2[r] * xscale[b] * (tot[b][r + 2] - bias[b]);
+          const float u = s2[r] * xscale[b] * (tot[b][r + CH] - bias[b]);
           yb[ch] = g / (1.0f + exp2f(-g * kLog2e)) * u;
         }
       } else {
@@ -309,7 +310,7 @@ hipError_t launch_mode(const GemvArgs& a, int grid, size_t lds, hipStream_t s) {
 
 template <int B>
 hipError_t launch_gemv_b(GemvMode mode, const GemvArgs& a, hipStream_t s) {
-  const int per_group = (mode == GEMV_GATEUP) ? 2 : rows_per_group(mode);
+  const int per_group = (mode == GEMV_GATEUP) ? rows_per_group(mode) / 2 : rows_per_group(mode);
   const int grid = gemv_grid((a.N + per_group - 1) / per_group);
   const size_t lds = gemv_lds_bytes(B, a.K);
   if (lds > kMaxGemvLds) return hipErrorInvalidValue;
