@@ -21,6 +21,8 @@
 // v_cvt_f32_ubyte gives b + 128 exactly; the bias is removed once per row as 128 * sum(x); the
 // per-row scale is applied after the wave reduction, fused with the epilogue (store, residual
 // add or SwiGLU). BF16 weights are widened by a shift.
+#include <algorithm>
+
 #include "device_common.hpp"
 #include "kernels.hpp"
 
@@ -290,10 +292,14 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) voi
   }
 }
 
-int gemv_grid(int n_groups) {
-  int waves = n_groups;
-  if (waves > kNumCu * kWgPerCu * 4) waves = kNumCu * kWgPerCu * 4;
-  int grid = (waves + 3) / 4;
+// One wave per group up to the workgroups that fit on the chip at once: kWgPerCu per CU, fewer
+// when the staged input limits them (160 KiB of LDS per CU). Past that, waves take several groups
+// each, so that no workgroup waits for a second round and stages the input again.
+int gemv_grid(int n_groups, size_t lds) {
+  constexpr size_t kLdsPerCu = 160 * 1024;
+  const int by_lds = int(kLdsPerCu / std::max<size_t>(lds + 64, 1));
+  const int per_cu = std::max(1, std::min(kWgPerCu, by_lds));
+  const int grid = std::min((n_groups + 3) / 4, kNumCu * per_cu);
   return grid < 1 ? 1 : grid;
 }
 
@@ -311,8 +317,8 @@ hipError_t launch_mode(const GemvArgs& a, int grid, size_t lds, hipStream_t s) {
 template <int B>
 hipError_t launch_gemv_b(GemvMode mode, const GemvArgs& a, hipStream_t s) {
   const int per_group = (mode == GEMV_GATEUP) ? rows_per_group(mode) / 2 : rows_per_group(mode);
-  const int grid = gemv_grid((a.N + per_group - 1) / per_group);
   const size_t lds = gemv_lds_bytes(B, a.K);
+  const int grid = gemv_grid((a.N + per_group - 1) / per_group, lds);
   if (lds > kMaxGemvLds) return hipErrorInvalidValue;
   switch (mode) {
     case GEMV_QKV: return launch_mode<B, GEMV_QKV>(a, grid, lds, s);
