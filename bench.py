@@ -488,6 +488,7 @@ def bench_request(args, wl):
             ev[3].record()
             torch.cuda.synchronize()
             pf.append(ev[2].elapsed_time(ev[3]))
+            print(f"[bench] {name}: request {len(req)}: {req[-1]:.1f} ms", file=sys.stderr, flush=True)
         req_ms, pf_ms = float(np.median(req)), float(np.median(pf))
         dec = (req_ms - pf_ms) / n_new
         rows.append({"plan": name, "request_ms": round(req_ms, 3), "prefill_ms": round(pf_ms, 3),

@@ -13,8 +13,8 @@
 // hence in one scale group: it loads the group's BF16 scale with them, forms the 16-byte dot
 // product in float32 (byte XOR 0x80 converted exactly to b + 128) and adds
 // scale * (dot - 128 * sum of the piece's 16 inputs); the piece sums are staged in LDS with the
-// input. The column map is staged in LDS; a kernel without one (other than gate/up) issues its
-// first tile before staging, as the per-row kernel does.
+// input. The column map is staged in LDS; a kernel without one issues its first tile before
+// staging, as the per-row kernel does.
 #include "device_common.hpp"
 #include "kernels.hpp"
 
@@ -96,10 +96,7 @@ __global__ __launch_bounds__(kBlock) void shared_gemv_kernel(SharedGemvArgs a) {
 
   int4 wa[kC][kR], wb[kC][kR];
   uint32_t sa[kC][kR], sb[kC][kR];
-  // the first tile flies during the staging, except for gate/up (the largest panel, fastest
-  // with its input staged before the weight stream) and where the column map must be staged first
-  constexpr bool kStageFirst = (MODE == GEMV_GATEUP);
-  if (!a.cols && !kStageFirst) issue(t_begin, wa, sa);
+  if (!a.cols) issue(t_begin, wa, sa);                   // in flight during the staging
 
   // stage x (times the gain) swizzled, the sums of its 16-column pieces and the column map
   {
@@ -136,8 +133,7 @@ __global__ __launch_bounds__(kBlock) void shared_gemv_kernel(SharedGemvArgs a) {
     __syncthreads();
   }
   const float xscale = NORM ? rsqrtf((red[0] + red[1] + red[2] + red[3]) / float(K) + a.eps) : 1.0f;
-  if (a.cols || kStageFirst) issue(t_begin, wa, sa);
-  issue(t_begin + 1, wb, sb);
+  if (a.cols) issue(t_begin, wa, sa);
 
   float acc[kR], res[kR];
   auto process = [&](const int4 (&w)[kC][kR], const uint32_t (&sv)[kC][kR], int t) {
@@ -192,10 +188,10 @@ __global__ __launch_bounds__(kBlock) void shared_gemv_kernel(SharedGemvArgs a) {
   };
 
   for (int t = t_begin; t < t_end; t += 2) {
+    issue(t + 1, wb, sb);
     process(wa, sa, t);
     issue(t + 2, wa, sa);
     if (t + 1 < t_end) process(wb, sb, t + 1);
-    issue(t + 3, wb, sb);
   }
 }
 
