@@ -64,7 +64,7 @@ def layer_bytes(sh, m_q, m_kv, c, pos, batch=1):
     s = 4 * ((m_q + 2 * m_kv) * dh + d + 2 * c + d)
     kv = batch * m_kv * (pos + 1) * dh * 2 * 2
     gateup = 2 * c * d + 2 * c * 4 + batch * (d * 4 + c * 4)
-    # split-KV attention + merge: cache rows, q/k/v in, new k/v rows written, o out
+    # split-KV attention with its merge: cache rows, q/k/v in, new k/v rows written, o out
     attention = kv + batch * ((m_q + 2 * m_kv) * dh * 4 + 2 * m_kv * dh * 2 + m_q * dh * 4)
     return {"weights": w, "scales": s, "kv": kv, "total": w + s + kv, "gateup": gateup,
             "attention": attention}

@@ -261,8 +261,8 @@ tasp_status tasp_decode_step_timed(tasp_plan plan, const float* x, tasp_kv_cache
 
 /* Profiling: average duration of one stage of layer `layer`, measured as n_plans * reps
  * back-to-back launches between two HIP events on `stream`. Stage `kind`: 1 attention at `pos`
- * (split-KV partials plus, when split, the merge kernel; rewrites cache row pos with the same
- * values), 3 the gate/up projection (RMSNorm + SwiGLU), 4 the down projection (writes the plan's
+ * (split-KV partials, merged by the last split of each group slot; rewrites cache row pos with
+ * the same values), 3 the gate/up projection (RMSNorm + SwiGLU), 4 the down projection (writes the plan's
  * scratch, not a caller buffer). Launch i uses plans[i % n_plans] with caches[i % n_plans] (bound
  * to that plan; its batch selects the batch-1 or the batched kernels), so distinct plan copies
  * keep every launch streaming from HBM rather than from cache. Each plan must have run a

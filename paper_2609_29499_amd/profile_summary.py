@@ -26,7 +26,6 @@ COPY_BYTES = 1 << 30
 
 def kind_of(name: str) -> str | None:
     rules = [
-        (r"attn_merge_kernel", "attn_merge"),
         (r"attn_decode_kernel", "attention"),
         (r"pf_attn_kernel", "prefill_attention"),
         (r"pf_rope_kernel", "rope_append"),
