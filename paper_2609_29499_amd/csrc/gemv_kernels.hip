@@ -195,6 +195,23 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) voi
     __builtin_amdgcn_s_setprio(0);
   };
 
+  // Epilogue operands (scales, residual) of the wave's first group: scalar loads issued ahead of
+  // the staging and held (the empty asm below keeps them there), so their latency is hidden by it
+  // instead of stalling the first group's epilogue (measured 0.2 us per 8B layer step).
+  float s1p[kR], s2p[CH], resp[B][kR];
+  {
+    const int row0 = row_of(g0, 0);
+#pragma unroll
+    for (int r = 0; r < kR; ++r) {
+      const int row = min(MODE == GEMV_GATEUP ? row0 + (r % CH) : row0 + r, N - 1);
+      s1p[r] = BF ? 1.0f : scale[row];
+      if (MODE == GEMV_GATEUP && r < CH) s2p[r] = scale2[row];
+#pragma unroll
+      for (int b = 0; b < B; ++b)
+        resp[b][r] = (MODE == GEMV_RESID) ? resid[size_t(b) * a.ldy + row] : 0.0f;
+    }
+  }
+
   // Order of the first loads (measured per projection at the 8B shapes): the gate/up panel, the
   // largest, is fastest with the input staged before any weight load (its input loads would
   // otherwise queue behind the whole launch's weight stream); the smaller panels put their first
@@ -209,6 +226,14 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) voi
                                [&] { issue(t_begin, wa); });
   }
   issue(t_begin + 1, wb);
+#pragma unroll
+  for (int r = 0; r < kR; ++r) {
+    asm volatile("" : "+s"(s1p[r]));
+#pragma unroll
+    for (int b = 0; b < B; ++b) asm volatile("" : "+s"(resp[b][r]));
+  }
+#pragma unroll
+  for (int r = 0; r < CH; ++r) asm volatile("" : "+s"(s2p[r]));
 
   float acc[B][kR];
   float s1[kR], s2[CH], res[B][kR];
@@ -222,6 +247,15 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) voi
 #pragma unroll
         for (int r = 0; r < kR; ++r) acc[b][r] = 0.0f;
       // epilogue operands: wave-uniform addresses -> scalar loads
+      if (gi == g0) {
+#pragma unroll
+        for (int r = 0; r < kR; ++r) {
+          s1[r] = s1p[r];
+          if (MODE == GEMV_GATEUP && r < CH) s2[r] = s2p[r];
+#pragma unroll
+          for (int b = 0; b < B; ++b) res[b][r] = resp[b][r];
+        }
+      } else
 #pragma unroll
       for (int r = 0; r < kR; ++r) {
         const int row = min(MODE == GEMV_GATEUP ? row0 + (r % CH) : row0 + r, N - 1);
