@@ -355,6 +355,7 @@ hipError_t launch_mode(const GemvArgs& a, int grid, size_t lds, hipStream_t s) {
 
 template <int B>
 hipError_t launch_gemv_b(GemvMode mode, const GemvArgs& a, hipStream_t s) {
+  if (a.N < 1) return hipSuccess;                       // no output rows: nothing to launch
   const int per_group = (mode == GEMV_GATEUP) ? rows_per_group(mode) / 2 : rows_per_group(mode);
   const size_t lds = gemv_lds_bytes(B, a.K);
   const int grid = gemv_grid((a.N + per_group - 1) / per_group, lds);
