@@ -1,7 +1,8 @@
 // Decode attention over the retained KV groups only (grouped-query attention, one new token).
 //
 // Grid (n_split, m_kv, B): workgroup (s, j, b) serves retained group slot j of sequence b over
-// cache rows [s*chunk, min((s+1)*chunk, pos+1)) for all of that group's retained query heads
+// cache rows [s*chunk, (s+1)*chunk), the last split over [s*chunk, pos+1) (it may be longer or
+// shorter than chunk), for all of that group's retained query heads
 // (1..8), so each K/V row is read from HBM once for every head that uses it. The slot -> group
 // and slot -> head-range tables of the layer travel inside the kernel arguments, so the cache
 // loads do not wait for an index load. The workgroup
@@ -35,6 +36,7 @@ constexpr int kSub = 64;               // rows per sub-block (two in flight per 
 constexpr int kMinChunk = 2 * kSub;    // rows per split are a multiple of this
 constexpr int kMaxSplit = 256;
 constexpr int kMergeBatch = 16;        // split records in flight per thread while merging
+constexpr int kNumCu = 256;
 
 __device__ __forceinline__ void unpack_bf16x8(const int4& w, float (&f)[8]) {
   f[0] = bf16_lo(uint32_t(w.x)); f[1] = bf16_hi(uint32_t(w.x));
@@ -93,7 +95,7 @@ __device__ __forceinline__ void attn_body(const AttnArgs& a, AttnSmem<DH>& sm, i
   const int g = a.kv_idx[j];
   const int h0 = a.slot_start[j];
   const int t0 = s * a.chunk;
-  const int t1 = min(t0 + a.chunk, a.pos + 1);
+  const int t1 = (s == a.n_split - 1) ? a.pos + 1 : t0 + a.chunk;
   const float* qkv = a.qkv + size_t(b) * a.ld_qkv;
   const size_t row_base = (size_t(b) * a.Hkv + g) * a.S;
   uint16_t* kc = a.kc + row_base * DH;
@@ -397,9 +399,33 @@ hipError_t launch_partials(const AttnArgs& a, dim3 grid, int nhm, hipStream_t s)
   return hipGetLastError();
 }
 
+template <int DH, int NHM>
+int resident_blocks() {
+  static const int n = [] {
+    int per_cu = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, attn_decode_kernel<DH, NHM>, kBlock,
+                                                     0) != hipSuccess || per_cu < 1)
+      per_cu = 1;
+    return per_cu * kNumCu;
+  }();
+  return n;
+}
+
+template <int DH>
+int resident_for(int nhm) {
+  if (nhm <= 1) return resident_blocks<DH, 1>();
+  if (nhm == 2) return resident_blocks<DH, 2>();
+  if (nhm <= 4) return resident_blocks<DH, 4>();
+  return resident_blocks<DH, 8>();
+}
+
 hipError_t launch_attn_decode(const AttnArgs& a, hipStream_t s) {
   if (a.m_kv == 0 || a.B == 0) return hipSuccess;
-  if (a.chunk % kMinChunk != 0 || (a.dh != 64 && a.dh != 128)) return hipErrorInvalidValue;
+  if (a.chunk < kMinChunk || a.chunk % kMinChunk != 0 || (a.dh != 64 && a.dh != 128))
+    return hipErrorInvalidValue;
+  // every split holds at least one row, and the merge takes at most kMaxSplit records
+  if (a.n_split < 1 || a.n_split > kMaxSplit || long(a.n_split - 1) * a.chunk > a.pos)
+    return hipErrorInvalidValue;
   int nhm = 0;
   for (int j = 0; j < a.m_kv; ++j) nhm = std::max(nhm, a.slot_start[j + 1] - a.slot_start[j]);
   if (nhm < 1 || nhm > kMaxHeads) return hipErrorInvalidValue;
@@ -410,5 +436,8 @@ hipError_t launch_attn_decode(const AttnArgs& a, hipStream_t s) {
 
 int attn_min_chunk() { return kMinChunk; }
 int attn_max_split() { return kMaxSplit; }
+int attn_resident_blocks(int dh, int nhm) {
+  return dh == 128 ? resident_for<128>(nhm) : resident_for<64>(nhm);
+}
 
 }  // namespace tasp

@@ -204,7 +204,7 @@ struct AttnArgs {
   uint16_t* kc; uint16_t* vc;      // this layer's cache base, [B][Hkv][S][dh]
   int Hkv, S;
   const float* rope_cos; const float* rope_sin;  // [max_seq][dh/2]
-  int pos, chunk, n_split;
+  int pos, chunk, n_split;          // split s: rows [s chunk, (s+1) chunk), the last one to pos
   float* part;                     // [B][m_kv][n_split][8][dh + 4] when n_split > 1
   int* cnt;                        // [B][m_kv] split counters, zero before and after a launch
   float* o; int ld_o;              // [B][ld_o] retained heads in ascending order
@@ -216,6 +216,9 @@ struct AttnArgs {
 hipError_t launch_attn_decode(const AttnArgs& a, hipStream_t s);
 int attn_min_chunk();   // rows per split are a multiple of this
 int attn_max_split();
+// decode-attention workgroups resident on the chip at once when the largest retained group of
+// the launch keeps nhm query heads (head dimension dh)
+int attn_resident_blocks(int dh, int nhm);
 
 // ----------------------------------------------------------------- router
 

@@ -37,7 +37,6 @@ tasp_status fail(tasp_status s, const char* fmt, ...) {
   } while (0)
 
 constexpr size_t kAlign = 256;
-constexpr int kAttnTargetBlocks = 1024;
 constexpr size_t kLdsLimit = 159 * 1024;
 
 size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
@@ -459,13 +458,26 @@ tasp::AttnArgs attn_args(const tasp_plan_s* p, int l, const tasp_kv_cache* cache
   const size_t layer_cache = size_t(B) * d.n_kv_heads * cache->max_seq * d.head_dim;
   const int total = pos + 1;
   tasp::AttnArgs a{};
-  // rows per split: a multiple of the kernel's sub-block, large enough that about
-  // kAttnTargetBlocks workgroups run and that the split count stays within the merge's limit
+  // Split rows: as short as keeps every workgroup of the launch resident at once (a workgroup
+  // that waits for a free slot runs a whole split after the others), in multiples of the kernel's
+  // sub-block pair, within the merge's split limit. Two ways to cover the rows: the last split
+  // takes the remainder on its own (ceil), or the remainder joins the last full split (floor);
+  // the one with the shorter longest split is taken, the separate remainder on a tie.
   const long sub = tasp::attn_min_chunk();
-  const long want = (long(total) * P.m_kv * B + kAttnTargetBlocks - 1) / kAttnTargetBlocks;
-  const long need = (long(total) + tasp::attn_max_split() - 1) / tasp::attn_max_split();
-  long chunk = std::max<long>(std::max(want, need), sub);
-  chunk = (chunk + sub - 1) / sub * sub;
+  int nhm = 1;
+  for (int q = 0; q < P.m_kv; ++q) nhm = std::max(nhm, P.slot_start[q + 1] - P.slot_start[q]);
+  const long per_split = std::max<long>(1, long(P.m_kv) * B);
+  const long smax = std::max<long>(
+      1, std::min<long>(tasp::attn_resident_blocks(d.head_dim, nhm) / per_split,
+                        tasp::attn_max_split()));
+  auto round_up = [&](long r) { return (std::max(r, sub) + sub - 1) / sub * sub; };
+  const long chunk_c = round_up((total + smax - 1) / smax);       // ceil(total / chunk) <= smax
+  const long chunk_f = round_up(total / (smax + 1) + 1);          // floor(total / chunk) <= smax
+  const long split_f = std::max<long>(1, total / chunk_f);
+  const long longest_f = total - (split_f - 1) * chunk_f;
+  const bool floor_wins = longest_f < std::min<long>(chunk_c, total);
+  const long chunk = floor_wins ? chunk_f : chunk_c;
+  const long n_split = floor_wins ? split_f : (total + chunk_c - 1) / chunk_c;
   a.qkv = p->qkv_buf; a.ld_qkv = p->ld_qkv; a.m_q = P.m_q; a.m_kv = P.m_kv; a.dh = d.head_dim;
   for (int q = 0; q < P.m_kv; ++q) a.kv_idx[q] = P.kv_idx[q];
   for (int q = 0; q <= P.m_kv; ++q) a.slot_start[q] = P.slot_start[q];
@@ -473,7 +485,7 @@ tasp::AttnArgs attn_args(const tasp_plan_s* p, int l, const tasp_kv_cache* cache
   a.vc = static_cast<uint16_t*>(cache->v) + l * layer_cache;
   a.Hkv = d.n_kv_heads; a.S = cache->max_seq; a.rope_cos = p->rope_cos;
   a.rope_sin = p->rope_sin; a.pos = pos; a.chunk = int(chunk);
-  a.n_split = int((total + chunk - 1) / chunk); a.part = p->part; a.cnt = p->acnt;
+  a.n_split = int(n_split); a.part = p->part; a.cnt = p->acnt;
   a.o = p->o_buf; a.ld_o = p->ld_obuf; a.B = B;
   if (hl) { a.o_hl = p->xo; a.ld_ohl = p->ld_xo; }
   return a;

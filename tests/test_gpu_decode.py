@@ -223,6 +223,22 @@ def test_batched_tall_panels():
     _check_cache_rows(case)
 
 
+@pytest.mark.parametrize("pos", [511, 512, 640])
+def test_attention_splits_sized_to_residency(pos):
+    """Eight sequences over eight groups of eight heads (head dimension 128): 64 attention
+    workgroups per split index, so the residency bound, not the 128-row minimum, sets the split
+    length. With 256 resident workgroups (one per CU at this kernel's register use), 512 rows
+    fill four splits exactly, 513 rows put the extra row into the last split (129 rows), and
+    641 rows take three 256-row splits, the last one short."""
+    _flush(f"case attention splits pos={pos}")
+    sh = synth.tiny_shape(d=8192, hq=64, hkv=8, dh=128, f=512, theta=500000.0)
+    q, kv, f = synth.all_kept_mask(sh)
+    f[0, 1::3] = 0
+    case, got, want = _decode_case(sh, (q, kv, f), 8, pos, max_seq=pos + 1)
+    assert_parity(got, want, what=f"splits pos {pos}")
+    _check_cache_rows(case)
+
+
 @pytest.mark.timeout(600)
 def test_llama3_8b_batch8_full_size():
     """One Llama-3-8B-shaped layer under the seed-1 budget mask, 8 sequences at 8192 prior
