@@ -22,7 +22,7 @@ __all__ = [
     "WEIGHT_NAMES", "to_bf16_bits", "bf16_bits_to_f32", "bf16_round", "quantize_rows",
     "layer_weights", "final_norm", "lm_head", "activations", "kv_prior", "tiny_mask",
     "budget_mask", "raw_mask", "all_kept_mask", "mask_counts", "embedding", "prompt_ids",
-    "quantize_groups", "quantize_rows_bf16", "GROUP",
+    "quantize_groups", "quantize_rows_bf16", "GROUP", "zero_dropped",
 ]
 
 GROUP = 128     # columns per scale group of the groupwise store
@@ -214,6 +214,31 @@ def raw_mask(sh: Shape, seed: int, p_q=0.7, p_kv=0.8, p_f=0.6, block: int = 1):
         return q, kv, np.repeat(fb, block, axis=1)
     f = (rng.uniform(size=(L, sh.d_ffn)) < p_f).astype(np.uint8)
     return q, kv, f
+
+
+def zero_dropped(layer: dict, sh: Shape, q_keep, kv_keep, f_keep) -> dict:
+    """A copy of one layer of the INT8 store in which the weights of dropped modules are zero and
+    every scale is unchanged: the W_q rows of each dropped query head and the W_o columns that
+    read it, the W_k and W_v rows of each dropped KV group, and the gate row, up row and W_down
+    column of each dropped FFN channel. ``*_keep`` are one layer's dependency-closed keep bits.
+    Dequantised, this is the zero-masked layer, so a dense plan over it computes the masked layer
+    with the dense launch shapes (the mask-as-zero control)."""
+    dh = sh.head_dim
+    dq = np.repeat(~np.asarray(q_keep, bool), dh)
+    dkv = np.repeat(~np.asarray(kv_keep, bool), dh)
+    df = ~np.asarray(f_keep, bool)
+    out = dict(layer)
+    for name, rows, cols in (("wq", dq, None), ("wk", dkv, None), ("wv", dkv, None),
+                             ("wo", None, dq), ("wg", df, None), ("wu", df, None),
+                             ("wd", None, df)):
+        w, sc = layer[name]
+        w = w.copy()
+        if rows is not None:
+            w[rows, :] = 0
+        if cols is not None:
+            w[:, cols] = 0
+        out[name] = (w, sc)
+    return out
 
 
 def mask_counts(q, kv, f):

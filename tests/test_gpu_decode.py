@@ -265,6 +265,28 @@ def test_llama3_8b_layer_full_size():
         torch.cuda.empty_cache()
 
 
+@pytest.mark.parametrize("batch", [1, 4])
+def test_mask_as_zero_control(batch):
+    """The mask-as-zero control at the Llama-3-8B layer shape (seed-1 budget mask, 512 prior
+    positions): a dense plan over the store whose dropped modules' INT8 weights are zeroed runs
+    the dense launch shapes yet computes the masked layer, so it meets the oracle's tolerance and
+    agrees with the compiled sparse plan to float32 rounding."""
+    _flush(f"case mask-as-zero control batch {batch}")
+    sh = synth.LLAMA3_8B.with_layers(1, vocab=0)
+    layer = synth.layer_weights(sh, 0)
+    sp, got_sp, want = _decode_case(sh, synth.budget_mask(sh, 1), batch, 512, store=[layer])
+    assert_parity(got_sp, want, what="compiled sparse")
+    qc, kvc, fc = sp.closed
+    del sp
+    torch.cuda.empty_cache()
+    zc = Case(sh, None, batch, 512, store=[synth.zero_dropped(layer, sh, qc[0], kvc[0], fc[0])])
+    assert zc.plan.counts(0) == (sh.n_q_heads, sh.n_kv_heads, sh.d_ffn)
+    got_z = zc.run()
+    m, s = assert_parity(got_z, want, what="mask as zero")
+    _flush(f"  max_rel={m:.2e} sum_rel={s:.2e}")
+    assert np.abs(got_z - got_sp).max() <= 1e-4 * np.abs(got_sp).max()
+
+
 @pytest.mark.parametrize("batch,f", [(1, 24576), (2, 12288)])
 def test_wide_ffn_group_of_eight(batch, f):
     """Eight query heads per KV group and a down-projection input wider than 64 KiB of LDS

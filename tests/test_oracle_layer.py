@@ -153,6 +153,26 @@ def test_compacted_equals_zero_masked_sweep():
             assert np.allclose(a, b, rtol=1e-12, atol=1e-12)
 
 
+def test_zeroed_store_is_the_zero_masked_layer():
+    """The store of the mask-as-zero control (dropped modules' INT8 weights zeroed, scales kept),
+    read as a dense layer, dequantises to the oracle's zero-masked layer and decodes to the same
+    output as the masked layer."""
+    sh, pos = SMALL, 128
+    layer = make_store(sh)[0]
+    mask = synth.raw_mask(sh, 5)
+    W, (qc, kvc, fc) = _masked(sh, layer, mask)
+    z = synth.zero_dropped(layer, sh, qc[0], kvc[0], fc[0])
+    Wz, _ = _masked(sh, z, synth.all_kept_mask(sh))
+    for name in W:
+        assert np.array_equal(W[name], Wz[name]), name
+    x = synth.activations(1, sh.d_model)
+    c1 = caches_f64(sh, 1, pos, pos + 1)
+    c2 = caches_f64(sh, 1, pos, pos + 1)
+    a = ref.decode_layer(W, x, c1[0][0], c1[0][1], pos, sh)
+    b = ref.decode_layer(Wz, x, c2[0][0], c2[0][1], pos, sh)
+    assert np.array_equal(a, b)
+
+
 @pytest.mark.parametrize("sh", [SMALL, synth.TINY], ids=["small", "tiny_cfg"])
 def test_compacted_equals_zero_masked_configs(sh):
     pos = 128
