@@ -139,8 +139,12 @@ struct PfArgs {
   const uint16_t* gamma_next;
   float* ssq_out; int n_ssq_out;      // MM_RESID with gamma_next: [T][ceil(N/64)]
   int T;
+  float* part; size_t part_floats;    // MM_QKV / MM_RESID K-split partials [splits][T][N] (or null)
 };
 hipError_t launch_pf_gemm(MfmaMode mode, const PfArgs& a, hipStream_t s);
+// floats of the K-split partial buffer of a plan (prompt chunks up to max_prefill tokens, panels
+// of up to n_max rows)
+size_t pf_split_buffer_floats(int max_prefill, int n_max);
 // x float32 [T][D] -> hi/lo planes of x * gamma and sums of squares per 64 elements [T][D/64].
 hipError_t launch_pf_prep(const float* x, int D, int T, const uint16_t* gamma, uint16_t* xo,
                           size_t plane, int ldxo, float* ssq, hipStream_t s);

@@ -14,6 +14,15 @@
 // in chunks of 32: the global loads of the next three chunks are in flight (in registers) while
 // the current chunk's MFMAs run from LDS (double-buffered, one barrier per chunk). LDS rows hold
 // one chunk (32 BF16) with their 16-byte quarters XOR-swizzled by row (bank-conflict free).
+//
+// Split K. Panels of d_model rows (QKV, O, down) give few tiles at prompt lengths of a few
+// hundred tokens (256 at 512 tokens: one workgroup per CU, latency-bound K loops). Their K range
+// is then split over blockIdx.z so that the launch holds about as many workgroups as the chip
+// keeps resident; each split writes its scaled partial tile to a float32 buffer and a second
+// kernel sums the splits in a fixed order and applies the epilogue (residual, next operand, sums
+// of squares).
+#include <algorithm>
+
 #include "device_common.hpp"
 #include "kernels.hpp"
 
@@ -29,6 +38,10 @@ constexpr int kKC = 32;                // k per chunk
 constexpr int kLdsRow = 32;            // BF16 per LDS row (one chunk of k)
 constexpr int kSsqBlk = 64;            // rows per sum-of-squares partial
 constexpr long kPfMinTiles = 384;      // fewer 128-token tiles than this: use 64-token tiles
+constexpr int kMaxKSplit = 4;          // K splits per tile at most
+constexpr int kMinSplitChunks = 8;     // k chunks per split at least
+constexpr long kSplitRowCap = 2048;    // (tokens x splits) the partial buffer is sized for
+constexpr int kNumCu = 256;
 
 template <int TM>
 struct PfSmem {
@@ -80,9 +93,13 @@ __global__ __launch_bounds__(kBlock) void pf_gemm_kernel(PfArgs a) {
   const int r = lane & 15, q = lane >> 4;
   const int wm = wave >> 1, wn = wave & 1;
   const int T = a.T, N = a.N, K = a.K;
-  const int m0 = blockIdx.y * TM;
-  const int n0 = blockIdx.x * (GU ? kTN / 2 : kTN);   // first row (gate/up: first channel)
-  const int nk = (K + kKC - 1) / kKC;
+  const int bx = blockIdx.x, by = blockIdx.y, bz = blockIdx.z;
+  const int m0 = by * TM;
+  const int n0 = bx * (GU ? kTN / 2 : kTN);           // first row (gate/up: first channel)
+  // this workgroup's k chunks: split bz of gridDim.z
+  const int nk_all = (K + kKC - 1) / kKC;
+  const int kc0 = int((long(bz) * nk_all) / gridDim.z);
+  const int nk = int((long(bz + 1) * nk_all) / gridDim.z) - kc0;
 
   // ---- global -> register staging of one chunk
   const __amdgpu_buffer_rsrc_t ra = make_rsrc(a.x, uint32_t(2 * a.plane) * 2u);
@@ -115,7 +132,7 @@ __global__ __launch_bounds__(kBlock) void pf_gemm_kernel(PfArgs a) {
     int4 bv[2];
   };
   auto load = [&](int kc, Stage& st) {
-    const int k0 = kc * kKC;
+    const int k0 = (kc0 + kc) * kKC;
 #pragma unroll
     for (int i = 0; i < APT; ++i) st.av[i] = buf_load16(ra, kc < nk ? a_off(i, k0) : kOOB);
     if (BF) {
@@ -214,6 +231,25 @@ __global__ __launch_bounds__(kBlock) void pf_gemm_kernel(PfArgs a) {
   }
 
   // ---- epilogue: lane holds tokens 4q + i of each token tile, panel row r of each row tile
+  if (!GU && !BF && a.part) {
+    // split K: this split's scaled partial; the reduction adds the splits and the epilogue
+    float* part = a.part + size_t(bz) * T * N;
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int tl = wm * (TM / 2) + mt * 16 + 4 * q + i;
+        const int t = m0 + tl;
+        if (t >= T) continue;
+        const float rb = a.ssq ? sm.rs[tl] : 1.0f;
+#pragma unroll
+        for (int nt = 0; nt < 4; ++nt) {
+          const int n = n0 + wn * 64 + nt * 16 + r;
+          if (n < N) part[size_t(t) * N + n] = acc[mt][nt][i] * a.scale[n] * rb;
+        }
+      }
+    return;
+  }
   const bool resid_on = (MODE == MM_RESID);
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt) {
@@ -272,6 +308,33 @@ __global__ __launch_bounds__(kBlock) void pf_prep_kernel(const float* __restrict
   if ((threadIdx.x & 63) == 0 && i < D) ssq[size_t(t) * n_ssq + i / kSsqBlk] = ss;
 }
 
+// Sum of the K splits of a prefill projection (in split order) and the projection's epilogue:
+// MM_QKV stores the sum; MM_RESID adds the residual, stores the row and, with a next gain, writes
+// the next operand's hi/lo planes and the per-64-row sums of squares. Thread = one (token, row);
+// a wave covers 64 consecutive rows, i.e. one sum-of-squares block.
+template <int MODE>
+__global__ __launch_bounds__(kBlock) void pf_split_reduce_kernel(PfArgs a, int ks) {
+  const int t = blockIdx.y, n = blockIdx.x * kBlock + threadIdx.x;
+  const int T = a.T, N = a.N;
+  const bool ok = n < N;
+  float v = 0.0f;
+  if (ok)
+    for (int z = 0; z < ks; ++z) v += a.part[(size_t(z) * T + t) * N + n];
+  if (MODE == MM_RESID) {
+    if (ok) {
+      v += a.resid[size_t(t) * a.ldy + n];
+      a.y[size_t(t) * a.ldy + n] = v;
+      if (a.gamma_next) store_hilo_pf(a.xo, a.plane_o, a.ldxo, t, n, v * bf16_to_f32(a.gamma_next[n]));
+    }
+    if (a.gamma_next) {
+      const float ss = wave_sum(ok ? v * v : 0.0f);
+      if ((threadIdx.x & 63) == 0 && ok) a.ssq_out[size_t(t) * a.n_ssq_out + n / kSsqBlk] = ss;
+    }
+  } else if (ok) {
+    a.y[size_t(t) * a.ldy + n] = v;
+  }
+}
+
 // RoPE of the T tokens' q and k at positions pos0 + t. q (scaled by log2(e) / sqrt(d_h)) goes to
 // the attention operand as hi/lo planes [2][m_q][T][d_h]; k and v are rounded to BF16 and
 // written to the cache rows pos0 + t of their retained groups.
@@ -315,11 +378,41 @@ __global__ __launch_bounds__(kBlock) void pf_rope_kernel(PfRopeArgs a) {
 }
 
 template <int MODE, int TM>
+int pf_resident() {
+  static const int n = [] {
+    int per_cu = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, pf_gemm_kernel<MODE, TM>, kBlock,
+                                                     0) != hipSuccess || per_cu < 1)
+      per_cu = 1;
+    return per_cu * kNumCu;
+  }();
+  return n;
+}
+
+template <int MODE, int TM>
 hipError_t launch_pf_tm(const PfArgs& a, hipStream_t s) {
   const int rows_per_tile = (MODE == MM_GATEUP) ? kTN / 2 : kTN;
-  const dim3 grid((a.N + rows_per_tile - 1) / rows_per_tile, (a.T + TM - 1) / TM);
-  if (grid.x == 0 || grid.y == 0) return hipSuccess;
-  hipLaunchKernelGGL((pf_gemm_kernel<MODE, TM>), grid, dim3(kBlock), 0, s, a);
+  const int gx = (a.N + rows_per_tile - 1) / rows_per_tile, gy = (a.T + TM - 1) / TM;
+  if (gx == 0 || gy == 0) return hipSuccess;
+  // K splits: as many as keep every workgroup resident, at least kMinSplitChunks chunks each,
+  // and no more than the partial buffer holds
+  int ks = 1;
+  if ((MODE == MM_QKV || MODE == MM_RESID) && a.part) {
+    const long tiles = long(gx) * gy;
+    const long per_split = long(a.T) * a.N;
+    ks = int(std::min<long>(kMaxKSplit, pf_resident<MODE, TM>() / tiles));
+    ks = std::min(ks, ((a.K + kKC - 1) / kKC) / kMinSplitChunks);
+    ks = int(std::min<long>(ks, per_split > 0 ? long(a.part_floats / size_t(per_split)) : 1));
+    ks = std::max(ks, 1);
+  }
+  PfArgs b = a;
+  if (ks == 1) b.part = nullptr;
+  hipLaunchKernelGGL((pf_gemm_kernel<MODE, TM>), dim3(gx, gy, ks), dim3(kBlock), 0, s, b);
+  if (ks == 1) return hipGetLastError();
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((pf_split_reduce_kernel<MODE == MM_QKV ? MM_QKV : MM_RESID>),
+                     dim3((a.N + kBlock - 1) / kBlock, a.T), dim3(kBlock), 0, s, b, ks);
   return hipGetLastError();
 }
 
@@ -361,5 +454,12 @@ hipError_t launch_pf_rope(const PfRopeArgs& a, hipStream_t s) {
 }
 
 int pf_ssq_block() { return kSsqBlk; }
+
+size_t pf_split_buffer_floats(int max_prefill, int n_max) {
+  // splits pay while the tiles leave CUs idle, i.e. up to a few hundred tokens; past the cap the
+  // launch takes fewer splits
+  const long rows = std::min<long>(long(kMaxKSplit) * std::max(max_prefill, 0), kSplitRowCap);
+  return size_t(rows) * size_t(std::max(n_max, 0));
+}
 
 }  // namespace tasp

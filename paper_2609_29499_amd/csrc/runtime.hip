@@ -142,6 +142,7 @@ struct Layout {
   size_t r_mid, r_io0, r_io1, qkv_buf, o_buf, h_buf, part, acnt;
   size_t xd, xo, xh, ssq;            // batched path: hi/lo operands and sums of squares
   size_t pxd, pxw, pq, pqkv, pr_mid, pr_io0, pr_io1, pssq;   // prefill scratch
+  size_t ppart, ppart_floats;                                // prefill K-split partials
   size_t qkv_rows, o_cols, down_cols;                        // shared-store plans: maps
   size_t zero_begin, zero_end;       // scratch cleared at compile
   size_t total;
@@ -224,6 +225,9 @@ Layout make_layout(const tasp_model_desc* d, const Closed& c) {
   Y.pr_io1 = take(P * D * 4);
   Y.pssq = take(P * ((D + 63) / 64) * 4);
   Y.zero_end = off;
+  // written in full by each split before it is read: not zeroed
+  Y.ppart_floats = P ? tasp::pf_split_buffer_floats(int(P), std::max(D, Y.ld_qkv)) : 0;
+  Y.ppart = take(Y.ppart_floats * 4);
   Y.total = off;
   return Y;
 }
@@ -325,6 +329,8 @@ struct tasp_plan_s {
   int ld_xd, ld_xo, ld_xh;
   uint16_t *pxd, *pxw, *pq;          // prefill operands: [2][max_prefill][ld_xd | ld_xw], q planes
   float *pqkv, *pr_mid, *pr_io[2], *pssq;
+  float* ppart;                      // prefill K-split partials
+  size_t ppart_floats;
   int ld_xw;
 };
 
@@ -587,6 +593,8 @@ tasp::PfArgs pf_base(const tasp_plan_s* p, int T) {
   a.eps = p->desc.rms_eps;
   a.n_ssq = (p->desc.d_model + tasp::pf_ssq_block() - 1) / tasp::pf_ssq_block();
   a.n_ssq_out = a.n_ssq;
+  a.part = p->ppart;
+  a.part_floats = p->ppart_floats;
   return a;
 }
 
@@ -1082,6 +1090,8 @@ tasp_status tasp_compile_plan(const tasp_model_desc* desc, const tasp_store* sto
   p->pr_io[0] = reinterpret_cast<float*>(at(Y.pr_io0));
   p->pr_io[1] = reinterpret_cast<float*>(at(Y.pr_io1));
   p->pssq = reinterpret_cast<float*>(at(Y.pssq));
+  p->ppart = reinterpret_cast<float*>(at(Y.ppart));
+  p->ppart_floats = Y.ppart_floats;
   p->ld_xw = Y.ld_xw;
 
   {
@@ -1230,7 +1240,8 @@ tasp_status tasp_compile_shared_plan(const tasp_model_desc* desc, const tasp_gst
   p->acnt = reinterpret_cast<int*>(at(Y.acnt));
   p->n_split_max = Y.n_split_max; p->ld_qkv = Y.ld_qkv; p->ld_obuf = Y.ld_obuf; p->ld_h = Y.ld_h;
   p->xd = p->xo = p->xh = p->pxd = p->pxw = p->pq = nullptr;
-  p->ssq = p->pqkv = p->pr_mid = p->pr_io[0] = p->pr_io[1] = p->pssq = nullptr;
+  p->ssq = p->pqkv = p->pr_mid = p->pr_io[0] = p->pr_io[1] = p->pssq = p->ppart = nullptr;
+  p->ppart_floats = 0;
   p->ld_xd = p->ld_xo = p->ld_xh = p->ld_xw = 0;
   if ((st = read_back_indices(p, c, Y, ws, s, h)) != TASP_OK) {
     delete p;
