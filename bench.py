@@ -113,6 +113,19 @@ class Rotation:
         for i in range(n % R):
             self.plans[i].decode(self.x, self.caches[i], self.pos, self.out)
 
+    def time_eager(self, n):
+        """Mean step time (ms) of n decode steps issued as plain launches (no graph)."""
+        torch = self.torch
+        R = len(self.plans)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for i in range(n):
+            self.plans[i % R].decode(self.x, self.caches[i % R], self.pos, self.out)
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / n
+
     def time_steps(self, n):
         torch = self.torch
         torch.cuda.synchronize()
@@ -907,10 +920,11 @@ def main():
         torch.cuda.synchronize()
         ms = rot.time_steps(args.steps)
         blocks = [rot.time_steps(200) for _ in range(args.blocks)]
+        eager = rot.time_eager(max(200, args.steps // 5))
         ktimes = rot.kernel_times(args.timed_launches)
         stage_ms = rot.stage_ms(STAGE_KIND[dominant])
         results[name] = {"counts": counts, "ledger": ledger, "bytes": nb, "ms": ms,
-                         "blocks": blocks, "kernels": ktimes, "copies": copies,
+                         "blocks": blocks, "eager": eager, "kernels": ktimes, "copies": copies,
                          "stage_ms": stage_ms}
         print(f"[bench] {name}: {ms*1e3:.2f} us/step  kernels(us)=" +
               " ".join(f"{k}={v*1e3:.2f}" for k, v in ktimes.items()), file=sys.stderr, flush=True)
@@ -954,6 +968,11 @@ def main():
         "step_bytes": {"sparse": sp["bytes"]["total"], "dense": dn["bytes"]["total"]},
         "blocks_ms": {"sparse": [round(b, 6) for b in sp["blocks"]],
                       "dense": [round(b, 6) for b in dn["blocks"]]},
+        "blocks_mean_sd_ms": {k: [round(float(np.mean(r["blocks"])), 6),
+                                  round(float(np.std(r["blocks"], ddof=1)), 6)]
+                              for k, r in (("sparse", sp), ("dense", dn)) if len(r["blocks"]) > 1},
+        "plain_launch_ms_per_token": {"sparse": round(sp["eager"], 6),
+                                      "dense": round(dn["eager"], 6)},
         "kernels_us": {k: {n: round(v * 1e3, 3) for n, v in r["kernels"].items()}
                        for k, r in results.items() if "kernels" in r},
         "roofline": {"bound": "hbm", "kernel": dominant, "achieved": round(st_gbps, 1),

@@ -224,7 +224,8 @@ tasp_status tasp_decode_step(tasp_plan plan, const float* x, tasp_kv_cache* cach
  * an LM head. Token t attends causally over rows 0..pos0+t; rows pos0..pos0+T-1 of every
  * retained group receive the BF16 k and v of the tokens. pos0 == 0 binds the cache to the plan;
  * pos0 > 0 requires it bound (else TASP_ERR_CACHE_PLAN_MISMATCH). Projections and attention run
- * on the matrix cores with activations split into hi/lo BF16 pairs. Stream-ordered, capturable. */
+ * on the matrix cores with activations split into hi/lo BF16 pairs. Stream-ordered, capturable;
+ * calls on one plan must be ordered (they share the plan's scratch). */
 tasp_status tasp_prefill(tasp_plan plan, const float* x, int32_t T, tasp_kv_cache* cache,
                          int32_t pos0, float* out, void* stream);
 

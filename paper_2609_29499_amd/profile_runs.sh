@@ -4,6 +4,7 @@
 #   decode_b1:  kernel trace of the default benchmark (8B layer, batch 1), then FETCH_SIZE and
 #               WRITE_SIZE passes of its sparse plan
 #   decode_b8:  kernel trace and FETCH_SIZE / WRITE_SIZE passes of the batch-8 benchmark
+#   decode_b8_busy: VALU and MFMA busy counters of the batch-8 benchmark's sparse plan
 #   prefill:    kernel trace and MFMA counter pass of the 512-token prefill benchmark
 #   router:     kernel trace of the router benchmark (one 7 KiB turn, then 512-prompt batches)
 #   shared:     kernel trace of the shared-store benchmark (8B layer, batch 1)
@@ -23,6 +24,9 @@ decode_b8)
   echo "[prof] b8 kernel trace" && timeout -k 10 400 rocprofv3 --kernel-trace --stats -d $O/b8_trace -o trace -- python3 -u bench.py --workload llama3_8b_batch8 --steps 200 --warmup 20 --cpu-seconds 3 > $O/b8_trace.json 2> $O/b8_trace.err &&
   echo "[prof] b8 FETCH_SIZE" && timeout -s KILL 300 rocprofv3 --pmc FETCH_SIZE -d $O/b8_fetch -o fetch -- python3 -u bench.py --workload llama3_8b_batch8 --sparse-only --no-cpu --steps 100 --warmup 10 --blocks 1 --timed-launches 8 > $O/b8_fetch.json 2> $O/b8_fetch.err &&
   echo "[prof] b8 WRITE_SIZE" && timeout -s KILL 300 rocprofv3 --pmc WRITE_SIZE -d $O/b8_write -o write -- python3 -u bench.py --workload llama3_8b_batch8 --sparse-only --no-cpu --steps 100 --warmup 10 --blocks 1 --timed-launches 8 > $O/b8_write.json 2> $O/b8_write.err
+  ;;
+decode_b8_busy)
+  echo "[prof] b8 VALU / MFMA busy" && timeout -s KILL 300 rocprofv3 --pmc VALUBusy MfmaUtil -d $O/b8_busy -o busy -- python3 -u bench.py --workload llama3_8b_batch8 --sparse-only --no-cpu --steps 100 --warmup 10 --blocks 1 --timed-launches 8 > $O/b8_busy.json 2> $O/b8_busy.err
   ;;
 prefill)
   echo "[prof] prefill kernel trace" && timeout -k 10 400 rocprofv3 --kernel-trace --stats -d $O/pf_trace -o trace -- python3 -u bench.py --workload llama3_8b_prefill512 --steps 200 --warmup 20 --cpu-seconds 3 > $O/pf_trace.json 2> $O/pf_trace.err &&

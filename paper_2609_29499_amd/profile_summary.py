@@ -42,6 +42,8 @@ def kind_of(name: str) -> str | None:
         (r"mfma_gemv_kernel<2,", "gateup_mfma"),
         (r"mfma_gemv_kernel<1,", "resid_mfma"),
         (r"mfma_gemv_kernel<3,", "lmhead_mfma"),
+        (r"pf_split_reduce_kernel<0>", "qkv_reduce"),
+        (r"pf_split_reduce_kernel<1>", "resid_reduce"),
         (r"pf_gemm_kernel<0,", "qkv_gemm"),
         (r"pf_gemm_kernel<2,", "gateup_gemm"),
         (r"pf_gemm_kernel<1,", "resid_gemm"),
@@ -60,12 +62,16 @@ def kind_of(name: str) -> str | None:
 
 
 def _named(kinds):
-    """Resolve resid_* into o_* / down_* by order: a residual GEMV right after gate/up is down."""
+    """Resolve resid_* into o_* / down_* by order: a residual GEMV right after gate/up is down;
+    a split-K reduction takes the name of the GEMM it follows."""
     out, prev = [], None
     for k in kinds:
         if k and k.startswith("resid_"):
             suffix = k.split("_", 1)[1]
-            k = ("down_" if prev and prev.startswith("gateup_") else "o_") + suffix
+            if suffix == "reduce" and prev in ("o_gemm", "down_gemm"):
+                k = prev.split("_", 1)[0] + "_reduce"
+            else:
+                k = ("down_" if prev and prev.startswith("gateup_") else "o_") + suffix
         out.append(k)
         if k:
             prev = k

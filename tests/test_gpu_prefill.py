@@ -47,6 +47,18 @@ def test_tiny_layer_prefill(masked):
     _check_cache(case)
 
 
+def test_prefill_repeat_bit_exact():
+    """The QKV, O and down GEMMs of this prefill split K (2 to 4 splits per tile, summed in split
+    order by the reduction): repeated prefills give the same bits."""
+    _flush("case prefill repeat")
+    sh = synth.TINY
+    case = PrefillCase(sh, synth.tiny_mask(sh), 128, 0)
+    first = case.run()
+    for _ in range(3):
+        assert np.array_equal(case.run(), first)
+    assert_parity(first, case.oracle(), what="prefill repeat")
+
+
 @pytest.mark.parametrize("T,pos0", [(1, 0), (77, 0), (77, 128), (130, 5), (200, 300)])
 def test_prefill_ragged_and_offset(T, pos0):
     """Token counts that are not tile multiples, and prompts continuing a prior cache."""
