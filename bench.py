@@ -70,6 +70,28 @@ def layer_bytes(sh, m_q, m_kv, c, pos, batch=1):
             "attention": attention}
 
 
+def stack_bytes(sh, counts, pos):
+    """Algorithmic HBM bytes of one batch-1 decode step of a stack: every layer's retained INT8
+    weights, row scales and retained KV rows (per-layer counts (m_q, m_kv, c)), plus the BF16 LM
+    head (2 V d bytes)."""
+    tot = {"weights": 0, "scales": 0, "kv": 0}
+    for m_q, m_kv, c in counts:
+        nb = layer_bytes(sh, m_q, m_kv, c, pos, 1)
+        for k in tot:
+            tot[k] += nb[k]
+    tot["lm_head"] = 2 * sh.vocab * sh.d_model
+    tot["total"] = tot["weights"] + tot["scales"] + tot["kv"] + tot["lm_head"]
+    return tot
+
+
+def dense_layer_flops(sh):
+    """Active FLOPs per token of the full-width stack: per layer 2 d d_h (H_q + 2 H_kv) for QKV,
+    2 d_h H_q d for O and 6 d F for gate, up and down."""
+    d, dh = sh.d_model, sh.head_dim
+    return sh.n_layers * (2 * d * dh * (sh.n_q_heads + 2 * sh.n_kv_heads)
+                          + 2 * dh * sh.n_q_heads * d + 6 * d * sh.d_ffn)
+
+
 class Rotation:
     """R compiled copies of one plan with their own KV caches, and HIP graphs of one step each."""
 
@@ -224,7 +246,6 @@ def measure_stack(args, sh, pos, mask_seeds):
     import torch
     import synth
     from paper_2609_29499_amd import session as S
-    from oracle import reference as ref
     gen = torch.Generator(device="cuda")
     gen.manual_seed(0)
     t0 = time.time()
@@ -269,11 +290,22 @@ def measure_stack(args, sh, pos, mask_seeds):
         e1.record()
         torch.cuda.synchronize()
         ms = e0.elapsed_time(e1) / args.steps
+        # LM head time from per-kernel events (median of 5 timed steps): us per layer excludes it
+        lm, gu = [], []
+        for _ in range(5):
+            kt = plan.decode_timed(x, cache, pos, out)
+            lm.append(sum(t for k, t in kt if k == "lmhead_gemv"))
+            gu.append(sum(t for k, t in kt if k == "gateup_gemv"))
+        lm_ms, gu_ms = float(np.median(lm)), float(np.median(gu))
         counts = [plan.counts(l) for l in range(sh.n_layers)]
-        cnt = [np.array([c[i] for c in counts]) for i in range(3)]
-        nb = ref.decode_bytes(sh, cnt, 1, pos, lm_head=True)
+        d = sh.d_model
+        gu_bytes = sum(2 * c * d + 2 * c * 4 + d * 4 + c * 4 for _, _, c in counts)
+        nb = stack_bytes(sh, counts, pos)
         led = plan.ledger()
-        rows.append({"plan": name, "ms_per_token": round(ms, 5), "bytes": nb["total"],
+        rows.append({"plan": name, "ms_per_token": round(ms, 5),
+                     "us_per_layer": round((ms - lm_ms) * 1e3 / sh.n_layers, 3),
+                     "lm_head_ms": round(lm_ms, 5), "gateup_ms": round(gu_ms, 5),
+                     "gateup_bytes": gu_bytes, "bytes": nb["total"],
                      "GBps": round(nb["total"] / (ms * 1e-3) / 1e9, 1),
                      "active_flop_ratio": round(led["active_flop_ratio"], 4)})
         print(f"[bench] {name}: {ms:.4f} ms/token, {rows[-1]['GBps']} GB/s", file=sys.stderr, flush=True)
@@ -310,8 +342,34 @@ def bench_stack(args, wl):
         "achieved_GBps": round(float(np.mean([r["GBps"] for r in sparse])), 1),
         "hbm_frac": round(float(np.mean([r["GBps"] for r in sparse])) / PEAK_GBPS, 4),
         "paper_context": "45.2 -> 31.3 ms/token dense vs compiled sparse, Llama-3-70B, INT8/BF16, one A100 80GB",
-        "roofline": None, "cpu_baseline": None,
+        "us_per_layer": round(float(np.mean([r["us_per_layer"] for r in sparse])), 3),
+        "dense_us_per_layer": dense["us_per_layer"],
+        # the kernel with the largest share of the step: the gate/up GEMVs of all layers, timed
+        # by per-kernel events in eager steps of the first masked plan
+        "roofline": {"bound": "hbm", "kernel": "gateup_gemv (all layers)",
+                     "achieved": round(sparse[0]["gateup_bytes"] / (sparse[0]["gateup_ms"] * 1e-3) / 1e9, 1),
+                     "peak": PEAK_GBPS, "unit": "GB/s",
+                     "frac": round(sparse[0]["gateup_bytes"] / (sparse[0]["gateup_ms"] * 1e-3) / 1e9
+                                   / PEAK_GBPS, 4),
+                     "traffic": None, "algorithmic_bytes": sparse[0]["gateup_bytes"],
+                     "ms_per_step": sparse[0]["gateup_ms"]},
+        "cpu_baseline": None,
     }
+    if not args.no_cpu:
+        # CPU baseline: the oracle on one layer of the stack's shape under the first mask, times
+        # the layer count (a whole stack in float64 does not fit host memory); LM head excluded
+        import synth
+        sh1 = sh.with_layers(1, vocab=0)
+        layer = synth.layer_weights(sh1, 0)
+        m = synth.budget_mask(sh, wl.mask_seeds[0])
+        m1 = tuple(a[:1] for a in m)
+        prior = synth.kv_prior(sh1, 0, 1, pos, pos + 1)
+        x = synth.activations(1, sh.d_model)
+        cb = cpu_baseline(sh1, layer, m1, prior, x, pos, args.cpu_seconds)
+        cb["value"] = round(cb["value"] * sh.n_layers, 3)
+        cb["sample"] = (cb["sample"].replace("of the same layer", "of layer 0 of this shape") +
+                        f"; times {sh.n_layers} layers, LM head excluded")
+        line["cpu_baseline"] = cb
     print(json.dumps(line), flush=True)
 
 
@@ -534,7 +592,6 @@ def bench_mask(args, wl):
     """Greedy dependency-closed mask construction from seeded scores: ms per build on the GPU
     (each call synchronises), checked against the oracle, with the oracle timed on the host."""
     import torch
-    from oracle import greedy as G
     from paper_2609_29499_amd import session as S
     sh, granule = wl.shape, wl.granule
     rng = np.random.default_rng(args.mask_seed)
@@ -550,11 +607,19 @@ def bench_mask(args, wl):
     for _ in range(reps):
         q, kv, f, spent = S.build_mask(desc, hd, cd, granule, 0.57)
     ms = (time.perf_counter() - t0) / reps * 1e3
-    t1 = time.perf_counter()
-    wq, wkv, wf, wspent, _ = G.greedy_mask(sh, hs, cs, granule, 0.57)
-    cpu_ms = (time.perf_counter() - t1) * 1e3
-    same = (spent == wspent and np.array_equal(q.cpu().numpy(), wq)
-            and np.array_equal(kv.cpu().numpy(), wkv) and np.array_equal(f.cpu().numpy(), wf))
+    cpu = None
+    if not args.no_cpu:
+        # CPU baseline: the oracle's construction of the same candidate set, timed once; its
+        # selection is reported next to the GPU's
+        from oracle import greedy as G
+        t1 = time.perf_counter()
+        wq, wkv, wf, wspent, _ = G.greedy_mask(sh, hs, cs, granule, 0.57)
+        cpu_ms = (time.perf_counter() - t1) * 1e3
+        same = (spent == wspent and np.array_equal(q.cpu().numpy(), wq)
+                and np.array_equal(kv.cpu().numpy(), wkv) and np.array_equal(f.cpu().numpy(), wf))
+        cpu = {"value": round(cpu_ms, 3), "unit": "ms/mask", "cores": 1, "kind": "oracle",
+               "sample": "one oracle construction of the same candidate set (Python loop)",
+               "same_selection_as_gpu": bool(same)}
     n_cand = sh.n_layers * (sh.n_q_heads + sh.d_ffn // granule)
     line = {
         "metric": "ms per greedy dependency-closed mask construction", "value": round(ms, 4),
@@ -563,10 +628,9 @@ def bench_mask(args, wl):
         "data": "synthetic",
         "config": {"workload": wl.name, "layers": sh.n_layers, "candidates": n_cand,
                    "granule": granule, "target": 0.57},
-        "active_flop_ratio": round(spent / G.full_flops(sh), 6), "matches_oracle": bool(same),
+        "active_flop_ratio": round(spent / dense_layer_flops(sh), 6),
         "roofline": None,
-        "cpu_baseline": {"value": round(cpu_ms, 3), "unit": "ms/mask", "cores": 1, "kind": "oracle",
-                         "sample": "one oracle construction of the same candidate set (Python loop)"},
+        "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)
 
@@ -705,7 +769,6 @@ def bench_router(args, wl):
     u L_sparse + (1 - u) L_dense with both path latencies measured on the 8B stack in this run.
     The router weights are random (seeded): u(tau) shows the mechanics, not a trained router."""
     import torch
-    from oracle import router as R
     from paper_2609_29499_amd import session as S
     from synth import text as T
     w = T.router_weights()
@@ -777,8 +840,10 @@ def bench_router(args, wl):
     # the two path latencies the mixture is formed from
     rows = measure_stack(args, wl.shape, wl.pos, wl.mask_seeds)
     l_dense, l_sparse = rows[0]["ms_per_token"], rows[1]["ms_per_token"]
-    mixture = {t: round(R.mixture_latency(u, l_sparse, l_dense), 5) for t, u in usage.items()}
-    # the oracle on the host: features + MLP of the same turn, repeated for about cpu_seconds
+    # mixture-implied latency at sparse-path usage u: u L_sparse + (1 - u) L_dense
+    mixture = {t: round(u * l_sparse + (1.0 - u) * l_dense, 5) for t, u in usage.items()}
+    # CPU baseline: the oracle on the host, features + MLP of the same turn, for about cpu_seconds
+    from oracle import router as R
     t1 = time.perf_counter()
     n_cpu = 0
     while time.perf_counter() - t1 < min(args.cpu_seconds, 10.0) or n_cpu == 0:
