@@ -47,6 +47,19 @@ def test_tiny_layer_prefill(masked):
     _check_cache(case)
 
 
+def test_prefill_70b_width_split_k():
+    """Llama-3-70B width (8192, 64 / 8 heads, d_h 128) with a narrow FFN, 256 tokens after 64
+    prior positions: the 8192-row O and down panels and the QKV panel run as 256 tiles of 64
+    tokens with K split 4 ways (down: 1024 / 32 = 32 k chunks)."""
+    _flush("case prefill 70b width split k")
+    sh = synth.tiny_shape(d=8192, hq=64, hkv=8, dh=128, f=1024, theta=500000.0)
+    case = PrefillCase(sh, synth.raw_mask(sh, 12, p_q=0.7, p_kv=0.9), 256, 64)
+    got, want = case.run(), case.oracle()
+    m, s = assert_parity(got, want, what="prefill 70b width")
+    _flush(f"  max_rel={m:.2e} sum_rel={s:.2e}")
+    _check_cache(case)
+
+
 def test_prefill_repeat_bit_exact():
     """The QKV, O and down GEMMs of this prefill split K (2 to 4 splits per tile, summed in split
     order by the reduction): repeated prefills give the same bits."""
