@@ -4,7 +4,8 @@
 // 16 qb .. 16 qb + 15 of every retained head of slot j, so each K/V row staged in LDS is shared by
 // the group's heads. Cache rows 0 .. pos0 + last query are walked in sub-blocks of 64:
 //   * K (row-major) and V (transposed, dimension-major) of the sub-block are staged in LDS, rows
-//     past the causal end read as zeros;
+//     past the causal end read as zeros; the next sub-block's rows are loaded into registers
+//     while the current one is computed;
 //   * per head, S = Q K^T with v_mfma_f32_16x16x32_bf16 (q as hi/lo BF16 planes, K exact BF16),
 //     already in base-2 units (q carries log2(e) / sqrt(d_h)); rows after a query's position are
 //     masked; an online softmax keeps each query row's running max and sum in the four rows a
@@ -83,25 +84,42 @@ __global__ __launch_bounds__(kBlock) void pf_attn_kernel(PfAttnArgs a) {
     }
   }
 
+  // K / V pieces of one sub-block per thread: piece tid + kBlock i is row p / PPR, 16-byte
+  // column piece p % PPR. The next sub-block's pieces are loaded into registers while the current
+  // one is computed from LDS.
+  constexpr int PPR = DH / 8;                           // 16-byte pieces per row
+  constexpr int KPT = kKB * PPR / kBlock;               // pieces per thread
+  static_assert(kKB * PPR % kBlock == 0, "sub-block pieces must divide over the workgroup");
+  int4 pk[KPT], pv[KPT];
+  auto load_sb = [&](int sb) {
+#pragma unroll
+    for (int i = 0; i < KPT; ++i) {
+      const int p = tid + kBlock * i;
+      const int t = sb * kKB + p / PPR;
+      const uint32_t off = t < kv_end ? (uint32_t(t) * DH + 8u * (p % PPR)) * 2u : kOOB;
+      pk[i] = buf_load16(rk, off);
+      pv[i] = buf_load16(rv, off);
+    }
+  };
+  load_sb(0);
+
   for (int sb = 0; sb < n_sb; ++sb) {
     const int tb = sb * kKB;
-    // ---- stage K and transposed V of rows tb .. tb + 63
+    // ---- stage K and transposed V of rows tb .. tb + 63, then start loading the next rows
     __syncthreads();                                    // previous sub-block fully consumed
-    constexpr int PPR = DH / 8;                         // 16-byte pieces per row
-    for (int p = tid; p < kKB * PPR; p += kBlock) {
+#pragma unroll
+    for (int i = 0; i < KPT; ++i) {
+      const int p = tid + kBlock * i;
       const int row = p / PPR, c8 = p % PPR;
-      const int t = tb + row;
-      const uint32_t off = t < kv_end ? (uint32_t(t) * DH + 8u * c8) * 2u : kOOB;
-      const int4 kv = buf_load16(rk, off);
-      const int4 vv = buf_load16(rv, off);
-      *reinterpret_cast<int4*>(&sm.k[row * KROW + 8 * c8]) = kv;
-      const uint32_t w[4] = {uint32_t(vv.x), uint32_t(vv.y), uint32_t(vv.z), uint32_t(vv.w)};
+      *reinterpret_cast<int4*>(&sm.k[row * KROW + 8 * c8]) = pk[i];
+      const uint32_t w[4] = {uint32_t(pv[i].x), uint32_t(pv[i].y), uint32_t(pv[i].z), uint32_t(pv[i].w)};
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         sm.vt[(8 * c8 + 2 * e) * kVtRow + row] = uint16_t(w[e] & 0xffffu);
         sm.vt[(8 * c8 + 2 * e + 1) * kVtRow + row] = uint16_t(w[e] >> 16);
       }
     }
+    if (sb + 1 < n_sb) load_sb(sb + 1);
     __syncthreads();
 
 #pragma unroll
