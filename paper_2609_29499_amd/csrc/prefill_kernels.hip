@@ -297,15 +297,32 @@ __global__ __launch_bounds__(kBlock) void pf_gemm_kernel(PfArgs a) {
 }
 
 // First operand of a prefill: x * gamma as hi/lo planes and per-64-element sums of squares of x.
+// Thread = four consecutive elements of token blockIdx.y; 16 lanes cover one 64-element block.
 __global__ __launch_bounds__(kBlock) void pf_prep_kernel(const float* __restrict__ x, int D,
                                                          const uint16_t* __restrict__ gamma,
                                                          uint16_t* xo, size_t plane, int ldxo,
                                                          float* ssq, int n_ssq) {
-  const int t = blockIdx.y, i = blockIdx.x * kBlock + threadIdx.x;
-  const float v = i < D ? x[size_t(t) * D + i] : 0.0f;
-  if (i < D) store_hilo_pf(xo, plane, ldxo, t, i, v * bf16_to_f32(gamma[i]));
-  const float ss = wave_sum(v * v);
-  if ((threadIdx.x & 63) == 0 && i < D) ssq[size_t(t) * n_ssq + i / kSsqBlk] = ss;
+  const int t = blockIdx.y, i0 = (blockIdx.x * kBlock + threadIdx.x) * 4;
+  const __amdgpu_buffer_rsrc_t rx = make_rsrc(x + size_t(t) * D, uint32_t(D) * 4u);
+  const float4 v = __builtin_bit_cast(float4, buf_load16(rx, i0 < D ? uint32_t(i0) * 4u : kOOB));
+  float ss = fmaf(v.x, v.x, fmaf(v.y, v.y, fmaf(v.z, v.z, v.w * v.w)));
+  if (i0 < D) {
+    const float e[4] = {v.x * bf16_to_f32(gamma[i0]), v.y * bf16_to_f32(gamma[i0 + 1]),
+                        v.z * bf16_to_f32(gamma[i0 + 2]), v.w * bf16_to_f32(gamma[i0 + 3])};
+    uint32_t hi[2], lo[2];
+#pragma unroll
+    for (int k = 0; k < 2; ++k) {
+      const uint16_t h0 = f32_to_bf16(e[2 * k]), h1 = f32_to_bf16(e[2 * k + 1]);
+      hi[k] = uint32_t(h0) | (uint32_t(h1) << 16);
+      lo[k] = uint32_t(f32_to_bf16(e[2 * k] - bf16_to_f32(h0))) |
+              (uint32_t(f32_to_bf16(e[2 * k + 1] - bf16_to_f32(h1))) << 16);
+    }
+    uint16_t* row = xo + size_t(t) * ldxo + i0;          // 8-byte aligned: ldxo % 64 == 0
+    *reinterpret_cast<uint2*>(row) = make_uint2(hi[0], hi[1]);
+    *reinterpret_cast<uint2*>(row + plane) = make_uint2(lo[0], lo[1]);
+  }
+  ss = row16_sum(ss);
+  if ((threadIdx.x & 15) == 0 && i0 < D) ssq[size_t(t) * n_ssq + i0 / kSsqBlk] = ss;
 }
 
 // Sum of the K splits of a prefill projection (in split order) and the projection's epilogue:
@@ -441,8 +458,8 @@ hipError_t launch_pf_gemm(MfmaMode mode, const PfArgs& a, hipStream_t s) {
 
 hipError_t launch_pf_prep(const float* x, int D, int T, const uint16_t* gamma, uint16_t* xo,
                           size_t plane, int ldxo, float* ssq, hipStream_t s) {
-  if (D % 16 != 0 || T < 1) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(pf_prep_kernel, dim3((D + kBlock - 1) / kBlock, T), dim3(kBlock), 0, s, x, D,
+  if (D % 16 != 0 || T < 1 || ldxo % 4 != 0 || plane % 4 != 0) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(pf_prep_kernel, dim3((D + 4 * kBlock - 1) / (4 * kBlock), T), dim3(kBlock), 0, s, x, D,
                      gamma, xo, plane, ldxo, ssq, (D + kSsqBlk - 1) / kSsqBlk);
   return hipGetLastError();
 }
