@@ -354,42 +354,61 @@ __global__ __launch_bounds__(kBlock) void pf_split_reduce_kernel(PfArgs a, int k
 
 // RoPE of the T tokens' q and k at positions pos0 + t. q (scaled by log2(e) / sqrt(d_h)) goes to
 // the attention operand as hi/lo planes [2][m_q][T][d_h]; k and v are rounded to BF16 and
-// written to the cache rows pos0 + t of their retained groups.
+// written to the cache rows pos0 + t of their retained groups. An item is four consecutive
+// rotation pairs (q, k) or four consecutive v elements.
+__device__ __forceinline__ void store_bf16x4(uint16_t* dst, const float (&v)[4]) {
+  const uint32_t a = uint32_t(f32_to_bf16(v[0])) | (uint32_t(f32_to_bf16(v[1])) << 16);
+  const uint32_t b = uint32_t(f32_to_bf16(v[2])) | (uint32_t(f32_to_bf16(v[3])) << 16);
+  *reinterpret_cast<uint2*>(dst) = make_uint2(a, b);
+}
+
 __global__ __launch_bounds__(kBlock) void pf_rope_kernel(PfRopeArgs a) {
   const int t = blockIdx.x;
-  const int dh = a.dh, half = dh / 2;
+  const int dh = a.dh, half = dh / 2, h4 = half / 4;
   const float* row = a.qkv + size_t(t) * a.ld_qkv;
   const int pos = a.pos0 + t;
   const float* cs = a.rope_cos + size_t(pos) * half;
   const float* sn = a.rope_sin + size_t(pos) * half;
   const float qscale = kLog2e * rsqrtf(float(dh));
-  const int nq = a.m_q * half, nk = a.m_kv * half, nv = a.m_kv * dh;
+  const int nq = a.m_q * h4, nk = a.m_kv * h4, nv = a.m_kv * (dh / 4);
   for (int it = threadIdx.x; it < nq + nk + nv; it += kBlock) {
     if (it < nq + nk) {
       const bool is_q = it < nq;
       const int u = is_q ? it : it - nq;
-      const int h = u / half, i = u % half;
+      const int h = u / h4, i = 4 * (u % h4);
       const float* src = row + (is_q ? h * dh : (a.m_q + h) * dh);
-      const float x1 = src[i], x2 = src[i + half];
-      const float y1 = x1 * cs[i] - x2 * sn[i];
-      const float y2 = x2 * cs[i] + x1 * sn[i];
+      const float4 x1 = *reinterpret_cast<const float4*>(src + i);
+      const float4 x2 = *reinterpret_cast<const float4*>(src + i + half);
+      const float4 c = *reinterpret_cast<const float4*>(cs + i);
+      const float4 sv = *reinterpret_cast<const float4*>(sn + i);
+      const float sc = is_q ? qscale : 1.0f;
+      const float y1[4] = {(x1.x * c.x - x2.x * sv.x) * sc, (x1.y * c.y - x2.y * sv.y) * sc,
+                           (x1.z * c.z - x2.z * sv.z) * sc, (x1.w * c.w - x2.w * sv.w) * sc};
+      const float y2[4] = {(x2.x * c.x + x1.x * sv.x) * sc, (x2.y * c.y + x1.y * sv.y) * sc,
+                           (x2.z * c.z + x1.z * sv.z) * sc, (x2.w * c.w + x1.w * sv.w) * sc};
       if (is_q) {
         uint16_t* qo = a.q_out + (size_t(h) * a.T_ld + t) * dh;
-        const float v1 = y1 * qscale, v2 = y2 * qscale;
-        const uint16_t h1 = f32_to_bf16(v1), h2 = f32_to_bf16(v2);
-        qo[i] = h1;
-        qo[i + half] = h2;
-        qo[a.q_plane + i] = f32_to_bf16(v1 - bf16_to_f32(h1));
-        qo[a.q_plane + i + half] = f32_to_bf16(v2 - bf16_to_f32(h2));
+        float l1[4], l2[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          l1[e] = y1[e] - bf16_to_f32(f32_to_bf16(y1[e]));
+          l2[e] = y2[e] - bf16_to_f32(f32_to_bf16(y2[e]));
+        }
+        store_bf16x4(qo + i, y1);
+        store_bf16x4(qo + i + half, y2);
+        store_bf16x4(qo + a.q_plane + i, l1);
+        store_bf16x4(qo + a.q_plane + i + half, l2);
       } else {
         uint16_t* kc = a.kc + (size_t(a.kv_idx[h]) * a.S + pos) * dh;
-        kc[i] = f32_to_bf16(y1);
-        kc[i + half] = f32_to_bf16(y2);
+        store_bf16x4(kc + i, y1);
+        store_bf16x4(kc + i + half, y2);
       }
     } else {
       const int u = it - nq - nk;
-      const int j = u / dh, e = u % dh;
-      a.vc[(size_t(a.kv_idx[j]) * a.S + pos) * dh + e] = f32_to_bf16(row[(a.m_q + a.m_kv + j) * dh + e]);
+      const int j = u / (dh / 4), e = 4 * (u % (dh / 4));
+      const float4 v = *reinterpret_cast<const float4*>(row + (a.m_q + a.m_kv + j) * dh + e);
+      const float w[4] = {v.x, v.y, v.z, v.w};
+      store_bf16x4(a.vc + (size_t(a.kv_idx[j]) * a.S + pos) * dh + e, w);
     }
   }
 }
