@@ -1,16 +1,18 @@
-"""Benchmark: decode latency of the compiled sparse plan vs the dense plan on one MI355X.
+"""Benchmark: decode latency of compiled structured-sparse plans vs the dense plan on one MI355X.
 
-Workload (default): one Llama-3-8B-shaped decoder layer (hidden 4096, 32/8 heads, head_dim 128,
-SwiGLU 14336), INT8 per-row weights, batch 1, 2048 prior positions in the BF16 cache, the seed-1
-43%-reduction mask and the dense plan. A step is one full decode step of the layer (QKV GEMV,
-attention, O GEMV, gate/up GEMV, down GEMV). A sparse layer is ~131 MB and fits the 256 MB
-Infinity Cache, so every timed sequence rotates over independent plan copies (>= 2.5 GB) and each
-step reads its panels from HBM. Steps are replayed from HIP graphs (one graph holds one step of
-every copy), which is how a serving loop issues a fixed plan.
+Workload (default, `llama3_70b_stack`): the full 80-layer Llama-3-70B-shaped decode step at batch
+1 (hidden 8192, 64 / 8 heads, head_dim 128, SwiGLU 28672, INT8 per-row weights, 4096 prior
+positions in the BF16 cache, final RMSNorm and the dense 128256 x 8192 BF16 LM head), the seed-1
+43%-reduction mask against the dense plan. A step is one token through every layer and the LM
+head, replayed from a HIP graph (how a serving loop issues a fixed plan). `value` is the mean of
+five timing blocks of 200 steps (each after 50 warm-up steps), as the paper times its decode.
 
 Output: one JSON line with the metric, the dense comparison, the achieved HBM bandwidth, the
-roofline of the dominant kernel (gate/up GEMV, timed per launch with HIP events on the launch
-stream), and the CPU oracle timed on the host cores as a baseline.
+roofline of the dominant kernel (the gate/up GEMVs of all layers, timed per launch with HIP events
+on the launch stream), the measured HBM traffic of that kernel where a counter summary of the
+current kernel source exists, the CPU oracle timed on the host cores as a baseline, a run manifest,
+and (default workload only) the one-layer and 32-layer Llama-3-8B-shaped numbers as extras.
+Other workloads: `--workload` (see synth.WORKLOADS).
 """
 from __future__ import annotations
 
@@ -38,12 +40,16 @@ def parse():
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--steps", type=int, default=1000)
     p.add_argument("--warmup", type=int, default=50)
-    p.add_argument("--workload", default="llama3_8b_layer")
+    p.add_argument("--workload", default="llama3_70b_stack")
     p.add_argument("--mask-seed", type=int, default=1)
     p.add_argument("--blocks", type=int, default=5)
     p.add_argument("--timed-launches", type=int, default=64)
     p.add_argument("--cpu-seconds", type=float, default=12.0)
     p.add_argument("--no-cpu", action="store_true")
+    p.add_argument("--no-extras", action="store_true",
+                   help="default workload: skip the 8B layer and 8B stack extras")
+    p.add_argument("--block-warmup", type=int, default=50)
+    p.add_argument("--block-steps", type=int, default=200)
     p.add_argument("--sparse-only", action="store_true",
                    help="time only the sparse plan (counter runs); no JSON metric line")
     return p.parse_args()
@@ -240,9 +246,42 @@ def device_layer(torch, sh, gen):
     return out
 
 
-def measure_stack(args, sh, pos, mask_seeds):
-    """ms/token of a full decode step (all layers + final norm + BF16 LM head) for the dense plan
-    and every seeded mask, batch 1, cache at pos prior positions: one row per plan, dense first."""
+def _graph_of(torch, S, plan, x, cache, pos, out):
+    """A HIP graph holding one decode step of `plan` (captured on a side stream after a warm
+    launch)."""
+    g = torch.cuda.CUDAGraph()
+    st = torch.cuda.Stream()
+    st.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(st):
+        plan.decode(x, cache, pos, out, stream=S.current_stream())
+    torch.cuda.current_stream().wait_stream(st)
+    torch.cuda.synchronize()
+    with torch.cuda.graph(g):
+        plan.decode(x, cache, pos, out, stream=S.current_stream())
+    torch.cuda.synchronize()
+    return g
+
+
+def _time_replays(torch, g, n):
+    """Mean ms per replay of n back-to-back replays between two events."""
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(n):
+        g.replay()
+    e1.record()
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / n
+
+
+def measure_stack(args, sh, pos, mask_seeds, timed_steps=5):
+    """ms/token of a full decode step (all layers + final norm + BF16 LM head) for every seeded
+    mask and then the dense plan, batch 1, cache at pos prior positions: one row per plan, in
+    that order (sparse first, so a kernel trace splits at the first dense-shaped launch).
+
+    Per plan: args.warmup replays, then args.steps timed replays (ms_per_step), then args.blocks
+    blocks of args.block_warmup + args.block_steps replays (the paper's protocol); per-kernel HIP
+    events over `timed_steps` eager steps give the gate/up GEMV and LM head durations."""
     import torch
     import synth
     from paper_2609_29499_amd import session as S
@@ -256,7 +295,11 @@ def measure_stack(args, sh, pos, mask_seeds):
     desc = S.desc_from_shape(sh, max_batch=1, max_seq=pos + 1)
     torch.cuda.synchronize()
     print(f"[bench] stack: store drawn in {time.time() - t0:.1f}s", file=sys.stderr, flush=True)
-    plans = [("dense", None)] + [(f"mask{sd}", synth.budget_mask(sh, sd)) for sd in mask_seeds]
+    plans = [(f"mask{sd}", synth.budget_mask(sh, sd)) for sd in mask_seeds]
+    if args.sparse_only:        # counter runs: the first mask alone
+        plans = plans[:1]
+    else:
+        plans.append(("dense", None))
     x = torch.randn(1, sh.d_model, generator=gen, device="cuda").to(torch.bfloat16).float()
     out = torch.empty(1, sh.vocab, device="cuda")
     rows = []
@@ -271,44 +314,43 @@ def measure_stack(args, sh, pos, mask_seeds):
         for _ in range(3):
             plan.decode(x, cache, pos, out)
         torch.cuda.synchronize()
-        g = torch.cuda.CUDAGraph()
-        st = torch.cuda.Stream()
-        st.wait_stream(torch.cuda.current_stream())
-        with torch.cuda.stream(st):
-            plan.decode(x, cache, pos, out, stream=S.current_stream())
-        torch.cuda.current_stream().wait_stream(st)
-        torch.cuda.synchronize()
-        with torch.cuda.graph(g):
-            plan.decode(x, cache, pos, out, stream=S.current_stream())
+        g = _graph_of(torch, S, plan, x, cache, pos, out)
         for _ in range(args.warmup):
             g.replay()
-        torch.cuda.synchronize()
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record()
-        for _ in range(args.steps):
-            g.replay()
-        e1.record()
-        torch.cuda.synchronize()
-        ms = e0.elapsed_time(e1) / args.steps
-        # LM head time from per-kernel events (median of 5 timed steps): us per layer excludes it
-        lm, gu = [], []
-        for _ in range(5):
+        ms = _time_replays(torch, g, args.steps)
+        blocks = []
+        for _ in range(args.blocks):
+            for _ in range(args.block_warmup):
+                g.replay()
+            blocks.append(_time_replays(torch, g, args.block_steps))
+        # per-kernel HIP events around every launch of eager steps on the launch stream
+        lm_ms, gu_launch = [], []
+        for _ in range(timed_steps):
             kt = plan.decode_timed(x, cache, pos, out)
-            lm.append(sum(t for k, t in kt if k == "lmhead_gemv"))
-            gu.append(sum(t for k, t in kt if k == "gateup_gemv"))
-        lm_ms, gu_ms = float(np.median(lm)), float(np.median(gu))
+            lm_ms.append(sum(t for k, t in kt if k == "lmhead_gemv"))
+            gu_launch += [t for k, t in kt if k == "gateup_gemv"]
+        lm_ms = float(np.median(lm_ms))
         counts = [plan.counts(l) for l in range(sh.n_layers)]
         d = sh.d_model
         gu_bytes = sum(2 * c * d + 2 * c * 4 + d * 4 + c * 4 for _, _, c in counts)
         nb = stack_bytes(sh, counts, pos)
         led = plan.ledger()
-        rows.append({"plan": name, "ms_per_token": round(ms, 5),
-                     "us_per_layer": round((ms - lm_ms) * 1e3 / sh.n_layers, 3),
-                     "lm_head_ms": round(lm_ms, 5), "gateup_ms": round(gu_ms, 5),
-                     "gateup_bytes": gu_bytes, "bytes": nb["total"],
-                     "GBps": round(nb["total"] / (ms * 1e-3) / 1e9, 1),
+        bmean = float(np.mean(blocks)) if blocks else ms
+        rows.append({"plan": name, "ms_per_token": round(bmean, 5), "ms_per_step": round(ms, 5),
+                     "blocks_ms": [round(b, 5) for b in blocks],
+                     "blocks_mean_sd_ms": [round(bmean, 5),
+                                           round(float(np.std(blocks, ddof=1)), 5) if len(blocks) > 1 else 0.0],
+                     "us_per_layer": round((bmean - lm_ms) * 1e3 / sh.n_layers, 3),
+                     "lm_head_ms": round(lm_ms, 5),
+                     "gateup_avg_launch_us": round(float(np.mean(gu_launch)) * 1e3, 3),
+                     "gateup_launches_timed": len(gu_launch),
+                     "gateup_bytes_per_launch": round(gu_bytes / sh.n_layers),
+                     "bytes": nb["total"], "kv_bytes": nb["kv"], "lm_head_bytes": nb["lm_head"],
+                     "GBps": round(nb["total"] / (bmean * 1e-3) / 1e9, 1),
                      "active_flop_ratio": round(led["active_flop_ratio"], 4)})
-        print(f"[bench] {name}: {ms:.4f} ms/token, {rows[-1]['GBps']} GB/s", file=sys.stderr, flush=True)
+        print(f"[bench] {name}: {bmean:.4f} ms/token (blocks), {ms:.4f} (timed steps), "
+              f"{rows[-1]['GBps']} GB/s, gate/up {rows[-1]['gateup_avg_launch_us']} us/launch",
+              file=sys.stderr, flush=True)
         del cache, g, plan
         torch.cuda.empty_cache()
     del store, layers
@@ -316,61 +358,174 @@ def measure_stack(args, sh, pos, mask_seeds):
     return rows
 
 
-def bench_stack(args, wl):
+def host_cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for ln in f:
+                if ln.startswith("model name"):
+                    return ln.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
+SOURCE_FILES = ["bench.py", "include/tasp.h", "paper_2609_29499_amd/session.py",
+                "paper_2609_29499_amd/binding.py"]
+
+
+def run_manifest():
+    """What ran where: the commit (when the tree is a git checkout) and a hash of the library and
+    bench sources, ROCm / torch / HIP versions, the GPU and the host CPU."""
+    import subprocess
+    import torch
+    man = {}
+    try:
+        r = subprocess.run(["git", "rev-parse", "HEAD"], cwd=ROOT, capture_output=True, text=True,
+                           timeout=10)
+        man["git_sha"] = r.stdout.strip() or None
+    except (OSError, subprocess.SubprocessError):
+        man["git_sha"] = None
+    csrc = os.path.join(ROOT, "paper_2609_29499_amd", "csrc")
+    files = SOURCE_FILES + sorted(os.path.join("paper_2609_29499_amd", "csrc", f)
+                                  for f in os.listdir(csrc))
+    man["source_sha"] = source_hash(files)
+    try:
+        with open("/opt/rocm/.info/version") as f:
+            man["rocm"] = f.read().strip()
+    except OSError:
+        man["rocm"] = None
+    man["torch"] = torch.__version__
+    man["hip_runtime"] = getattr(torch.version, "hip", None)
+    props = torch.cuda.get_device_properties(0)
+    man["gpu"] = props.name
+    man["gpu_arch"] = getattr(props, "gcnArchName", None)
+    man["host_cpu"] = host_cpu_model()
+    man["host_cpus"] = len(os.sched_getaffinity(0))
+    return man
+
+
+def stack_line(args, wl, rows):
+    """The JSON line of a stack workload from measure_stack's rows."""
     sh, pos = wl.shape, wl.pos
-    rows = measure_stack(args, sh, pos, wl.mask_seeds)
-    dense = rows[0]
-    sparse = rows[1:]
+    sparse = [r for r in rows if r["plan"] != "dense"]
+    dense = next((r for r in rows if r["plan"] == "dense"), None)
     mean_sparse = float(np.mean([r["ms_per_token"] for r in sparse]))
-    bts = np.array([r["bytes"] for r in rows], float)
-    tms = np.array([r["ms_per_token"] for r in rows], float)
-    slope, icpt = np.polyfit(bts, tms, 1)
-    pred = slope * bts + icpt
-    r2 = 1.0 - float(((tms - pred) ** 2).sum() / ((tms - tms.mean()) ** 2).sum())
+    ms_steps = float(np.mean([r["ms_per_step"] for r in sparse]))
+    sp0 = sparse[0]
+    gu_gbps = sp0["gateup_bytes_per_launch"] / (sp0["gateup_avg_launch_us"] * 1e-6) / 1e9
     line = {
         "metric": METRIC, "value": round(mean_sparse, 5), "unit": "ms/token", "n_gpus": 1,
-        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(mean_sparse, 5),
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_steps, 5),
         "higher_is_better": False, "scaling": "weak", "vs_baseline": None, "dtype": "int8w-f32",
         "data": "synthetic",
-        "config": {"workload": wl.name, "d_model": sh.d_model, "layers": sh.n_layers,
-                   "vocab": sh.vocab, "batch": 1, "pos": pos, "masks": list(wl.mask_seeds)},
-        "dense_ms_per_token": dense["ms_per_token"],
-        "speedup_vs_dense": round(dense["ms_per_token"] / mean_sparse, 4),
+        "config": {"workload": wl.name, "d_model": sh.d_model, "n_q_heads": sh.n_q_heads,
+                   "n_kv_heads": sh.n_kv_heads, "head_dim": sh.head_dim, "d_ffn": sh.d_ffn,
+                   "layers": sh.n_layers, "vocab": sh.vocab, "batch": 1, "pos": pos,
+                   "masks": list(wl.mask_seeds)},
+        "value_protocol": f"mean of {args.blocks} blocks x {args.block_steps} graph replays "
+                          f"(each after {args.block_warmup} warm-up replays) over the sparse plans",
         "plans": rows,
-        "time_vs_bytes": {"slope_ms_per_GB": round(slope * 1e9, 4), "intercept_ms": round(icpt, 4),
-                          "r2": round(r2, 4)},
         "achieved_GBps": round(float(np.mean([r["GBps"] for r in sparse])), 1),
         "hbm_frac": round(float(np.mean([r["GBps"] for r in sparse])) / PEAK_GBPS, 4),
-        "paper_context": "45.2 -> 31.3 ms/token dense vs compiled sparse, Llama-3-70B, INT8/BF16, one A100 80GB",
         "us_per_layer": round(float(np.mean([r["us_per_layer"] for r in sparse])), 3),
-        "dense_us_per_layer": dense["us_per_layer"],
-        # the kernel with the largest share of the step: the gate/up GEMVs of all layers, timed
-        # by per-kernel events in eager steps of the first masked plan
-        "roofline": {"bound": "hbm", "kernel": "gateup_gemv (all layers)",
-                     "achieved": round(sparse[0]["gateup_bytes"] / (sparse[0]["gateup_ms"] * 1e-3) / 1e9, 1),
-                     "peak": PEAK_GBPS, "unit": "GB/s",
-                     "frac": round(sparse[0]["gateup_bytes"] / (sparse[0]["gateup_ms"] * 1e-3) / 1e9
-                                   / PEAK_GBPS, 4),
-                     "traffic": None, "algorithmic_bytes": sparse[0]["gateup_bytes"],
-                     "ms_per_step": sparse[0]["gateup_ms"]},
+        "paper_context": "45.2 -> 31.3 ms/token dense vs compiled sparse, Llama-3-70B, INT8/BF16, one A100 80GB",
+        # the kernel that moves the most bytes of the step: the gate/up GEMVs (one per layer),
+        # per-launch HIP events on the launch stream in eager steps of the first masked plan
+        "roofline": {"bound": "hbm", "kernel": "gateup_gemv",
+                     "achieved": round(gu_gbps, 1), "peak": PEAK_GBPS, "unit": "GB/s",
+                     "frac": round(gu_gbps / PEAK_GBPS, 4),
+                     "traffic": load_traffic("gateup_gemv", wl.name),
+                     "algorithmic_bytes": sp0["gateup_bytes_per_launch"],
+                     "avg_launch_us": sp0["gateup_avg_launch_us"],
+                     "launches_timed": sp0["gateup_launches_timed"]},
         "cpu_baseline": None,
     }
+    if dense is not None:
+        line["dense_ms_per_token"] = dense["ms_per_token"]
+        line["speedup_vs_dense"] = round(dense["ms_per_token"] / mean_sparse, 4)
+        line["dense_us_per_layer"] = dense["us_per_layer"]
+        line["byte_ratio_sparse_over_dense"] = round(sp0["bytes"] / dense["bytes"], 4)
+        line["time_ratio_sparse_over_dense"] = round(sp0["ms_per_token"] / dense["ms_per_token"], 4)
+        bts = np.array([r["bytes"] for r in rows], float)
+        tms = np.array([r["ms_per_token"] for r in rows], float)
+        slope, icpt = np.polyfit(bts, tms, 1)
+        pred = slope * bts + icpt
+        ss = float(((tms - tms.mean()) ** 2).sum())
+        r2 = 1.0 - float(((tms - pred) ** 2).sum() / ss) if ss > 0 else 1.0
+        line["time_vs_bytes"] = {"slope_ms_per_GB": round(slope * 1e9, 4),
+                                 "intercept_ms": round(icpt, 4), "r2": round(r2, 4),
+                                 "bandwidth_of_slope_GBps": round(1.0 / slope / 1e6, 1) if slope > 0 else None}
+    return line
+
+
+def stack_cpu_baseline(args, wl):
+    """The oracle on layer 0 of the stack's shape under the first mask, times the layer count (a
+    whole stack in float64 does not fit host memory); LM head excluded."""
+    import synth
+    sh, pos = wl.shape, wl.pos
+    sh1 = sh.with_layers(1, vocab=0)
+    t0 = time.time()
+    layer = synth.layer_weights(sh1, 0)
+    m = synth.budget_mask(sh, wl.mask_seeds[0])
+    m1 = tuple(a[:1] for a in m)
+    prior = synth.kv_prior(sh1, 0, 1, pos, pos + 1)
+    x = synth.activations(1, sh.d_model)
+    print(f"[bench] CPU oracle layer drawn in {time.time() - t0:.1f}s", file=sys.stderr, flush=True)
+    cb = cpu_baseline(sh1, layer, m1, prior, x, pos, args.cpu_seconds)
+    cb["per_layer_ms"] = round(cb["value"], 3)
+    cb["value"] = round(cb["value"] * sh.n_layers, 3)
+    cb["sample"] = (cb["sample"].replace("of the same layer", "of layer 0 of this shape") +
+                    f"; times {sh.n_layers} layers, LM head excluded")
+    return cb
+
+
+def bench_stack(args, wl):
+    import torch
+    from paper_2609_29499_amd import binding as B
+    t0 = time.time()
+    rows = measure_stack(args, wl.shape, wl.pos, wl.mask_seeds)
+    line = stack_line(args, wl, rows)
+    # the plain 1 GiB copy: a bandwidth reference, and the calibration of counter runs
+    probe = copy_probe_gbps(torch, B)
+    line["copy_probe_GBps"] = round(probe, 1)
+    line["frac_of_copy_probe"] = round(line["achieved_GBps"] / probe, 4)
+    print(f"[bench] {wl.name}: timing done in {time.time() - t0:.1f}s", file=sys.stderr, flush=True)
     if not args.no_cpu:
-        # CPU baseline: the oracle on one layer of the stack's shape under the first mask, times
-        # the layer count (a whole stack in float64 does not fit host memory); LM head excluded
-        import synth
-        sh1 = sh.with_layers(1, vocab=0)
-        layer = synth.layer_weights(sh1, 0)
-        m = synth.budget_mask(sh, wl.mask_seeds[0])
-        m1 = tuple(a[:1] for a in m)
-        prior = synth.kv_prior(sh1, 0, 1, pos, pos + 1)
-        x = synth.activations(1, sh.d_model)
-        cb = cpu_baseline(sh1, layer, m1, prior, x, pos, args.cpu_seconds)
-        cb["value"] = round(cb["value"] * sh.n_layers, 3)
-        cb["sample"] = (cb["sample"].replace("of the same layer", "of layer 0 of this shape") +
-                        f"; times {sh.n_layers} layers, LM head excluded")
-        line["cpu_baseline"] = cb
+        line["cpu_baseline"] = stack_cpu_baseline(args, wl)
+    if wl.name == "llama3_70b_stack" and not args.no_extras and not args.sparse_only:
+        line["extras"] = default_extras(args)
+    line["manifest"] = run_manifest()
     print(json.dumps(line), flush=True)
+
+
+def default_extras(args):
+    """The Llama-3-8B-shaped single layer (2048 prior positions) and 32-layer stack (4096) at
+    batch 1, sparse vs dense, with the same timing protocol (no CPU baseline, no control)."""
+    import copy
+    import synth
+    ex = {}
+    a = copy.copy(args)
+    a.no_cpu, a.control = True, False
+    t0 = time.time()
+    ln = bench_layer(a, synth.WORKLOADS["llama3_8b_layer"])
+    ex["llama3_8b_layer"] = {k: ln[k] for k in (
+        "value", "unit", "us_per_layer", "dense_ms_per_token", "speedup_vs_dense",
+        "byte_ratio_sparse_over_dense", "time_ratio_sparse_over_dense", "achieved_GBps",
+        "hbm_frac", "blocks_mean_sd_ms", "kernels_us", "roofline")}
+    ex["llama3_8b_layer"]["config"] = ln["config"]
+    print(f"[bench] extra 8B layer in {time.time() - t0:.1f}s", file=sys.stderr, flush=True)
+    t0 = time.time()
+    wl = synth.WORKLOADS["llama3_8b_stack"]
+    sl = stack_line(a, wl, measure_stack(a, wl.shape, wl.pos, wl.mask_seeds))
+    ex["llama3_8b_stack"] = {k: sl.get(k) for k in (
+        "value", "unit", "us_per_layer", "dense_ms_per_token", "speedup_vs_dense",
+        "dense_us_per_layer", "achieved_GBps", "hbm_frac", "time_vs_bytes", "roofline")}
+    ex["llama3_8b_stack"]["plans"] = [{k: r[k] for k in ("plan", "ms_per_token", "bytes", "GBps",
+                                                         "us_per_layer", "active_flop_ratio")}
+                                      for r in sl["plans"]]
+    ex["llama3_8b_stack"]["config"] = sl["config"]
+    print(f"[bench] extra 8B stack in {time.time() - t0:.1f}s", file=sys.stderr, flush=True)
+    return ex
 
 
 KERNEL_SOURCES = {
@@ -839,7 +994,8 @@ def bench_router(args, wl):
     usage = {f"{t:.2f}": round(u, 4) for t, u in used.items()}
     # the two path latencies the mixture is formed from
     rows = measure_stack(args, wl.shape, wl.pos, wl.mask_seeds)
-    l_dense, l_sparse = rows[0]["ms_per_token"], rows[1]["ms_per_token"]
+    l_sparse = rows[0]["ms_per_token"]
+    l_dense = next(r["ms_per_token"] for r in rows if r["plan"] == "dense")
     # mixture-implied latency at sparse-path usage u: u L_sparse + (1 - u) L_dense
     mixture = {t: round(u * l_sparse + (1.0 - u) * l_dense, 5) for t, u in usage.items()}
     # CPU baseline: the oracle on the host, features + MLP of the same turn, for about cpu_seconds
@@ -956,9 +1112,25 @@ def main():
     if sh.n_layers != 1 or wl.prefill_tokens:
         print(json.dumps({"error": f"workload {args.workload} is not a single-layer decode"}))
         sys.exit(2)
+    line = bench_layer(args, wl)
+    if line is not None:
+        line["manifest"] = run_manifest()
+        print(json.dumps(line), flush=True)
+
+
+def bench_layer(args, wl):
+    """One decoder layer (batch 1 or 8) over rotating plan copies: the sparse plan of the seed
+    mask and the dense plan. Returns the JSON line (None for --sparse-only counter runs, which
+    print their own summary)."""
+    import torch
+
+    import synth
+    from paper_2609_29499_amd import binding as B
+    from paper_2609_29499_amd import session as S
+    sh, pos = wl.shape, wl.pos
     batch = wl.batch
     t_setup = time.time()
-    print(f"[bench] generating {args.workload}", file=sys.stderr, flush=True)
+    print(f"[bench] generating {wl.name}", file=sys.stderr, flush=True)
     layer = synth.layer_weights(sh, 0)
     mask = synth.budget_mask(sh, args.mask_seed)
     prior = synth.kv_prior(sh, 0, batch, pos, pos + 1)
@@ -995,7 +1167,7 @@ def main():
               " ".join(f"{k}={v*1e3:.2f}" for k, v in ktimes.items()), file=sys.stderr, flush=True)
         del rot
         torch.cuda.empty_cache()
-    if not args.sparse_only:
+    if not args.sparse_only and getattr(args, "control", True):
         results["mask_as_zero"] = mask_as_zero_control(args, S, B, torch, sh, desc, dstore, layer,
                                                        mask, prior, x, pos, batch)
     probe = copy_probe_gbps(torch, B)
@@ -1003,33 +1175,36 @@ def main():
         print(json.dumps({"sparse_ms_per_step": results["sparse"]["ms"],
                           "kernels_us": {k: v * 1e3 for k, v in results["sparse"]["kernels"].items()},
                           "copy_probe_GBps": probe}), flush=True)
-        return
+        return None
     sp, dn = results["sparse"], results["dense"]
-    gbps = sp["bytes"]["total"] / (sp["ms"] * 1e-3) / 1e9
+    sp_block = float(np.mean(sp["blocks"])) if sp["blocks"] else sp["ms"]
+    dn_block = float(np.mean(dn["blocks"])) if dn["blocks"] else dn["ms"]
     st_ms = sp["stage_ms"]
     st_bytes = sp["bytes"]["attention" if dominant == "attention" else "gateup"]
     st_gbps = st_bytes / (st_ms * 1e-3) / 1e9
     traffic = load_traffic("gateup_mfma" if dominant == "gateup_gemv" and batch > 1 else dominant,
-                           args.workload)
+                           wl.name)
+    gbps = sp["bytes"]["total"] / (sp_block * 1e-3) / 1e9
     line = {
-        "metric": METRIC, "value": round(sp["ms"], 6), "unit": "ms/token", "n_gpus": 1,
+        "metric": METRIC, "value": round(sp_block, 6), "unit": "ms/token", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(sp["ms"], 6),
         "higher_is_better": False, "scaling": "weak", "vs_baseline": None, "dtype": "int8w-f32",
         "data": "synthetic",
-        "config": {"workload": args.workload, "d_model": sh.d_model, "n_q_heads": sh.n_q_heads,
+        "config": {"workload": wl.name, "d_model": sh.d_model, "n_q_heads": sh.n_q_heads,
                    "n_kv_heads": sh.n_kv_heads, "head_dim": sh.head_dim, "d_ffn": sh.d_ffn,
                    "layers": 1, "batch": batch, "pos": pos, "mask_seed": args.mask_seed,
                    "active_flop_ratio": round(sp["ledger"]["active_flop_ratio"], 4),
                    "retained": {"q_heads": sp["counts"][0], "kv_groups": sp["counts"][1],
                                 "ffn_channels": sp["counts"][2]}},
-        "us_per_layer": round(sp["ms"] * 1e3, 3),
-        "dense_ms_per_token": round(dn["ms"], 6),
-        "speedup_vs_dense": round(dn["ms"] / sp["ms"], 4),
+        "value_protocol": f"mean of {len(sp['blocks'])} blocks x 200 graph-replayed steps",
+        "us_per_layer": round(sp_block * 1e3, 3),
+        "dense_ms_per_token": round(dn_block, 6),
+        "speedup_vs_dense": round(dn_block / sp_block, 4),
         "byte_ratio_sparse_over_dense": round(sp["bytes"]["total"] / dn["bytes"]["total"], 4),
-        "time_ratio_sparse_over_dense": round(sp["ms"] / dn["ms"], 4),
+        "time_ratio_sparse_over_dense": round(sp_block / dn_block, 4),
         "achieved_GBps": round(gbps, 1), "hbm_frac": round(gbps / PEAK_GBPS, 4),
         "copy_probe_GBps": round(probe, 1), "frac_of_copy_probe": round(gbps / probe, 4),
-        "dense_achieved_GBps": round(dn["bytes"]["total"] / (dn["ms"] * 1e-3) / 1e9, 1),
+        "dense_achieved_GBps": round(dn["bytes"]["total"] / (dn_block * 1e-3) / 1e9, 1),
         "step_bytes": {"sparse": sp["bytes"]["total"], "dense": dn["bytes"]["total"]},
         "blocks_ms": {"sparse": [round(b, 6) for b in sp["blocks"]],
                       "dense": [round(b, 6) for b in dn["blocks"]]},
@@ -1046,18 +1221,19 @@ def main():
                      "avg_launch_us": round(st_ms * 1e3, 3)},
         "paper_context": "45.2 -> 31.3 ms/token dense vs compiled sparse, Llama-3-70B, INT8/BF16, one A100 80GB",
         "rotation_copies": {"sparse": sp["copies"], "dense": dn["copies"]},
-        "mask_as_zero": {"ms_per_token": round(results["mask_as_zero"]["ms"], 6),
-                         "speedup_vs_dense": round(dn["ms"] / results["mask_as_zero"]["ms"], 4),
-                         "paper_context": "mask-as-zero 1.03x vs compiled 1.44x over dense "
-                                          "(Llama-3-70B, one A100)"},
     }
+    if "mask_as_zero" in results:
+        line["mask_as_zero"] = {"ms_per_token": round(results["mask_as_zero"]["ms"], 6),
+                                "speedup_vs_dense": round(dn["ms"] / results["mask_as_zero"]["ms"], 4),
+                                "paper_context": "mask-as-zero 1.03x vs compiled 1.44x over dense "
+                                                 "(Llama-3-70B, one A100)"}
     print(f"[bench] setup+timing {time.time()-t_setup:.1f}s", file=sys.stderr, flush=True)
     if not args.no_cpu:
         print("[bench] timing the CPU oracle", file=sys.stderr, flush=True)
         line["cpu_baseline"] = cpu_baseline(sh, layer, mask, prior, x, pos, args.cpu_seconds)
     else:
         line["cpu_baseline"] = None
-    print(json.dumps(line), flush=True)
+    return line
 
 
 if __name__ == "__main__":

@@ -120,8 +120,12 @@ enum { TASP_IDX_Q = 0, TASP_IDX_KV = 1, TASP_IDX_QKVSLOT = 2, TASP_IDX_FFN = 3 }
 enum { TASP_PANEL_QKV = 0, TASP_PANEL_O = 1, TASP_PANEL_GATE = 2, TASP_PANEL_UP = 3,
        TASP_PANEL_DOWN = 4 };
 
-/* Workspace bytes that tasp_compile_plan needs for this mask (panels, copies of the gains and
- * LM head, RoPE table, decode and prefill scratch). The mask is closed on the host to size it. */
+/* Workspace bytes that tasp_compile_plan needs for this mask (paper, Sec. "Dependency-Closed
+ * Masks and Cache-Consistent Routing": each mask's retained units are packed into contiguous
+ * tensors; Eqs. flop-attn and flop-mlp give the retained panel shapes): panels, copies of the
+ * gains and LM head, RoPE table, decode and prefill scratch. The mask is closed on the host to
+ * size it. desc, mask: host; *bytes (host) receives the size. Errors: TASP_ERR_SHAPE for an
+ * unsupported desc, TASP_ERR_MASK for a byte other than 0 / 1. */
 tasp_status tasp_plan_workspace_bytes(const tasp_model_desc* desc, const tasp_mask* mask,
                                       size_t* bytes);
 
@@ -181,18 +185,27 @@ tasp_status tasp_compile_shared_plan(const tasp_model_desc* desc, const tasp_gst
                                      const tasp_mask* mask, void* workspace,
                                      size_t workspace_bytes, void* stream, tasp_plan* out);
 
-/* Retained counts of one layer after closure: query heads, KV groups, SwiGLU channels. */
+/* Retained counts of one layer after closure (paper, Eqs. flop-attn and flop-mlp: m^q, m^kv and
+ * c of that layer): query heads, KV groups, SwiGLU channels, written to host int32s.
+ * TASP_ERR_INVALID_ARG for a NULL pointer or a layer outside 0..n_layers-1. */
 tasp_status tasp_plan_counts(tasp_plan plan, int32_t layer, int32_t* m_q, int32_t* m_kv,
                              int32_t* n_ffn);
 
-/* Copy one ascending index list of a layer as computed on the device (host dst of cap entries):
- * TASP_IDX_Q retained query heads, TASP_IDX_KV retained KV groups, TASP_IDX_QKVSLOT the rank of
- * each retained head's group among the retained groups, TASP_IDX_FFN retained channels. */
+/* Copy one ascending index list of a layer as computed on the device by the closure (paper,
+ * Sec. "Dependency-Closed Masks and Cache-Consistent Routing": a KV group stays active while any
+ * of its query heads is retained, heads keep their group, and a SwiGLU channel is kept or removed
+ * in gate, up and down together) into host dst of cap entries: TASP_IDX_Q retained query heads,
+ * TASP_IDX_KV retained KV groups, TASP_IDX_QKVSLOT the rank of each retained head's group among
+ * the retained groups, TASP_IDX_FFN retained channels. *n (if not NULL) receives the list length; dst NULL
+ * only queries it. TASP_ERR_INVALID_ARG if the length exceeds cap, or for a bad layer / `which`. */
 tasp_status tasp_plan_indices(tasp_plan plan, int32_t layer, int32_t which, int32_t* dst,
                               int32_t cap, int32_t* n);
 
-/* Where a panel of a layer lives: device int8 rows [rows][ld] (columns >= cols are zero) and its
- * float32 scales [rows]. QKV rows: retained q heads, then K, then V rows of retained groups. */
+/* Where a panel of a layer lives (paper, appendix "Backing-store semantics": the contiguous
+ * retained tensors a plan launches on): device int8 rows [rows][ld] (columns >= cols are zero)
+ * and its float32 scales [rows], both inside the plan's workspace (not owned by the caller's
+ * pointers; valid until tasp_plan_destroy). QKV rows: retained q heads, then K, then V rows of
+ * retained groups. TASP_ERR_UNSUPPORTED for a shared-store plan (it has no panels). */
 tasp_status tasp_plan_panel(tasp_plan plan, int32_t layer, int32_t which, const int8_t** w,
                             const float** scale, int64_t* rows, int64_t* cols, int64_t* ld);
 
@@ -202,14 +215,22 @@ tasp_status tasp_plan_panel(tasp_plan plan, int32_t layer, int32_t which, const 
 tasp_status tasp_plan_ledger(tasp_plan plan, double* active_flop_ratio, uint64_t* weight_bytes,
                              uint64_t* scale_bytes, uint64_t* signature);
 
+/* Release a plan's host metadata (paper, appendix "Backing-store semantics": a mask owns plan
+ * metadata only). The workspace given to the compile call stays the caller's to free once the
+ * plan's queued work has completed. NULL is accepted. */
 tasp_status tasp_plan_destroy(tasp_plan plan);
 
 /* Adopt a cache whose rows 0..pos-1 were filled outside the library (already rotated keys) for
- * this plan: checks its shape and sets cache->plan_sig. */
+ * this plan (paper, Sec. "Dependency-Closed Masks and Cache-Consistent Routing": cache contents
+ * belong to one mask and are not carried to an incompatible one): checks its shape against the
+ * plan (TASP_ERR_SHAPE: batch outside 1..max_batch, max_seq above the plan's) and sets
+ * cache->plan_sig (host struct; the device arrays are not touched). */
 tasp_status tasp_kv_bind(tasp_plan plan, tasp_kv_cache* cache);
 
-/* One decode step for cache->batch sequences that share `pos` (prior positions, 0 <= pos <
- * cache->max_seq). x (device) float32 [batch][d_model]; out (device) float32 [batch][d_model], or
+/* One decode step (paper, Sec. "Dependency-Closed Masks and Cache-Consistent Routing": the
+ * plan chosen for a turn runs every decode step; Table "systems": the timed decode latency) for
+ * cache->batch sequences that share `pos` (prior positions, 0 <= pos < cache->max_seq, else
+ * TASP_ERR_POS_RANGE; a cache bound to another plan gives TASP_ERR_CACHE_PLAN_MISMATCH). x (device) float32 [batch][d_model]; out (device) float32 [batch][d_model], or
  * logits [batch][vocab] when the plan has an LM head. x and out may not overlap. Stream-ordered
  * and asynchronous; launches only the plan's kernels and allocates nothing, so it may be captured
  * into a HIP graph. Calls on one plan must be ordered (they share the plan's scratch). */
@@ -217,8 +238,9 @@ tasp_status tasp_decode_step(tasp_plan plan, const float* x, tasp_kv_cache* cach
                              float* out, void* stream);
 
 /* Prefill of T tokens of one sequence (cache->batch must be 1) at positions pos0..pos0+T-1
- * (paper, Sec. "Deployment": the plan fixed at the start of a turn serves the prompt and every
- * later decode step). 1 <= T <= max_prefill (TASP_ERR_UNSUPPORTED for a plan compiled with
+ * (paper, Sec. "Dependency-Closed Masks and Cache-Consistent Routing": the plan fixed at the start
+ * of a turn serves the prompt and every later decode step; Table "configuration": the timed
+ * request begins with a prefill). 1 <= T <= max_prefill (TASP_ERR_UNSUPPORTED for a plan compiled with
  * max_prefill 0), pos0 + T <= cache->max_seq (else TASP_ERR_POS_RANGE). x (device) float32
  * [T][d_model]; out (device, not overlapping x) float32 [T][d_model], or logits [T][vocab] with
  * an LM head. Token t attends causally over rows 0..pos0+t; rows pos0..pos0+T-1 of every
@@ -245,13 +267,16 @@ tasp_status tasp_generate(tasp_plan plan, const int8_t* embed, const float* embe
                           const int32_t* prompt, int32_t T, int32_t n_new, tasp_kv_cache* cache,
                           int32_t* out_ids, float* x_scratch, float* logits, void* stream);
 
-/* Profiling variant of tasp_prefill: an event pair around every kernel; kinds as for
- * tasp_decode_step_timed, plus 7 for the RoPE / cache-append kernel. Synchronises `stream`. */
+/* Profiling variant of tasp_prefill (per-kernel split of the prefill time of Table "systems"):
+ * an event pair around every kernel; kinds as for tasp_decode_step_timed, plus 7 for the RoPE /
+ * cache-append kernel. kernel_ms, kinds: host arrays of cap entries; *n the kernels launched.
+ * Synchronises `stream`. */
 tasp_status tasp_prefill_timed(tasp_plan plan, const float* x, int32_t T, tasp_kv_cache* cache,
                                int32_t pos0, float* out, void* stream, float* kernel_ms,
                                int32_t* kinds, int32_t cap, int32_t* n);
 
-/* Profiling variant of tasp_decode_step: records a HIP event pair around every kernel it launches,
+/* Profiling variant of tasp_decode_step (per-kernel split of the decode latency of Table
+ * "systems"): records a HIP event pair around every kernel it launches,
  * synchronises `stream`, and writes each kernel's duration in milliseconds to kernel_ms[i] and a
  * kernel-kind code to kinds[i] (0 QKV, 1 attention, 2 O, 3 gate/up, 4 down, 5 LM head, 6 batched
  * operand preparation) for up to
@@ -260,7 +285,8 @@ tasp_status tasp_decode_step_timed(tasp_plan plan, const float* x, tasp_kv_cache
                                    int32_t pos, float* out, void* stream, float* kernel_ms,
                                    int32_t* kinds, int32_t cap, int32_t* n);
 
-/* Profiling: average duration of one stage of layer `layer`, measured as n_plans * reps
+/* Profiling (the timing protocol of Sec. "Experimental Design": back-to-back runs between
+ * events, here for one stage): average duration of one stage of layer `layer`, measured as n_plans * reps
  * back-to-back launches between two HIP events on `stream`. Stage `kind`: 1 attention at `pos`
  * (split-KV partials, merged by the last split of each group slot; rewrites cache row pos with
  * the same values), 3 the gate/up projection (RMSNorm + SwiGLU), 4 the down projection (writes the plan's
@@ -354,8 +380,9 @@ tasp_status tasp_route(const tasp_router* router, const uint8_t* text, int32_t n
                        int32_t* choice, void* stream);
 
 /* One user turn with routing and dispatch (paper, Sec. "Dependency-Closed Masks and
- * Cache-Consistent Routing": the decision is made once per turn, the chosen plan serves the
- * turn's prefill and every decode step, and a KV cache is never reused across different masks).
+ * Cache-Consistent Routing"): one routing decision per turn; the plan it picks runs all of that
+ * turn's prefill and decode work; cache rows written under one closed mask are kept only when the
+ * same plan serves the next turn, and are otherwise discarded and rebuilt.
  *   1. routes the turn's text (device bytes [n_text], one prompt) with proxy_logprob (device
  *      float32 [1]) and waits for the decision (this synchronises `stream`);
  *   2. takes task_plans[choice], or dense_plan for choice -1 (all n_tasks + 1 plans must share
@@ -379,10 +406,15 @@ tasp_status tasp_serve_turn(const tasp_router* router, const tasp_plan* task_pla
                             size_t workspace_bytes, int32_t* chosen, int32_t* reused,
                             void* stream);
 
-/* Plain streaming copy of `bytes` (multiple of 16) from src to dst (device): the reference kernel
- * whose counter readings calibrate memory-traffic measurements. */
+/* Plain streaming copy of `bytes` (multiple of 16) from src to dst (device, not overlapping):
+ * the reference kernel whose counter readings calibrate memory-traffic measurements (the byte
+ * ledger of appendix "FLOP and storage validation" checked against hardware counters).
+ * TASP_ERR_INVALID_ARG for NULL pointers or a size not a multiple of 16. */
 tasp_status tasp_copy_probe(void* dst, const void* src, size_t bytes, void* stream);
 
+/* Text of a status code, and the thread-local detail of the last failing call on this thread
+ * (static / thread-owned strings; the caller does not free them). They report the host-side
+ * validation that precedes every enqueue (all entry points above). */
 const char* tasp_status_string(tasp_status s);
 const char* tasp_last_error(void);
 

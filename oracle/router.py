@@ -1,11 +1,12 @@
 """Oracle for router inference and dense-fallback dispatch (test infrastructure only).
 
 Paper, Sec. "Dependency-Closed Masks and Cache-Consistent Routing" and the appendix paragraph
-"Router feature specification": once per user turn a three-layer MLP (hidden widths 512 and 256)
-maps a fixed feature vector of the prompt to a distribution over the task plans; temperature
-scaling is applied to its logits; when the largest probability is below tau (0.85) the turn runs
-on the dense INT8 plan, otherwise on the plan of the most probable task. The plan is fixed for
-the turn's prefill and decode, and a KV cache is never reused across different masks. Appendix
+"Router feature specification": each user turn is routed once. An MLP with two hidden layers
+(512 and 256 wide) turns the prompt's feature vector into task logits, which are divided by a
+temperature and normalised; a turn whose top probability falls short of tau (0.85) goes to the
+dense INT8 plan, any other turn to its top task's plan. That plan then handles the whole turn
+(prefill and decode), and cached K/V rows only carry over to a turn served by the same closed
+mask. Appendix
 "Routing, Calibration, and Task-Switching Robustness", Eq. for L(tau): the mixture-implied decode
 latency u L_sparse + (1 - u) L_dense, u the fraction of turns on the sparse path.
 

@@ -7,6 +7,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <initializer_list>
 #include <new>
 #include <string>
 #include <vector>
@@ -848,17 +849,56 @@ tasp_status tasp_plan_workspace_bytes(const tasp_model_desc* desc, const tasp_ma
 
 namespace {
 
-// Signature of a plan: the model shape, the closed mask and the store format (0 per-row panels,
-// 1 groupwise shared store); equal signatures mean interchangeable cache contents.
-uint64_t plan_signature(const tasp_model_desc& d, const Closed& c, int32_t format) {
+// Signature of a plan: the model shape, the RMSNorm epsilon and RoPE base, the closed mask, the
+// store format (0 per-row panels, 1 groupwise shared store) and the store's identity (a hash of
+// every device address it names); equal signatures mean interchangeable cache contents. Two
+// stores at distinct addresses, or one mask under another epsilon or RoPE base, never share a
+// cache. (A store freed and re-filled at the same addresses keeps its identity: the caller owns
+// that lifetime.)
+uint64_t plan_signature(const tasp_model_desc& d, const Closed& c, int32_t format,
+                        uint64_t store_id) {
   uint64_t sig = 1469598103934665603ull;
   const int32_t shape[7] = {d.n_layers, d.d_model, d.n_q_heads, d.n_kv_heads, d.head_dim, d.d_ffn, d.vocab};
   sig = fnv1a(sig, shape, sizeof shape);
+  sig = fnv1a(sig, &d.rms_eps, sizeof d.rms_eps);
+  sig = fnv1a(sig, &d.rope_theta, sizeof d.rope_theta);
   sig = fnv1a(sig, c.q.data(), c.q.size());
   sig = fnv1a(sig, c.kv.data(), c.kv.size());
   sig = fnv1a(sig, c.f.data(), c.f.size());
-  if (format) sig = fnv1a(sig, &format, sizeof format);
+  sig = fnv1a(sig, &format, sizeof format);
+  sig = fnv1a(sig, &store_id, sizeof store_id);
   return sig ? sig : 1;
+}
+
+uint64_t hash_ptrs(uint64_t h, std::initializer_list<const void*> ptrs) {
+  for (const void* q : ptrs) {
+    const uintptr_t v = reinterpret_cast<uintptr_t>(q);
+    h = fnv1a(h, &v, sizeof v);
+  }
+  return h;
+}
+
+// identity of a per-row INT8 store: every weight, scale and gain address it names
+uint64_t store_identity(const tasp_store& st, int n_layers) {
+  uint64_t h = 1469598103934665603ull;
+  for (int l = 0; l < n_layers; ++l) {
+    const tasp_layer& S = st.layers[l];
+    h = hash_ptrs(h, {S.wq.w, S.wq.scale, S.wk.w, S.wk.scale, S.wv.w, S.wv.scale, S.wo.w,
+                      S.wo.scale, S.wg.w, S.wg.scale, S.wu.w, S.wu.scale, S.wd.w, S.wd.scale,
+                      S.attn_norm, S.ffn_norm});
+  }
+  return hash_ptrs(h, {st.final_norm, st.lm_head});
+}
+
+// identity of a groupwise shared store
+uint64_t store_identity(const tasp_gstore& st, int n_layers) {
+  uint64_t h = 1099511628211ull;
+  for (int l = 0; l < n_layers; ++l) {
+    const tasp_glayer& S = st.layers[l];
+    h = hash_ptrs(h, {S.wqkv.w, S.wqkv.scale, S.wo.w, S.wo.scale, S.wg.w, S.wg.scale, S.wu.w,
+                      S.wu.scale, S.wd.w, S.wd.scale, S.attn_norm, S.ffn_norm});
+  }
+  return hash_ptrs(h, {st.final_norm, st.lm_head});
 }
 
 // A shared-store plan decodes one sequence: its scale groups of 128 must tile every input
@@ -1114,7 +1154,7 @@ tasp_status tasp_compile_plan(const tasp_model_desc* desc, const tasp_store* sto
   p->ratio = num / den;
   p->weight_bytes = wb;
   p->scale_bytes = sb;
-  p->sig = plan_signature(d, c, 0);
+  p->sig = plan_signature(d, c, 0, store_identity(*store, L));
   *out = p;
   return TASP_OK;
 }
@@ -1293,7 +1333,7 @@ tasp_status tasp_compile_shared_plan(const tasp_model_desc* desc, const tasp_gst
   p->ratio = num / den;
   p->weight_bytes = wb;
   p->scale_bytes = sb;
-  p->sig = plan_signature(d, c, 1);
+  p->sig = plan_signature(d, c, 1, store_identity(*store, L));
   *out = p;
   return TASP_OK;
 }

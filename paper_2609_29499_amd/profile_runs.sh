@@ -8,6 +8,9 @@
 #   prefill:    kernel trace and MFMA counter pass of the 512-token prefill benchmark
 #   router:     kernel trace of the router benchmark (one 7 KiB turn, then 512-prompt batches)
 #   shared:     kernel trace of the shared-store benchmark (8B layer, batch 1)
+#   stack70:    kernel trace of the default benchmark (80-layer 70B stack, seed-1 mask then the
+#               dense plan; extras off), then FETCH_SIZE and WRITE_SIZE passes of its sparse plan
+#   stack8:     the same three runs for the 32-layer 8B stack (seed-1 mask)
 set -o pipefail
 export TMPDIR=/tmp
 R=$(pwd)
@@ -34,6 +37,16 @@ prefill)
   ;;
 router)
   echo "[prof] router kernel trace" && timeout -k 10 400 rocprofv3 --kernel-trace --stats -d $O/rt_trace -o trace -- python3 -u bench.py --workload router_llama3_8b --steps 200 --warmup 20 --cpu-seconds 3 > $O/rt_trace.json 2> $O/rt_trace.err
+  ;;
+stack70)
+  echo "[prof] 70B stack kernel trace" && timeout -k 10 600 rocprofv3 --kernel-trace --stats -d $O/s70_trace -o trace -- python3 -u bench.py --no-extras --steps 40 --warmup 5 --blocks 1 --block-warmup 5 --block-steps 50 --cpu-seconds 3 > $O/s70_trace.json 2> $O/s70_trace.err &&
+  echo "[prof] 70B stack FETCH_SIZE" && timeout -s KILL 400 rocprofv3 --pmc FETCH_SIZE -d $O/s70_fetch -o fetch -- python3 -u bench.py --sparse-only --no-cpu --steps 4 --warmup 1 --blocks 0 > $O/s70_fetch.json 2> $O/s70_fetch.err &&
+  echo "[prof] 70B stack WRITE_SIZE" && timeout -s KILL 400 rocprofv3 --pmc WRITE_SIZE -d $O/s70_write -o write -- python3 -u bench.py --sparse-only --no-cpu --steps 4 --warmup 1 --blocks 0 > $O/s70_write.json 2> $O/s70_write.err
+  ;;
+stack8)
+  echo "[prof] 8B stack kernel trace" && timeout -k 10 600 rocprofv3 --kernel-trace --stats -d $O/s8_trace -o trace -- python3 -u bench.py --workload llama3_8b_stack --steps 40 --warmup 5 --blocks 1 --block-warmup 5 --block-steps 50 --cpu-seconds 3 > $O/s8_trace.json 2> $O/s8_trace.err &&
+  echo "[prof] 8B stack FETCH_SIZE" && timeout -s KILL 400 rocprofv3 --pmc FETCH_SIZE -d $O/s8_fetch -o fetch -- python3 -u bench.py --workload llama3_8b_stack --sparse-only --no-cpu --steps 4 --warmup 1 --blocks 0 > $O/s8_fetch.json 2> $O/s8_fetch.err &&
+  echo "[prof] 8B stack WRITE_SIZE" && timeout -s KILL 400 rocprofv3 --pmc WRITE_SIZE -d $O/s8_write -o write -- python3 -u bench.py --workload llama3_8b_stack --sparse-only --no-cpu --steps 4 --warmup 1 --blocks 0 > $O/s8_write.json 2> $O/s8_write.err
   ;;
 shared)
   echo "[prof] shared kernel trace" && timeout -k 10 400 rocprofv3 --kernel-trace --stats -d $O/sh_trace -o trace -- python3 -u bench.py --workload llama3_8b_layer_shared --steps 200 --warmup 20 --cpu-seconds 3 > $O/sh_trace.json 2> $O/sh_trace.err

@@ -1,8 +1,10 @@
 """Summaries of rocprofv3 result databases for the library's kernels.
 
-    python -m paper_2609_29499_amd.profile_summary trace DB [--split KIND:GRID_X] [--by-grid]
+    python -m paper_2609_29499_amd.profile_summary trace DB [--split KIND:GRID_X]
+                                                               [--split-nth KIND:N] [--by-grid]
         per-kernel dispatch count / mean / median / min duration (us); with --split the run is cut
-        at the first dispatch of KIND with that grid size in work-items (the benchmark times the
+        at the first dispatch of KIND with that grid size in work-items, with --split-nth at the
+        N-th dispatch of KIND (e.g. closure:2, the second plan compile: the benchmarks time the
         sparse plan first, then the dense one)
     python -m paper_2609_29499_amd.profile_summary traffic FETCH_DB WRITE_DB KIND
         HBM bytes per dispatch of KIND from a FETCH_SIZE and a WRITE_SIZE run, each scaled by what
@@ -54,6 +56,7 @@ def kind_of(name: str) -> str | None:
         (r"embed_kernel", "embed"),
         (r"argmax_kernel", "argmax"),
         (r"copy_kernel", "copy_probe"),
+        (r"closure_kernel", "closure"),
     ]
     for pat, k in rules:
         if re.search(pat, name):
@@ -78,7 +81,7 @@ def _named(kinds):
     return out
 
 
-def trace(db, split=None, by_grid=False):
+def trace(db, split=None, by_grid=False, split_nth=None):
     con = sqlite3.connect(db)
     rows = con.execute("select name, grid_x, start, end from kernels order by start").fetchall()
     kinds = _named([kind_of(r[0]) for r in rows])
@@ -87,9 +90,13 @@ def trace(db, split=None, by_grid=False):
         sk, sg = split.split(":")
         cand = [r[2] for r, k in zip(rows, kinds) if k == sk and r[1] == int(sg)]
         t_split = min(cand) if cand else None
+    if split_nth:
+        sk, n = split_nth.split(":")
+        cand = [r[2] for r, k in zip(rows, kinds) if k == sk]
+        t_split = cand[int(n) - 1] if len(cand) >= int(n) else None
     stats = collections.defaultdict(list)
     for r, k in zip(rows, kinds):
-        if not k or k == "copy_probe":
+        if not k or k in ("copy_probe", "closure"):
             continue
         phase = "all" if t_split is None else ("second" if r[2] >= t_split else "first")
         stats[(phase, k, r[1] if by_grid else "")].append((r[3] - r[2]) / 1000.0)
@@ -155,6 +162,7 @@ def main():
     t = sub.add_parser("trace")
     t.add_argument("db")
     t.add_argument("--split")
+    t.add_argument("--split-nth")
     t.add_argument("--by-grid", action="store_true", help="one row per (kernel, grid size)")
     f = sub.add_parser("traffic")
     f.add_argument("fetch_db")
@@ -166,7 +174,7 @@ def main():
     p.add_argument("--grid", type=int, help="only dispatches of this grid size (work-items)")
     a = ap.parse_args()
     if a.cmd == "trace":
-        trace(a.db, a.split, a.by_grid)
+        trace(a.db, a.split, a.by_grid, a.split_nth)
     elif a.cmd == "traffic":
         import json
         print(json.dumps(traffic(a.fetch_db, a.write_db, a.kind), indent=1))

@@ -19,17 +19,20 @@ NAN_BF16 = np.uint16(0x7FC0)
 
 class Case:
     def __init__(self, sh, mask, batch, pos, max_seq=None, seed_w=0, seed_x=1, seed_kv=2,
-                 with_lm_head=None, store=None, device="cuda", shared=False):
-        """shared: a groupwise store (BF16 scales per 128 inputs) and a shared-store plan."""
+                 with_lm_head=None, store=None, device="cuda", shared=False, lm=None):
+        """shared: a groupwise store (BF16 scales per 128 inputs) and a shared-store plan;
+        lm: a pre-drawn (final norm, LM head) pair for this shape (large heads are drawn once)."""
         self.sh, self.batch, self.pos = sh, batch, pos
         self.max_seq = max_seq or pos + 1
         self.mask = mask
         quant = "group" if shared else "row"
         self.store = store if store is not None else [synth.layer_weights(sh, l, seed_w, quant=quant)
                                                       for l in range(sh.n_layers)]
+        pre = lm
         lm = sh.vocab > 0 if with_lm_head is None else with_lm_head
-        self.final_norm = synth.final_norm(sh, seed_w) if lm else None
-        self.lm_head = synth.lm_head(sh, seed_w) if lm else None
+        self.final_norm, self.lm_head = (pre if pre is not None else
+                                         (synth.final_norm(sh, seed_w), synth.lm_head(sh, seed_w))
+                                         ) if lm else (None, None)
         self.closed = ref.close_mask(*(mask if mask is not None else synth.all_kept_mask(sh)),
                                      sh.group_size)
         self.x = synth.activations(batch, sh.d_model, seed_x)
@@ -76,15 +79,17 @@ class PrefillCase:
     cache, everything else NaN until the prefill writes it), with the oracle's result."""
 
     def __init__(self, sh, mask, T, pos0, max_seq=None, max_prefill=None, seed_w=0, seed_x=3,
-                 seed_kv=2, store=None, device="cuda"):
+                 seed_kv=2, store=None, device="cuda", lm=None):
         self.sh, self.T, self.pos0 = sh, T, pos0
         self.max_seq = max_seq or pos0 + T
         self.mask = mask
         self.store = store if store is not None else [synth.layer_weights(sh, l, seed_w)
                                                       for l in range(sh.n_layers)]
+        pre = lm
         lm = sh.vocab > 0
-        self.final_norm = synth.final_norm(sh, seed_w) if lm else None
-        self.lm_head = synth.lm_head(sh, seed_w) if lm else None
+        self.final_norm, self.lm_head = (pre if pre is not None else
+                                         (synth.final_norm(sh, seed_w), synth.lm_head(sh, seed_w))
+                                         ) if lm else (None, None)
         self.closed = ref.close_mask(*(mask if mask is not None else synth.all_kept_mask(sh)),
                                      sh.group_size)
         self.x = synth.activations(T, sh.d_model, seed_x)

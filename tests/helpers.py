@@ -102,3 +102,36 @@ def hf_prefill(sh, Wd, x):
         cos, sin = rot(h, pid)
         out = layer(h, attention_mask=mask, position_ids=pid, position_embeddings=(cos, sin))
     return out[0].numpy()
+
+
+def teacher_forced_rows(layer_source, closed, table, scales, prompt, ids, sh, fn, lm):
+    """The oracle's logits along a sequence whose generated part is given (teacher forcing):
+    one prefill of prompt + ids[:-1] from an empty cache, which equals the oracle's request loop
+    (pinned in tests/test_oracle_generate.py); row s holds the logits that chose ids[s]."""
+    from oracle import reference as ref
+    T = len(prompt)
+    seq = np.concatenate([np.asarray(prompt), np.asarray(ids[:-1])]).astype(np.int64)
+    S_ = len(seq)
+    caches = [(np.zeros((sh.n_kv_heads, S_, sh.head_dim)), np.zeros((sh.n_kv_heads, S_, sh.head_dim)))
+              for _ in range(sh.n_layers)]
+    logits = ref.prefill_stack(layer_source, closed, ref.embed_rows(table, scales, seq), caches, 0,
+                               sh, fn, lm)
+    return logits[T - 1:]
+
+
+def check_greedy_ids(ids, oracle_rows, what=""):
+    """Greedy ids decided in floating point (several ids can be correct at a near tie): every
+    step's id must be one whose oracle logit lies within the parity tolerance (1e-2 max|logit|)
+    of the oracle's maximum, so a wrong id anywhere fails while a legitimate near tie passes.
+    Returns the number of steps whose oracle decision was clear of the tolerance (those ids are
+    then necessarily the oracle's argmax)."""
+    clear = 0
+    for s, (i, row) in enumerate(zip(ids, oracle_rows)):
+        tol = 1e-2 * np.abs(row).max()
+        assert row[i] >= row.max() - tol, \
+            f"{what} step {s}: id {i} logit {row[i]:.6g} vs max {row.max():.6g} (tol {tol:.3g})"
+        top2 = np.sort(row)[-2:]
+        if top2[1] - top2[0] > tol:
+            assert i == int(np.argmax(row))
+            clear += 1
+    return clear

@@ -10,8 +10,8 @@ import synth
 from oracle import compact, reference as ref
 from paper_2609_29499_amd import binding as B
 from paper_2609_29499_amd import session as S
-from tests.gpu_case import Case
-from tests.helpers import assert_parity, rel_errors
+from tests.gpu_case import Case, PrefillCase
+from tests.helpers import assert_parity, check_greedy_ids, rel_errors
 
 pytestmark = pytest.mark.gpu
 
@@ -321,8 +321,36 @@ def test_llama3_8b_two_layer_stack_with_lm_head():
     case, got, want = _decode_case(sh, synth.budget_mask(sh, 2), 2, 512)
     m, s = assert_parity(got, want, what="8b stack logits")
     _flush(f"  max_rel={m:.2e} sum_rel={s:.2e}")
-    assert (got.argmax(axis=1) == want.argmax(axis=1)).all()
+    check_greedy_ids(got.argmax(axis=1), want, "8b stack")
     assert np.abs(got - want).max() < 2e-3 * max(1.0, np.abs(want).max())
+
+
+@pytest.mark.timeout(900)
+def test_llama3_70b_two_layer_stack_with_lm_head():
+    """Full Llama-3-70B width (8192, 64 / 8 heads, 28672) with the dense 128256 x 8192 BF16 LM
+    head (2,101,346,304 bytes: the largest panel one buffer resource addresses): two layers under
+    the seed-1 budget mask, 256 prior positions, batch 1 (the VALU head) and batch 2 (the
+    matrix-core head); then a 5-token prefill through the same stack, whose LM head runs as a
+    GEMM. Logits at parity, every greedy token admissible."""
+    sh = synth.LLAMA3_70B.with_layers(2)
+    _flush("case 70b 2-layer stack + lm head: drawing the store")
+    store = [synth.layer_weights(sh, l) for l in range(sh.n_layers)]
+    lm = (synth.final_norm(sh), synth.lm_head(sh))
+    mask = synth.budget_mask(sh, 1)
+    for batch in (1, 2):
+        _flush(f"case 70b 2-layer stack + lm head batch {batch}")
+        case, got, want = _decode_case(sh, mask, batch, 256, store=store, lm=lm)
+        m, s = assert_parity(got, want, what=f"70b stack logits batch {batch}")
+        _flush(f"  max_rel={m:.2e} sum_rel={s:.2e}")
+        check_greedy_ids(got.argmax(axis=1), want, f"70b stack batch {batch}")
+        del case
+        torch.cuda.empty_cache()
+    _flush("case 70b 2-layer stack + lm head prefill T=5")
+    pc = PrefillCase(sh, mask, 5, 0, store=store, lm=lm)
+    got, want = pc.run(), pc.oracle()
+    m, s = assert_parity(got, want, what="70b stack prefill logits")
+    _flush(f"  max_rel={m:.2e} sum_rel={s:.2e}")
+    check_greedy_ids(got.argmax(axis=1), want, "70b stack prefill")
 
 
 @pytest.mark.parametrize("batch", [1, 4])
@@ -386,6 +414,20 @@ def test_cache_plan_binding_errors():
     same = S.Plan(a.desc, a.dstore, a.mask)
     assert same.ledger()["signature"] == a.plan.ledger()["signature"]
     assert plan_b.ledger()["signature"] != a.plan.ledger()["signature"]
+    # the signature also names the store and the numerics: the same mask over a second copy of
+    # the weights, or under another RMSNorm epsilon or RoPE base, gets a cache of its own
+    sig = a.plan.ledger()["signature"]
+    assert S.Plan(a.desc, S.DeviceStore(a.store), a.mask).ledger()["signature"] != sig
+    d_eps = S.model_desc(sh.n_layers, sh.d_model, sh.n_q_heads, sh.n_kv_heads, sh.head_dim,
+                         sh.d_ffn, sh.vocab, 1, 8, 0, 1e-6, sh.rope_theta)
+    d_theta = S.model_desc(sh.n_layers, sh.d_model, sh.n_q_heads, sh.n_kv_heads, sh.head_dim,
+                           sh.d_ffn, sh.vocab, 1, 8, 0, sh.rms_eps, 10000.0)
+    for d in (d_eps, d_theta):
+        other = S.Plan(d, a.dstore, a.mask)
+        assert other.ledger()["signature"] != sig
+        with pytest.raises(B.TaspError) as e:
+            other.decode(a.xd, a.cache, a.pos, a.out)
+        assert e.value.status == -6
     with pytest.raises(B.TaspError) as e:
         a.plan.decode(a.xd, a.cache, 8, a.out)
     assert e.value.status == -5

@@ -169,6 +169,19 @@ def test_llama3_8b_prefill512_full_size():
     _check_cache(case)
 
 
+@pytest.mark.timeout(600)
+def test_llama3_8b_prefill2048_full_size():
+    """One Llama-3-8B-shaped layer under the seed-1 budget mask: a 2048-token prompt from an empty
+    cache, the prompt length of the timed request (Table "configuration")."""
+    _flush("case 8b prefill 2048")
+    sh = synth.LLAMA3_8B.with_layers(1, vocab=0)
+    case = PrefillCase(sh, synth.budget_mask(sh, 1), 2048, 0)
+    got, want = case.run(), case.oracle()
+    m, s = assert_parity(got, want, what="prefill 8b 2048")
+    _flush(f"  max_rel={m:.2e} sum_rel={s:.2e}")
+    _check_cache(case)
+
+
 def test_prefill_errors():
     _flush("case prefill errors")
     sh = SMALL
