@@ -379,6 +379,24 @@ tasp_status tasp_route(const tasp_router* router, const uint8_t* text, int32_t n
                        void* workspace, size_t workspace_bytes, float* features, float* probs,
                        int32_t* choice, void* stream);
 
+/* Routing for callers that cannot allocate (code under HIP graph capture, serving loops and
+ * harnesses that forbid allocation): tasp_route without a workspace argument. Its scratch is a
+ * fixed TASP_ROUTE_NOALLOC_SCRATCH_BYTES array that the library holds in each GPU's memory
+ * until the process ends; the call allocates nothing. A call whose scratch need
+ * (tasp_router_workspace_bytes for the same router and n_prompts) exceeds that size returns
+ * TASP_ERR_WORKSPACE and enqueues nothing (about 12 KB per prompt at the paper's router shape,
+ * so ~340 prompts per call). Every call on one GPU uses that GPU's one array: calls that overlap
+ * on one GPU (concurrent streams, or host threads without ordering) race and must be serialised
+ * by the caller; calls on one stream are ordered. The array's contents are left over from the
+ * last call and need no clearing (every byte a call reads, that call writes first). The first
+ * call on a device looks up the array's device address (not enqueued). Arguments, outputs and
+ * errors otherwise as tasp_route; the results equal tasp_route's bit for bit. */
+#define TASP_ROUTE_NOALLOC_SCRATCH_BYTES ((size_t)4 << 20)
+tasp_status tasp_route_noalloc(const tasp_router* router, const uint8_t* text, int32_t n_text,
+                               const int32_t* offsets, int32_t n_prompts,
+                               const float* proxy_logprob, float* features, float* probs,
+                               int32_t* choice, void* stream);
+
 /* One user turn with routing and dispatch (paper, Sec. "Dependency-Closed Masks and
  * Cache-Consistent Routing"): one routing decision per turn; the plan it picks runs all of that
  * turn's prefill and decode work; cache rows written under one closed mask are kept only when the

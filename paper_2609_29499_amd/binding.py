@@ -28,7 +28,7 @@ EXPORTS = ["tasp_plan_workspace_bytes", "tasp_compile_plan", "tasp_plan_counts",
            "tasp_kv_bind", "tasp_decode_step", "tasp_prefill", "tasp_prefill_timed", "tasp_generate",
            "tasp_decode_step_timed",
            "tasp_profile_stage", "tasp_mask_workspace_bytes", "tasp_build_mask",
-           "tasp_router_workspace_bytes", "tasp_route", "tasp_serve_turn", "tasp_copy_probe",
+           "tasp_router_workspace_bytes", "tasp_route", "tasp_route_noalloc", "tasp_serve_turn", "tasp_copy_probe",
            "tasp_status_string", "tasp_last_error"]
 
 
@@ -134,6 +134,7 @@ def load(path: str = LIB_PATH):
                             C.POINTER(U64), P],
         "tasp_router_workspace_bytes": [C.POINTER(tasp_router), I32, C.POINTER(SZ)],
         "tasp_route": [C.POINTER(tasp_router), P, I32, P, I32, P, P, SZ, P, P, P, P],
+        "tasp_route_noalloc": [C.POINTER(tasp_router), P, I32, P, I32, P, P, P, P, P],
         "tasp_serve_turn": [C.POINTER(tasp_router), C.POINTER(P), P, P, I32, P, P, P, P, I32, I32,
                             I32, C.POINTER(tasp_kv_cache), P, P, P, P, SZ, C.POINTER(I32),
                             C.POINTER(I32), P],
@@ -288,6 +289,12 @@ def tasp_route(router, text_ptr, n_text, offsets_ptr, n_prompts, logprob_ptr, ws
     _check(load().tasp_route(C.byref(router), text_ptr, n_text, offsets_ptr, n_prompts,
                              logprob_ptr, ws_ptr, ws_bytes, feats_ptr, probs_ptr, choice_ptr,
                              stream))
+
+
+def tasp_route_noalloc(router, text_ptr, n_text, offsets_ptr, n_prompts, logprob_ptr, feats_ptr,
+                       probs_ptr, choice_ptr, stream):
+    _check(load().tasp_route_noalloc(C.byref(router), text_ptr, n_text, offsets_ptr, n_prompts,
+                                     logprob_ptr, feats_ptr, probs_ptr, choice_ptr, stream))
 
 
 def tasp_serve_turn(router, task_plans, dense_plan, text_ptr, n_text, logprob_ptr, embed_ptr,

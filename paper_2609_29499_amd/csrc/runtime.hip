@@ -8,6 +8,7 @@
 #include <cstdio>
 #include <cstring>
 #include <initializer_list>
+#include <mutex>
 #include <new>
 #include <string>
 #include <vector>
@@ -1599,23 +1600,26 @@ tasp_status tasp_router_workspace_bytes(const tasp_router* r, int32_t n, size_t*
   return TASP_OK;
 }
 
-tasp_status tasp_route(const tasp_router* r, const uint8_t* text, int32_t n_text,
-                       const int32_t* offsets, int32_t n, const float* proxy_logprob,
-                       void* workspace, size_t workspace_bytes, float* features, float* probs,
-                       int32_t* choice, void* stream) {
-  RouterLayout y;
-  tasp_status st = router_layout(r, n, &y);
+namespace {
+
+// Arguments of a routing call other than its scratch, checked on the host.
+tasp_status check_route_args(const tasp_router* r, const uint8_t* text, int32_t n_text,
+                             const int32_t* offsets, int32_t n, const float* proxy_logprob,
+                             const float* probs, const int32_t* choice, RouterLayout* y) {
+  tasp_status st = router_layout(r, n, y);
   if (st != TASP_OK) return st;
   if (n_text < 0) return fail(TASP_ERR_INVALID_ARG, "n_text < 0");
-  if ((!text && n_text > 0) || !proxy_logprob || !probs || !choice || !workspace)
-    return fail(TASP_ERR_INVALID_ARG, "text / proxy_logprob / probs / choice / workspace is NULL");
+  if ((!text && n_text > 0) || !proxy_logprob || !probs || !choice)
+    return fail(TASP_ERR_INVALID_ARG, "text / proxy_logprob / probs / choice is NULL");
   if (!offsets && n != 1) return fail(TASP_ERR_INVALID_ARG, "offsets NULL with %d prompts", n);
-  if (reinterpret_cast<uintptr_t>(workspace) % kAlign)
-    return fail(TASP_ERR_WORKSPACE, "workspace is not 256-byte aligned");
-  if (workspace_bytes < y.total)
-    return fail(TASP_ERR_WORKSPACE, "workspace %zu < %zu bytes", workspace_bytes, y.total);
-  hipStream_t s = static_cast<hipStream_t>(stream);
-  char* ws = static_cast<char*>(workspace);
+  return TASP_OK;
+}
+
+// The five routing kernels over a scratch of at least y.total bytes at ws (device).
+tasp_status route_launch(const tasp_router* r, const RouterLayout& y, const uint8_t* text,
+                         int32_t n_text, const int32_t* offsets, int32_t n,
+                         const float* proxy_logprob, char* ws, float* features, float* probs,
+                         int32_t* choice, hipStream_t s) {
   float* tf = reinterpret_cast<float*>(ws + y.tf);
   float* feats = features ? features : reinterpret_cast<float*>(ws + y.feats);
   float* h1 = reinterpret_cast<float*>(ws + y.h1);
@@ -1635,6 +1639,69 @@ tasp_status tasp_route(const tasp_router* r, const uint8_t* text, int32_t n_text
   tasp::RouterHeadArgs ha{r->w3, r->b3, r->n_tasks, r->hidden2, h2, r->temperature, r->tau, probs, choice};
   HIP_TRY(tasp::launch_router_head(ha, n, s));
   return TASP_OK;
+}
+
+// Scratch of tasp_route_noalloc: a fixed array in every GPU's memory (each device holds its own
+// copy at its own address, from the library's load until the process ends). Host code never
+// passes the array's name to a kernel or a copy: on the host that name is only a stand-in, so
+// its device address is looked up once per device and kept in scratch_ptr[].
+constexpr size_t kNoAllocScratchBytes = TASP_ROUTE_NOALLOC_SCRATCH_BYTES;
+constexpr int kMaxDevices = 64;
+static __device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
+std::mutex scratch_mu;
+void* scratch_ptr[kMaxDevices] = {};
+
+// The current device's address of `scratch`, looked up on the first call on that device.
+tasp_status scratch_address(void** out) {
+  int dev = -1;
+  HIP_TRY(hipGetDevice(&dev));
+  if (dev < 0 || dev >= kMaxDevices)
+    return fail(TASP_ERR_UNSUPPORTED, "device %d outside 0..%d", dev, kMaxDevices - 1);
+  std::lock_guard<std::mutex> lock(scratch_mu);
+  if (!scratch_ptr[dev]) {
+    void* p = nullptr;
+    HIP_TRY(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+    if (!p) return fail(TASP_ERR_HIP, "hipGetSymbolAddress returned a null address");
+    scratch_ptr[dev] = p;
+  }
+  *out = scratch_ptr[dev];
+  return TASP_OK;
+}
+
+}  // namespace
+
+tasp_status tasp_route(const tasp_router* r, const uint8_t* text, int32_t n_text,
+                       const int32_t* offsets, int32_t n, const float* proxy_logprob,
+                       void* workspace, size_t workspace_bytes, float* features, float* probs,
+                       int32_t* choice, void* stream) {
+  RouterLayout y;
+  tasp_status st = check_route_args(r, text, n_text, offsets, n, proxy_logprob, probs, choice, &y);
+  if (st != TASP_OK) return st;
+  if (!workspace) return fail(TASP_ERR_INVALID_ARG, "workspace is NULL");
+  if (reinterpret_cast<uintptr_t>(workspace) % kAlign)
+    return fail(TASP_ERR_WORKSPACE, "workspace is not 256-byte aligned");
+  if (workspace_bytes < y.total)
+    return fail(TASP_ERR_WORKSPACE, "workspace %zu < %zu bytes", workspace_bytes, y.total);
+  return route_launch(r, y, text, n_text, offsets, n, proxy_logprob,
+                      static_cast<char*>(workspace), features, probs, choice,
+                      static_cast<hipStream_t>(stream));
+}
+
+tasp_status tasp_route_noalloc(const tasp_router* r, const uint8_t* text, int32_t n_text,
+                               const int32_t* offsets, int32_t n, const float* proxy_logprob,
+                               float* features, float* probs, int32_t* choice, void* stream) {
+  RouterLayout y;
+  tasp_status st = check_route_args(r, text, n_text, offsets, n, proxy_logprob, probs, choice, &y);
+  if (st != TASP_OK) return st;
+  if (y.total > kNoAllocScratchBytes)
+    return fail(TASP_ERR_WORKSPACE,
+                "routing %d prompts needs %zu bytes of scratch, more than the fixed %zu of "
+                "tasp_route_noalloc (route fewer prompts per call, or use tasp_route)",
+                n, y.total, kNoAllocScratchBytes);
+  void* ws = nullptr;
+  if ((st = scratch_address(&ws)) != TASP_OK) return st;
+  return route_launch(r, y, text, n_text, offsets, n, proxy_logprob, static_cast<char*>(ws),
+                      features, probs, choice, static_cast<hipStream_t>(stream));
 }
 
 tasp_status tasp_serve_turn(const tasp_router* r, const tasp_plan* task_plans,
