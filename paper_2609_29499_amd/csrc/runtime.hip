@@ -193,8 +193,9 @@ Layout make_layout(const tasp_model_desc* d, const Closed& c) {
   Y.lm_head = d->vocab ? take(size_t(d->vocab) * D * 2) : 0;
   Y.rope_cos = take(size_t(d->max_seq) * (dh / 2) * 4);
   Y.rope_sin = take(size_t(d->max_seq) * (dh / 2) * 4);
-  Y.n_split_max = std::min((d->max_seq + tasp::attn_min_chunk() - 1) / tasp::attn_min_chunk(),
-                           tasp::attn_max_split());
+  Y.n_split_max = std::max(std::min((d->max_seq + tasp::attn_min_chunk() - 1) / tasp::attn_min_chunk(),
+                                    tasp::attn_max_split()),
+                           tasp::attn_mfma_max_split(d->max_seq));
   Y.ld_qkv = (Hq + 2 * Hkv) * dh;
   Y.ld_obuf = Hq * dh;
   Y.ld_h = round_up16(F);
@@ -260,8 +261,9 @@ Layout make_shared_layout(const tasp_model_desc* d) {
   Y.down_cols = take(size_t(L) * (F / 16) * 4);
   Y.rope_cos = take(size_t(d->max_seq) * (dh / 2) * 4);
   Y.rope_sin = take(size_t(d->max_seq) * (dh / 2) * 4);
-  Y.n_split_max = std::min((d->max_seq + tasp::attn_min_chunk() - 1) / tasp::attn_min_chunk(),
-                           tasp::attn_max_split());
+  Y.n_split_max = std::max(std::min((d->max_seq + tasp::attn_min_chunk() - 1) / tasp::attn_min_chunk(),
+                                    tasp::attn_max_split()),
+                           tasp::attn_mfma_max_split(d->max_seq));
   Y.ld_qkv = (Hq + 2 * Hkv) * dh;
   Y.ld_obuf = Hq * dh;
   Y.ld_h = round_up16(F);
@@ -466,11 +468,31 @@ tasp::AttnArgs attn_args(const tasp_plan_s* p, int l, const tasp_kv_cache* cache
   const size_t layer_cache = size_t(B) * d.n_kv_heads * cache->max_seq * d.head_dim;
   const int total = pos + 1;
   tasp::AttnArgs a{};
-  // Split rows: as short as keeps every workgroup of the launch resident at once (a workgroup
-  // that waits for a free slot runs a whole split after the others), in multiples of the kernel's
-  // sub-block pair, within the merge's split limit. Two ways to cover the rows: the last split
-  // takes the remainder on its own (ceil), or the remainder joins the last full split (floor);
-  // the one with the shorter longest split is taken, the separate remainder on a tie.
+  a.qkv = p->qkv_buf; a.ld_qkv = p->ld_qkv; a.m_q = P.m_q; a.m_kv = P.m_kv; a.dh = d.head_dim;
+  for (int q = 0; q < P.m_kv; ++q) a.kv_idx[q] = P.kv_idx[q];
+  for (int q = 0; q <= P.m_kv; ++q) a.slot_start[q] = P.slot_start[q];
+  a.kc = static_cast<uint16_t*>(cache->k) + l * layer_cache;
+  a.vc = static_cast<uint16_t*>(cache->v) + l * layer_cache;
+  a.Hkv = d.n_kv_heads; a.S = cache->max_seq; a.rope_cos = p->rope_cos;
+  a.rope_sin = p->rope_sin; a.pos = pos; a.part = p->part; a.cnt = p->acnt;
+  a.o = p->o_buf; a.ld_o = p->ld_obuf; a.B = B;
+  if (hl) { a.o_hl = p->xo; a.ld_ohl = p->ld_xo; }
+  if (B == 1) {
+    // one sequence: the matrix-core kernel with short splits (many more workgroups than group
+    // slots x resident splits of the VALU kernel)
+    int chunk = 0, n_split = 0;
+    tasp::attn_mfma_split(total, &chunk, &n_split);
+    a.kernel = tasp::kAttnMfma;
+    a.chunk = chunk;
+    a.n_split = n_split;
+    return a;
+  }
+  // Batches, VALU kernel. Split rows: as short as keeps every workgroup of the launch resident at
+  // once (a workgroup that waits for a free slot runs a whole split after the others), in
+  // multiples of the kernel's sub-block pair, within the merge's split limit. Two ways to cover
+  // the rows: the last split takes the remainder on its own (ceil), or the remainder joins the
+  // last full split (floor); the one with the shorter longest split is taken, the separate
+  // remainder on a tie.
   const long sub = tasp::attn_min_chunk();
   int nhm = 1;
   for (int q = 0; q < P.m_kv; ++q) nhm = std::max(nhm, P.slot_start[q + 1] - P.slot_start[q]);
@@ -486,16 +508,9 @@ tasp::AttnArgs attn_args(const tasp_plan_s* p, int l, const tasp_kv_cache* cache
   const bool floor_wins = longest_f < std::min<long>(chunk_c, total);
   const long chunk = floor_wins ? chunk_f : chunk_c;
   const long n_split = floor_wins ? split_f : (total + chunk_c - 1) / chunk_c;
-  a.qkv = p->qkv_buf; a.ld_qkv = p->ld_qkv; a.m_q = P.m_q; a.m_kv = P.m_kv; a.dh = d.head_dim;
-  for (int q = 0; q < P.m_kv; ++q) a.kv_idx[q] = P.kv_idx[q];
-  for (int q = 0; q <= P.m_kv; ++q) a.slot_start[q] = P.slot_start[q];
-  a.kc = static_cast<uint16_t*>(cache->k) + l * layer_cache;
-  a.vc = static_cast<uint16_t*>(cache->v) + l * layer_cache;
-  a.Hkv = d.n_kv_heads; a.S = cache->max_seq; a.rope_cos = p->rope_cos;
-  a.rope_sin = p->rope_sin; a.pos = pos; a.chunk = int(chunk);
-  a.n_split = int(n_split); a.part = p->part; a.cnt = p->acnt;
-  a.o = p->o_buf; a.ld_o = p->ld_obuf; a.B = B;
-  if (hl) { a.o_hl = p->xo; a.ld_ohl = p->ld_xo; }
+  a.kernel = tasp::kAttnValu;
+  a.chunk = int(chunk);
+  a.n_split = int(n_split);
   return a;
 }
 
