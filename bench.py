@@ -323,13 +323,18 @@ def measure_stack(args, sh, pos, mask_seeds, timed_steps=5):
             for _ in range(args.block_warmup):
                 g.replay()
             blocks.append(_time_replays(torch, g, args.block_steps))
-        # per-kernel HIP events around every launch of eager steps on the launch stream
-        lm_ms, gu_launch = [], []
+        # LM head: HIP events around each kernel of eager steps on the launch stream; gate/up:
+        # back-to-back launches of every layer's gate/up GEMV between two HIP events on the launch
+        # stream (each launch reads another layer's panel, as in a step)
+        lm_ms = []
         for _ in range(timed_steps):
             kt = plan.decode_timed(x, cache, pos, out)
             lm_ms.append(sum(t for k, t in kt if k == "lmhead_gemv"))
-            gu_launch += [t for k, t in kt if k == "gateup_gemv"]
         lm_ms = float(np.median(lm_ms))
+        gu_reps = 2
+        gu_launch_ms = S.B.tasp_profile_stage([plan.handle], [cache.struct], -1, STAGE_KIND["gateup_gemv"],
+                                              pos, gu_reps, S.current_stream())
+        gu_launch = [gu_launch_ms] * (gu_reps * sum(1 for l in range(sh.n_layers) if plan.counts(l)[2] > 0))
         counts = [plan.counts(l) for l in range(sh.n_layers)]
         d = sh.d_model
         gu_bytes = sum(2 * c * d + 2 * c * 4 + d * 4 + c * 4 for _, _, c in counts)

@@ -287,9 +287,10 @@ tasp_status tasp_decode_step_timed(tasp_plan plan, const float* x, tasp_kv_cache
 
 /* Profiling (the timing protocol of Sec. "Experimental Design": back-to-back runs between
  * events, here for one stage): average duration of one stage of layer `layer`, measured as n_plans * reps
- * back-to-back launches between two HIP events on `stream`. Stage `kind`: 1 attention at `pos`
+ * back-to-back launches between two HIP events on `stream` (layer -1: every layer that has the stage,
+ * in order, so that each launch of a stack reads another layer's panel). Stage `kind`: 1 attention at `pos`
  * (split-KV partials, merged by the last split of each group slot; rewrites cache row pos with
- * the same values), 3 the gate/up projection (RMSNorm + SwiGLU), 4 the down projection (writes the plan's
+ * the same values, or for layer -1 every layer's row pos with the last decoded layer's k, v), 3 the gate/up projection (RMSNorm + SwiGLU), 4 the down projection (writes the plan's
  * scratch, not a caller buffer). Launch i uses plans[i % n_plans] with caches[i % n_plans] (bound
  * to that plan; its batch selects the batch-1 or the batched kernels), so distinct plan copies
  * keep every launch streaming from HBM rather than from cache. Each plan must have run a

@@ -1469,11 +1469,16 @@ tasp_status tasp_profile_stage(const tasp_plan* plans, const tasp_kv_cache* cach
     return fail(TASP_ERR_INVALID_ARG, "plans / caches / n_plans / reps / ms_per_launch");
   if (kind != 1 && kind != 3 && kind != 4)
     return fail(TASP_ERR_UNSUPPORTED, "stage kind %d is not profiled", kind);
-  std::vector<tasp::GemvArgs> args(n_plans);
-  std::vector<tasp::MfmaArgs> margs(n_plans);
-  std::vector<tasp::AttnArgs> aargs(n_plans);
-  std::vector<tasp::SharedGemvArgs> sargs(n_plans);
-  std::vector<char> shared(n_plans, 0);
+  // one launch per (layer, plan); layer -1 takes every layer that has the stage, in order
+  struct Item {
+    int plan, layer;
+    bool shared;
+    tasp::GemvArgs g;
+    tasp::MfmaArgs m;
+    tasp::AttnArgs at;
+    tasp::SharedGemvArgs sg;
+  };
+  std::vector<Item> items;
   int batch = 0;
   for (int i = 0; i < n_plans; ++i) {
     const tasp_plan_s* p = plans[i];
@@ -1483,29 +1488,44 @@ tasp_status tasp_profile_stage(const tasp_plan* plans, const tasp_kv_cache* cach
     if (caches[i].plan_sig != p->sig) return fail(TASP_ERR_CACHE_PLAN_MISMATCH, "caches[%d]", i);
     if (i > 0 && caches[i].batch != batch) return fail(TASP_ERR_SHAPE, "caches differ in batch");
     batch = caches[i].batch;
-    if (layer < 0 || layer >= p->desc.n_layers) return fail(TASP_ERR_INVALID_ARG, "bad layer %d", layer);
+    if (layer < -1 || layer >= p->desc.n_layers) return fail(TASP_ERR_INVALID_ARG, "bad layer %d", layer);
     if (pos < 0 || pos >= caches[i].max_seq) return fail(TASP_ERR_POS_RANGE, "pos %d", pos);
-    const LayerPlan& P = p->layers[layer];
-    if (kind == 3 && P.c == 0) return fail(TASP_ERR_SHAPE, "layer has no FFN channels");
-    if (kind == 1 && P.m_kv == 0) return fail(TASP_ERR_SHAPE, "layer has no retained KV group");
-    shared[i] = p->shared;
-    if (kind == 1)
-      aargs[i] = attn_args(p, layer, &caches[i], pos, batch, batch > 1);
-    else if (p->shared)
-      sargs[i] = (kind == 3) ? shared_gateup_args(p, layer) : shared_down_args(p, layer, p->r_io[layer & 1]);
-    else if (batch == 1)
-      args[i] = (kind == 3) ? gateup_args(p, layer, batch)
-                            : down_args(p, layer, batch, p->r_io[layer & 1]);
-    else
-      margs[i] = (kind == 3) ? gateup_mm_args(p, layer, batch)
-                             : down_mm_args(p, layer, batch, p->r_io[layer & 1]);
+    if (i > 0 && p->desc.n_layers != plans[0]->desc.n_layers)
+      return fail(TASP_ERR_SHAPE, "plans differ in layer count");
   }
+  const int L = plans[0]->desc.n_layers;
+  for (int l = (layer < 0 ? 0 : layer); l < (layer < 0 ? L : layer + 1); ++l) {
+    for (int i = 0; i < n_plans; ++i) {
+      const tasp_plan_s* p = plans[i];
+      const LayerPlan& P = p->layers[l];
+      if ((kind == 3 && P.c == 0) || (kind == 1 && P.m_kv == 0)) {
+        if (layer >= 0)
+          return fail(TASP_ERR_SHAPE, kind == 3 ? "layer has no FFN channels"
+                                                : "layer has no retained KV group");
+        continue;
+      }
+      Item it{};
+      it.plan = i;
+      it.layer = l;
+      it.shared = p->shared;
+      if (kind == 1)
+        it.at = attn_args(p, l, &caches[i], pos, batch, batch > 1);
+      else if (p->shared)
+        it.sg = (kind == 3) ? shared_gateup_args(p, l) : shared_down_args(p, l, p->r_io[l & 1]);
+      else if (batch == 1)
+        it.g = (kind == 3) ? gateup_args(p, l, batch) : down_args(p, l, batch, p->r_io[l & 1]);
+      else
+        it.m = (kind == 3) ? gateup_mm_args(p, l, batch) : down_mm_args(p, l, batch, p->r_io[l & 1]);
+      items.push_back(it);
+    }
+  }
+  if (items.empty()) return fail(TASP_ERR_SHAPE, "no layer has this stage");
   const tasp::GemvMode mode = (kind == 3) ? tasp::GEMV_GATEUP : tasp::GEMV_RESID;
   const tasp::MfmaMode mmode = (kind == 3) ? tasp::MM_GATEUP : tasp::MM_RESID;
-  auto launch = [&](int i, hipStream_t s) {
-    if (kind == 1) return tasp::launch_attn_decode(aargs[i], s);
-    if (shared[i]) return tasp::launch_shared_gemv(mode, sargs[i], s);
-    return (batch == 1) ? tasp::launch_gemv(mode, args[i], s) : tasp::launch_mfma_gemv(mmode, margs[i], s);
+  auto launch = [&](const Item& it, hipStream_t s) {
+    if (kind == 1) return tasp::launch_attn_decode(it.at, s);
+    if (it.shared) return tasp::launch_shared_gemv(mode, it.sg, s);
+    return (batch == 1) ? tasp::launch_gemv(mode, it.g, s) : tasp::launch_mfma_gemv(mmode, it.m, s);
   };
   hipStream_t s = static_cast<hipStream_t>(stream);
   hipEvent_t e0, e1;
@@ -1513,7 +1533,7 @@ tasp_status tasp_profile_stage(const tasp_plan* plans, const tasp_kv_cache* cach
   HIP_TRY(hipEventCreate(&e1));
   hipError_t h = hipEventRecord(e0, s);
   for (int r = 0; r < reps && h == hipSuccess; ++r)
-    for (int i = 0; i < n_plans && h == hipSuccess; ++i) h = launch(i, s);
+    for (size_t k = 0; k < items.size() && h == hipSuccess; ++k) h = launch(items[k], s);
   if (h == hipSuccess) h = hipEventRecord(e1, s);
   if (h == hipSuccess) h = hipEventSynchronize(e1);
   float ms = 0.0f;
@@ -1521,7 +1541,7 @@ tasp_status tasp_profile_stage(const tasp_plan* plans, const tasp_kv_cache* cach
   (void)hipEventDestroy(e0);
   (void)hipEventDestroy(e1);
   if (h != hipSuccess) return fail(TASP_ERR_HIP, "profile: %s", hipGetErrorString(h));
-  *ms_per_launch = ms / float(reps * n_plans);
+  *ms_per_launch = ms / float(size_t(reps) * items.size());
   return TASP_OK;
 }
 

@@ -124,13 +124,15 @@ def _per_dispatch(db):
 
 
 def _calibration(per, counter):
-    """Bytes per counted KiB, from the 1 GiB copy-probe dispatches (the largest copy grid; the
-    plan compile also copies small buffers with the same kernel)."""
-    copies = [(g, c[counter]) for k, g, c in per if k == "copy_probe" and counter in c]
+    """Bytes per counted KiB, from the 1 GiB copy-probe dispatches. The benchmarks run the probe
+    last, so these are the copy dispatches after the last dispatch of any other kernel (plan
+    compiles use the same copy kernel for their own buffers, the LM head copy among them)."""
+    last_other = max((i for i, (k, g, c) in enumerate(per) if k not in (None, "copy_probe")),
+                     default=-1)
+    copies = [c[counter] for k, g, c in per[last_other + 1:] if k == "copy_probe" and counter in c]
     if not copies:
-        raise SystemExit(f"no copy-probe dispatches with {counter}")
-    gmax = max(g for g, _ in copies)
-    return COPY_BYTES / statistics.median(v for g, v in copies if g == gmax)
+        raise SystemExit(f"no copy-probe dispatches with {counter} after the last other kernel")
+    return COPY_BYTES / statistics.median(copies)
 
 
 def traffic(fetch_db, write_db, kind):
