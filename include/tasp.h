@@ -168,8 +168,8 @@ typedef struct {
 } tasp_gstore;
 
 /* Workspace bytes of a shared-store plan: masks, index lists, the maps into the store, the RoPE
- * table and batch-1 decode scratch; the same for every mask. The desc must have max_batch 1 and
- * max_prefill 0, and d_model, n_q_heads * head_dim and d_ffn divisible by 128. */
+ * table and the decode (max_batch sequences) and prefill (max_prefill tokens) scratch; the same
+ * for every mask. d_model, n_q_heads * head_dim and d_ffn must be divisible by 128. */
 tasp_status tasp_shared_plan_workspace_bytes(const tasp_model_desc* desc, size_t* bytes);
 
 /* Compile a plan over the shared store: closes the mask (as tasp_compile_plan), builds on the
@@ -177,10 +177,13 @@ tasp_status tasp_shared_plan_workspace_bytes(const tasp_model_desc* desc, size_t
  * retained heads and groups, W_o columns of the retained heads, gate / up rows and W_down column
  * blocks of the retained channels) and checks them on the host; copies no weights. The retained
  * channels of every layer must come in aligned blocks of 16 (else TASP_ERR_UNSUPPORTED; the
- * paper's channel groups are 1,024 wide). Such a plan serves tasp_decode_step at batch 1
- * (and tasp_decode_step_timed, tasp_profile_stage); tasp_prefill and tasp_plan_panel return
- * TASP_ERR_UNSUPPORTED. Its signature differs from a per-row plan of the same mask, so caches
- * are not shared between the two formats. Synchronises `stream`. */
+ * paper's channel groups are 1,024 wide). Such a plan serves every call a per-row plan serves
+ * (decode at batch 1..max_batch, prefill, tasp_generate, tasp_serve_turn, the profiling calls),
+ * reading the store in place: batch 1 with per-lane group scales, batches and prefill on the
+ * matrix cores with each weight times its group scale split exactly into BF16 hi and lo parts;
+ * only tasp_plan_panel returns TASP_ERR_UNSUPPORTED (there are no panels). Its signature differs
+ * from a per-row plan of the same mask, so caches are not shared between the two formats.
+ * Synchronises `stream`. */
 tasp_status tasp_compile_shared_plan(const tasp_model_desc* desc, const tasp_gstore* store,
                                      const tasp_mask* mask, void* workspace,
                                      size_t workspace_bytes, void* stream, tasp_plan* out);

@@ -101,6 +101,17 @@ hipError_t launch_shared_maps(const SharedMapsArgs& a, int n_layers, hipStream_t
 // rsqrt(inv_d * sum(ssq[b][0..n_ssq)) + eps) when ssq is given, else 1.
 enum MfmaMode { MM_QKV = 0, MM_RESID = 1, MM_GATEUP = 2, MM_LMHEAD = 3 };
 
+// A projection read from the groupwise shared store instead of a panel: INT8 rows [store_rows][ld]
+// with one BF16 scale per row and 128 columns; plan row n is store row rows[n] (identity when
+// rows is null), plan columns 16 p .. 16 p + 15 are store columns cols[p] .. cols[p] + 15
+// (identity when cols is null). Gate/up use w / gs for the gate and w2 / gs2 for the up matrix.
+struct StoreView {
+  const int8_t* w; const int8_t* w2;
+  const uint16_t* gs; const uint16_t* gs2;
+  int ld, store_rows;
+  const int* rows; const int* cols;
+};
+
 struct MfmaArgs {
   const void* w;              // panel rows [N][ld] (gate/up: gate rows)
   uint32_t w2_off;            // gate/up: byte offset of the up rows from w
@@ -115,6 +126,7 @@ struct MfmaArgs {
   const uint16_t* gamma_next; // MM_RESID: gain of the next RMSNorm
   float* ssq_out; int n_tiles_out;  // MM_RESID with gamma_next: [B][n_tiles_out], n_tiles_out = ceil(N/16)
   int B;
+  StoreView sv;               // gs set: weights read from a groupwise store (w, w2_off, scale unused)
 };
 hipError_t launch_mfma_gemv(MfmaMode mode, const MfmaArgs& a, hipStream_t s);
 // The first operand of a step from float32 input rows x [B][ldx]: x * gamma as hi/lo and the
@@ -140,6 +152,7 @@ struct PfArgs {
   float* ssq_out; int n_ssq_out;      // MM_RESID with gamma_next: [T][ceil(N/64)]
   int T;
   float* part; size_t part_floats;    // MM_QKV / MM_RESID K-split partials [splits][T][N] (or null)
+  StoreView sv;                       // gs set: weights read from a groupwise store
 };
 hipError_t launch_pf_gemm(MfmaMode mode, const PfArgs& a, hipStream_t s);
 // floats of the K-split partial buffer of a plan (prompt chunks up to max_prefill tokens, panels

@@ -16,6 +16,13 @@
 // branch-free buffer loads, double-buffered so the next steps' loads are in flight during the
 // current steps' MFMAs. The partial tiles of the waves are summed through LDS, then the epilogue
 // applies scale, inverse RMS, residual / SwiGLU, and writes the next operand.
+//
+// Groupwise store (shared-store plans). The weights come from the store through the plan's row
+// map (QKV, gate/up) or 16-column piece map (O, down, staged in LDS), and a lane's 16 bytes lie in
+// one piece, hence in one group of 128 columns: it loads the group's BF16 scale with them and
+// forms w = q * s in float32, exact (7 + 8 significant bits), then splits it into BF16 hi and lo
+// parts (exact as well: the lo part keeps at most 7 bits). Both parts meet the hi/lo activation
+// columns, so one step costs four MFMAs instead of two and no per-row scale remains.
 #include "device_common.hpp"
 #include "kernels.hpp"
 
@@ -55,7 +62,32 @@ template <int RT>
 struct Frag {
   int4 a[RT];    // 16 weight bytes (INT8) or 8 BF16 weights of each row tile
   int4 x0, x1;   // activation fragments for the step's two k halves (x1 unused for BF16 weights)
+  uint32_t gs[RT];   // groupwise store: the BF16 scale of the row tile's 16 bytes
 };
+
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ uint32_t cvt_bf16x2(float a, float b) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{a, b}, bf16x2_t));
+}
+
+// 8 signed INT8 weights (two words) times a group scale -> the exact products as BF16 hi and lo
+__device__ __forceinline__ void widen_scaled(uint32_t w0, uint32_t w1, float sc, bf16x8& hi, bf16x8& lo) {
+  const uint32_t w[2] = {w0, w1};
+  uint32_t h[4], l[4];
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const float f0 = float(int8_t(w[i] & 0xffu)) * sc, f1 = float(int8_t((w[i] >> 8) & 0xffu)) * sc;
+    const float f2 = float(int8_t((w[i] >> 16) & 0xffu)) * sc, f3 = float(int8_t(w[i] >> 24)) * sc;
+    h[2 * i] = cvt_bf16x2(f0, f1);
+    h[2 * i + 1] = cvt_bf16x2(f2, f3);
+    l[2 * i] = cvt_bf16x2(f0 - bf16_lo(h[2 * i]), f1 - bf16_hi(h[2 * i]));
+    l[2 * i + 1] = cvt_bf16x2(f2 - bf16_lo(h[2 * i + 1]), f3 - bf16_hi(h[2 * i + 1]));
+  }
+  hi = __builtin_bit_cast(bf16x8, make_int4(int(h[0]), int(h[1]), int(h[2]), int(h[3])));
+  lo = __builtin_bit_cast(bf16x8, make_int4(int(l[0]), int(l[1]), int(l[2]), int(l[3])));
+}
 
 // Per-thread epilogue operands of one tile (thread -> (row, sequence) of the output tile).
 struct EpiOps {
@@ -69,10 +101,12 @@ struct EpiOps {
 // tile boundary at the same flattened step and the cross-wave reduction lines up. The load
 // stream runs across tile boundaries: the first steps of the next tile are in flight while the
 // current tile is reduced and stored.
-template <int MODE, int WAVES, int RT>
+template <int MODE, int WAVES, int RT, bool SH>
 __global__ __launch_bounds__(WAVES * kWave) void mfma_gemv_kernel(MfmaArgs a) {
   constexpr int kPF = kStepsPerBatch / RT;             // steps per load batch (two batches in flight)
   constexpr bool BF = (MODE == MM_LMHEAD);
+  static_assert(!(SH && BF), "the LM head is dense BF16 in every store");
+  extern __shared__ int cmap_s[];                      // groupwise store with a column map
   constexpr bool GU = (MODE == MM_GATEUP);
   constexpr int KS = BF ? 32 : 64;                      // k per wave step
   constexpr int ROWS = 16 * RT;                         // tile rows
@@ -93,9 +127,20 @@ __global__ __launch_bounds__(WAVES * kWave) void mfma_gemv_kernel(MfmaArgs a) {
   const int total = my_tiles * spw;
 
   const uint32_t esz = BF ? 2u : 1u;
-  const uint32_t row_bytes = uint32_t(a.ld) * esz;
-  const uint32_t w_bytes = GU ? a.w2_off + uint32_t(N) * row_bytes : uint32_t(N) * row_bytes;
-  const __amdgpu_buffer_rsrc_t rw = make_rsrc(a.w, w_bytes);
+  const uint32_t row_bytes = SH ? uint32_t(a.sv.ld) : uint32_t(a.ld) * esz;
+  const uint32_t w_bytes = SH ? uint32_t(a.sv.store_rows) * row_bytes
+                              : (GU ? a.w2_off + uint32_t(N) * row_bytes : uint32_t(N) * row_bytes);
+  const __amdgpu_buffer_rsrc_t rw = make_rsrc(SH ? static_cast<const void*>(a.sv.w) : a.w, w_bytes);
+  const __amdgpu_buffer_rsrc_t rw2 = make_rsrc(SH && GU ? a.sv.w2 : nullptr, SH && GU ? w_bytes : 0u);
+  const uint32_t sgroups = SH ? uint32_t(a.sv.ld / 128) : 0u;
+  const __amdgpu_buffer_rsrc_t rg1 = make_rsrc(SH ? a.sv.gs : nullptr, SH ? uint32_t(a.sv.store_rows) * sgroups * 2u : 0u);
+  const __amdgpu_buffer_rsrc_t rg2 = make_rsrc(SH && GU ? a.sv.gs2 : nullptr,
+                                               SH && GU ? uint32_t(a.sv.store_rows) * sgroups * 2u : 0u);
+  const bool has_cols = SH && a.sv.cols != nullptr;
+  if (has_cols) {                                       // column map of the plan's K range
+    for (int i = tid; i < (K + 15) / 16; i += WAVES * kWave) cmap_s[i] = a.sv.cols[i];
+    __syncthreads();
+  }
   const __amdgpu_buffer_rsrc_t rx = make_rsrc(a.x, uint32_t(2 * B) * uint32_t(a.ldx) * 2u);
   const uint32_t x_base = uint32_t(r) * uint32_t(a.ldx) * 2u;   // >= the record count when r >= 2B
   const int lane_k = q * (BF ? 8 : 16);                 // first k of the lane inside a step
@@ -105,10 +150,9 @@ __global__ __launch_bounds__(WAVES * kWave) void mfma_gemv_kernel(MfmaArgs a) {
     if (GU) return tile * RPT + (RT == 1 ? (r & 7) : r);
     return tile * ROWS + 16 * rt + r;
   };
-  auto lane_half = [&](int rt) -> uint32_t {
-    if (!GU) return 0u;
-    return (RT == 1 ? (r >= 8) : (rt == 1)) ? a.w2_off : 0u;
-  };
+  // gate/up: whether the lane's rows of row tile rt are up rows, and their byte offset
+  auto lane_up = [&](int rt) -> bool { return GU && (RT == 1 ? (r >= 8) : (rt == 1)); };
+  auto lane_half = [&](int rt) -> uint32_t { return lane_up(rt) ? a.w2_off : 0u; };
 
   // epilogue thread roles and their operand resources (out-of-range offsets read zero)
   const int e_b = tid / RPT, e_r = tid % RPT;           // gate/up: channel e_r, else row e_r
@@ -124,8 +168,8 @@ __global__ __launch_bounds__(WAVES * kWave) void mfma_gemv_kernel(MfmaArgs a) {
     const int row = tile * RPT + e_r;
     const bool ok = e_b < B && row < N;
     const uint32_t o4 = ok ? uint32_t(row) * 4u : kOOB;
-    e.s1 = BF ? 1.0f : __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rs1, int(o4), 0, 0));
-    e.s2 = GU ? __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rs2, int(o4), 0, 0)) : 1.0f;
+    e.s1 = (BF || SH) ? 1.0f : __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rs1, int(o4), 0, 0));
+    e.s2 = (GU && !SH) ? __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rs2, int(o4), 0, 0)) : 1.0f;
     e.res = resid_on ? __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
                            rres, int(ok ? (uint32_t(e_b) * uint32_t(a.ldy) + uint32_t(row)) * 4u : kOOB), 0, 0))
                      : 0.0f;
@@ -134,12 +178,33 @@ __global__ __launch_bounds__(WAVES * kWave) void mfma_gemv_kernel(MfmaArgs a) {
   };
 
   EpiOps ops0{}, ops1{};
+  // groupwise store: store row of this lane in each row tile of the current tile (row map loads
+  // once per tile)
+  int srow_tile = -1;
+  int srow[RT];
+#pragma unroll
+  for (int rt = 0; rt < RT; ++rt) srow[rt] = -1;
   auto issue = [&](int g, Frag<RT> (&f)[kPF]) {
     const int i = g / spw, jb = g - i * spw;
     const int tile = wg + i * grid;
     const bool ok_t = g < total;
     if (ok_t && jb == 0) {
-      if (i & 1) load_ops(tile, ops1); else load_ops(tile, ops0);
+      // select values, not references (a select of addresses puts both structs in memory)
+      EpiOps e;
+      load_ops(tile, e);
+      const bool odd = (i & 1) != 0;
+      ops1.s1 = odd ? e.s1 : ops1.s1; ops1.s2 = odd ? e.s2 : ops1.s2;
+      ops1.res = odd ? e.res : ops1.res; ops1.g = odd ? e.g : ops1.g;
+      ops0.s1 = odd ? ops0.s1 : e.s1; ops0.s2 = odd ? ops0.s2 : e.s2;
+      ops0.res = odd ? ops0.res : e.res; ops0.g = odd ? ops0.g : e.g;
+    }
+    if (SH && ok_t && tile != srow_tile) {
+      srow_tile = tile;
+#pragma unroll
+      for (int rt = 0; rt < RT; ++rt) {
+        const int row = lane_row(tile, rt);
+        srow[rt] = row < N ? (a.sv.rows ? a.sv.rows[row] : row) : -1;
+      }
     }
 #pragma unroll
     for (int u = 0; u < kPF; ++u) {
@@ -148,10 +213,31 @@ __global__ __launch_bounds__(WAVES * kWave) void mfma_gemv_kernel(MfmaArgs a) {
       const bool ok = ok_t && step < n_steps;
 #pragma unroll
       for (int rt = 0; rt < RT; ++rt) {
-        const int row = lane_row(tile, rt);
-        const uint32_t wo = (ok && row < N && k < a.ld)
-                                ? lane_half(rt) + uint32_t(row) * row_bytes + uint32_t(k) * esz : kOOB;
-        f[u].a[rt] = buf_load16_stream(rw, wo);
+        if constexpr (SH) {
+          const bool okr = ok && srow[rt] >= 0 && k < K;
+          const int scol = okr ? (has_cols ? cmap_s[k >> 4] : k) : 0;
+          const uint32_t wo = okr ? uint32_t(srow[rt]) * row_bytes + uint32_t(scol) : kOOB;
+          const uint32_t so = okr ? (uint32_t(srow[rt]) * sgroups + uint32_t(scol) / 128u) * 2u : kOOB;
+          if constexpr (GU) {
+            // gate and up rows of one wave come from two store matrices: a resource must be
+            // wave-uniform, so each lane loads from both with the other offset out of range
+            // (no traffic) and keeps the union
+            const bool up = lane_up(rt);
+            const int4 g4 = buf_load16_stream(rw, up ? kOOB : wo);
+            const int4 u4 = buf_load16_stream(rw2, up ? wo : kOOB);
+            f[u].a[rt] = make_int4(g4.x | u4.x, g4.y | u4.y, g4.z | u4.z, g4.w | u4.w);
+            f[u].gs[rt] = __builtin_amdgcn_raw_buffer_load_b16(rg1, int(up ? kOOB : so), 0, 0) |
+                          __builtin_amdgcn_raw_buffer_load_b16(rg2, int(up ? so : kOOB), 0, 0);
+          } else {
+            f[u].a[rt] = buf_load16_stream(rw, wo);
+            f[u].gs[rt] = __builtin_amdgcn_raw_buffer_load_b16(rg1, int(so), 0, 0);
+          }
+        } else {
+          const int row = lane_row(tile, rt);
+          const uint32_t wo = (ok && row < N && k < a.ld)
+                                  ? lane_half(rt) + uint32_t(row) * row_bytes + uint32_t(k) * esz : kOOB;
+          f[u].a[rt] = buf_load16_stream(rw, wo);
+        }
       }
       const uint32_t xo = ok ? x_base + uint32_t(k) * 2u : kOOB;
       f[u].x0 = buf_load16(rx, xo);
@@ -221,6 +307,16 @@ __global__ __launch_bounds__(WAVES * kWave) void mfma_gemv_kernel(MfmaArgs a) {
         if (BF) {
           acc0[rt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, f[u].a[rt]),
                                                              __builtin_bit_cast(bf16x8, f[u].x0), acc0[rt], 0, 0, 0);
+        } else if constexpr (SH) {
+          const float sc = bf16_to_f32(uint16_t(f[u].gs[rt]));
+          bf16x8 h0, l0, h1, l1;
+          widen_scaled(uint32_t(f[u].a[rt].x), uint32_t(f[u].a[rt].y), sc, h0, l0);
+          widen_scaled(uint32_t(f[u].a[rt].z), uint32_t(f[u].a[rt].w), sc, h1, l1);
+          const bf16x8 x0 = __builtin_bit_cast(bf16x8, f[u].x0), x1 = __builtin_bit_cast(bf16x8, f[u].x1);
+          acc0[rt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(h0, x0, acc0[rt], 0, 0, 0);
+          acc1[rt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(h1, x1, acc1[rt], 0, 0, 0);
+          acc0[rt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(l0, x0, acc0[rt], 0, 0, 0);
+          acc1[rt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(l1, x1, acc1[rt], 0, 0, 0);
         } else {
           const bf16x8 w_lo = widen_i8(uint32_t(f[u].a[rt].x), uint32_t(f[u].a[rt].y));
           const bf16x8 w_hi = widen_i8(uint32_t(f[u].a[rt].z), uint32_t(f[u].a[rt].w));
@@ -277,21 +373,23 @@ __global__ __launch_bounds__(kBlock) void mfma_prep_kernel(const float* __restri
   if ((threadIdx.x & 15) == 0 && i < D) ssq[size_t(b) * n_tiles + (i >> 4)] = ss;
 }
 
-template <int MODE, int WAVES, int RT>
+template <int MODE, int WAVES, int RT, bool SH>
 hipError_t launch_mm(const MfmaArgs& a, hipStream_t s) {
   const int rpt = (MODE == MM_GATEUP) ? 8 * RT : 16 * RT;
   const int tiles = (a.N + rpt - 1) / rpt;
   if (tiles == 0) return hipSuccess;
+  // dynamic LDS: the column map of a groupwise-store projection
+  const size_t lds = (SH && a.sv.cols) ? size_t((a.K + 15) / 16) * 4 : 0;
   // resident workgroups per CU at this kernel's register and LDS use, queried once
   static int per_cu = [] {
     int n = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, mfma_gemv_kernel<MODE, WAVES, RT>,
-                                                     WAVES * kWave, 0) != hipSuccess || n < 1)
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, mfma_gemv_kernel<MODE, WAVES, RT, SH>,
+                                                     WAVES * kWave, SH ? 8192 : 0) != hipSuccess || n < 1)
       n = 1;
     return n;
   }();
   const int grid = tiles < per_cu * kNumCu ? tiles : per_cu * kNumCu;
-  hipLaunchKernelGGL((mfma_gemv_kernel<MODE, WAVES, RT>), dim3(grid), dim3(WAVES * kWave), 0, s, a);
+  hipLaunchKernelGGL((mfma_gemv_kernel<MODE, WAVES, RT, SH>), dim3(grid), dim3(WAVES * kWave), lds, s, a);
   return hipGetLastError();
 }
 
@@ -300,16 +398,31 @@ hipError_t launch_mm_mode(const MfmaArgs& a, hipStream_t s) {
   // two row tiles per wave halve the activation reads per weight byte; panels with few rows
   // keep one so that every CU gets a tile, with more waves per tile so that enough loads fly
   const int rows = (MODE == MM_GATEUP) ? 2 * a.N : a.N;
-  if (rows >= kMmTwoTileRows) return launch_mm<MODE, 4, 2>(a, s);
-  return launch_mm<MODE, 8, 1>(a, s);
+  if constexpr (MODE != MM_LMHEAD) {
+    if (a.sv.gs) {
+      if (rows >= kMmTwoTileRows) return launch_mm<MODE, 4, 2, true>(a, s);
+      return launch_mm<MODE, 8, 1, true>(a, s);
+    }
+  }
+  if (rows >= kMmTwoTileRows) return launch_mm<MODE, 4, 2, false>(a, s);
+  return launch_mm<MODE, 8, 1, false>(a, s);
 }
 
 }  // namespace
 
 hipError_t launch_mfma_gemv(MfmaMode mode, const MfmaArgs& a, hipStream_t s) {
-  if (a.B < 1 || a.B > 8 || a.K < 0 || a.K > a.ld || a.ld % 16 != 0 || a.ldx % 64 != 0 ||
-      a.ldx < a.K)
+  if (a.sv.gs) {
+    // groupwise store: plan columns within the operand, store rows of 16-byte multiples in 128
+    // column groups, a column map only for piece-aligned K, no LM head
+    if (mode == MM_LMHEAD || a.B < 1 || a.B > 8 || a.K < 0 || a.K % 16 != 0 || a.ldx % 64 != 0 ||
+        a.ldx < a.K || a.sv.ld % 128 != 0 || a.sv.store_rows < 1 ||
+        (mode == MM_GATEUP && (!a.sv.w2 || !a.sv.gs2)))
+      return hipErrorInvalidValue;
+    if (size_t((a.K + 15) / 16) * 4 > 64 * 1024) return hipErrorInvalidValue;
+  } else if (a.B < 1 || a.B > 8 || a.K < 0 || a.K > a.ld || a.ld % 16 != 0 || a.ldx % 64 != 0 ||
+             a.ldx < a.K) {
     return hipErrorInvalidValue;
+  }
   switch (mode) {
     case MM_QKV: return launch_mm_mode<MM_QKV>(a, s);
     case MM_RESID: return launch_mm_mode<MM_RESID>(a, s);

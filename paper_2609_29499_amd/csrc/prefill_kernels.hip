@@ -21,6 +21,13 @@
 // keeps resident; each split writes its scaled partial tile to a float32 buffer and a second
 // kernel sums the splits in a fixed order and applies the epilogue (residual, next operand, sums
 // of squares).
+//
+// Groupwise store (shared-store plans). Panel rows come from the store through the plan's row map
+// (QKV, gate/up) and plan columns through its 16-column piece map (O, down; staged in LDS); each
+// thread's 16 staged bytes lie in one piece, hence in one group of 128 columns with one BF16
+// scale. The staged weight is the exact product q * s (7 + 8 significant bits) split into BF16 hi
+// and lo planes (both exact), and a tile pair costs three MFMAs (a_hi w_hi, a_lo w_hi, a_hi w_lo;
+// a_lo w_lo is below 2^-16 of the product) with no per-row scale left for the epilogue.
 #include <algorithm>
 
 #include "device_common.hpp"
@@ -43,12 +50,40 @@ constexpr int kMinSplitChunks = 8;     // k chunks per split at least
 constexpr long kSplitRowCap = 2048;    // (tokens x splits) the partial buffer is sized for
 constexpr int kNumCu = 256;
 
-template <int TM>
+template <int TM, bool SH>
 struct PfSmem {
   uint16_t a[2][2][TM * kLdsRow];      // [buffer][hi/lo][swizzled token row]
-  uint16_t b[2][kTN * kLdsRow];        // [buffer][swizzled panel row]
+  uint16_t b[2][SH ? 2 : 1][kTN * kLdsRow];   // [buffer][hi/lo (store weights)][swizzled panel row]
   float rs[TM];                        // inverse RMS of the tile's tokens
 };
+
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ uint32_t cvt_bf16x2(float a, float b) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{a, b}, bf16x2_t));
+}
+
+// 16 signed INT8 weights times their group scale -> the exact products as BF16 hi and lo parts
+// (each as two 16-byte halves)
+__device__ __forceinline__ void widen16_scaled(const int4& w, float sc, int4& hlo, int4& hhi,
+                                               int4& llo, int4& lhi) {
+  const uint32_t v[4] = {uint32_t(w.x), uint32_t(w.y), uint32_t(w.z), uint32_t(w.w)};
+  uint32_t h[8], l[8];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const float f0 = float(int8_t(v[i] & 0xffu)) * sc, f1 = float(int8_t((v[i] >> 8) & 0xffu)) * sc;
+    const float f2 = float(int8_t((v[i] >> 16) & 0xffu)) * sc, f3 = float(int8_t(v[i] >> 24)) * sc;
+    h[2 * i] = cvt_bf16x2(f0, f1);
+    h[2 * i + 1] = cvt_bf16x2(f2, f3);
+    l[2 * i] = cvt_bf16x2(f0 - bf16_lo(h[2 * i]), f1 - bf16_hi(h[2 * i]));
+    l[2 * i + 1] = cvt_bf16x2(f2 - bf16_lo(h[2 * i + 1]), f3 - bf16_hi(h[2 * i + 1]));
+  }
+  hlo = make_int4(int(h[0]), int(h[1]), int(h[2]), int(h[3]));
+  hhi = make_int4(int(h[4]), int(h[5]), int(h[6]), int(h[7]));
+  llo = make_int4(int(l[0]), int(l[1]), int(l[2]), int(l[3]));
+  lhi = make_int4(int(l[4]), int(l[5]), int(l[6]), int(l[7]));
+}
 
 // LDS offset (BF16 elements) of 16-byte quarter qu of LDS row `row`. Quarters are XOR-swizzled
 // with bits 1-4 of the row: the 8 or 16 lanes served together by a 16-byte read (one fragment
@@ -81,13 +116,15 @@ __device__ __forceinline__ void store_hilo_pf(uint16_t* xo, size_t plane, int ld
   xo[plane + size_t(t) * ld + col] = f32_to_bf16(v - bf16_to_f32(hi));
 }
 
-template <int MODE, int TM>
+template <int MODE, int TM, bool SH>
 __global__ __launch_bounds__(kBlock) void pf_gemm_kernel(PfArgs a) {
   constexpr bool BF = (MODE == MM_LMHEAD);
   constexpr bool GU = (MODE == MM_GATEUP);
+  static_assert(!(SH && BF), "the LM head is dense BF16 in every store");
   constexpr int MT = TM / 32;                           // token tiles of 16 per wave
   constexpr int APT = TM / 32;                          // A pieces per thread and chunk
-  __shared__ __attribute__((aligned(16))) PfSmem<TM> sm;
+  __shared__ __attribute__((aligned(16))) PfSmem<TM, SH> sm;
+  extern __shared__ int cmap_s[];                       // groupwise store: column map of K
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int r = lane & 15, q = lane >> 4;
@@ -104,9 +141,19 @@ __global__ __launch_bounds__(kBlock) void pf_gemm_kernel(PfArgs a) {
   // ---- global -> register staging of one chunk
   const __amdgpu_buffer_rsrc_t ra = make_rsrc(a.x, uint32_t(2 * a.plane) * 2u);
   const uint32_t esz = BF ? 2u : 1u;
-  const uint32_t row_bytes = uint32_t(a.ld) * esz;
-  const uint32_t w_bytes = GU ? a.w2_off + uint32_t(N) * row_bytes : uint32_t(N) * row_bytes;
-  const __amdgpu_buffer_rsrc_t rw = make_rsrc(a.w, w_bytes);
+  const uint32_t row_bytes = SH ? uint32_t(a.sv.ld) : uint32_t(a.ld) * esz;
+  const uint32_t w_bytes = SH ? uint32_t(a.sv.store_rows) * row_bytes
+                              : (GU ? a.w2_off + uint32_t(N) * row_bytes : uint32_t(N) * row_bytes);
+  const __amdgpu_buffer_rsrc_t rw = make_rsrc(SH ? static_cast<const void*>(a.sv.w) : a.w, w_bytes);
+  const __amdgpu_buffer_rsrc_t rw2 = make_rsrc(SH && GU ? a.sv.w2 : nullptr, SH && GU ? w_bytes : 0u);
+  const uint32_t sgroups = SH ? uint32_t(a.sv.ld / 128) : 0u;
+  const __amdgpu_buffer_rsrc_t rg1 = make_rsrc(SH ? a.sv.gs : nullptr, SH ? uint32_t(a.sv.store_rows) * sgroups * 2u : 0u);
+  const __amdgpu_buffer_rsrc_t rg2 = make_rsrc(SH && GU ? a.sv.gs2 : nullptr,
+                                               SH && GU ? uint32_t(a.sv.store_rows) * sgroups * 2u : 0u);
+  const bool has_cols = SH && a.sv.cols != nullptr;
+  // groupwise store: store row of this thread's staged panel row (fixed for the workgroup)
+  int srow = -1;
+  bool srow_up = false;
   // A pieces: thread t loads pieces t + 256 i (i < APT): plane, token row, 16-byte quarter
   auto a_off = [&](int i, int k0) -> uint32_t {
     const int p = tid + kBlock * i;
@@ -130,6 +177,7 @@ __global__ __launch_bounds__(kBlock) void pf_gemm_kernel(PfArgs a) {
   struct Stage {
     int4 av[APT];
     int4 bv[2];
+    uint32_t gs;                                        // groupwise store: scale of bv[0]
   };
   auto load = [&](int kc, Stage& st) {
     const int k0 = (kc0 + kc) * kKC;
@@ -140,6 +188,24 @@ __global__ __launch_bounds__(kBlock) void pf_gemm_kernel(PfArgs a) {
       for (int i = 0; i < 2; ++i) {
         const int p = tid + kBlock * i;
         st.bv[i] = buf_load16(rw, kc < nk ? w_off(p >> 2, (k0 + 8 * (p & 3)) * 2) : kOOB);
+      }
+    } else if constexpr (SH) {
+      const int k = k0 + 16 * (tid & 1);
+      const bool ok = kc < nk && srow >= 0 && k < K;
+      const int scol = ok ? (has_cols ? cmap_s[k >> 4] : k) : 0;
+      const uint32_t wo = ok ? uint32_t(srow) * row_bytes + uint32_t(scol) : kOOB;
+      const uint32_t so = ok ? (uint32_t(srow) * sgroups + uint32_t(scol) / 128u) * 2u : kOOB;
+      if constexpr (GU) {
+        // gate and up rows come from two store matrices (resources must be wave-uniform): load
+        // from both, the other offset out of range, and keep the union
+        const int4 g4 = buf_load16(rw, srow_up ? kOOB : wo);
+        const int4 u4 = buf_load16(rw2, srow_up ? wo : kOOB);
+        st.bv[0] = make_int4(g4.x | u4.x, g4.y | u4.y, g4.z | u4.z, g4.w | u4.w);
+        st.gs = __builtin_amdgcn_raw_buffer_load_b16(rg1, int(srow_up ? kOOB : so), 0, 0) |
+                __builtin_amdgcn_raw_buffer_load_b16(rg2, int(srow_up ? so : kOOB), 0, 0);
+      } else {
+        st.bv[0] = buf_load16(rw, wo);
+        st.gs = __builtin_amdgcn_raw_buffer_load_b16(rg1, int(so), 0, 0);
       }
     } else {
       st.bv[0] = buf_load16(rw, kc < nk ? w_off(tid >> 1, k0 + 16 * (tid & 1)) : kOOB);
@@ -156,16 +222,34 @@ __global__ __launch_bounds__(kBlock) void pf_gemm_kernel(PfArgs a) {
 #pragma unroll
       for (int i = 0; i < 2; ++i) {
         const int p = tid + kBlock * i;
-        *reinterpret_cast<int4*>(&sm.b[buf][lds_q(p >> 2, p & 3)]) = st.bv[i];
+        *reinterpret_cast<int4*>(&sm.b[buf][0][lds_q(p >> 2, p & 3)]) = st.bv[i];
       }
+    } else if constexpr (SH) {
+      int4 hlo, hhi, llo, lhi;
+      widen16_scaled(st.bv[0], bf16_to_f32(uint16_t(st.gs)), hlo, hhi, llo, lhi);
+      const int row = tid >> 1, h = tid & 1;
+      *reinterpret_cast<int4*>(&sm.b[buf][0][lds_q(row, 2 * h)]) = hlo;
+      *reinterpret_cast<int4*>(&sm.b[buf][0][lds_q(row, 2 * h + 1)]) = hhi;
+      *reinterpret_cast<int4*>(&sm.b[buf][1][lds_q(row, 2 * h)]) = llo;
+      *reinterpret_cast<int4*>(&sm.b[buf][1][lds_q(row, 2 * h + 1)]) = lhi;
     } else {
       int4 lo, hi;
       widen16(st.bv[0], lo, hi);
       const int row = tid >> 1, h = tid & 1;
-      *reinterpret_cast<int4*>(&sm.b[buf][lds_q(row, 2 * h)]) = lo;
-      *reinterpret_cast<int4*>(&sm.b[buf][lds_q(row, 2 * h + 1)]) = hi;
+      *reinterpret_cast<int4*>(&sm.b[buf][0][lds_q(row, 2 * h)]) = lo;
+      *reinterpret_cast<int4*>(&sm.b[buf][0][lds_q(row, 2 * h + 1)]) = hi;
     }
   };
+
+  if constexpr (SH) {
+    const int lr = tid >> 1, row = w_row(lr);
+    srow_up = GU && ((lr & 63) >= 32);
+    srow = row < N ? (a.sv.rows ? a.sv.rows[row] : row) : -1;
+    if (has_cols) {                                     // column map of the plan's K range
+      for (int i = tid; i < (K + 15) / 16; i += kBlock) cmap_s[i] = a.sv.cols[i];
+      __syncthreads();
+    }
+  }
 
   // three chunks in flight in registers: chunk c is loaded while chunk c - 3 is computed and
   // committed to LDS after chunk c - 1 has been computed
@@ -206,10 +290,12 @@ __global__ __launch_bounds__(kBlock) void pf_gemm_kernel(PfArgs a) {
   auto step = [&](int kc, Stage& mine, const Stage& next) {
     const int buf = kc & 1;
     load(kc + 3, mine);                                 // chunk kc was committed already
-    bf16x8 bw[4];
+    bf16x8 bw[4], bl[SH ? 4 : 1];
 #pragma unroll
-    for (int nt = 0; nt < 4; ++nt)
-      bw[nt] = *reinterpret_cast<const bf16x8*>(&sm.b[buf][lds_q(wn * 64 + nt * 16 + r, q)]);
+    for (int nt = 0; nt < 4; ++nt) {
+      bw[nt] = *reinterpret_cast<const bf16x8*>(&sm.b[buf][0][lds_q(wn * 64 + nt * 16 + r, q)]);
+      if constexpr (SH) bl[nt] = *reinterpret_cast<const bf16x8*>(&sm.b[buf][1][lds_q(wn * 64 + nt * 16 + r, q)]);
+    }
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
       const int ar = lds_q(wm * (TM / 2) + mt * 16 + r, q);
@@ -219,6 +305,7 @@ __global__ __launch_bounds__(kBlock) void pf_gemm_kernel(PfArgs a) {
       for (int nt = 0; nt < 4; ++nt) {
         acc[mt][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ahi, bw[nt], acc[mt][nt], 0, 0, 0);
         acc[mt][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(alo, bw[nt], acc[mt][nt], 0, 0, 0);
+        if constexpr (SH) acc[mt][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ahi, bl[nt], acc[mt][nt], 0, 0, 0);
       }
     }
     if (kc + 1 < nk) commit(buf ^ 1, next);
@@ -245,7 +332,7 @@ __global__ __launch_bounds__(kBlock) void pf_gemm_kernel(PfArgs a) {
 #pragma unroll
         for (int nt = 0; nt < 4; ++nt) {
           const int n = n0 + wn * 64 + nt * 16 + r;
-          if (n < N) part[size_t(t) * N + n] = acc[mt][nt][i] * a.scale[n] * rb;
+          if (n < N) part[size_t(t) * N + n] = acc[mt][nt][i] * (SH ? 1.0f : a.scale[n]) * rb;
         }
       }
     return;
@@ -264,8 +351,8 @@ __global__ __launch_bounds__(kBlock) void pf_gemm_kernel(PfArgs a) {
         for (int nt = 0; nt < 2; ++nt) {
           const int ch = n0 + 32 * wn + 16 * nt + r;
           if (t_ok && ch < N) {
-            const float gv = acc[mt][nt][i] * a.scale[ch] * rb;
-            const float uv = acc[mt][nt + 2][i] * a.scale2[ch] * rb;
+            const float gv = acc[mt][nt][i] * (SH ? 1.0f : a.scale[ch]) * rb;
+            const float uv = acc[mt][nt + 2][i] * (SH ? 1.0f : a.scale2[ch]) * rb;
             store_hilo_pf(a.xo, a.plane_o, a.ldxo, t, ch, gv / (1.0f + exp2f(-gv * kLog2e)) * uv);
           }
         }
@@ -280,11 +367,11 @@ __global__ __launch_bounds__(kBlock) void pf_gemm_kernel(PfArgs a) {
         if (MODE == MM_LMHEAD) {
           v = acc[mt][nt][i] * rb;
         } else if (resid_on) {
-          v = ok ? a.resid[size_t(t) * a.ldy + n] + acc[mt][nt][i] * a.scale[n] : 0.0f;
+          v = ok ? a.resid[size_t(t) * a.ldy + n] + acc[mt][nt][i] * (SH ? 1.0f : a.scale[n]) : 0.0f;
           if (ok && a.gamma_next) store_hilo_pf(a.xo, a.plane_o, a.ldxo, t, n, v * bf16_to_f32(a.gamma_next[n]));
           ss = fmaf(v, v, ss);
         } else {
-          v = ok ? acc[mt][nt][i] * a.scale[n] * rb : 0.0f;
+          v = ok ? acc[mt][nt][i] * (SH ? 1.0f : a.scale[n]) * rb : 0.0f;
         }
         if (ok) a.y[size_t(t) * a.ldy + n] = v;
       }
@@ -413,19 +500,19 @@ __global__ __launch_bounds__(kBlock) void pf_rope_kernel(PfRopeArgs a) {
   }
 }
 
-template <int MODE, int TM>
+template <int MODE, int TM, bool SH>
 int pf_resident() {
   static const int n = [] {
     int per_cu = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, pf_gemm_kernel<MODE, TM>, kBlock,
-                                                     0) != hipSuccess || per_cu < 1)
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, pf_gemm_kernel<MODE, TM, SH>, kBlock,
+                                                     SH ? 8192 : 0) != hipSuccess || per_cu < 1)
       per_cu = 1;
     return per_cu * kNumCu;
   }();
   return n;
 }
 
-template <int MODE, int TM>
+template <int MODE, int TM, bool SH>
 hipError_t launch_pf_tm(const PfArgs& a, hipStream_t s) {
   const int rows_per_tile = (MODE == MM_GATEUP) ? kTN / 2 : kTN;
   const int gx = (a.N + rows_per_tile - 1) / rows_per_tile, gy = (a.T + TM - 1) / TM;
@@ -436,14 +523,15 @@ hipError_t launch_pf_tm(const PfArgs& a, hipStream_t s) {
   if ((MODE == MM_QKV || MODE == MM_RESID) && a.part) {
     const long tiles = long(gx) * gy;
     const long per_split = long(a.T) * a.N;
-    ks = int(std::min<long>(kMaxKSplit, pf_resident<MODE, TM>() / tiles));
+    ks = int(std::min<long>(kMaxKSplit, pf_resident<MODE, TM, SH>() / tiles));
     ks = std::min(ks, ((a.K + kKC - 1) / kKC) / kMinSplitChunks);
     ks = int(std::min<long>(ks, per_split > 0 ? long(a.part_floats / size_t(per_split)) : 1));
     ks = std::max(ks, 1);
   }
   PfArgs b = a;
   if (ks == 1) b.part = nullptr;
-  hipLaunchKernelGGL((pf_gemm_kernel<MODE, TM>), dim3(gx, gy, ks), dim3(kBlock), 0, s, b);
+  const size_t lds = (SH && a.sv.cols) ? size_t((a.K + 15) / 16) * 4 : 0;
+  hipLaunchKernelGGL((pf_gemm_kernel<MODE, TM, SH>), dim3(gx, gy, ks), dim3(kBlock), lds, s, b);
   if (ks == 1) return hipGetLastError();
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
@@ -452,20 +540,35 @@ hipError_t launch_pf_tm(const PfArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
-template <int MODE>
-hipError_t launch_pf(const PfArgs& a, hipStream_t s) {
+template <int MODE, bool SH>
+hipError_t launch_pf_sh(const PfArgs& a, hipStream_t s) {
   // 128-token tiles halve the panel re-reads; smaller ones when that leaves CUs idle
   const int rows_per_tile = (MODE == MM_GATEUP) ? kTN / 2 : kTN;
   const long tiles = long((a.N + rows_per_tile - 1) / rows_per_tile) * ((a.T + kTMax - 1) / kTMax);
-  if (tiles >= kPfMinTiles) return launch_pf_tm<MODE, kTMax>(a, s);
-  return launch_pf_tm<MODE, kTMax / 2>(a, s);
+  if (tiles >= kPfMinTiles) return launch_pf_tm<MODE, kTMax, SH>(a, s);
+  return launch_pf_tm<MODE, kTMax / 2, SH>(a, s);
+}
+
+template <int MODE>
+hipError_t launch_pf(const PfArgs& a, hipStream_t s) {
+  if constexpr (MODE != MM_LMHEAD) {
+    if (a.sv.gs) return launch_pf_sh<MODE, true>(a, s);
+  }
+  return launch_pf_sh<MODE, false>(a, s);
 }
 
 }  // namespace
 
 hipError_t launch_pf_gemm(MfmaMode mode, const PfArgs& a, hipStream_t s) {
-  if (a.T < 1 || a.K < 0 || a.K > a.ld || a.ld % 16 != 0 || a.ldx % 64 != 0 || a.ldx < a.K)
+  if (a.sv.gs) {
+    // groupwise store: piece-aligned plan columns, 128-column scale groups, no LM head
+    if (mode == MM_LMHEAD || a.T < 1 || a.K < 0 || a.K % 16 != 0 || a.ldx % 64 != 0 ||
+        a.ldx < a.K || a.sv.ld % 128 != 0 || a.sv.store_rows < 1 ||
+        (mode == MM_GATEUP && (!a.sv.w2 || !a.sv.gs2)) || size_t((a.K + 15) / 16) * 4 > 64 * 1024)
+      return hipErrorInvalidValue;
+  } else if (a.T < 1 || a.K < 0 || a.K > a.ld || a.ld % 16 != 0 || a.ldx % 64 != 0 || a.ldx < a.K) {
     return hipErrorInvalidValue;
+  }
   switch (mode) {
     case MM_QKV: return launch_pf<MM_QKV>(a, s);
     case MM_RESID: return launch_pf<MM_RESID>(a, s);

@@ -151,48 +151,14 @@ struct Layout {
   int n_split_max, ld_qkv, ld_obuf, ld_h, ld_xd, ld_xo, ld_xh, ld_xw;
 };
 
-Layout make_layout(const tasp_model_desc* d, const Closed& c) {
-  Layout Y;
-  size_t off = 0;
-  auto take = [&](size_t bytes) {
-    const size_t at = off;
-    off = align_up(off + bytes, kAlign);
-    return at;
-  };
-  const int L = d->n_layers, D = d->d_model, Hq = d->n_q_heads, Hkv = d->n_kv_heads;
+// Decode and prefill scratch of a plan (every format): residuals, q/k/v, attention partials and
+// split counters, batched operands (max_batch > 1) and prefill operands (max_prefill > 0).
+// zero_begin .. zero_end is cleared at compile; the prefill split partials after it are written
+// in full before they are read.
+template <class Take>
+void scratch_layout(Layout& Y, const tasp_model_desc* d, Take&& take, size_t& off) {
+  const int D = d->d_model, Hq = d->n_q_heads, Hkv = d->n_kv_heads;
   const int dh = d->head_dim, F = d->d_ffn, B = d->max_batch;
-  Y.layers.resize(L);
-  for (int l = 0; l < L; ++l) {
-    LayerLayout& P = Y.layers[l];
-    P.n_qkv = (c.m_q[l] + 2 * c.m_kv[l]) * dh;
-    P.ld_o = c.m_q[l] * dh;
-    P.ld_d = round_up16(c.c[l]);
-    P.qkv = take(size_t(P.n_qkv) * D);
-    P.s_qkv = take(size_t(P.n_qkv) * 4);
-    P.o = take(size_t(D) * P.ld_o);
-    P.s_o = take(size_t(D) * 4);
-    P.g = take(size_t(c.c[l]) * D);
-    P.u = take(size_t(c.c[l]) * D);
-    P.s_g = take(size_t(c.c[l]) * 4);
-    P.s_u = take(size_t(c.c[l]) * 4);
-    P.dn = take(size_t(D) * P.ld_d);
-    P.s_d = take(size_t(D) * 4);
-    P.an = take(size_t(D) * 2);
-    P.fn = take(size_t(D) * 2);
-  }
-  Y.mask_q = take(size_t(L) * Hq);
-  Y.mask_kv = take(size_t(L) * Hkv);
-  Y.mask_f = take(size_t(L) * F);
-  Y.idx_q = take(size_t(L) * Hq * 4);
-  Y.idx_kv = take(size_t(L) * Hkv * 4);
-  Y.idx_slot = take(size_t(L) * Hq * 4);
-  Y.idx_slot_start = take(size_t(L) * (Hkv + 1) * 4);
-  Y.idx_ffn = take(size_t(L) * F * 4);
-  Y.counts = take(size_t(L) * 4 * 4);
-  Y.final_norm = d->vocab ? take(size_t(D) * 2) : 0;
-  Y.lm_head = d->vocab ? take(size_t(d->vocab) * D * 2) : 0;
-  Y.rope_cos = take(size_t(d->max_seq) * (dh / 2) * 4);
-  Y.rope_sin = take(size_t(d->max_seq) * (dh / 2) * 4);
   Y.n_split_max = std::max(std::min((d->max_seq + tasp::attn_min_chunk() - 1) / tasp::attn_min_chunk(),
                                     tasp::attn_max_split()),
                            tasp::attn_mfma_max_split(d->max_seq));
@@ -228,15 +194,59 @@ Layout make_layout(const tasp_model_desc* d, const Closed& c) {
   Y.pr_io1 = take(P * D * 4);
   Y.pssq = take(P * ((D + 63) / 64) * 4);
   Y.zero_end = off;
-  // written in full by each split before it is read: not zeroed
   Y.ppart_floats = P ? tasp::pf_split_buffer_floats(int(P), std::max(D, Y.ld_qkv)) : 0;
   Y.ppart = take(Y.ppart_floats * 4);
+}
+
+Layout make_layout(const tasp_model_desc* d, const Closed& c) {
+  Layout Y;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = off;
+    off = align_up(off + bytes, kAlign);
+    return at;
+  };
+  const int L = d->n_layers, D = d->d_model, Hq = d->n_q_heads, Hkv = d->n_kv_heads;
+  const int dh = d->head_dim, F = d->d_ffn;
+  Y.layers.resize(L);
+  for (int l = 0; l < L; ++l) {
+    LayerLayout& P = Y.layers[l];
+    P.n_qkv = (c.m_q[l] + 2 * c.m_kv[l]) * dh;
+    P.ld_o = c.m_q[l] * dh;
+    P.ld_d = round_up16(c.c[l]);
+    P.qkv = take(size_t(P.n_qkv) * D);
+    P.s_qkv = take(size_t(P.n_qkv) * 4);
+    P.o = take(size_t(D) * P.ld_o);
+    P.s_o = take(size_t(D) * 4);
+    P.g = take(size_t(c.c[l]) * D);
+    P.u = take(size_t(c.c[l]) * D);
+    P.s_g = take(size_t(c.c[l]) * 4);
+    P.s_u = take(size_t(c.c[l]) * 4);
+    P.dn = take(size_t(D) * P.ld_d);
+    P.s_d = take(size_t(D) * 4);
+    P.an = take(size_t(D) * 2);
+    P.fn = take(size_t(D) * 2);
+  }
+  Y.mask_q = take(size_t(L) * Hq);
+  Y.mask_kv = take(size_t(L) * Hkv);
+  Y.mask_f = take(size_t(L) * F);
+  Y.idx_q = take(size_t(L) * Hq * 4);
+  Y.idx_kv = take(size_t(L) * Hkv * 4);
+  Y.idx_slot = take(size_t(L) * Hq * 4);
+  Y.idx_slot_start = take(size_t(L) * (Hkv + 1) * 4);
+  Y.idx_ffn = take(size_t(L) * F * 4);
+  Y.counts = take(size_t(L) * 4 * 4);
+  Y.final_norm = d->vocab ? take(size_t(D) * 2) : 0;
+  Y.lm_head = d->vocab ? take(size_t(d->vocab) * D * 2) : 0;
+  Y.rope_cos = take(size_t(d->max_seq) * (dh / 2) * 4);
+  Y.rope_sin = take(size_t(d->max_seq) * (dh / 2) * 4);
+  scratch_layout(Y, d, take, off);
   Y.total = off;
   return Y;
 }
 
 // A shared-store plan holds no weights: masks and index lists, the maps into the store, the
-// RoPE table and the batch-1 decode scratch. Its size does not depend on the mask.
+// RoPE table and the decode / prefill scratch. Its size does not depend on the mask.
 Layout make_shared_layout(const tasp_model_desc* d) {
   Layout Y{};
   size_t off = 0;
@@ -245,7 +255,7 @@ Layout make_shared_layout(const tasp_model_desc* d) {
     off = align_up(off + bytes, kAlign);
     return at;
   };
-  const int L = d->n_layers, D = d->d_model, Hq = d->n_q_heads, Hkv = d->n_kv_heads;
+  const int L = d->n_layers, Hq = d->n_q_heads, Hkv = d->n_kv_heads;
   const int dh = d->head_dim, F = d->d_ffn;
   Y.mask_q = take(size_t(L) * Hq);
   Y.mask_kv = take(size_t(L) * Hkv);
@@ -261,22 +271,7 @@ Layout make_shared_layout(const tasp_model_desc* d) {
   Y.down_cols = take(size_t(L) * (F / 16) * 4);
   Y.rope_cos = take(size_t(d->max_seq) * (dh / 2) * 4);
   Y.rope_sin = take(size_t(d->max_seq) * (dh / 2) * 4);
-  Y.n_split_max = std::max(std::min((d->max_seq + tasp::attn_min_chunk() - 1) / tasp::attn_min_chunk(),
-                                    tasp::attn_max_split()),
-                           tasp::attn_mfma_max_split(d->max_seq));
-  Y.ld_qkv = (Hq + 2 * Hkv) * dh;
-  Y.ld_obuf = Hq * dh;
-  Y.ld_h = round_up16(F);
-  Y.zero_begin = off;
-  Y.r_mid = take(size_t(D) * 4);
-  Y.r_io0 = take(size_t(D) * 4);
-  Y.r_io1 = take(size_t(D) * 4);
-  Y.qkv_buf = take(size_t(Y.ld_qkv) * 4);
-  Y.o_buf = take(size_t(Y.ld_obuf) * 4);
-  Y.h_buf = take(size_t(Y.ld_h) * 4);
-  Y.part = take(size_t(Hkv) * Y.n_split_max * 8 * (dh + 4) * 4);
-  Y.acnt = take(size_t(Hkv) * 4);
-  Y.zero_end = off;
+  scratch_layout(Y, d, take, off);
   Y.total = off;
   return Y;
 }
@@ -339,6 +334,62 @@ struct tasp_plan_s {
 };
 
 namespace {
+
+// Pointers of a plan into the decode / prefill scratch of its workspace (scratch_layout).
+void set_scratch(tasp_plan_s* p, const Layout& Y, char* ws) {
+  auto at = [&](size_t off) { return ws + off; };
+  p->r_mid = reinterpret_cast<float*>(at(Y.r_mid));
+  p->r_io[0] = reinterpret_cast<float*>(at(Y.r_io0));
+  p->r_io[1] = reinterpret_cast<float*>(at(Y.r_io1));
+  p->qkv_buf = reinterpret_cast<float*>(at(Y.qkv_buf));
+  p->o_buf = reinterpret_cast<float*>(at(Y.o_buf));
+  p->h_buf = reinterpret_cast<float*>(at(Y.h_buf));
+  p->part = reinterpret_cast<float*>(at(Y.part));
+  p->acnt = reinterpret_cast<int*>(at(Y.acnt));
+  p->n_split_max = Y.n_split_max; p->ld_qkv = Y.ld_qkv; p->ld_obuf = Y.ld_obuf; p->ld_h = Y.ld_h;
+  p->xd = reinterpret_cast<uint16_t*>(at(Y.xd));
+  p->xo = reinterpret_cast<uint16_t*>(at(Y.xo));
+  p->xh = reinterpret_cast<uint16_t*>(at(Y.xh));
+  p->ssq = reinterpret_cast<float*>(at(Y.ssq));
+  p->ld_xd = Y.ld_xd; p->ld_xo = Y.ld_xo; p->ld_xh = Y.ld_xh;
+  p->pxd = reinterpret_cast<uint16_t*>(at(Y.pxd));
+  p->pxw = reinterpret_cast<uint16_t*>(at(Y.pxw));
+  p->pq = reinterpret_cast<uint16_t*>(at(Y.pq));
+  p->pqkv = reinterpret_cast<float*>(at(Y.pqkv));
+  p->pr_mid = reinterpret_cast<float*>(at(Y.pr_mid));
+  p->pr_io[0] = reinterpret_cast<float*>(at(Y.pr_io0));
+  p->pr_io[1] = reinterpret_cast<float*>(at(Y.pr_io1));
+  p->pssq = reinterpret_cast<float*>(at(Y.pssq));
+  p->ppart = reinterpret_cast<float*>(at(Y.ppart));
+  p->ppart_floats = Y.ppart_floats;
+  p->ld_xw = Y.ld_xw;
+}
+
+// The store view of one projection of a shared-store plan's layer (for the matrix-core kernels):
+// 0 QKV (row map), 1 O (column map), 3 gate/up (row map, two matrices), 4 down (column map).
+tasp::StoreView store_view(const tasp_plan_s* p, int l, int which) {
+  const SharedLayer& Q = p->sl[l];
+  const tasp_model_desc& d = p->desc;
+  tasp::StoreView v{};
+  switch (which) {
+    case 0:
+      v.w = Q.qkv; v.gs = Q.s_qkv; v.ld = d.d_model;
+      v.store_rows = (d.n_q_heads + 2 * d.n_kv_heads) * d.head_dim; v.rows = Q.qkv_rows;
+      break;
+    case 1:
+      v.w = Q.o; v.gs = Q.s_o; v.ld = d.n_q_heads * d.head_dim; v.store_rows = d.d_model;
+      v.cols = Q.o_cols;
+      break;
+    case 3:
+      v.w = Q.g; v.w2 = Q.u; v.gs = Q.s_g; v.gs2 = Q.s_u; v.ld = d.d_model; v.store_rows = d.d_ffn;
+      v.rows = Q.ffn_rows;
+      break;
+    default:
+      v.w = Q.d; v.gs = Q.s_d; v.ld = d.d_ffn; v.store_rows = d.d_model; v.cols = Q.down_cols;
+      break;
+  }
+  return v;
+}
 
 struct Timer {
   std::vector<hipEvent_t> ev;
@@ -533,6 +584,7 @@ tasp::MfmaArgs gateup_mm_args(const tasp_plan_s* p, int l, int B) {
   a.w = P.g; a.w2_off = uint32_t(reinterpret_cast<const char*>(P.u) - reinterpret_cast<const char*>(P.g));
   a.scale = P.s_g; a.scale2 = P.s_u; a.N = P.c; a.K = p->desc.d_model; a.ld = p->desc.d_model;
   a.x = p->xd; a.ldx = p->ld_xd; a.ssq = p->ssq; a.xo = p->xh; a.ldxo = p->ld_xh;
+  if (p->shared) a.sv = store_view(p, l, 3);
   return a;
 }
 
@@ -545,6 +597,7 @@ tasp::MfmaArgs down_mm_args(const tasp_plan_s* p, int l, int B, float* y) {
   a.x = p->xh; a.ldx = p->ld_xh; a.resid = p->r_mid; a.y = y; a.ldy = d.d_model;
   a.gamma_next = (l + 1 < d.n_layers) ? p->layers[l + 1].an : (d.vocab ? p->final_norm : nullptr);
   a.xo = p->xd; a.ldxo = p->ld_xd; a.ssq_out = p->ssq;
+  if (p->shared) a.sv = store_view(p, l, 4);
   return a;
 }
 
@@ -565,6 +618,7 @@ tasp_status decode_batched(tasp_plan p, const float* x, tasp_kv_cache* cache, in
       tasp::MfmaArgs a = mm_base(p, B);
       a.w = P.qkv; a.scale = P.s_qkv; a.N = P.n_qkv; a.K = D; a.ld = D;
       a.x = p->xd; a.ldx = p->ld_xd; a.ssq = p->ssq; a.y = p->qkv_buf; a.ldy = p->ld_qkv;
+      if (p->shared) a.sv = store_view(p, l, 0);
       if ((st = run_kernel(tm, 0, s, [&] { return tasp::launch_mfma_gemv(tasp::MM_QKV, a, s); })))
         return st;
     }
@@ -577,6 +631,7 @@ tasp_status decode_batched(tasp_plan p, const float* x, tasp_kv_cache* cache, in
       a.w = P.o; a.scale = P.s_o; a.N = D; a.K = P.m_q * dh; a.ld = P.ld_o;
       a.x = p->xo; a.ldx = p->ld_xo; a.resid = in; a.y = p->r_mid; a.ldy = D;
       a.gamma_next = P.fn; a.xo = p->xd; a.ldxo = p->ld_xd; a.ssq_out = p->ssq;
+      if (p->shared) a.sv = store_view(p, l, 1);
       if ((st = run_kernel(tm, 2, s, [&] { return tasp::launch_mfma_gemv(tasp::MM_RESID, a, s); })))
         return st;
     }
@@ -639,6 +694,7 @@ tasp_status prefill_impl(tasp_plan p, const float* x, int T, tasp_kv_cache* cach
       a.w = P.qkv; a.scale = P.s_qkv; a.N = P.n_qkv; a.K = D; a.ld = D;
       a.x = p->pxd; a.ldx = p->ld_xd; a.plane = plane_d; a.ssq = p->pssq;
       a.y = p->pqkv; a.ldy = p->ld_qkv;
+      if (p->shared) a.sv = store_view(p, l, 0);
       if ((st = run_kernel(tm, 0, s, [&] { return tasp::launch_pf_gemm(tasp::MM_QKV, a, s); })))
         return st;
     }
@@ -662,12 +718,18 @@ tasp_status prefill_impl(tasp_plan p, const float* x, int T, tasp_kv_cache* cach
       a.w = P.o; a.scale = P.s_o; a.N = D; a.K = P.m_q * dh; a.ld = P.ld_o;
       a.x = p->pxw; a.ldx = p->ld_xw; a.plane = plane_w; a.resid = in; a.y = p->pr_mid; a.ldy = D;
       a.gamma_next = P.fn; a.xo = p->pxd; a.ldxo = p->ld_xd; a.plane_o = plane_d; a.ssq_out = p->pssq;
+      if (p->shared) a.sv = store_view(p, l, 1);
       if ((st = run_kernel(tm, 2, s, [&] { return tasp::launch_pf_gemm(tasp::MM_RESID, a, s); })))
         return st;
     }
     if (P.c > 0) {
       tasp::PfArgs a = pf_base(p, T);
-      a.w = P.g; a.w2_off = uint32_t(reinterpret_cast<const char*>(P.u) - reinterpret_cast<const char*>(P.g));
+      if (p->shared) {
+        a.sv = store_view(p, l, 3);
+      } else {
+        a.w = P.g;
+        a.w2_off = uint32_t(reinterpret_cast<const char*>(P.u) - reinterpret_cast<const char*>(P.g));
+      }
       a.scale = P.s_g; a.scale2 = P.s_u; a.N = P.c; a.K = D; a.ld = D;
       a.x = p->pxd; a.ldx = p->ld_xd; a.plane = plane_d; a.ssq = p->pssq;
       a.xo = p->pxw; a.ldxo = p->ld_xw; a.plane_o = plane_w;
@@ -678,6 +740,7 @@ tasp_status prefill_impl(tasp_plan p, const float* x, int T, tasp_kv_cache* cach
       tasp::PfArgs a = pf_base(p, T);
       a.w = P.dn; a.scale = P.s_d; a.N = D; a.K = P.c; a.ld = P.ld_d;
       a.x = p->pxw; a.ldx = p->ld_xw; a.plane = plane_w; a.resid = p->pr_mid; a.y = lo; a.ldy = D;
+      if (p->shared) a.sv = store_view(p, l, 4);
       a.gamma_next = (l + 1 < L) ? p->layers[l + 1].an : (d.vocab ? p->final_norm : nullptr);
       a.xo = p->pxd; a.ldxo = p->ld_xd; a.plane_o = plane_d; a.ssq_out = p->pssq;
       if ((st = run_kernel(tm, 4, s, [&] { return tasp::launch_pf_gemm(tasp::MM_RESID, a, s); })))
@@ -917,14 +980,11 @@ uint64_t store_identity(const tasp_gstore& st, int n_layers) {
   return hash_ptrs(h, {st.final_norm, st.lm_head});
 }
 
-// A shared-store plan decodes one sequence: its scale groups of 128 must tile every input
-// dimension, and its widest GEMV input (with the piece sums and the column map) must fit LDS.
+// A shared-store plan: its scale groups of 128 must tile every input dimension, and its widest
+// batch-1 GEMV input (with the piece sums and the column map) must fit LDS.
 tasp_status check_shared_desc(const tasp_model_desc* d) {
   tasp_status st = check_desc(d);
   if (st != TASP_OK) return st;
-  if (d->max_batch != 1 || d->max_prefill != 0)
-    return fail(TASP_ERR_UNSUPPORTED, "shared-store plans decode one sequence (max_batch 1, "
-                "max_prefill 0)");
   if (d->d_model % 128 || (d->n_q_heads * d->head_dim) % 128 || d->d_ffn % 128)
     return fail(TASP_ERR_SHAPE, "the groupwise store needs d_model, n_q_heads*head_dim and d_ffn "
                 "divisible by 128");
@@ -1124,31 +1184,7 @@ tasp_status tasp_compile_plan(const tasp_model_desc* desc, const tasp_store* sto
   hipError_t h = hipMemcpyAsync(p->rope_cos, tc.data(), tc.size() * 4, hipMemcpyHostToDevice, s);
   if (h == hipSuccess) h = hipMemcpyAsync(p->rope_sin, ts.data(), ts.size() * 4, hipMemcpyHostToDevice, s);
   if (h == hipSuccess) h = tasp::launch_fill_zero(at(Y.zero_begin), Y.zero_end - Y.zero_begin, s);
-  p->r_mid = reinterpret_cast<float*>(at(Y.r_mid));
-  p->r_io[0] = reinterpret_cast<float*>(at(Y.r_io0));
-  p->r_io[1] = reinterpret_cast<float*>(at(Y.r_io1));
-  p->qkv_buf = reinterpret_cast<float*>(at(Y.qkv_buf));
-  p->o_buf = reinterpret_cast<float*>(at(Y.o_buf));
-  p->h_buf = reinterpret_cast<float*>(at(Y.h_buf));
-  p->part = reinterpret_cast<float*>(at(Y.part));
-  p->acnt = reinterpret_cast<int*>(at(Y.acnt));
-  p->n_split_max = Y.n_split_max; p->ld_qkv = Y.ld_qkv; p->ld_obuf = Y.ld_obuf; p->ld_h = Y.ld_h;
-  p->xd = reinterpret_cast<uint16_t*>(at(Y.xd));
-  p->xo = reinterpret_cast<uint16_t*>(at(Y.xo));
-  p->xh = reinterpret_cast<uint16_t*>(at(Y.xh));
-  p->ssq = reinterpret_cast<float*>(at(Y.ssq));
-  p->ld_xd = Y.ld_xd; p->ld_xo = Y.ld_xo; p->ld_xh = Y.ld_xh;
-  p->pxd = reinterpret_cast<uint16_t*>(at(Y.pxd));
-  p->pxw = reinterpret_cast<uint16_t*>(at(Y.pxw));
-  p->pq = reinterpret_cast<uint16_t*>(at(Y.pq));
-  p->pqkv = reinterpret_cast<float*>(at(Y.pqkv));
-  p->pr_mid = reinterpret_cast<float*>(at(Y.pr_mid));
-  p->pr_io[0] = reinterpret_cast<float*>(at(Y.pr_io0));
-  p->pr_io[1] = reinterpret_cast<float*>(at(Y.pr_io1));
-  p->pssq = reinterpret_cast<float*>(at(Y.pssq));
-  p->ppart = reinterpret_cast<float*>(at(Y.ppart));
-  p->ppart_floats = Y.ppart_floats;
-  p->ld_xw = Y.ld_xw;
+  set_scratch(p, Y, ws);
 
   {
     const tasp_status rb = read_back_indices(p, c, Y, ws, s, h);
@@ -1286,19 +1322,7 @@ tasp_status tasp_compile_shared_plan(const tasp_model_desc* desc, const tasp_gst
   hipError_t h = hipMemcpyAsync(p->rope_cos, tc.data(), tc.size() * 4, hipMemcpyHostToDevice, s);
   if (h == hipSuccess) h = hipMemcpyAsync(p->rope_sin, ts.data(), ts.size() * 4, hipMemcpyHostToDevice, s);
   if (h == hipSuccess) h = tasp::launch_fill_zero(at(Y.zero_begin), Y.zero_end - Y.zero_begin, s);
-  p->r_mid = reinterpret_cast<float*>(at(Y.r_mid));
-  p->r_io[0] = reinterpret_cast<float*>(at(Y.r_io0));
-  p->r_io[1] = reinterpret_cast<float*>(at(Y.r_io1));
-  p->qkv_buf = reinterpret_cast<float*>(at(Y.qkv_buf));
-  p->o_buf = reinterpret_cast<float*>(at(Y.o_buf));
-  p->h_buf = reinterpret_cast<float*>(at(Y.h_buf));
-  p->part = reinterpret_cast<float*>(at(Y.part));
-  p->acnt = reinterpret_cast<int*>(at(Y.acnt));
-  p->n_split_max = Y.n_split_max; p->ld_qkv = Y.ld_qkv; p->ld_obuf = Y.ld_obuf; p->ld_h = Y.ld_h;
-  p->xd = p->xo = p->xh = p->pxd = p->pxw = p->pq = nullptr;
-  p->ssq = p->pqkv = p->pr_mid = p->pr_io[0] = p->pr_io[1] = p->pssq = p->ppart = nullptr;
-  p->ppart_floats = 0;
-  p->ld_xd = p->ld_xo = p->ld_xh = p->ld_xw = 0;
+  set_scratch(p, Y, ws);
   if ((st = read_back_indices(p, c, Y, ws, s, h)) != TASP_OK) {
     delete p;
     return st;
@@ -1507,10 +1531,10 @@ tasp_status tasp_profile_stage(const tasp_plan* plans, const tasp_kv_cache* cach
       Item it{};
       it.plan = i;
       it.layer = l;
-      it.shared = p->shared;
+      it.shared = p->shared && batch == 1;
       if (kind == 1)
         it.at = attn_args(p, l, &caches[i], pos, batch, batch > 1);
-      else if (p->shared)
+      else if (p->shared && batch == 1)
         it.sg = (kind == 3) ? shared_gateup_args(p, l) : shared_down_args(p, l, p->r_io[l & 1]);
       else if (batch == 1)
         it.g = (kind == 3) ? gateup_args(p, l, batch) : down_args(p, l, batch, p->r_io[l & 1]);

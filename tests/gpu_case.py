@@ -79,11 +79,13 @@ class PrefillCase:
     cache, everything else NaN until the prefill writes it), with the oracle's result."""
 
     def __init__(self, sh, mask, T, pos0, max_seq=None, max_prefill=None, seed_w=0, seed_x=3,
-                 seed_kv=2, store=None, device="cuda", lm=None):
+                 seed_kv=2, store=None, device="cuda", lm=None, shared=False):
+        """shared: a groupwise store (BF16 scales per 128 inputs) and a shared-store plan."""
         self.sh, self.T, self.pos0 = sh, T, pos0
         self.max_seq = max_seq or pos0 + T
         self.mask = mask
-        self.store = store if store is not None else [synth.layer_weights(sh, l, seed_w)
+        quant = "group" if shared else "row"
+        self.store = store if store is not None else [synth.layer_weights(sh, l, seed_w, quant=quant)
                                                       for l in range(sh.n_layers)]
         pre = lm
         lm = sh.vocab > 0
@@ -95,8 +97,12 @@ class PrefillCase:
         self.x = synth.activations(T, sh.d_model, seed_x)
         self.desc = S.desc_from_shape(sh, max_batch=1, max_seq=self.max_seq,
                                       max_prefill=max_prefill or T)
-        self.dstore = S.DeviceStore(self.store, self.final_norm, self.lm_head, device)
-        self.plan = S.Plan(self.desc, self.dstore, mask)
+        if shared:
+            self.dstore = S.GroupStore(self.store, self.final_norm, self.lm_head, device)
+            self.plan = S.Plan.shared(self.desc, self.dstore, mask)
+        else:
+            self.dstore = S.DeviceStore(self.store, self.final_norm, self.lm_head, device)
+            self.plan = S.Plan(self.desc, self.dstore, mask)
         torch.cuda.synchronize()
         self.priors = [synth.kv_prior(sh, l, 1, pos0, self.max_seq, seed_kv)
                        for l in range(sh.n_layers)]

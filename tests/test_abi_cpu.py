@@ -191,15 +191,17 @@ def test_router_workspace_and_argument_checks():
 
 
 def test_shared_plan_host_checks():
-    """Shared-store plans: mask-independent workspace, one-sequence descs, 128-divisible widths,
-    and retained channels in aligned blocks of 16; all rejected before any GPU work."""
+    """Shared-store plans: mask-independent workspace that grows with the batch and prefill
+    scratch, 128-divisible widths, and retained channels in aligned blocks of 16; all rejected
+    before any GPU work."""
     _lib()
     d = _desc(d_model=512, d_ffn=1536, max_batch=1)
     n = B.tasp_shared_plan_workspace_bytes(d)
     assert n > 0 and n < B.tasp_plan_workspace_bytes(d, None)
-    for bad, status in ((dict(max_batch=2), "TASP_ERR_UNSUPPORTED"),
-                        (dict(max_prefill=16), "TASP_ERR_UNSUPPORTED"),
-                        (dict(d_model=528), "TASP_ERR_SHAPE"),
+    big = _desc(d_model=512, d_ffn=1536, max_batch=4, max_prefill=64)
+    nb = B.tasp_shared_plan_workspace_bytes(big)
+    assert n < nb < B.tasp_plan_workspace_bytes(big, None)
+    for bad, status in ((dict(d_model=528), "TASP_ERR_SHAPE"),
                         (dict(d_ffn=1552), "TASP_ERR_SHAPE")):
         with pytest.raises(B.TaspError) as e:
             B.tasp_shared_plan_workspace_bytes(_desc(**{**dict(d_model=512, d_ffn=1536, max_batch=1), **bad}))

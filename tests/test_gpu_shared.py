@@ -10,8 +10,9 @@ import torch
 import synth
 from paper_2609_29499_amd import binding as B
 from paper_2609_29499_amd import session as S
-from tests.gpu_case import Case
-from tests.helpers import assert_parity
+from oracle import reference as ref
+from tests.gpu_case import Case, PrefillCase
+from tests.helpers import assert_parity, check_greedy_ids, teacher_forced_rows
 
 pytestmark = pytest.mark.gpu
 
@@ -137,9 +138,6 @@ def test_shared_plan_rejections():
     with pytest.raises(B.TaspError, match="UNSUPPORTED"):
         plan.panel(0, B.PANEL_QKV)
     cache = S.KVCache(desc, 1, 64)
-    x = torch.zeros((4, sh.d_model), device="cuda")
-    with pytest.raises(B.TaspError, match="UNSUPPORTED"):
-        plan.prefill(x, 4, cache, 0, torch.empty((4, sh.d_model), device="cuda"))
     # a cache filled under the per-row plan of the same mask is refused
     mat = S.Plan(desc, S.DeviceStore([synth.layer_weights(sh, 0)]), synth.raw_mask(sh, 1, block=16))
     mat.bind(cache)
@@ -197,5 +195,151 @@ def test_one_store_validation_greedy_decode():
             agree += int(np.argmax(a) == np.argmax(b))
             total += 1
             tok = int(np.argmax(a))
+    assert worst < 2e-3, worst
+    assert agree / total >= 0.9998, (agree, total)
+
+
+# ---- prefill and batched decode from the shared store (matrix cores: each weight times its
+# group scale split exactly into BF16 hi and lo parts)
+
+
+@pytest.mark.parametrize("batch,pos", [(2, 0), (5, 77), (8, 130)])
+def test_batched_decode(batch, pos):
+    _flush(f"case shared batched decode B={batch} pos={pos}")
+    sh = synth.tiny_shape(layers=2, **TINY)
+    _check(Case(sh, synth.raw_mask(sh, 40 + batch, block=16), batch, pos, shared=True))
+
+
+def test_batched_decode_head_dim_128_and_empty_modules():
+    _flush("case shared batched decode dh128 / empty modules")
+    sh = synth.tiny_shape(d=512, hq=8, hkv=2, dh=128, f=1024, layers=1)
+    _check(Case(sh, synth.raw_mask(sh, 5, block=16), 3, 129, shared=True))
+    sh = synth.tiny_shape(layers=2, **TINY)
+    q, kv, f = synth.all_kept_mask(sh)
+    q[0, :] = 0
+    f[1, :] = 0
+    _check(Case(sh, (q, kv, f), 4, 33, shared=True))
+
+
+@pytest.mark.parametrize("T,pos0", [(77, 0), (40, 33), (1, 5)])
+def test_prefill(T, pos0):
+    _flush(f"case shared prefill T={T} pos0={pos0}")
+    sh = synth.tiny_shape(layers=2, **TINY)
+    case = PrefillCase(sh, synth.raw_mask(sh, 50 + T, block=16), T, pos0, shared=True)
+    got, want = case.run(), case.oracle()
+    m, s_ = assert_parity(got, want, what="shared prefill")
+    _flush(f"  max_rel={m:.2e} sum_rel={s_:.2e}")
+
+
+def test_prefill_head_dim_128_empty_modules_and_lm_head():
+    _flush("case shared prefill dh128 / empty / lm head")
+    sh = synth.tiny_shape(d=512, hq=8, hkv=2, dh=128, f=1024, layers=1)
+    case = PrefillCase(sh, synth.raw_mask(sh, 7, block=16), 130, 0, shared=True)
+    assert_parity(case.run(), case.oracle(), what="shared prefill dh128")
+    sh = synth.tiny_shape(layers=2, **TINY)
+    q, kv, f = synth.all_kept_mask(sh)
+    q[1, :] = 0
+    f[0, :] = 0
+    case = PrefillCase(sh, (q, kv, f), 20, 0, shared=True)
+    assert_parity(case.run(), case.oracle(), what="shared prefill empty modules")
+    sh = synth.tiny_shape(layers=3, vocab=3000, **TINY)
+    case = PrefillCase(sh, synth.raw_mask(sh, 8, block=16), 9, 0, shared=True)
+    got, want = case.run(), case.oracle()
+    assert_parity(got, want, what="shared prefill logits")
+    check_greedy_ids(got.argmax(axis=1), want, "shared prefill")
+
+
+@pytest.mark.timeout(600)
+def test_llama3_8b_layer_prefill_and_batch8():
+    """Full Llama-3-8B layer from the groupwise store under the seed-1 budget mask: a 512-token
+    prefill, and decode of 8 sequences at 2048 prior positions."""
+    sh = synth.LLAMA3_8B.with_layers(1, vocab=0)
+    store = [synth.layer_weights(sh, 0, quant="group")]
+    mask = synth.budget_mask(sh, 1)
+    _flush("case shared 8B prefill 512")
+    case = PrefillCase(sh, mask, 512, 0, store=store, shared=True)
+    m, s_ = assert_parity(case.run(), case.oracle(), what="shared 8B prefill")
+    _flush(f"  max_rel={m:.2e} sum_rel={s_:.2e}")
+    del case
+    torch.cuda.empty_cache()
+    _flush("case shared 8B batch 8")
+    m, s_ = _check(Case(sh, mask, 8, 2048, store=store, shared=True))
+    _flush(f"  max_rel={m:.2e} sum_rel={s_:.2e}")
+
+
+def test_generate_on_shared_plan():
+    """tasp_generate on a shared-store plan (prefill + greedy decode from the one store),
+    teacher-forced against the oracle."""
+    _flush("case shared generate")
+    sh = synth.tiny_shape(layers=3, vocab=3000, **TINY)
+    layers = [synth.layer_weights(sh, l, quant="group") for l in range(sh.n_layers)]
+    fn, lm = synth.final_norm(sh), synth.lm_head(sh)
+    table, scales = synth.embedding(sh)
+    T, n_new = 24, 10
+    prompt = synth.prompt_ids(T, sh.vocab, seed=12)
+    mask = synth.raw_mask(sh, 9, block=16)
+    desc = S.desc_from_shape(sh, max_batch=1, max_seq=T + n_new, max_prefill=T)
+    plan = S.Plan.shared(desc, S.GroupStore(layers, fn, lm), mask)
+    cache = S.KVCache(desc, 1, T + n_new)
+    scratch = (torch.empty((T, sh.d_model), device="cuda"), torch.empty((T, sh.vocab), device="cuda"))
+    ids = plan.generate(torch.from_numpy(table).cuda(), torch.from_numpy(scales).cuda(),
+                        torch.from_numpy(prompt).cuda(), n_new, cache, scratch=scratch)
+    torch.cuda.synchronize()
+    got = ids.cpu().numpy()
+    last = scratch[1][0].cpu().numpy().astype(np.float64)
+    closed = ref.close_mask(*mask, sh.group_size)
+    rows = teacher_forced_rows(lambda l: layers[l], closed, table, scales, prompt, got, sh, fn, lm)
+    check_greedy_ids(got, rows, "shared generate")
+    assert_parity(last, rows[-1], what="shared generate last logits")
+
+
+def test_one_store_validation_prefill_and_batches():
+    """The one-store validation with prefill and batched decode: shared-store vs materialised
+    plans (identical quantisation) over a 32-token prefill (logits of every position) and 16
+    teacher-forced decode steps of 4 sequences: max |logit difference| < 2e-3 and >= 99.98 %
+    greedy agreement."""
+    _flush("case one-store validation prefill + batches")
+    sh = synth.tiny_shape(layers=3, vocab=4000, **TINY)
+    rows, groups = _equal_scale_stores(sh)
+    fn, lm = synth.final_norm(sh), synth.lm_head(sh)
+    table, scales = synth.embedding(sh)
+    T, steps, Bt = 32, 16, 4
+    desc = S.desc_from_shape(sh, max_batch=Bt, max_seq=T + steps, max_prefill=T)
+    mstore, gstore = S.DeviceStore(rows, fn, lm), S.GroupStore(groups, fn, lm)
+    emb = lambda ids: torch.from_numpy(  # noqa: E731
+        (table[np.asarray(ids)].astype(np.float32) * scales[np.asarray(ids), None]).astype(np.float32)).cuda()
+    worst, agree, total = 0.0, 0, 0
+    for seed in (31, 32):
+        mask = synth.raw_mask(sh, seed, block=16)
+        pm, ps = S.Plan(desc, mstore, mask), S.Plan.shared(desc, gstore, mask)
+        # prefill of one sequence
+        prompt = synth.prompt_ids(T, sh.vocab, seed=seed)
+        outs = []
+        for plan in (pm, ps):
+            c1 = S.KVCache(desc, 1, T + steps)
+            o = torch.empty((T, sh.vocab), device="cuda")
+            plan.prefill(emb(prompt), T, c1, 0, o)
+            outs.append(o.cpu().numpy())
+        worst = max(worst, float(np.abs(outs[0] - outs[1]).max()))
+        agree += int((outs[0].argmax(1) == outs[1].argmax(1)).sum())
+        total += T
+        # batched decode of Bt sequences from position 0, teacher-forced on the materialised ids
+        cm, cs = S.KVCache(desc, Bt, T + steps), S.KVCache(desc, Bt, T + steps)
+        pm.bind(cm)
+        ps.bind(cs)
+        toks = [7, 11, 13, 17]
+        om = torch.empty((Bt, sh.vocab), device="cuda")
+        os_ = torch.empty((Bt, sh.vocab), device="cuda")
+        for pos in range(steps):
+            x = emb(toks)
+            pm.decode(x, cm, pos, om)
+            ps.decode(x, cs, pos, os_)
+            torch.cuda.synchronize()
+            a, b = om.cpu().numpy(), os_.cpu().numpy()
+            assert np.all(np.isfinite(b))
+            worst = max(worst, float(np.abs(a - b).max()))
+            agree += int((a.argmax(1) == b.argmax(1)).sum())
+            total += Bt
+            toks = [int(v) for v in a.argmax(1)]
     assert worst < 2e-3, worst
     assert agree / total >= 0.9998, (agree, total)
