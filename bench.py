@@ -796,29 +796,35 @@ def bench_mask(args, wl):
 
 
 def shared_ledger(S, B, sh, seeds):
-    """Device bytes of the store and of 1 .. len(seeds) plans in both formats, from the
-    library's workspace queries (no allocation): a shared-store plan adds its fixed metadata
-    and scratch; a materialised plan holds its own panels (its store can be freed)."""
+    """Device bytes at the paper's request shape (2,048-token prefill + 256 decode steps, batch
+    1) from the library's workspace queries (no allocation): the groupwise store, 1 .. len(seeds)
+    shared-store plans (fixed metadata each) over one scratch arena and the KV cache, against
+    materialised plans (each holds its own panels and scratch; their store can be freed)."""
     import synth
     d, dh, F = sh.d_model, sh.head_dim, sh.d_ffn
     per_layer = ((sh.n_q_heads + 2 * sh.n_kv_heads) * dh * d + d * sh.n_q_heads * dh + 3 * F * d)
     weights = sh.n_layers * per_layer
     scales = weights // 128 * 2
     gains = sh.n_layers * 2 * d * 2 + (d * 2 + sh.vocab * d * 2 if sh.vocab else 0)
-    desc = S.desc_from_shape(sh, max_batch=1, max_seq=4096)
-    ws_shared = B.tasp_shared_plan_workspace_bytes(desc)
+    S_ = 2048 + 256
+    desc = S.desc_from_shape(sh, max_batch=1, max_seq=S_, max_prefill=2048)
+    plan_b, arena_b = B.tasp_shared_plan_workspace_bytes(desc)
+    kv = 2 * sh.n_layers * sh.n_kv_heads * S_ * dh * 2
     mats = []
     for sd in seeds:
         mptr, keep = S.mask_struct(synth.budget_mask(sh, sd))
         mats.append(B.tasp_plan_workspace_bytes(desc, mptr))
     rows = []
     for n in (1, 3, len(seeds)):
-        rows.append({"masks": n, "shared_GB": round((weights + scales + gains + n * ws_shared) / 1e9, 3),
-                     "shared_metadata_GB": round(n * ws_shared / 1e9, 4),
-                     "materialised_GB": round(sum(mats[:n]) / 1e9, 3)})
+        rows.append({"masks": n,
+                     "shared_GB": round((weights + scales + gains + n * plan_b + arena_b + kv) / 1e9, 3),
+                     "shared_metadata_GB": round(n * plan_b / 1e9, 4),
+                     "materialised_GB": round((sum(mats[:n]) + kv) / 1e9, 3)})
     return {"store_weight_GB": round(weights / 1e9, 3), "store_scale_GB": round(scales / 1e9, 3),
-            "plan_workspace_MB": round(ws_shared / 1e6, 2), "by_masks": rows,
-            "note": "workspaces include the RoPE table and decode scratch at max_seq 4096"}
+            "gains_and_lm_head_GB": round(gains / 1e9, 3), "kv_cache_GB": round(kv / 1e9, 3),
+            "plan_MB": round(plan_b / 1e6, 2), "shared_scratch_arena_MB": round(arena_b / 1e6, 1),
+            "by_masks": rows,
+            "note": "max_seq 2304, max_prefill 2048, batch 1; every shared plan uses one scratch arena"}
 
 
 def bench_shared(args, wl):
@@ -902,7 +908,7 @@ def bench_shared(args, wl):
                      "traffic": None, "algorithmic_bytes": gu_bytes,
                      "avg_launch_us": round(sp["stage_ms"] * 1e3, 3)},
         "memory": {"layer_store_MB": round(store_bytes / 1e6, 1),
-                   "shared_plan_workspace_MB": round(B.tasp_shared_plan_workspace_bytes(desc) / 1e6, 3),
+                   "shared_plan_workspace_MB": round(sum(B.tasp_shared_plan_workspace_bytes(desc)) / 1e6, 3),
                    "materialised_plan_workspace_MB": round(mat_ws / 1e6, 1),
                    "llama3_8b": shared_ledger(S, B, synth.LLAMA3_8B, (1, 2, 3, 4, 5)),
                    "llama3_70b": shared_ledger(S, B, synth.LLAMA3_70B, (1, 2, 3, 4, 5))},

@@ -167,10 +167,14 @@ typedef struct {
   const uint16_t* lm_head;
 } tasp_gstore;
 
-/* Workspace bytes of a shared-store plan: masks, index lists, the maps into the store, the RoPE
- * table and the decode (max_batch sequences) and prefill (max_prefill tokens) scratch; the same
- * for every mask. d_model, n_q_heads * head_dim and d_ffn must be divisible by 128. */
-tasp_status tasp_shared_plan_workspace_bytes(const tasp_model_desc* desc, size_t* bytes);
+/* Bytes of a shared-store plan (paper, appendix "Backing-store semantics": a plan over the one
+ * store is block-selection and launch metadata). *plan_bytes: masks, index lists, the maps into
+ * the store and the RoPE table, the same for every mask. *scratch_bytes: the decode (max_batch
+ * sequences) and prefill (max_prefill tokens) scratch, which any number of shared plans of equal
+ * scratch size may share (see tasp_compile_shared_plan). d_model, n_q_heads * head_dim and d_ffn
+ * must be divisible by 128. */
+tasp_status tasp_shared_plan_workspace_bytes(const tasp_model_desc* desc, size_t* plan_bytes,
+                                             size_t* scratch_bytes);
 
 /* Compile a plan over the shared store: closes the mask (as tasp_compile_plan), builds on the
  * device the maps from plan rows / column pieces to store rows / columns (QKV rows of the
@@ -183,10 +187,16 @@ tasp_status tasp_shared_plan_workspace_bytes(const tasp_model_desc* desc, size_t
  * matrix cores with each weight times its group scale split exactly into BF16 hi and lo parts;
  * only tasp_plan_panel returns TASP_ERR_UNSUPPORTED (there are no panels). Its signature differs
  * from a per-row plan of the same mask, so caches are not shared between the two formats.
- * Synchronises `stream`. */
+ * `workspace` (256-byte aligned, plan_bytes) holds the plan's metadata. `scratch` (256-byte
+ * aligned, scratch_bytes) is its scratch arena and may be passed to several shared plans: their
+ * calls, and this compile (it clears the arena's counters), must then be ordered one after
+ * another (one stream, or synchronised streams); overlapping calls race. With scratch NULL the
+ * arena is the workspace's tail (workspace_bytes >= plan_bytes + scratch_bytes). Both buffers stay
+ * owned by the caller and must outlive the plan. Synchronises `stream`. */
 tasp_status tasp_compile_shared_plan(const tasp_model_desc* desc, const tasp_gstore* store,
                                      const tasp_mask* mask, void* workspace,
-                                     size_t workspace_bytes, void* stream, tasp_plan* out);
+                                     size_t workspace_bytes, void* scratch, size_t scratch_bytes,
+                                     void* stream, tasp_plan* out);
 
 /* Retained counts of one layer after closure (paper, Eqs. flop-attn and flop-mlp: m^q, m^kv and
  * c of that layer): query heads, KV groups, SwiGLU channels, written to host int32s.

@@ -110,9 +110,9 @@ def load(path: str = LIB_PATH):
         "tasp_plan_workspace_bytes": [C.POINTER(tasp_model_desc), C.POINTER(tasp_mask), C.POINTER(SZ)],
         "tasp_compile_plan": [C.POINTER(tasp_model_desc), C.POINTER(tasp_store), C.POINTER(tasp_mask),
                               P, SZ, P, C.POINTER(P)],
-        "tasp_shared_plan_workspace_bytes": [C.POINTER(tasp_model_desc), C.POINTER(SZ)],
+        "tasp_shared_plan_workspace_bytes": [C.POINTER(tasp_model_desc), C.POINTER(SZ), C.POINTER(SZ)],
         "tasp_compile_shared_plan": [C.POINTER(tasp_model_desc), C.POINTER(tasp_gstore),
-                                     C.POINTER(tasp_mask), P, SZ, P, C.POINTER(P)],
+                                     C.POINTER(tasp_mask), P, SZ, P, SZ, P, C.POINTER(P)],
         "tasp_plan_counts": [P, I32, C.POINTER(I32), C.POINTER(I32), C.POINTER(I32)],
         "tasp_plan_indices": [P, I32, I32, C.POINTER(I32), I32, C.POINTER(I32)],
         "tasp_plan_panel": [P, I32, I32, C.POINTER(P), C.POINTER(P), C.POINTER(C.c_int64),
@@ -174,15 +174,18 @@ def tasp_compile_plan(desc, store, mask, workspace_ptr, workspace_bytes, stream)
 
 
 def tasp_shared_plan_workspace_bytes(desc):
-    n = C.c_size_t()
-    _check(load().tasp_shared_plan_workspace_bytes(C.byref(desc), C.byref(n)))
-    return n.value
+    """(plan_bytes, scratch_bytes)."""
+    n, m = C.c_size_t(), C.c_size_t()
+    _check(load().tasp_shared_plan_workspace_bytes(C.byref(desc), C.byref(n), C.byref(m)))
+    return n.value, m.value
 
 
-def tasp_compile_shared_plan(desc, store, mask, workspace_ptr, workspace_bytes, stream):
+def tasp_compile_shared_plan(desc, store, mask, workspace_ptr, workspace_bytes, scratch_ptr,
+                             scratch_bytes, stream):
     out = C.c_void_p()
     _check(load().tasp_compile_shared_plan(C.byref(desc), C.byref(store), mask, workspace_ptr,
-                                           workspace_bytes, stream, C.byref(out)))
+                                           workspace_bytes, scratch_ptr, scratch_bytes, stream,
+                                           C.byref(out)))
     return out
 
 

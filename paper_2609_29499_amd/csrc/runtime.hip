@@ -148,6 +148,7 @@ struct Layout {
   size_t qkv_rows, o_cols, down_cols;                        // shared-store plans: maps
   size_t zero_begin, zero_end;       // scratch cleared at compile
   size_t total;
+  size_t scratch_total = 0;          // shared-store plans: bytes of the separate scratch arena
   int n_split_max, ld_qkv, ld_obuf, ld_h, ld_xd, ld_xo, ld_xh, ld_xw;
 };
 
@@ -245,8 +246,9 @@ Layout make_layout(const tasp_model_desc* d, const Closed& c) {
   return Y;
 }
 
-// A shared-store plan holds no weights: masks and index lists, the maps into the store, the
-// RoPE table and the decode / prefill scratch. Its size does not depend on the mask.
+// A shared-store plan holds no weights: masks and index lists, the maps into the store and the
+// RoPE table (Y.total bytes, the same for every mask). Its decode / prefill scratch is a separate
+// arena of Y.scratch_total bytes (offsets relative to the arena) that plans may share.
 Layout make_shared_layout(const tasp_model_desc* d) {
   Layout Y{};
   size_t off = 0;
@@ -271,8 +273,15 @@ Layout make_shared_layout(const tasp_model_desc* d) {
   Y.down_cols = take(size_t(L) * (F / 16) * 4);
   Y.rope_cos = take(size_t(d->max_seq) * (dh / 2) * 4);
   Y.rope_sin = take(size_t(d->max_seq) * (dh / 2) * 4);
-  scratch_layout(Y, d, take, off);
   Y.total = off;
+  size_t soff = 0;
+  auto stake = [&](size_t bytes) {
+    const size_t at = soff;
+    soff = align_up(soff + bytes, kAlign);
+    return at;
+  };
+  scratch_layout(Y, d, stake, soff);
+  Y.scratch_total = soff;
   return Y;
 }
 
@@ -1211,23 +1220,27 @@ tasp_status tasp_compile_plan(const tasp_model_desc* desc, const tasp_store* sto
   return TASP_OK;
 }
 
-tasp_status tasp_shared_plan_workspace_bytes(const tasp_model_desc* desc, size_t* bytes) {
-  if (!bytes) return fail(TASP_ERR_INVALID_ARG, "bytes is NULL");
+tasp_status tasp_shared_plan_workspace_bytes(const tasp_model_desc* desc, size_t* plan_bytes,
+                                             size_t* scratch_bytes) {
+  if (!plan_bytes || !scratch_bytes) return fail(TASP_ERR_INVALID_ARG, "plan_bytes / scratch_bytes is NULL");
   tasp_status st = check_shared_desc(desc);
   if (st != TASP_OK) return st;
-  *bytes = make_shared_layout(desc).total;
+  const Layout Y = make_shared_layout(desc);
+  *plan_bytes = Y.total;
+  *scratch_bytes = Y.scratch_total;
   return TASP_OK;
 }
 
 tasp_status tasp_compile_shared_plan(const tasp_model_desc* desc, const tasp_gstore* store,
                                      const tasp_mask* mask, void* workspace,
-                                     size_t workspace_bytes, void* stream, tasp_plan* out) {
+                                     size_t workspace_bytes, void* scratch, size_t scratch_bytes,
+                                     void* stream, tasp_plan* out) {
   tasp_status st = check_shared_desc(desc);
   if (st != TASP_OK) return st;
   if (!store || !store->layers || !out) return fail(TASP_ERR_INVALID_ARG, "store / out is NULL");
   if (!workspace) return fail(TASP_ERR_INVALID_ARG, "workspace is NULL");
-  if (reinterpret_cast<uintptr_t>(workspace) % kAlign)
-    return fail(TASP_ERR_WORKSPACE, "workspace not %zu-byte aligned", kAlign);
+  if (reinterpret_cast<uintptr_t>(workspace) % kAlign || reinterpret_cast<uintptr_t>(scratch) % kAlign)
+    return fail(TASP_ERR_WORKSPACE, "workspace / scratch not %zu-byte aligned", kAlign);
   const tasp_model_desc& d = *desc;
   for (int l = 0; l < d.n_layers; ++l) {
     const tasp_glayer& S = store->layers[l];
@@ -1253,9 +1266,14 @@ tasp_status tasp_compile_shared_plan(const tasp_model_desc* desc, const tasp_gst
                       "layer %d: channels %d..%d are partly retained (shared-store plans keep "
                       "channels in aligned blocks of 16)", l, j0, j0 + 15);
   const Layout Y = make_shared_layout(desc);
-  if (workspace_bytes < Y.total)
-    return fail(TASP_ERR_WORKSPACE, "workspace %zu < %zu bytes", workspace_bytes, Y.total);
+  // the scratch arena: the caller's (shareable), else the workspace's tail
+  const size_t need = scratch ? Y.total : Y.total + Y.scratch_total;
+  if (workspace_bytes < need)
+    return fail(TASP_ERR_WORKSPACE, "workspace %zu < %zu bytes", workspace_bytes, need);
+  if (scratch && scratch_bytes < Y.scratch_total)
+    return fail(TASP_ERR_WORKSPACE, "scratch %zu < %zu bytes", scratch_bytes, Y.scratch_total);
   char* ws = static_cast<char*>(workspace);
+  char* sc = scratch ? static_cast<char*>(scratch) : ws + Y.total;
   hipStream_t s = static_cast<hipStream_t>(stream);
   auto at = [&](size_t off) { return ws + off; };
 
@@ -1321,8 +1339,8 @@ tasp_status tasp_compile_shared_plan(const tasp_model_desc* desc, const tasp_gst
   p->rope_sin = reinterpret_cast<float*>(at(Y.rope_sin));
   hipError_t h = hipMemcpyAsync(p->rope_cos, tc.data(), tc.size() * 4, hipMemcpyHostToDevice, s);
   if (h == hipSuccess) h = hipMemcpyAsync(p->rope_sin, ts.data(), ts.size() * 4, hipMemcpyHostToDevice, s);
-  if (h == hipSuccess) h = tasp::launch_fill_zero(at(Y.zero_begin), Y.zero_end - Y.zero_begin, s);
-  set_scratch(p, Y, ws);
+  if (h == hipSuccess) h = tasp::launch_fill_zero(sc + Y.zero_begin, Y.zero_end - Y.zero_begin, s);
+  set_scratch(p, Y, sc);
   if ((st = read_back_indices(p, c, Y, ws, s, h)) != TASP_OK) {
     delete p;
     return st;

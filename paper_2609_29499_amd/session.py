@@ -130,6 +130,16 @@ class KVCache:
         return t[layer].view(torch.int16).cpu().numpy().view(np.uint16)
 
 
+class SharedScratch:
+    """Decode / prefill scratch arena that several shared-store plans of one desc may share
+    (their calls must then run in order, e.g. on one stream)."""
+
+    def __init__(self, desc, device="cuda"):
+        self.bytes = B.tasp_shared_plan_workspace_bytes(desc)[1]
+        self.buf = torch.empty(self.bytes + 256, dtype=torch.uint8, device=device)
+        self.base = self.buf.data_ptr() + (-self.buf.data_ptr()) % 256
+
+
 class Plan:
     """A compiled plan with its torch-owned workspace."""
 
@@ -155,19 +165,21 @@ class Plan:
             self.handle = None
 
     @classmethod
-    def shared(cls, desc, gstore, mask=None, stream=None, device="cuda"):
-        """A plan over the shared groupwise store (no weight copies)."""
+    def shared(cls, desc, gstore, mask=None, stream=None, device="cuda", scratch=None):
+        """A plan over the shared groupwise store (no weight copies). ``scratch``: a
+        SharedScratch to share with other plans (else the plan gets its own)."""
         self = cls.__new__(cls)
         self.desc = desc
         self.store = gstore
         mptr, self._mask_keep = mask_struct(mask)
-        self.ws_bytes = B.tasp_shared_plan_workspace_bytes(desc)
+        self.ws_bytes = B.tasp_shared_plan_workspace_bytes(desc)[0]
         self.ws = torch.empty(self.ws_bytes + 256, dtype=torch.uint8, device=device)
         off = (-self.ws.data_ptr()) % 256
         self.ws_base = self.ws.data_ptr() + off
         self.ws_off = off
+        self.scratch = scratch if scratch is not None else SharedScratch(desc, device)
         self.handle = B.tasp_compile_shared_plan(desc, gstore.struct, mptr, self.ws_base,
-                                                 self.ws_bytes,
+                                                 self.ws_bytes, self.scratch.base, self.scratch.bytes,
                                                  stream if stream is not None else current_stream())
         return self
 

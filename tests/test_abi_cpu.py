@@ -196,11 +196,12 @@ def test_shared_plan_host_checks():
     before any GPU work."""
     _lib()
     d = _desc(d_model=512, d_ffn=1536, max_batch=1)
-    n = B.tasp_shared_plan_workspace_bytes(d)
-    assert n > 0 and n < B.tasp_plan_workspace_bytes(d, None)
+    n, ns = B.tasp_shared_plan_workspace_bytes(d)
+    assert n > 0 and ns > 0 and n + ns < B.tasp_plan_workspace_bytes(d, None)
     big = _desc(d_model=512, d_ffn=1536, max_batch=4, max_prefill=64)
-    nb = B.tasp_shared_plan_workspace_bytes(big)
-    assert n < nb < B.tasp_plan_workspace_bytes(big, None)
+    nb, nbs = B.tasp_shared_plan_workspace_bytes(big)
+    # the plan's own bytes do not depend on the batch or prefill scratch; the arena does
+    assert nb == n and nbs > ns and nb + nbs < B.tasp_plan_workspace_bytes(big, None)
     for bad, status in ((dict(d_model=528), "TASP_ERR_SHAPE"),
                         (dict(d_ffn=1552), "TASP_ERR_SHAPE")):
         with pytest.raises(B.TaspError) as e:
@@ -215,8 +216,39 @@ def test_shared_plan_host_checks():
     f[0, 5] = 0                             # breaks the block of channels 0..15
     m = B.tasp_mask(q.ctypes.data, None, f.ctypes.data)
     with pytest.raises(B.TaspError) as e:
-        B.tasp_compile_shared_plan(d, store, C.pointer(m), 1 << 30, n, None)
+        B.tasp_compile_shared_plan(d, store, C.pointer(m), 1 << 30, n, 1 << 31, ns, None)
     assert B.STATUS[e.value.status] == "TASP_ERR_UNSUPPORTED"
-    with pytest.raises(B.TaspError) as e:
-        B.tasp_compile_shared_plan(d, store, None, (1 << 30) + 8, n, None)
-    assert B.STATUS[e.value.status] == "TASP_ERR_WORKSPACE"
+    for ws, wsb, sc, scb in (((1 << 30) + 8, n, 1 << 31, ns),      # misaligned workspace
+                             (1 << 30, n, (1 << 31) + 8, ns),      # misaligned scratch
+                             (1 << 30, n, 1 << 31, ns - 1),        # short scratch
+                             (1 << 30, n + ns - 1, None, 0),       # arena in the workspace: short
+                             (1 << 30, n - 1, 1 << 31, ns)):       # short workspace
+        with pytest.raises(B.TaspError) as e:
+            B.tasp_compile_shared_plan(d, store, None, ws, wsb, sc, scb, None)
+        assert B.STATUS[e.value.status] == "TASP_ERR_WORKSPACE", (ws, wsb, sc, scb)
+
+
+def test_shared_store_memory_ledger_llama3_70b():
+    """Memory of five Llama-3-70B masks over one groupwise store with the paper's request shape
+    enabled (2,048-token prefill, 256 decode steps; paper, appendix "Backing-store semantics"
+    and Table "memory"): the plans add metadata only, all five share one scratch arena, and the
+    total stays far from five duplicated stores."""
+    _lib()
+    import synth
+    sh = synth.LLAMA3_70B
+    d = S.desc_from_shape(sh, max_batch=1, max_seq=2048 + 256, max_prefill=2048)
+    plan, arena = B.tasp_shared_plan_workspace_bytes(d)
+    dh, D, F = sh.head_dim, sh.d_model, sh.d_ffn
+    per_layer = (sh.n_q_heads + 2 * sh.n_kv_heads) * dh * D + D * sh.n_q_heads * dh + 3 * F * D
+    weights = sh.n_layers * per_layer
+    scales = weights // 128 * 2
+    kv = 2 * sh.n_layers * sh.n_kv_heads * (2048 + 256) * dh * 2
+    five = weights + scales + 5 * plan + arena + kv
+    one = weights + scales + plan + arena + kv
+    assert five - one == 4 * plan
+    assert 5 * plan < 0.1e9                      # metadata of five plans, decimal GB
+    assert arena < 1.0e9                         # one prefill-sized scratch for all of them
+    assert five < weights * 1.05 and five < 0.25 * 5 * weights
+    # the decode-only desc needs the same plan bytes and a smaller arena
+    p0, a0 = B.tasp_shared_plan_workspace_bytes(S.desc_from_shape(sh, max_batch=1, max_seq=2304))
+    assert p0 == plan and a0 < arena

@@ -100,21 +100,44 @@ def test_graph_replay_and_timed_kernels():
 
 
 def test_shared_plans_own_no_weights():
-    """Five masks over one store: every plan's workspace has the same small size (metadata and
-    scratch), no weights are copied, and the device allocation grows by the workspaces only."""
+    """Five masks over one store, prefill and batches enabled: every plan's workspace has the
+    same small size (metadata), all five share one scratch arena, no weights are copied, and
+    the device allocation grows by the workspaces and the arena only. Requests then alternate
+    over the five plans on the shared arena at parity with the oracle."""
     _flush("case shared memory ledger")
     sh = synth.tiny_shape(layers=2, vocab=1000, **TINY)
     layers = [synth.layer_weights(sh, l, quant="group") for l in range(sh.n_layers)]
-    desc = S.desc_from_shape(sh, max_batch=1, max_seq=256)
+    desc = S.desc_from_shape(sh, max_batch=4, max_seq=256, max_prefill=64)
     store = S.GroupStore(layers, synth.final_norm(sh), synth.lm_head(sh))
     torch.cuda.synchronize()
     before = torch.cuda.memory_allocated()
-    plans = [S.Plan.shared(desc, store, synth.raw_mask(sh, 10 + i, block=16)) for i in range(5)]
+    arena = S.SharedScratch(desc)
+    masks = [synth.raw_mask(sh, 10 + i, block=16) for i in range(5)]
+    plans = [S.Plan.shared(desc, store, m, scratch=arena) for m in masks]
     torch.cuda.synchronize()
     grown = torch.cuda.memory_allocated() - before
     ws = {p.ws_bytes for p in plans}
     assert len(ws) == 1
-    assert grown <= 5 * (ws.pop() + 1024)
+    assert grown <= 5 * (ws.pop() + 1024) + arena.bytes + 1024
+    # prefill then decode on each plan in turn, all on the one arena
+    table, scales = synth.embedding(sh)
+    fn, lm = synth.final_norm(sh), synth.lm_head(sh)
+    T = 12
+    for i in (0, 3, 1, 4, 2, 0):
+        prompt = synth.prompt_ids(T + 1, sh.vocab, seed=40 + i)
+        x = ref.embed_rows(table, scales, prompt).astype(np.float32).astype(np.float64)
+        cache = S.KVCache(desc, 1, 64)
+        out = torch.empty((T, sh.vocab), device="cuda")
+        plans[i].prefill(torch.from_numpy(x[:T].astype(np.float32)).cuda(), T, cache, 0, out)
+        o1 = torch.empty((1, sh.vocab), device="cuda")
+        plans[i].decode(torch.from_numpy(x[T:].astype(np.float32)).cuda(), cache, T, o1)
+        torch.cuda.synchronize()
+        closed = ref.close_mask(*masks[i], sh.group_size)
+        caches = [(np.zeros((sh.n_kv_heads, T + 1, sh.head_dim)), np.zeros((sh.n_kv_heads, T + 1, sh.head_dim)))
+                  for _ in range(sh.n_layers)]
+        want = ref.prefill_stack(lambda l: layers[l], closed, x, caches, 0, sh, fn, lm)
+        got = np.concatenate([out.cpu().numpy(), o1.cpu().numpy()]).astype(np.float64)
+        assert_parity(got, want, what=f"plan {i} on the shared arena")
     # a materialised plan of the same mask holds its panels
     mat = S.Plan(S.desc_from_shape(sh, max_batch=1, max_seq=256),
                  S.DeviceStore([synth.layer_weights(sh, l) for l in range(2)], synth.final_norm(sh),
@@ -309,9 +332,10 @@ def test_one_store_validation_prefill_and_batches():
     emb = lambda ids: torch.from_numpy(  # noqa: E731
         (table[np.asarray(ids)].astype(np.float32) * scales[np.asarray(ids), None]).astype(np.float32)).cuda()
     worst, agree, total = 0.0, 0, 0
+    arena = S.SharedScratch(desc)                 # one scratch arena for both shared plans
     for seed in (31, 32):
         mask = synth.raw_mask(sh, seed, block=16)
-        pm, ps = S.Plan(desc, mstore, mask), S.Plan.shared(desc, gstore, mask)
+        pm, ps = S.Plan(desc, mstore, mask), S.Plan.shared(desc, gstore, mask, scratch=arena)
         # prefill of one sequence
         prompt = synth.prompt_ids(T, sh.vocab, seed=seed)
         outs = []
