@@ -19,9 +19,9 @@ mkdir -p $O
 which=${1:-decode_b1}
 case $which in
 decode_b1)
-  echo "[prof] b1 kernel trace" && timeout -k 10 400 rocprofv3 --kernel-trace --stats -d $O/b1_trace -o trace -- python3 -u bench.py --cpu-seconds 3 > $O/b1_trace.json 2> $O/b1_trace.err &&
-  echo "[prof] b1 FETCH_SIZE" && timeout -s KILL 300 rocprofv3 --pmc FETCH_SIZE -d $O/b1_fetch -o fetch -- python3 -u bench.py --sparse-only --no-cpu --steps 200 --warmup 20 --blocks 1 --timed-launches 8 > $O/b1_fetch.json 2> $O/b1_fetch.err &&
-  echo "[prof] b1 WRITE_SIZE" && timeout -s KILL 300 rocprofv3 --pmc WRITE_SIZE -d $O/b1_write -o write -- python3 -u bench.py --sparse-only --no-cpu --steps 200 --warmup 20 --blocks 1 --timed-launches 8 > $O/b1_write.json 2> $O/b1_write.err
+  echo "[prof] b1 kernel trace" && timeout -k 10 400 rocprofv3 --kernel-trace --stats -d $O/b1_trace -o trace -- python3 -u bench.py --workload llama3_8b_layer --cpu-seconds 3 > $O/b1_trace.json 2> $O/b1_trace.err &&
+  echo "[prof] b1 FETCH_SIZE" && timeout -s KILL 300 rocprofv3 --pmc FETCH_SIZE -d $O/b1_fetch -o fetch -- python3 -u bench.py --workload llama3_8b_layer --sparse-only --no-cpu --steps 200 --warmup 20 --blocks 1 --timed-launches 8 > $O/b1_fetch.json 2> $O/b1_fetch.err &&
+  echo "[prof] b1 WRITE_SIZE" && timeout -s KILL 300 rocprofv3 --pmc WRITE_SIZE -d $O/b1_write -o write -- python3 -u bench.py --workload llama3_8b_layer --sparse-only --no-cpu --steps 200 --warmup 20 --blocks 1 --timed-launches 8 > $O/b1_write.json 2> $O/b1_write.err
   ;;
 decode_b8)
   echo "[prof] b8 kernel trace" && timeout -k 10 400 rocprofv3 --kernel-trace --stats -d $O/b8_trace -o trace -- python3 -u bench.py --workload llama3_8b_batch8 --steps 200 --warmup 20 --cpu-seconds 3 > $O/b8_trace.json 2> $O/b8_trace.err &&
