@@ -11,7 +11,8 @@ import ctypes as C
 import os
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(HERE, "libtasp.so")
+# TASP_LIB selects another build of the same library (the host-sanitizer build of the tests)
+LIB_PATH = os.environ.get("TASP_LIB") or os.path.join(HERE, "libtasp.so")
 
 TASP_OK = 0
 STATUS = {0: "TASP_OK", -1: "TASP_ERR_INVALID_ARG", -2: "TASP_ERR_SHAPE", -3: "TASP_ERR_MASK",

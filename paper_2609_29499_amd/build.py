@@ -56,5 +56,35 @@ def build(verbose: bool = False, jobs: int = 4) -> str:
     return LIB
 
 
+# Host-side sanitizers for the argument checks (device code is built as usual): each -fsanitize
+# goes to the host compilation only.
+SAN_FLAGS = ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined"]
+
+
+def build_sanitized(out_dir: str) -> str:
+    """libtasp_san.so in out_dir: runtime.hip (every host-side check of the C ABI) rebuilt with
+    AddressSanitizer and UndefinedBehaviorSanitizer, linked with the kernel objects of the last
+    build(). Load it with the sanitizer runtime preloaded (asan_runtime())."""
+    others = [os.path.join(OBJ, os.path.splitext(s)[0] + ".o") for s in SOURCES if s != "runtime.hip"]
+    missing = [o for o in others if not os.path.exists(o)]
+    if missing:
+        raise RuntimeError(f"kernel objects missing (run build() first): {missing}")
+    os.makedirs(out_dir, exist_ok=True)
+    obj = os.path.join(out_dir, "runtime_san.o")
+    flags = [f for f in FLAGS if f != "-O3"] + ["-O1", "-g", "-fno-omit-frame-pointer"]
+    _run([HIPCC, *flags, *SAN_FLAGS, "-c", os.path.join(CSRC, "runtime.hip"), "-o", obj])
+    lib = os.path.join(out_dir, "libtasp_san.so")
+    _run([HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", *SAN_FLAGS, "-shared-libsan", "-o", lib,
+          *others, obj])
+    return lib
+
+
+def asan_runtime() -> str:
+    """Path of the compiler's shared AddressSanitizer runtime."""
+    r = subprocess.run([HIPCC, "-print-file-name=libclang_rt.asan-x86_64.so"], capture_output=True,
+                       text=True, check=True)
+    return r.stdout.strip()
+
+
 if __name__ == "__main__":
     print(build(verbose=True))
