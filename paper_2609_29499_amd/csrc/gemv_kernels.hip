@@ -62,7 +62,7 @@ __device__ __forceinline__ void fma_bf16x4(float& acc, uint32_t w0, uint32_t w1,
 // its first weight tile there. Vector loads retire in issue order, so waiting for the input
 // batch then does not wait for the weights, and the weight stream starts before the input
 // arrives.
-template <int B, bool NORM, bool I8, class F>
+template <int B, bool NORM, bool I8, int NW, class F>
 __device__ __forceinline__ void stage_inputs(const float* __restrict__ x, int ldx, int K, int KP,
                                              const uint16_t* __restrict__ gamma, float eps,
                                              float* xs, float* red2, float* xscale, float* bias,
@@ -70,7 +70,8 @@ __device__ __forceinline__ void stage_inputs(const float* __restrict__ x, int ld
   constexpr int kBatch = I8 ? 8 : 4;                    // BF16 rows: fewer registers in flight
   const int tid = threadIdx.x;
   const int n4 = (K + 3) >> 2;                          // float4 slots holding valid columns
-  const int npass = KP >> 10;
+  constexpr int NT = NW * kWave;                        // threads of the workgroup
+  const int npass = (KP + 4 * NT - 1) / (4 * NT);       // passes of one float4 per thread
   const __amdgpu_buffer_rsrc_t rg = make_rsrc(gamma, uint32_t(NORM ? K : 0) * 2u);
 #pragma unroll
   for (int b = 0; b < B; ++b) {
@@ -81,7 +82,7 @@ __device__ __forceinline__ void stage_inputs(const float* __restrict__ x, int ld
     auto load_batch = [&](int i0) {
 #pragma unroll
       for (int u = 0; u < kBatch; ++u) {
-        const int c4 = ((i0 + u) << 8) + tid;           // float4 index
+        const int c4 = (i0 + u) * NT + tid;             // float4 index
         xv[u] = buf_load16(rx, c4 < n4 ? uint32_t(c4) * 16u : kOOB);
         if (NORM)
           gv[u] = __builtin_bit_cast(int2, __builtin_amdgcn_raw_buffer_load_b64(
@@ -93,7 +94,8 @@ __device__ __forceinline__ void stage_inputs(const float* __restrict__ x, int ld
       for (int u = 0; u < kBatch; ++u) {
         const int i = i0 + u;
         if (i >= npass) break;
-        const int k = (i << 10) + (tid << 2);
+        const int k = (i * NT + tid) << 2;
+        if (k >= KP) break;
         float4 v = __builtin_bit_cast(float4, xv[u]);
         // columns K.. of a partial float4 are zero
         if (k + 0 >= K) v.x = 0.0f;
@@ -129,17 +131,23 @@ __device__ __forceinline__ void stage_inputs(const float* __restrict__ x, int ld
       red2[(tid >> 6) * 2 + 1] = sx;
     }
     __syncthreads();
-    const float tss = red2[0] + red2[2] + red2[4] + red2[6];
-    const float tsx = red2[1] + red2[3] + red2[5] + red2[7];
+    float tss = 0.0f, tsx = 0.0f;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) {
+      tss += red2[2 * w];
+      tsx += red2[2 * w + 1];
+    }
     xscale[b] = NORM ? rsqrtf(tss / float(K) + eps) : 1.0f;
     bias[b] = I8 ? 128.0f * tsx : 0.0f;
   }
   __syncthreads();
 }
 
-// At most 128 VGPRs, so that four waves share each SIMD (the grid is sized for that).
-template <int B, int MODE>
-__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) void gemv_kernel(GemvArgs a) {
+// At most 128 VGPRs, so that four waves share each SIMD (the grid is sized for that). NW waves
+// per workgroup: 4, or 8 where the staged input leaves room for fewer than four workgroups per
+// CU (the same waves per CU with half the staging).
+template <int B, int MODE, int NW>
+__global__ __launch_bounds__(NW * kWave) __attribute__((amdgpu_waves_per_eu(4))) void gemv_kernel(GemvArgs a) {
   constexpr int kR = rows_per_group(MODE);
   // 1 KiB chunks per tile: 1 for gate/up (measured 1.5 % faster than 2 or 4), 2 otherwise
   constexpr int kC = (MODE == GEMV_GATEUP) ? 1 : ::tasp::kC;
@@ -148,7 +156,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) voi
   constexpr int CPC = BF ? 512 : 1024;                 // columns per 1 KiB chunk
   constexpr int LCOL = BF ? 8 : 16;                    // columns per lane load
   extern __shared__ __attribute__((aligned(16))) float xs[];
-  __shared__ float red2[8];
+  __shared__ float red2[2 * NW];
   const float* __restrict__ scale = a.scale;
   const float* __restrict__ scale2 = a.scale2;
   const float* __restrict__ resid = a.resid;
@@ -159,8 +167,8 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) voi
   // writes the epilogue (residual + 0)
   const int KB = max(1, (nchunks + kC - 1) / kC);
   const int lane = threadIdx.x & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(blockIdx.x * (kBlock / kWave) + (threadIdx.x >> 6));
-  const int nwaves = gridDim.x * (kBlock / kWave);
+  const int wave = __builtin_amdgcn_readfirstlane(blockIdx.x * NW + (threadIdx.x >> 6));
+  const int nwaves = gridDim.x * NW;
   constexpr int CH = kR / 2;                           // gate/up: channels per group
   const int per_group = (MODE == GEMV_GATEUP) ? CH : kR;
   const int G = (N + per_group - 1) / per_group;
@@ -219,11 +227,11 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) voi
   int4 wa[kC][kR], wb[kC][kR];
   float xscale[B], bias[B];
   if (MODE == GEMV_GATEUP) {
-    stage_inputs<B, NORM, !BF>(a.x, a.ldx, K, KP, a.gamma, a.eps, xs, red2, xscale, bias, [] {});
+    stage_inputs<B, NORM, !BF, NW>(a.x, a.ldx, K, KP, a.gamma, a.eps, xs, red2, xscale, bias, [] {});
     issue(t_begin, wa);
   } else {
-    stage_inputs<B, NORM, !BF>(a.x, a.ldx, K, KP, a.gamma, a.eps, xs, red2, xscale, bias,
-                               [&] { issue(t_begin, wa); });
+    stage_inputs<B, NORM, !BF, NW>(a.x, a.ldx, K, KP, a.gamma, a.eps, xs, red2, xscale, bias,
+                                   [&] { issue(t_begin, wa); });
   }
   issue(t_begin + 1, wb);
 #pragma unroll
@@ -334,23 +342,35 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) voi
 // One wave per group up to the workgroups that fit on the chip at once: kWgPerCu per CU, fewer
 // when the staged input limits them (160 KiB of LDS per CU). Past that, waves take several groups
 // each, so that no workgroup waits for a second round and stages the input again.
-int gemv_grid(int n_groups, size_t lds) {
+int gemv_per_cu(size_t lds) {
   constexpr size_t kLdsPerCu = 160 * 1024;
   const int by_lds = int(kLdsPerCu / std::max<size_t>(lds + 64, 1));
-  const int per_cu = std::max(1, std::min(kWgPerCu, by_lds));
-  const int grid = std::min((n_groups + 3) / 4, kNumCu * per_cu);
+  return std::max(1, std::min(kWgPerCu, by_lds));
+}
+
+int gemv_grid(int n_groups, int per_cu, int nw) {
+  const int grid = std::min((n_groups + nw - 1) / nw, kNumCu * per_cu);
   return grid < 1 ? 1 : grid;
 }
 
-template <int B, int MODE>
+template <int B, int MODE, int NW>
 hipError_t launch_mode(const GemvArgs& a, int grid, size_t lds, hipStream_t s) {
   // dynamic LDS above 64 KiB must be allowed per kernel; done once per instantiation
   static const hipError_t attr = hipFuncSetAttribute(
-      reinterpret_cast<const void*>(&gemv_kernel<B, MODE>),
+      reinterpret_cast<const void*>(&gemv_kernel<B, MODE, NW>),
       hipFuncAttributeMaxDynamicSharedMemorySize, int(kMaxGemvLds));
   if (attr != hipSuccess) return attr;
-  hipLaunchKernelGGL((gemv_kernel<B, MODE>), dim3(grid), dim3(kBlock), lds, s, a);
+  hipLaunchKernelGGL((gemv_kernel<B, MODE, NW>), dim3(grid), dim3(NW * kWave), lds, s, a);
   return hipGetLastError();
+}
+
+template <int B, int MODE>
+hipError_t launch_mode_nw(const GemvArgs& a, int n_groups, size_t lds, hipStream_t s) {
+  // a wide input (staging LDS for fewer than kWgPerCu workgroups per CU) gets 8-wave workgroups,
+  // so that each CU still holds about 16 waves of loads in flight
+  const int per_cu = gemv_per_cu(lds);
+  if (per_cu < kWgPerCu) return launch_mode<B, MODE, 8>(a, gemv_grid(n_groups, per_cu, 8), lds, s);
+  return launch_mode<B, MODE, 4>(a, gemv_grid(n_groups, per_cu, 4), lds, s);
 }
 
 template <int B>
@@ -358,13 +378,13 @@ hipError_t launch_gemv_b(GemvMode mode, const GemvArgs& a, hipStream_t s) {
   if (a.N < 1) return hipSuccess;                       // no output rows: nothing to launch
   const int per_group = (mode == GEMV_GATEUP) ? rows_per_group(mode) / 2 : rows_per_group(mode);
   const size_t lds = gemv_lds_bytes(B, a.K);
-  const int grid = gemv_grid((a.N + per_group - 1) / per_group, lds);
+  const int n_groups = (a.N + per_group - 1) / per_group;
   if (lds > kMaxGemvLds) return hipErrorInvalidValue;
   switch (mode) {
-    case GEMV_QKV: return launch_mode<B, GEMV_QKV>(a, grid, lds, s);
-    case GEMV_RESID: return launch_mode<B, GEMV_RESID>(a, grid, lds, s);
-    case GEMV_GATEUP: return launch_mode<B, GEMV_GATEUP>(a, grid, lds, s);
-    case GEMV_LMHEAD: return launch_mode<B, GEMV_LMHEAD>(a, grid, lds, s);
+    case GEMV_QKV: return launch_mode_nw<B, GEMV_QKV>(a, n_groups, lds, s);
+    case GEMV_RESID: return launch_mode_nw<B, GEMV_RESID>(a, n_groups, lds, s);
+    case GEMV_GATEUP: return launch_mode_nw<B, GEMV_GATEUP>(a, n_groups, lds, s);
+    case GEMV_LMHEAD: return launch_mode_nw<B, GEMV_LMHEAD>(a, n_groups, lds, s);
   }
   return hipErrorInvalidValue;
 }
