@@ -116,6 +116,81 @@ __device__ __forceinline__ void store_hilo_pf(uint16_t* xo, size_t plane, int ld
   xo[plane + size_t(t) * ld + col] = f32_to_bf16(v - bf16_to_f32(hi));
 }
 
+// Epilogue of a prefill projection tile: lane (r, q) of wave (wm, wn) holds tokens 4q + i of each
+// of its token tiles for panel row r of each row tile; rs = inverse RMS of the tile's tokens.
+template <int MODE, int TM, bool SH>
+__device__ __forceinline__ void pf_epilogue(const PfArgs& a, const f32x4 (&acc)[TM / 32][4],
+                                            const float* rs, int m0, int n0, int bz, int wm, int wn,
+                                            int q, int r) {
+  constexpr bool BF = (MODE == MM_LMHEAD);
+  constexpr bool GU = (MODE == MM_GATEUP);
+  constexpr int MT = TM / 32;
+  const int T = a.T, N = a.N;
+  if (!GU && !BF && a.part) {
+    // split K: this split's scaled partial; the reduction adds the splits and the epilogue
+    float* part = a.part + size_t(bz) * T * N;
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int tl = wm * (TM / 2) + mt * 16 + 4 * q + i;
+        const int t = m0 + tl;
+        if (t >= T) continue;
+        const float rb = a.ssq ? rs[tl] : 1.0f;
+#pragma unroll
+        for (int nt = 0; nt < 4; ++nt) {
+          const int n = n0 + wn * 64 + nt * 16 + r;
+          if (n < N) part[size_t(t) * N + n] = acc[mt][nt][i] * (SH ? 1.0f : a.scale[n]) * rb;
+        }
+      }
+    return;
+  }
+  const bool resid_on = (MODE == MM_RESID);
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int tl = wm * (TM / 2) + mt * 16 + 4 * q + i;
+      const int t = m0 + tl;
+      const bool t_ok = t < T;
+      const float rb = a.ssq ? rs[tl] : 1.0f;
+      if (GU) {
+#pragma unroll
+        for (int nt = 0; nt < 2; ++nt) {
+          const int ch = n0 + 32 * wn + 16 * nt + r;
+          if (t_ok && ch < N) {
+            const float gv = acc[mt][nt][i] * (SH ? 1.0f : a.scale[ch]) * rb;
+            const float uv = acc[mt][nt + 2][i] * (SH ? 1.0f : a.scale2[ch]) * rb;
+            store_hilo_pf(a.xo, a.plane_o, a.ldxo, t, ch, gv / (1.0f + exp2f(-gv * kLog2e)) * uv);
+          }
+        }
+        continue;
+      }
+      float ss = 0.0f;
+#pragma unroll
+      for (int nt = 0; nt < 4; ++nt) {
+        const int n = n0 + wn * 64 + nt * 16 + r;
+        const bool ok = t_ok && n < N;
+        float v = 0.0f;
+        if (MODE == MM_LMHEAD) {
+          v = acc[mt][nt][i] * rb;
+        } else if (resid_on) {
+          v = ok ? a.resid[size_t(t) * a.ldy + n] + acc[mt][nt][i] * (SH ? 1.0f : a.scale[n]) : 0.0f;
+          if (ok && a.gamma_next) store_hilo_pf(a.xo, a.plane_o, a.ldxo, t, n, v * bf16_to_f32(a.gamma_next[n]));
+          ss = fmaf(v, v, ss);
+        } else {
+          v = ok ? acc[mt][nt][i] * (SH ? 1.0f : a.scale[n]) * rb : 0.0f;
+        }
+        if (ok) a.y[size_t(t) * a.ldy + n] = v;
+      }
+      if (resid_on && a.gamma_next) {
+        ss = row16_sum(ss);                             // the 16 lanes of this token
+        if (r == 0 && t_ok && n0 + wn * 64 < N) a.ssq_out[size_t(t) * a.n_ssq_out + (n0 + wn * 64) / kSsqBlk] = ss;
+      }
+    }
+  }
+}
+
 template <int MODE, int TM, bool SH>
 __global__ __launch_bounds__(kBlock) void pf_gemm_kernel(PfArgs a) {
   constexpr bool BF = (MODE == MM_LMHEAD);
@@ -317,70 +392,193 @@ __global__ __launch_bounds__(kBlock) void pf_gemm_kernel(PfArgs a) {
     if (kc + 2 < nk) step(kc + 2, s2, s0);
   }
 
-  // ---- epilogue: lane holds tokens 4q + i of each token tile, panel row r of each row tile
-  if (!GU && !BF && a.part) {
-    // split K: this split's scaled partial; the reduction adds the splits and the epilogue
-    float* part = a.part + size_t(bz) * T * N;
+  pf_epilogue<MODE, TM, SH>(a, acc, sm.rs, m0, n0, bz, wm, wn, q, r);
+}
+
+// ---- per-row INT8 panels: operands copied straight from memory into LDS
+//
+// The activation planes and the INT8 panel rows go from memory to LDS by buffer loads with an LDS
+// destination (no register staging, no LDS store instructions), through four stages, so that
+// the loads of the next three chunks are in flight while a chunk is multiplied; one barrier
+// per chunk. INT8 panel bytes stay INT8 in LDS (half the LDS traffic of BF16) and each wave widens
+// its 8-byte fragments exactly to BF16 before the MFMAs. An LDS-destination load writes lane l's
+// 16 bytes at l * 16 from the wave's base, so the bank swizzle is applied on the memory side: the
+// lane that fills LDS slot s of a row fetches the row's 16-byte piece s ^ swizzle(row). Used
+// when K is a whole number of chunks, so that no load crosses the end of a panel row.
+
+template <int TM>
+struct PfDmaStage {
+  uint16_t a[2][TM * kLdsRow];         // [hi/lo][token row x 32 BF16], quarters swizzled
+  uint8_t b[kTN * kKC];                // [panel row x 32 INT8], 16-byte halves swizzled
+};
+
+// slot of quarter qu (16 bytes) of A row `row` (the 8 lanes served together by a 16-byte read,
+// 8 consecutive rows of one quarter, hit distinct banks), and of half h of B row `row` (an
+// 8-byte read of 16 consecutive rows meets each bank at most twice, the least for 8-byte reads
+// of one word position)
+__device__ __forceinline__ int dma_a_q(int row, int qu) { return qu ^ (((row >> 1) ^ (row >> 3)) & 3); }
+__device__ __forceinline__ int dma_b_h(int row, int h) { return h ^ ((row >> 3) & 1); }
+
+// s_waitcnt: vector memory count <= n, the other counters not waited on
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+// 8 signed INT8 (two words) -> 8 BF16 (exact)
+__device__ __forceinline__ bf16x8 widen8(uint32_t w0, uint32_t w1) {
+  const uint32_t v[2] = {w0, w1};
+  uint32_t o[4];
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int tl = wm * (TM / 2) + mt * 16 + 4 * q + i;
-        const int t = m0 + tl;
-        if (t >= T) continue;
-        const float rb = a.ssq ? sm.rs[tl] : 1.0f;
-#pragma unroll
-        for (int nt = 0; nt < 4; ++nt) {
-          const int n = n0 + wn * 64 + nt * 16 + r;
-          if (n < N) part[size_t(t) * N + n] = acc[mt][nt][i] * (SH ? 1.0f : a.scale[n]) * rb;
-        }
-      }
-    return;
+  for (int i = 0; i < 2; ++i) {
+    o[2 * i] = pack_exact(float(int8_t(v[i] & 0xffu)), float(int8_t((v[i] >> 8) & 0xffu)));
+    o[2 * i + 1] = pack_exact(float(int8_t((v[i] >> 16) & 0xffu)), float(int8_t(v[i] >> 24)));
   }
-  const bool resid_on = (MODE == MM_RESID);
+  return __builtin_bit_cast(bf16x8, make_int4(int(o[0]), int(o[1]), int(o[2]), int(o[3])));
+}
+
+template <int MODE, int TM>
+__global__ __launch_bounds__(kBlock) void pf_dma_kernel(PfArgs a) {
+  constexpr bool GU = (MODE == MM_GATEUP);
+  constexpr int MT = TM / 32;                           // token tiles of 16 per wave
+  constexpr int A_PER_WAVE = TM / 32;                   // A loads (16 rows x 64 B) per wave and chunk
+  constexpr int PER_CHUNK = A_PER_WAVE + 1;             // + one B load (32 rows x 32 B)
+  static_assert(MODE == MM_QKV || MODE == MM_RESID || MODE == MM_GATEUP, "INT8 projections");
+  __shared__ __attribute__((aligned(16))) PfDmaStage<TM> st0;
+  __shared__ __attribute__((aligned(16))) PfDmaStage<TM> st1;
+  __shared__ __attribute__((aligned(16))) PfDmaStage<TM> st2;
+  __shared__ __attribute__((aligned(16))) PfDmaStage<TM> st3;
+  // the inverse RMS of the tile's tokens goes to LDS after the last chunk, over stage 0
+  float* rs = reinterpret_cast<float*>(&st0);
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int r = lane & 15, q = lane >> 4;
+  const int wm = wave >> 1, wn = wave & 1;
+  const int T = a.T, N = a.N;
+  const int bx = blockIdx.x, by = blockIdx.y, bz = blockIdx.z;
+  const int m0 = by * TM;
+  const int n0 = bx * (GU ? kTN / 2 : kTN);
+  const int nk_all = (a.K + kKC - 1) / kKC;
+  const int kc0 = int((long(bz) * nk_all) / gridDim.z);
+  const int nk = int((long(bz + 1) * nk_all) / gridDim.z) - kc0;
+
+  const __amdgpu_buffer_rsrc_t ra = make_rsrc(a.x, uint32_t(2 * a.plane) * 2u);
+  const uint32_t row_bytes = uint32_t(a.ld);
+  const __amdgpu_buffer_rsrc_t rw =
+      make_rsrc(a.w, GU ? a.w2_off + uint32_t(N) * row_bytes : uint32_t(N) * row_bytes);
+
+  // this lane's share of a chunk's loads: A load j covers plane (i / (TM / 16)) rows
+  // 16 (i % (TM / 16)) .. + 16 with i = wave + 4 j; the B load covers LDS rows 32 wave .. + 32
+  uint32_t a_base[A_PER_WAVE];
+  int a_lds[A_PER_WAVE];
 #pragma unroll
-  for (int mt = 0; mt < MT; ++mt) {
+  for (int j = 0; j < A_PER_WAVE; ++j) {
+    const int i = wave + 4 * j;
+    const int plane = i / (TM / 16), r0 = (i % (TM / 16)) * 16;
+    const int row = r0 + (lane >> 2), t = m0 + row;
+    const int k8 = 8 * dma_a_q(row, lane & 3);          // BF16 column of this lane's piece
+    a_base[j] = t < T ? uint32_t(plane) * a.plane * 2u + (uint32_t(t) * uint32_t(a.ldx) + uint32_t(k8)) * 2u
+                      : kOOB;
+    a_lds[j] = plane * (TM * kLdsRow) + r0 * kLdsRow;   // wave-uniform (BF16 elements)
+  }
+  const int b_lr = 32 * wave + (lane >> 1);
+  const int b_row = GU ? n0 + 32 * (b_lr >> 6) + (b_lr & 31) : n0 + b_lr;
+  const bool b_up = GU && ((b_lr & 63) >= 32);
+  const int b_k = 16 * dma_b_h(b_lr, lane & 1);
+  const uint32_t b_base =
+      b_row < N ? (b_up ? a.w2_off : 0u) + uint32_t(b_row) * row_bytes + uint32_t(b_k) : kOOB;
+
+  auto issue = [&](int kc, PfDmaStage<TM>& S) {
+    const int k0 = (kc0 + kc) * kKC;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int tl = wm * (TM / 2) + mt * 16 + 4 * q + i;
-      const int t = m0 + tl;
-      const bool t_ok = t < T;
-      const float rb = a.ssq ? sm.rs[tl] : 1.0f;
-      if (GU) {
+    for (int j = 0; j < A_PER_WAVE; ++j) {
+      // columns past ldx are beyond the plane row: never read (ldx is a multiple of 64)
+      const uint32_t off = a_base[j] == kOOB ? kOOB : a_base[j] + uint32_t(k0) * 2u;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, static_cast<void*>(&S.a[0][a_lds[j]]), 16, int(off), 0, 0, 0);
+    }
+    const uint32_t boff = (b_base == kOOB || k0 + b_k >= int(row_bytes)) ? kOOB : b_base + uint32_t(k0);
+    // (the LDS operand is passed as void*: a typed pointer leaves the host stub of the kernel
+    // unemitted)
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rw, static_cast<void*>(&S.b[32 * wave * kKC]), 16, int(boff), 0, 0, 0);
+  };
+
+  // the inverse RMS loads go first, so that waiting for them does not wait for the chunks
+  float rsv = 0.0f;
+  {
+    const int row = tid >> 1, half = tid & 1, t = m0 + row;
+    if (a.ssq && row < TM) {
+      const __amdgpu_buffer_rsrc_t rq = make_rsrc(a.ssq, uint32_t(T) * uint32_t(a.n_ssq) * 4u);
+      for (int j0 = 0; j0 < a.n_ssq; j0 += 16) {
+        float tv[8];
 #pragma unroll
-        for (int nt = 0; nt < 2; ++nt) {
-          const int ch = n0 + 32 * wn + 16 * nt + r;
-          if (t_ok && ch < N) {
-            const float gv = acc[mt][nt][i] * (SH ? 1.0f : a.scale[ch]) * rb;
-            const float uv = acc[mt][nt + 2][i] * (SH ? 1.0f : a.scale2[ch]) * rb;
-            store_hilo_pf(a.xo, a.plane_o, a.ldxo, t, ch, gv / (1.0f + exp2f(-gv * kLog2e)) * uv);
-          }
+        for (int u = 0; u < 8; ++u) {
+          const int j = j0 + 2 * u + half;
+          tv[u] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
+                                                rq, int((t < T && j < a.n_ssq) ? (uint32_t(t) * uint32_t(a.n_ssq) + uint32_t(j)) * 4u : kOOB), 0, 0));
         }
-        continue;
-      }
-      float ss = 0.0f;
 #pragma unroll
-      for (int nt = 0; nt < 4; ++nt) {
-        const int n = n0 + wn * 64 + nt * 16 + r;
-        const bool ok = t_ok && n < N;
-        float v = 0.0f;
-        if (MODE == MM_LMHEAD) {
-          v = acc[mt][nt][i] * rb;
-        } else if (resid_on) {
-          v = ok ? a.resid[size_t(t) * a.ldy + n] + acc[mt][nt][i] * (SH ? 1.0f : a.scale[n]) : 0.0f;
-          if (ok && a.gamma_next) store_hilo_pf(a.xo, a.plane_o, a.ldxo, t, n, v * bf16_to_f32(a.gamma_next[n]));
-          ss = fmaf(v, v, ss);
-        } else {
-          v = ok ? acc[mt][nt][i] * (SH ? 1.0f : a.scale[n]) * rb : 0.0f;
-        }
-        if (ok) a.y[size_t(t) * a.ldy + n] = v;
-      }
-      if (resid_on && a.gamma_next) {
-        ss = row16_sum(ss);                             // the 16 lanes of this token
-        if (r == 0 && t_ok && n0 + wn * 64 < N) a.ssq_out[size_t(t) * a.n_ssq_out + (n0 + wn * 64) / kSsqBlk] = ss;
+        for (int u = 0; u < 8; ++u) rsv += tv[u];
       }
     }
   }
+  if (nk > 0) issue(0, st0);
+  if (nk > 1) issue(1, st1);
+  if (nk > 2) issue(2, st2);
+  if (a.ssq) {
+    rsv += __shfl_xor(rsv, 1, kWave);
+    rsv = rsqrtf(rsv * a.inv_d + a.eps);
+  }
+
+  f32x4 acc[MT][4];
+#pragma unroll
+  for (int i = 0; i < MT; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+
+  auto compute = [&](const PfDmaStage<TM>& S) {
+    bf16x8 bw[4];
+#pragma unroll
+    for (int nt = 0; nt < 4; ++nt) {
+      const int lr = wn * 64 + nt * 16 + r;
+      const uint2 w = *reinterpret_cast<const uint2*>(&S.b[lr * kKC + 16 * dma_b_h(lr, q >> 1) + 8 * (q & 1)]);
+      bw[nt] = widen8(w.x, w.y);
+    }
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+      const int row = wm * (TM / 2) + mt * 16 + r;
+      const int o = row * kLdsRow + 8 * dma_a_q(row, q);
+      const bf16x8 ahi = *reinterpret_cast<const bf16x8*>(&S.a[0][o]);
+      const bf16x8 alo = *reinterpret_cast<const bf16x8*>(&S.a[1][o]);
+#pragma unroll
+      for (int nt = 0; nt < 4; ++nt) {
+        acc[mt][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ahi, bw[nt], acc[mt][nt], 0, 0, 0);
+        acc[mt][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(alo, bw[nt], acc[mt][nt], 0, 0, 0);
+      }
+    }
+  };
+  // chunk kc sits in stage kc % 4: wait for this wave's loads of it (those of later chunks may
+  // stay in flight), meet the other waves (their loads of it have landed, and all of them are
+  // done with the stage loaded next), load chunk kc + 3 into the stage chunk kc - 1 used,
+  // multiply chunk kc
+  auto step = [&](int kc, const PfDmaStage<TM>& cur, PfDmaStage<TM>& nxt) {
+    if (kc + 2 < nk) wait_vm<2 * PER_CHUNK>();
+    else if (kc + 1 < nk) wait_vm<PER_CHUNK>();
+    else wait_vm<0>();
+    __builtin_amdgcn_s_barrier();
+    if (kc + 3 < nk) issue(kc + 3, nxt);
+    compute(cur);
+  };
+  for (int kc = 0; kc < nk; kc += 4) {
+    step(kc, st0, st3);
+    if (kc + 1 < nk) step(kc + 1, st1, st0);
+    if (kc + 2 < nk) step(kc + 2, st2, st1);
+    if (kc + 3 < nk) step(kc + 3, st3, st2);
+  }
+  __syncthreads();                                      // every wave is done with the stages
+  if (a.ssq && (tid & 1) == 0 && (tid >> 1) < TM) rs[tid >> 1] = rsv;
+  __syncthreads();
+  pf_epilogue<MODE, TM, false>(a, acc, rs, m0, n0, bz, wm, wn, q, r);
 }
 
 // First operand of a prefill: x * gamma as hi/lo planes and per-64-element sums of squares of x.
@@ -512,18 +710,37 @@ int pf_resident() {
   return n;
 }
 
+template <int MODE, int TM>
+int pf_dma_resident() {
+  static const int n = [] {
+    int per_cu = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, pf_dma_kernel<MODE, TM>, kBlock, 0) !=
+            hipSuccess || per_cu < 1)
+      per_cu = 1;
+    return per_cu * kNumCu;
+  }();
+  return n;
+}
+
 template <int MODE, int TM, bool SH>
 hipError_t launch_pf_tm(const PfArgs& a, hipStream_t s) {
   const int rows_per_tile = (MODE == MM_GATEUP) ? kTN / 2 : kTN;
   const int gx = (a.N + rows_per_tile - 1) / rows_per_tile, gy = (a.T + TM - 1) / TM;
   if (gx == 0 || gy == 0) return hipSuccess;
+  // per-row INT8 panels with K in whole chunks take the LDS-destination kernel
+  constexpr bool kDmaMode = !SH && (MODE == MM_QKV || MODE == MM_RESID || MODE == MM_GATEUP);
+  const bool dma = kDmaMode && a.K % kKC == 0 && a.K > 0;
   // K splits: as many as keep every workgroup resident, at least kMinSplitChunks chunks each,
   // and no more than the partial buffer holds
   int ks = 1;
   if ((MODE == MM_QKV || MODE == MM_RESID) && a.part) {
     const long tiles = long(gx) * gy;
     const long per_split = long(a.T) * a.N;
-    ks = int(std::min<long>(kMaxKSplit, pf_resident<MODE, TM, SH>() / tiles));
+    int resident = pf_resident<MODE, TM, SH>();
+    if constexpr (kDmaMode) {
+      if (dma) resident = pf_dma_resident<MODE, TM>();
+    }
+    ks = int(std::min<long>(kMaxKSplit, resident / tiles));
     ks = std::min(ks, ((a.K + kKC - 1) / kKC) / kMinSplitChunks);
     ks = int(std::min<long>(ks, per_split > 0 ? long(a.part_floats / size_t(per_split)) : 1));
     ks = std::max(ks, 1);
@@ -531,7 +748,15 @@ hipError_t launch_pf_tm(const PfArgs& a, hipStream_t s) {
   PfArgs b = a;
   if (ks == 1) b.part = nullptr;
   const size_t lds = (SH && a.sv.cols) ? size_t((a.K + 15) / 16) * 4 : 0;
-  hipLaunchKernelGGL((pf_gemm_kernel<MODE, TM, SH>), dim3(gx, gy, ks), dim3(kBlock), lds, s, b);
+  bool launched = false;
+  if constexpr (kDmaMode) {
+    if (dma) {
+      hipLaunchKernelGGL((pf_dma_kernel<MODE, TM>), dim3(gx, gy, ks), dim3(kBlock), 0, s, b);
+      launched = true;
+    }
+  }
+  if (!launched)
+    hipLaunchKernelGGL((pf_gemm_kernel<MODE, TM, SH>), dim3(gx, gy, ks), dim3(kBlock), lds, s, b);
   if (ks == 1) return hipGetLastError();
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;

@@ -36,6 +36,11 @@ def test_every_declared_symbol_is_exported():
         c_names = {l.split()[-1] for l in out.splitlines()
                    if l.split()[1:2] == ["T"] and not l.split()[-1].startswith("_Z")}
         assert c_names == declared, c_names ^ declared
+        # every kernel the library launches is defined in it (a missing host stub is an
+        # undefined symbol that only shows when the library is loaded on a GPU host)
+        undef = subprocess.run([nm, "-D", "--undefined-only", B.LIB_PATH], capture_output=True,
+                               text=True, check=True).stdout
+        assert not [l for l in undef.splitlines() if "tasp" in l], undef
 
 
 def _desc(**kw):
