@@ -32,10 +32,10 @@ def kind_of(name: str) -> str | None:
         (r"pf_attn_kernel", "prefill_attention"),
         (r"pf_rope_kernel", "rope_append"),
         (r"pf_prep_kernel|mfma_prep_kernel", "operand_prep"),
-        (r"gemv_kernel<1, 0>", "qkv_gemv"),
-        (r"gemv_kernel<1, 2>", "gateup_gemv"),
-        (r"gemv_kernel<1, 1>", "resid_gemv"),
-        (r"gemv_kernel<1, 3>", "lmhead_gemv"),
+        (r"gemv_kernel<1, 0[,>]", "qkv_gemv"),
+        (r"gemv_kernel<1, 2[,>]", "gateup_gemv"),
+        (r"gemv_kernel<1, 1[,>]", "resid_gemv"),
+        (r"gemv_kernel<1, 3[,>]", "lmhead_gemv"),
         (r"shared_gemv_kernel<0>", "qkv_shared"),
         (r"shared_gemv_kernel<2>", "gateup_shared"),
         (r"shared_gemv_kernel<1>", "resid_shared"),
@@ -46,9 +46,9 @@ def kind_of(name: str) -> str | None:
         (r"mfma_gemv_kernel<3,", "lmhead_mfma"),
         (r"pf_split_reduce_kernel<0>", "qkv_reduce"),
         (r"pf_split_reduce_kernel<1>", "resid_reduce"),
-        (r"pf_gemm_kernel<0,", "qkv_gemm"),
-        (r"pf_gemm_kernel<2,", "gateup_gemm"),
-        (r"pf_gemm_kernel<1,", "resid_gemm"),
+        (r"pf_(gemm|dma)_kernel<0,", "qkv_gemm"),
+        (r"pf_(gemm|dma)_kernel<2,", "gateup_gemm"),
+        (r"pf_(gemm|dma)_kernel<1,", "resid_gemm"),
         (r"pf_gemm_kernel<3,", "lmhead_gemm"),
         (r"router_features_kernel", "router_features"),
         (r"router_dense_kernel", "router_dense"),
