@@ -4,8 +4,8 @@
 // first-byte latency, the last wave's work) weigh as much as the stream.
 //
 // Work decomposition: rows are taken in groups (2 rows for QKV, O and down; 4 for the LM head;
-// for gate/up one SwiGLU channel = its gate and up rows). A tile is one group x 2 KiB of each of
-// its rows (2 chunks of 1 KiB; for gate/up one chunk); a wave reads whole contiguous KiB, 16 bytes
+// for gate/up one SwiGLU channel = its gate and up rows). A tile is one group x 1 KiB of each of
+// its rows (the LM head: 2 KiB); a wave reads whole contiguous KiB, 16 bytes
 // per lane. Several workgroups per CU and small tiles keep the slowest wave's share short. Each
 // wave owns a contiguous range of whole groups and walks its tiles with two register buffers in
 // ping-pong: the next tile's buffer loads are in flight while the current tile is dequantised and
@@ -32,7 +32,7 @@ namespace {
 // the BF16 LM head. At the 8B shapes 2-row groups measured 4-8 % faster per launch than 4-row
 // groups (twice the waves, half the bytes in flight per wave).
 constexpr int rows_per_group(int mode) { return mode == GEMV_LMHEAD ? 4 : 2; }
-constexpr int kC = 2;             // 1 KiB chunks per tile
+constexpr int kC = 2;             // 1 KiB chunks per tile of the LM head (INT8 projections: 1)
 constexpr int kWgPerCu = 4;
 constexpr int kNumCu = 256;
 constexpr size_t kMaxGemvLds = 159 * 1024;     // gfx950: 160 KiB of LDS per workgroup, minus statics
@@ -149,8 +149,10 @@ __device__ __forceinline__ void stage_inputs(const float* __restrict__ x, int ld
 template <int B, int MODE, int NW>
 __global__ __launch_bounds__(NW * kWave) __attribute__((amdgpu_waves_per_eu(4))) void gemv_kernel(GemvArgs a) {
   constexpr int kR = rows_per_group(MODE);
-  // 1 KiB chunks per tile: 1 for gate/up (measured 1.5 % faster than 2 or 4), 2 otherwise
-  constexpr int kC = (MODE == GEMV_GATEUP) ? 1 : ::tasp::kC;
+  // 1 KiB chunks per tile: 1 for the INT8 projections (gate/up 1.5 % faster than 2 or 4 at the 8B
+  // shape; QKV, O and down at the 70B shape 8.73 -> 8.65 ms per token, the 8B layer unchanged),
+  // 2 for the LM head
+  constexpr int kC = (MODE == GEMV_LMHEAD) ? ::tasp::kC : 1;
   constexpr bool BF = (MODE == GEMV_LMHEAD);
   constexpr bool NORM = (MODE != GEMV_RESID);
   constexpr int CPC = BF ? 512 : 1024;                 // columns per 1 KiB chunk
@@ -220,19 +222,13 @@ __global__ __launch_bounds__(NW * kWave) __attribute__((amdgpu_waves_per_eu(4)))
     }
   }
 
-  // Order of the first loads (measured per projection at the 8B shapes): the gate/up panel, the
-  // largest, is fastest with the input staged before any weight load (its input loads would
-  // otherwise queue behind the whole launch's weight stream); the smaller panels put their first
-  // tile in flight between the input loads and their use.
+  // The first weight tile is issued between the input loads and their use, so that the weight
+  // stream starts one memory latency before the staged input is ready (for gate/up too: at the
+  // 70B shape 8.86 -> 8.75 ms per token, neutral at the 8B layer).
   int4 wa[kC][kR], wb[kC][kR];
   float xscale[B], bias[B];
-  if (MODE == GEMV_GATEUP) {
-    stage_inputs<B, NORM, !BF, NW>(a.x, a.ldx, K, KP, a.gamma, a.eps, xs, red2, xscale, bias, [] {});
-    issue(t_begin, wa);
-  } else {
-    stage_inputs<B, NORM, !BF, NW>(a.x, a.ldx, K, KP, a.gamma, a.eps, xs, red2, xscale, bias,
-                                   [&] { issue(t_begin, wa); });
-  }
+  stage_inputs<B, NORM, !BF, NW>(a.x, a.ldx, K, KP, a.gamma, a.eps, xs, red2, xscale, bias,
+                                 [&] { issue(t_begin, wa); });
   issue(t_begin + 1, wb);
 #pragma unroll
   for (int r = 0; r < kR; ++r) {
