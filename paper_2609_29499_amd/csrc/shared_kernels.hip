@@ -8,7 +8,7 @@
 //   cols: plan piece of 16 columns -> store column of its first element (the retained heads'
 //         columns of W_o, the retained channel blocks of W_down), null for all columns.
 // Work decomposition follows the per-row kernel: groups of 2 rows (gate/up: one channel's gate
-// and up row), tiles of 2 x 1 KiB per row in the plan's column space, each wave a contiguous
+// and up row), tiles of 1 KiB per row in the plan's column space, each wave a contiguous
 // range of groups with two register buffers in ping-pong. A lane's 16 bytes lie in one piece,
 // hence in one scale group: it loads the group's BF16 scale with them, forms the 16-byte dot
 // product in float32 (byte XOR 0x80 converted exactly to b + 128) and adds
@@ -27,7 +27,7 @@ namespace {
 // groups (measured 7 % faster per 8B layer step).
 constexpr int kR = 2;
 constexpr int kCH = kR / 2;
-constexpr int kC = 2;
+constexpr int kC = 1;                 // 1 KiB chunks per tile (2 measured 1 % slower at the 8B layer)
 constexpr int kNumCu = 256;
 constexpr int kWgPerCu = 4;
 constexpr int kScaleGroup = 128;
