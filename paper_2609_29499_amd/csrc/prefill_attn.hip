@@ -1,7 +1,9 @@
 // Causal prefill attention on the matrix cores, over the retained heads only.
 //
-// Grid (query blocks of 64, retained heads): workgroup (qb, h) serves queries 64 qb .. 64 qb + 63
-// of retained head h, wave w the 16 queries 64 qb + 16 w + i. Cache rows 0 .. pos0 + last query of
+// Grid (retained heads, query blocks of 64): workgroup (h, qb) serves queries 64 qb .. 64 qb + 63
+// of retained head h, wave w the 16 queries 64 qb + 16 w + i. Query blocks are dealt last first
+// (blockIdx.y = 0 is the last block): the longest rows of the causal triangle start first and
+// the short ones fill in behind them. Cache rows 0 .. pos0 + last query of
 // the block are walked in sub-blocks of 64, staged in LDS once per workgroup (K row-major, V
 // transposed into units of 4 rows x 1 dimension), the next sub-block's rows loaded into registers
 // while the current one is computed; one barrier per sub-block. Per 16-row tile:
@@ -71,7 +73,7 @@ __global__ __launch_bounds__(kBlock) void pf_attn_kernel(PfAttnArgs a) {
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int r = lane & 15, c = lane >> 4;
-  const int qb = blockIdx.x, h = blockIdx.y;
+  const int h = blockIdx.x, qb = gridDim.y - 1 - blockIdx.y;
   int j = 0;                                            // group slot of head h
   while (j + 1 < a.m_kv && a.slot_start[j + 1] <= h) ++j;
   const int g = a.kv_idx[j];
@@ -235,7 +237,7 @@ hipError_t launch_pf_attn(const PfAttnArgs& a, hipStream_t s) {
   if (a.m_kv == 0 || a.T < 1) return hipSuccess;
   const int m_q = a.slot_start[a.m_kv];
   if (m_q < 1 || a.m_kv > 64) return hipErrorInvalidValue;
-  const dim3 grid((a.T + kQB - 1) / kQB, m_q);
+  const dim3 grid(m_q, (a.T + kQB - 1) / kQB);
   if (a.dh == 128) hipLaunchKernelGGL((pf_attn_kernel<128>), grid, dim3(kBlock), 0, s, a);
   else if (a.dh == 64) hipLaunchKernelGGL((pf_attn_kernel<64>), grid, dim3(kBlock), 0, s, a);
   else return hipErrorInvalidValue;
