@@ -6,6 +6,7 @@
 #   decode_b8:  kernel trace and FETCH_SIZE / WRITE_SIZE passes of the batch-8 benchmark
 #   decode_b8_busy: VALU and MFMA busy counters of the batch-8 benchmark's sparse plan
 #   prefill:    kernel trace and MFMA counter pass of the 512-token prefill benchmark
+#   prefill2048: kernel trace of the 2048-token prefill benchmark
 #   router:     kernel trace of the router benchmark (one 7 KiB turn, then 512-prompt batches)
 #   shared:     kernel trace of the shared-store benchmark (8B layer, batch 1)
 #   stack70:    kernel trace of the default benchmark (80-layer 70B stack, seed-1 mask then the
@@ -34,6 +35,9 @@ decode_b8_busy)
 prefill)
   echo "[prof] prefill kernel trace" && timeout -k 10 400 rocprofv3 --kernel-trace --stats -d $O/pf_trace -o trace -- python3 -u bench.py --workload llama3_8b_prefill512 --steps 200 --warmup 20 --cpu-seconds 3 > $O/pf_trace.json 2> $O/pf_trace.err &&
   echo "[prof] prefill MFMA counters" && timeout -s KILL 300 rocprofv3 --pmc MfmaUtil SQ_INSTS_VALU_MFMA_MOPS_BF16 SQ_BUSY_CU_CYCLES -d $O/pf_mfma -o mfma -- python3 -u bench.py --workload llama3_8b_prefill512 --no-cpu --steps 40 --warmup 4 > $O/pf_mfma.json 2> $O/pf_mfma.err
+  ;;
+prefill2048)
+  echo "[prof] prefill 2048 kernel trace" && timeout -k 10 400 rocprofv3 --kernel-trace --stats -d $O/pf2k_trace -o trace -- python3 -u bench.py --workload llama3_8b_prefill2048 --steps 50 --warmup 5 --cpu-seconds 3 > $O/pf2k_trace.json 2> $O/pf2k_trace.err
   ;;
 router)
   echo "[prof] router kernel trace" && timeout -k 10 400 rocprofv3 --kernel-trace --stats -d $O/rt_trace -o trace -- python3 -u bench.py --workload router_llama3_8b --steps 200 --warmup 20 --cpu-seconds 3 > $O/rt_trace.json 2> $O/rt_trace.err
