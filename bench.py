@@ -619,7 +619,7 @@ def bench_prefill(args, wl):
         del g, plans, caches
         torch.cuda.empty_cache()
     sp, dn = results["sparse"], results["dense"]
-    gu_ms = sp["kernels"]["gateup_gemv"]
+    gu_ms = sp["kernels"]["gateup_gemm"]
     gu_tf = sp["flops"]["gateup"] / (gu_ms * 1e-3) / 1e12
     line = {
         "metric": METRIC, "value": round(sp["ms"], 5), "unit": "ms/prefill", "n_gpus": 1,

@@ -22,6 +22,8 @@ IDX_Q, IDX_KV, IDX_QKVSLOT, IDX_FFN = 0, 1, 2, 3
 PANEL_QKV, PANEL_O, PANEL_GATE, PANEL_UP, PANEL_DOWN = 0, 1, 2, 3, 4
 KERNEL_KINDS = {0: "qkv_gemv", 1: "attention", 2: "o_gemv", 3: "gateup_gemv", 4: "down_gemv",
                 5: "lmhead_gemv", 6: "operand_prep", 7: "rope_append"}
+# the same stages in a prefill, where the projections are GEMMs over the prompt's tokens
+PREFILL_KINDS = {k: v.replace("_gemv", "_gemm") for k, v in KERNEL_KINDS.items()}
 
 EXPORTS = ["tasp_plan_workspace_bytes", "tasp_compile_plan", "tasp_plan_counts",
            "tasp_plan_indices", "tasp_plan_panel", "tasp_plan_ledger", "tasp_plan_destroy",
@@ -246,7 +248,7 @@ def tasp_prefill_timed(plan, x_ptr, T, cache, pos0, out_ptr, stream, cap=4096):
     n = C.c_int32()
     _check(load().tasp_prefill_timed(plan, x_ptr, T, C.byref(cache), pos0, out_ptr, stream, ms,
                                      kinds, cap, C.byref(n)))
-    return [(KERNEL_KINDS[kinds[i]], ms[i]) for i in range(n.value)]
+    return [(PREFILL_KINDS[kinds[i]], ms[i]) for i in range(n.value)]
 
 
 def tasp_decode_step_timed(plan, x_ptr, cache, pos, out_ptr, stream, cap=4096):
