@@ -182,6 +182,19 @@ def test_llama3_8b_prefill2048_full_size():
     _check_cache(case)
 
 
+@pytest.mark.timeout(600)
+def test_llama3_8b_prefill_ragged_wide_tiles():
+    """8B layer, seed-1 mask, 700 tokens after 48 prior positions: every projection's last
+    128-token tile holds 60 tokens, at the full width of the layer."""
+    _flush("case 8b prefill 700 at pos0 48")
+    sh = synth.LLAMA3_8B.with_layers(1, vocab=0)
+    case = PrefillCase(sh, synth.budget_mask(sh, 1), 700, 48)
+    got, want = case.run(), case.oracle()
+    m, s = assert_parity(got, want, what="prefill 8b 700")
+    _flush(f"  max_rel={m:.2e} sum_rel={s:.2e}")
+    _check_cache(case)
+
+
 def test_prefill_errors():
     _flush("case prefill errors")
     sh = SMALL
