@@ -183,8 +183,14 @@ struct PfAttnArgs {
   const uint16_t* kc; const uint16_t* vc;         // [Hkv][S][dh]
   int S, pos0, T;
   uint16_t* o; int ldo; uint32_t o_plane;         // hi/lo operand [2][T][ldo]
+  // split query blocks: partial records (part_floats, nullable: no split) and one counter per
+  // (retained head, query block), zero on entry and left zero
+  float* part; size_t part_floats; int* cnt; int cnt_len;
+  int split_sb;                                   // set by the launch: chunk length, 0 = none
 };
 hipError_t launch_pf_attn(const PfAttnArgs& a, hipStream_t s);
+// floats of the partial records a prefill of up to max_prefill tokens may need (n_q_heads heads)
+size_t pf_attn_record_floats(int max_prefill, int n_q_heads, int dh);
 
 // ----------------------------------------------------------------- request loop
 

@@ -1,12 +1,17 @@
 // Causal prefill attention on the matrix cores, over the retained heads only.
 //
-// Grid (retained heads, query blocks of 64): workgroup (h, qb) serves queries 64 qb .. 64 qb + 63
-// of retained head h, wave w the 16 queries 64 qb + 16 w + i. Query blocks are dealt last first
-// (blockIdx.y = 0 is the last block): the longest rows of the causal triangle start first and
-// the short ones fill in behind them. Cache rows 0 .. pos0 + last query of
-// the block are walked in sub-blocks of 64, staged in LDS once per workgroup (K row-major, V
-// transposed into units of 4 rows x 1 dimension), the next sub-block's rows loaded into registers
-// while the current one is computed; one barrier per sub-block. Per 16-row tile:
+// Grid (retained heads, work units): a unit serves queries 64 qb .. 64 qb + 63 of retained head h
+// (wave w the 16 queries 64 qb + 16 w + i) over cache rows 0 .. pos0 + last query of the block,
+// walked in sub-blocks of 64. Query blocks are dealt last first (blockIdx.y = 0 is the last
+// block): the longest rows of the causal triangle start first and the short ones fill in behind
+// them. A block whose rows span more than split_sb sub-blocks is served by two units (chunk 0:
+// sub-blocks 0 .. split_sb - 1, chunk 1: the rest), so that the last blocks do not leave the
+// chip waiting on one long chain: each writes its running maxima, sums and unnormalised outputs
+// to a record (device-coherent, in the lanes' own layout), counts itself done, and the second to
+// finish combines the other's record with its own registers (the scheme of the decode
+// attention's splits). Sub-blocks are staged in LDS once per workgroup (K row-major, V
+// transposed into units of 4 rows x 1 dimension), the next sub-block's rows loaded into
+// registers while the current one is computed; one barrier per sub-block. Per 16-row tile:
 //   * S^T = K Q^T on v_mfma_f32_16x16x32_bf16: K rows are the A operand, q (hi/lo BF16 planes, in
 //     base-2 units: q carries log2(e) / sqrt(d_h)) the B operand, so lane (r, c) receives the
 //     scores of query r against rows 4 c .. 4 c + 3 of the tile, which is exactly the A-operand
@@ -17,6 +22,8 @@
 //     the output holds query 4 c + i in lane (r, c), so the per-query rescale factors move there
 //     by a lane permute.
 // The output O / l is written as the hi/lo operand of the O projection.
+#include <algorithm>
+
 #include "device_common.hpp"
 #include "kernels.hpp"
 
@@ -61,6 +68,29 @@ __device__ __forceinline__ float lane_read(float v, int src) {
   return __int_as_float(__builtin_amdgcn_ds_bpermute(src << 2, __float_as_int(v)));
 }
 
+// sub-blocks of cache rows that query block qb attends
+__host__ __device__ inline int sub_blocks(const PfAttnArgs& a, int qb) {
+  const int kv_end = a.pos0 + (qb * kQB + kQB < a.T ? qb * kQB + kQB : a.T);
+  return (kv_end + kKB - 1) / kKB;
+}
+// A CU retires sub-blocks at about the same rate with one workgroup or two (the loop is
+// issue-bound), so the kernel takes about max(longest chain, all sub-blocks / CUs) sub-block
+// times. Blocks are split (in halves of the longest block's chain) only where the longest chain
+// dominates: at least kMinSplitChain sub-blocks and over 1.5 times the per-CU share. Measured on
+// the 8B layer: 512 tokens 22.3 -> 17.5 us; at 2048 tokens, where the share (37) exceeds the
+// chain (32), splitting made it slower (84 -> 86 us).
+constexpr int kMinSplitChain = 4;
+constexpr int kNumCuAttn = 256;
+int choose_split_sb(const PfAttnArgs& a, int m_q) {
+  const int nqb = (a.T + kQB - 1) / kQB;
+  const int longest = sub_blocks(a, nqb - 1);
+  long total = 0;
+  for (int qb = 0; qb < nqb; ++qb) total += sub_blocks(a, qb);
+  total *= m_q;
+  if (longest < kMinSplitChain || 2L * longest * kNumCuAttn <= 3L * total) return 0;
+  return (longest + 1) / 2;
+}
+
 template <int DH>
 __global__ __launch_bounds__(kBlock) void pf_attn_kernel(PfAttnArgs a) {
   constexpr int NKC = DH / 32;         // k chunks of the score MFMAs
@@ -73,13 +103,29 @@ __global__ __launch_bounds__(kBlock) void pf_attn_kernel(PfAttnArgs a) {
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int r = lane & 15, c = lane >> 4;
-  const int h = blockIdx.x, qb = gridDim.y - 1 - blockIdx.y;
+  const int h = blockIdx.x;
+  // unit -> (query block, chunk): blocks last first, each block's chunks in order
+  const int nqb = (a.T + kQB - 1) / kQB;
+  const int ssb = a.part ? a.split_sb : 0;
+  int qb = nqb - 1, ch = 0;
+  for (int u = blockIdx.y; qb >= 0; --qb) {
+    const int n = (ssb > 0 && sub_blocks(a, qb) > ssb) ? 2 : 1;
+    if (u < n) {
+      ch = u;
+      break;
+    }
+    u -= n;
+  }
+  if (qb < 0) return;                                   // past the units (not launched)
   int j = 0;                                            // group slot of head h
   while (j + 1 < a.m_kv && a.slot_start[j + 1] <= h) ++j;
   const int g = a.kv_idx[j];
   const int t_block = qb * kQB, t_first = t_block + 16 * wave;
   const int kv_end = a.pos0 + min(t_block + kQB, a.T);  // rows 0 .. kv_end - 1 are attended
   const int n_sb = (kv_end + kKB - 1) / kKB;
+  const bool split = ssb > 0 && n_sb > ssb;
+  const int sb_begin = (split && ch == 1) ? ssb : 0;
+  const int sb_end = (split && ch == 0) ? ssb : n_sb;
   const int wave_last = a.pos0 + min(t_first + 15, a.T - 1);   // last row this wave attends
   const uint16_t* kc = a.kc + size_t(g) * a.S * DH;
   const uint16_t* vc = a.vc + size_t(g) * a.S * DH;
@@ -141,11 +187,11 @@ __global__ __launch_bounds__(kBlock) void pf_attn_kernel(PfAttnArgs a) {
     }
   };
 
-  load_sb(0);
-  for (int sb = 0; sb < n_sb; ++sb) {
-    const int buf = sb & 1, tb = sb * kKB;
+  load_sb(sb_begin);
+  for (int sb = sb_begin; sb < sb_end; ++sb) {
+    const int buf = (sb - sb_begin) & 1, tb = sb * kKB;
     stage_sb(buf);                                      // this buffer's readers finished at sb - 2
-    if (sb + 1 < n_sb) load_sb(sb + 1);
+    if (sb + 1 < sb_end) load_sb(sb + 1);
     __syncthreads();
     if (tb > wave_last) continue;                       // every row of the sub-block is after the wave's queries
     // scores: tile ct, lane (r, c): query t_first + r, rows tb + 16 ct + 4 c + i
@@ -211,11 +257,56 @@ __global__ __launch_bounds__(kBlock) void pf_attn_kernel(PfAttnArgs a) {
       }
   }
 
+  float inv[4];
+  if (split) {
+    // record of (h, qb, ch): per wave, o[d][i] of every lane, then (max, sum) of every lane
+    constexpr int WREC = NDT * 4 * kWave + 2 * kWave;
+    const size_t rec_floats = size_t(4) * WREC;
+    const size_t slot = (size_t(h) * nqb + qb) * 2;
+    const __amdgpu_buffer_rsrc_t rp = make_rsrc(a.part, uint32_t(a.part_floats * 4u));
+    const uint32_t mine = uint32_t(((slot + ch) * rec_floats + size_t(wave) * WREC) * 4u);
+    const uint32_t other = uint32_t(((slot + 1 - ch) * rec_floats + size_t(wave) * WREC) * 4u);
+#pragma unroll
+    for (int d = 0; d < NDT; ++d)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) buf_store4f_device(o[d][i], rp, mine + uint32_t(((d * 4 + i) * kWave + lane) * 4));
+    buf_store4f_device(m_run, rp, mine + uint32_t((NDT * 4 * kWave + lane) * 4));
+    buf_store4f_device(l_run, rp, mine + uint32_t((NDT * 4 * kWave + kWave + lane) * 4));
+    __builtin_amdgcn_s_waitcnt(0);                      // this thread's record is at the coherence point
+    __syncthreads();                                    // ... and every thread's
+    __shared__ int last;
+    int* cnt = a.cnt + size_t(h) * nqb + qb;
+    if (tid == 0) {
+      last = __hip_atomic_fetch_add(cnt, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 1;
+      if (last) __hip_atomic_store(cnt, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    __syncthreads();
+    if (!last) return;
+    // the other chunk's maximum and sum of query t_first + r, and the combined weights; chunk 0
+    // holds row 0 for every query, so the combined maximum is finite
+    const float m_o = buf_load4f_device(rp, other + uint32_t((NDT * 4 * kWave + lane) * 4));
+    const float l_o = buf_load4f_device(rp, other + uint32_t((NDT * 4 * kWave + kWave + lane) * 4));
+    float oo[NDT][4];
+#pragma unroll
+    for (int d = 0; d < NDT; ++d)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) oo[d][i] = buf_load4f_device(rp, other + uint32_t(((d * 4 + i) * kWave + lane) * 4));
+    const float mm = fmaxf(m_run, m_o);
+    const float ws = __builtin_amdgcn_exp2f(m_run - mm), wo = __builtin_amdgcn_exp2f(m_o - mm);
+    const float lsum = l_run * ws + l_o * wo;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const float s_i = lane_read(ws, 4 * c + i), o_i = lane_read(wo, 4 * c + i);
+      inv[i] = 1.0f / lane_read(lsum, 4 * c + i);
+#pragma unroll
+      for (int d = 0; d < NDT; ++d) o[d][i] = o[d][i] * s_i + oo[d][i] * o_i;
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) inv[i] = 1.0f / lane_read(l_run, 4 * c + i);
+  }
   // O / l as the hi/lo operand of the O projection: lane (r, c) holds queries t_first + 4 c + i,
   // dimensions 16 d + r
-  float inv[4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i) inv[i] = 1.0f / lane_read(l_run, 4 * c + i);
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const int t = t_first + 4 * c + i;
@@ -233,11 +324,26 @@ __global__ __launch_bounds__(kBlock) void pf_attn_kernel(PfAttnArgs a) {
 
 }  // namespace
 
-hipError_t launch_pf_attn(const PfAttnArgs& a, hipStream_t s) {
-  if (a.m_kv == 0 || a.T < 1) return hipSuccess;
-  const int m_q = a.slot_start[a.m_kv];
-  if (m_q < 1 || a.m_kv > 64) return hipErrorInvalidValue;
-  const dim3 grid(m_q, (a.T + kQB - 1) / kQB);
+size_t pf_attn_record_floats(int max_prefill, int n_q_heads, int dh) {
+  const size_t nqb = size_t(std::max(max_prefill, 0) + kQB - 1) / kQB;
+  return nqb * size_t(std::max(n_q_heads, 0)) * 2 * 4 * (size_t(dh / 16) * 4 * kWave + 2 * kWave);
+}
+
+hipError_t launch_pf_attn(const PfAttnArgs& a0, hipStream_t s) {
+  if (a0.m_kv == 0 || a0.T < 1) return hipSuccess;
+  const int m_q = a0.slot_start[a0.m_kv];
+  if (m_q < 1 || a0.m_kv > 64) return hipErrorInvalidValue;
+  // blocks are split only when the records and counters of every (head, block) fit
+  PfAttnArgs a = a0;
+  const int nqb = (a.T + kQB - 1) / kQB;
+  if (!a.part || !a.cnt || a.part_floats < pf_attn_record_floats(a.T, m_q, a.dh) ||
+      a.part_floats * 4 >= size_t(kOOB) || long(a.cnt_len) < long(m_q) * nqb)
+    a.part = nullptr;
+  a.split_sb = a.part ? choose_split_sb(a, m_q) : 0;
+  if (a.split_sb == 0) a.part = nullptr;
+  int units = nqb;
+  for (int qb = 0; qb < nqb && a.part; ++qb) units += sub_blocks(a, qb) > a.split_sb ? 1 : 0;
+  const dim3 grid(m_q, units);
   if (a.dh == 128) hipLaunchKernelGGL((pf_attn_kernel<128>), grid, dim3(kBlock), 0, s, a);
   else if (a.dh == 64) hipLaunchKernelGGL((pf_attn_kernel<64>), grid, dim3(kBlock), 0, s, a);
   else return hipErrorInvalidValue;

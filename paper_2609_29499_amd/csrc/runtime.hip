@@ -144,7 +144,10 @@ struct Layout {
   size_t r_mid, r_io0, r_io1, qkv_buf, o_buf, h_buf, part, acnt;
   size_t xd, xo, xh, ssq;            // batched path: hi/lo operands and sums of squares
   size_t pxd, pxw, pq, pqkv, pr_mid, pr_io0, pr_io1, pssq;   // prefill scratch
-  size_t ppart, ppart_floats;                                // prefill K-split partials
+  size_t ppart, ppart_floats;                                // prefill K-split partials and
+                                                             // split attention records
+  size_t pacnt;                      // prefill attention: counter per (head, query block)
+  int pacnt_len = 0;
   size_t qkv_rows, o_cols, down_cols;                        // shared-store plans: maps
   size_t zero_begin, zero_end;       // scratch cleared at compile
   size_t total;
@@ -194,8 +197,12 @@ void scratch_layout(Layout& Y, const tasp_model_desc* d, Take&& take, size_t& of
   Y.pr_io0 = take(P * D * 4);
   Y.pr_io1 = take(P * D * 4);
   Y.pssq = take(P * ((D + 63) / 64) * 4);
+  Y.pacnt_len = int(size_t(Hq) * ((P + 63) / 64));
+  Y.pacnt = take(size_t(Y.pacnt_len) * 4);
   Y.zero_end = off;
-  Y.ppart_floats = P ? tasp::pf_split_buffer_floats(int(P), std::max(D, Y.ld_qkv)) : 0;
+  Y.ppart_floats = P ? std::max(tasp::pf_split_buffer_floats(int(P), std::max(D, Y.ld_qkv)),
+                                tasp::pf_attn_record_floats(int(P), Hq, dh))
+                     : 0;
   Y.ppart = take(Y.ppart_floats * 4);
 }
 
@@ -337,8 +344,10 @@ struct tasp_plan_s {
   int ld_xd, ld_xo, ld_xh;
   uint16_t *pxd, *pxw, *pq;          // prefill operands: [2][max_prefill][ld_xd | ld_xw], q planes
   float *pqkv, *pr_mid, *pr_io[2], *pssq;
-  float* ppart;                      // prefill K-split partials
+  float* ppart;                      // prefill K-split partials, split attention records
   size_t ppart_floats;
+  int* pacnt;                        // prefill attention counters, zero between launches
+  int pacnt_len;
   int ld_xw;
 };
 
@@ -371,6 +380,8 @@ void set_scratch(tasp_plan_s* p, const Layout& Y, char* ws) {
   p->pssq = reinterpret_cast<float*>(at(Y.pssq));
   p->ppart = reinterpret_cast<float*>(at(Y.ppart));
   p->ppart_floats = Y.ppart_floats;
+  p->pacnt = reinterpret_cast<int*>(at(Y.pacnt));
+  p->pacnt_len = Y.pacnt_len;
   p->ld_xw = Y.ld_xw;
 }
 
@@ -720,6 +731,7 @@ tasp_status prefill_impl(tasp_plan p, const float* x, int T, tasp_kv_cache* cach
       for (int q = 0; q <= P.m_kv; ++q) a.slot_start[q] = P.slot_start[q];
       a.kc = kc; a.vc = vc; a.S = cache->max_seq; a.pos0 = pos0; a.T = T;
       a.o = p->pxw; a.ldo = p->ld_xw; a.o_plane = plane_w;
+      a.part = p->ppart; a.part_floats = p->ppart_floats; a.cnt = p->pacnt; a.cnt_len = p->pacnt_len;
       if ((st = run_kernel(tm, 1, s, [&] { return tasp::launch_pf_attn(a, s); }))) return st;
     }
     {

@@ -60,12 +60,15 @@ def test_prefill_70b_width_split_k():
     _check_cache(case)
 
 
-def test_prefill_repeat_bit_exact():
-    """The QKV, O and down GEMMs of this prefill split K (2 to 4 splits per tile, summed in split
-    order by the reduction): repeated prefills give the same bits."""
-    _flush("case prefill repeat")
+@pytest.mark.parametrize("T,pos0", [(128, 0), (330, 100)])
+def test_prefill_repeat_bit_exact(T, pos0):
+    """The QKV, O and down GEMMs of these prefills split K (2 to 4 splits per tile, summed in split
+    order by the reduction), and at 330 tokens after 100 prior positions the attention splits its
+    longest query blocks over two workgroups (the second to finish combines the records, in an
+    order-independent way): repeated prefills give the same bits."""
+    _flush(f"case prefill repeat T={T} pos0={pos0}")
     sh = synth.TINY
-    case = PrefillCase(sh, synth.tiny_mask(sh), 128, 0)
+    case = PrefillCase(sh, synth.tiny_mask(sh), T, pos0)
     first = case.run()
     for _ in range(3):
         assert np.array_equal(case.run(), first)
