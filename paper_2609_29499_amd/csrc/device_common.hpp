@@ -127,11 +127,5 @@ __device__ __forceinline__ void buf_store8_device(const int2& v, __amdgpu_buffer
   __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(__attribute__((ext_vector_type(2))) unsigned, v),
                                         r, (int)off, 0, kCpolDevice);
 }
-__device__ __forceinline__ float buf_load4f_device(__amdgpu_buffer_rsrc_t r, uint32_t off) {
-  return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, (int)off, 0, kCpolDevice));
-}
-__device__ __forceinline__ void buf_store4f_device(float v, __amdgpu_buffer_rsrc_t r, uint32_t off) {
-  __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, v), r, (int)off, 0, kCpolDevice);
-}
 
 }  // namespace tasp

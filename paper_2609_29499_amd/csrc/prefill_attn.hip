@@ -50,6 +50,15 @@ __device__ __forceinline__ uint32_t cvt_bf16x2(float a, float b) {
   return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{a, b}, bf16x2_t));
 }
 
+// 4-byte device-coherent accesses (cache-policy bit sc1, as the 16-byte ones of the common
+// header) for the split records
+__device__ __forceinline__ float buf_load4f_device(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, (int)off, 0, kCpolDevice));
+}
+__device__ __forceinline__ void buf_store4f_device(float v, __amdgpu_buffer_rsrc_t r, uint32_t off) {
+  __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, v), r, (int)off, 0, kCpolDevice);
+}
+
 // reductions over the four lanes r, r + 16, r + 32, r + 48 (one query's lanes)
 __device__ __forceinline__ float quad_max(float v) {
   const auto p = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
