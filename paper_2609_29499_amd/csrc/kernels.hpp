@@ -198,7 +198,14 @@ size_t pf_attn_record_floats(int max_prefill, int n_q_heads, int dh);
 hipError_t launch_embed(const int8_t* table, const float* scale, int V, int d, const int* ids,
                         int n, float* x, hipStream_t s);
 // ids_out[r] = argmax of logits row r of n rows of V (lowest id among equal maxima)
-hipError_t launch_argmax(const float* logits, int n, int V, int* ids_out, hipStream_t s);
+// with part (2 floats per chunk of kArgmaxChunk logits and row) and cnt (one per row, zero on
+// entry and left zero) for n <= kArgmaxMaxRows rows of at most kArgmaxMaxChunks chunks, the rows
+// are split over workgroups; otherwise one workgroup per row
+constexpr int kArgmaxChunk = 4096;
+constexpr int kArgmaxMaxChunks = 256;
+constexpr int kArgmaxMaxRows = 8;
+hipError_t launch_argmax(const float* logits, int n, int V, int* ids_out, float* part, int* cnt,
+                         hipStream_t s);
 
 // ----------------------------------------------------------------- mask construction
 

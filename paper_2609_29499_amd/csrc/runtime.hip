@@ -148,6 +148,7 @@ struct Layout {
                                                              // split attention records
   size_t pacnt;                      // prefill attention: counter per (head, query block)
   int pacnt_len = 0;
+  size_t arg_part, arg_cnt;          // request loop: argmax partials and counters
   size_t qkv_rows, o_cols, down_cols;                        // shared-store plans: maps
   size_t zero_begin, zero_end;       // scratch cleared at compile
   size_t total;
@@ -199,7 +200,9 @@ void scratch_layout(Layout& Y, const tasp_model_desc* d, Take&& take, size_t& of
   Y.pssq = take(P * ((D + 63) / 64) * 4);
   Y.pacnt_len = int(size_t(Hq) * ((P + 63) / 64));
   Y.pacnt = take(size_t(Y.pacnt_len) * 4);
+  Y.arg_cnt = take(size_t(tasp::kArgmaxMaxRows) * 4);
   Y.zero_end = off;
+  Y.arg_part = take(size_t(tasp::kArgmaxMaxRows) * tasp::kArgmaxMaxChunks * 2 * 4);
   Y.ppart_floats = P ? std::max(tasp::pf_split_buffer_floats(int(P), std::max(D, Y.ld_qkv)),
                                 tasp::pf_attn_record_floats(int(P), Hq, dh))
                      : 0;
@@ -348,6 +351,8 @@ struct tasp_plan_s {
   size_t ppart_floats;
   int* pacnt;                        // prefill attention counters, zero between launches
   int pacnt_len;
+  float* arg_part;                   // argmax partials and counters (zero between launches)
+  int* arg_cnt;
   int ld_xw;
 };
 
@@ -382,6 +387,8 @@ void set_scratch(tasp_plan_s* p, const Layout& Y, char* ws) {
   p->ppart_floats = Y.ppart_floats;
   p->pacnt = reinterpret_cast<int*>(at(Y.pacnt));
   p->pacnt_len = Y.pacnt_len;
+  p->arg_part = reinterpret_cast<float*>(at(Y.arg_part));
+  p->arg_cnt = reinterpret_cast<int*>(at(Y.arg_cnt));
   p->ld_xw = Y.ld_xw;
 }
 
@@ -1623,11 +1630,12 @@ tasp_status generate_impl(tasp_plan p, const int8_t* embed, const float* embed_s
   const int n = T - pos0;
   HIP_TRY(tasp::launch_embed(embed, embed_scale, d.vocab, d.d_model, prompt + pos0, n, x_scratch, s));
   if ((st = prefill_checked(p, x_scratch, n, cache, pos0, logits, stream, nullptr)) != TASP_OK) return st;
-  HIP_TRY(tasp::launch_argmax(logits + size_t(n - 1) * d.vocab, 1, d.vocab, out_ids, s));
+  HIP_TRY(tasp::launch_argmax(logits + size_t(n - 1) * d.vocab, 1, d.vocab, out_ids, p->arg_part,
+                              p->arg_cnt, s));
   for (int i = 0; i < n_new; ++i) {
     HIP_TRY(tasp::launch_embed(embed, embed_scale, d.vocab, d.d_model, out_ids + i, 1, x_scratch, s));
     if ((st = decode_impl(p, x_scratch, cache, T + i, logits, stream, nullptr)) != TASP_OK) return st;
-    HIP_TRY(tasp::launch_argmax(logits, 1, d.vocab, out_ids + i + 1, s));
+    HIP_TRY(tasp::launch_argmax(logits, 1, d.vocab, out_ids + i + 1, p->arg_part, p->arg_cnt, s));
   }
   return TASP_OK;
 }
