@@ -264,6 +264,16 @@ tasp_status tasp_decode_step(tasp_plan plan, const float* x, tasp_kv_cache* cach
 tasp_status tasp_prefill(tasp_plan plan, const float* x, int32_t T, tasp_kv_cache* cache,
                          int32_t pos0, float* out, void* stream);
 
+/* The same prefill returning only the last token's logits (paper, Sec. "Dependency-Closed Masks
+ * and Cache-Consistent Routing" and Table "configuration": greedy decoding continues from the
+ * prompt's last position, so no other position's logits are needed). Arguments and errors as
+ * tasp_prefill, with out (device, not overlapping x) float32 [vocab]: the final RMSNorm and LM
+ * head of token T - 1 only, by the decode LM head kernel (TASP_ERR_UNSUPPORTED without an LM
+ * head). The cache rows and every other effect are those of tasp_prefill. tasp_generate and
+ * tasp_serve_turn prefill this way. */
+tasp_status tasp_prefill_last(tasp_plan plan, const float* x, int32_t T, tasp_kv_cache* cache,
+                              int32_t pos0, float* out, void* stream);
+
 /* One request under the plan (paper, Sec. "Dependency-Closed Masks and Cache-Consistent Routing":
  * the plan stays fixed through prefill and every decode step; Table "configuration": the timed
  * request is a prefill followed by greedy decoding). The prompt's ids (device int32 [T]) are

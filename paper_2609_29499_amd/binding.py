@@ -28,7 +28,8 @@ PREFILL_KINDS = {k: v.replace("_gemv", "_gemm") for k, v in KERNEL_KINDS.items()
 EXPORTS = ["tasp_plan_workspace_bytes", "tasp_compile_plan", "tasp_plan_counts",
            "tasp_plan_indices", "tasp_plan_panel", "tasp_plan_ledger", "tasp_plan_destroy",
            "tasp_shared_plan_workspace_bytes", "tasp_compile_shared_plan",
-           "tasp_kv_bind", "tasp_decode_step", "tasp_prefill", "tasp_prefill_timed", "tasp_generate",
+           "tasp_kv_bind", "tasp_decode_step", "tasp_prefill", "tasp_prefill_last", "tasp_prefill_timed",
+           "tasp_generate",
            "tasp_decode_step_timed",
            "tasp_profile_stage", "tasp_mask_workspace_bytes", "tasp_build_mask",
            "tasp_router_workspace_bytes", "tasp_route", "tasp_route_noalloc", "tasp_serve_turn", "tasp_copy_probe",
@@ -125,6 +126,7 @@ def load(path: str = LIB_PATH):
         "tasp_kv_bind": [P, C.POINTER(tasp_kv_cache)],
         "tasp_decode_step": [P, P, C.POINTER(tasp_kv_cache), I32, P, P],
         "tasp_prefill": [P, P, I32, C.POINTER(tasp_kv_cache), I32, P, P],
+        "tasp_prefill_last": [P, P, I32, C.POINTER(tasp_kv_cache), I32, P, P],
         "tasp_generate": [P, P, P, P, I32, I32, C.POINTER(tasp_kv_cache), P, P, P, P],
         "tasp_prefill_timed": [P, P, I32, C.POINTER(tasp_kv_cache), I32, P, P, C.POINTER(C.c_float),
                                C.POINTER(I32), I32, C.POINTER(I32)],
@@ -234,6 +236,10 @@ def tasp_decode_step(plan, x_ptr, cache, pos, out_ptr, stream):
 
 def tasp_prefill(plan, x_ptr, T, cache, pos0, out_ptr, stream):
     _check(load().tasp_prefill(plan, x_ptr, T, C.byref(cache), pos0, out_ptr, stream))
+
+
+def tasp_prefill_last(plan, x_ptr, T, cache, pos0, out_ptr, stream):
+    _check(load().tasp_prefill_last(plan, x_ptr, T, C.byref(cache), pos0, out_ptr, stream))
 
 
 def tasp_generate(plan, embed_ptr, scale_ptr, prompt_ptr, T, n_new, cache, out_ids_ptr, x_ptr,

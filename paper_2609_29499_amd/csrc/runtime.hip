@@ -697,8 +697,10 @@ tasp::PfArgs pf_base(const tasp_plan_s* p, int T) {
   return a;
 }
 
+// last_only: with an LM head, only the last token's logits (out [vocab]), by the decode LM head
+// GEMV over that token's final residual (greedy decoding needs no other row)
 tasp_status prefill_impl(tasp_plan p, const float* x, int T, tasp_kv_cache* cache, int pos0,
-                         float* out, hipStream_t s, Timer* tm) {
+                         float* out, hipStream_t s, Timer* tm, bool last_only = false) {
   const tasp_model_desc& d = p->desc;
   const int D = d.d_model, dh = d.head_dim, L = d.n_layers, Pm = d.max_prefill;
   const uint32_t plane_d = uint32_t(size_t(Pm) * p->ld_xd);
@@ -775,7 +777,15 @@ tasp_status prefill_impl(tasp_plan p, const float* x, int T, tasp_kv_cache* cach
         return st;
     }
   }
-  if (d.vocab) {
+  if (d.vocab && last_only) {
+    tasp::GemvArgs a{};
+    a.w = p->lm_head; a.N = d.vocab; a.K = D; a.ld = 2 * D;
+    a.x = p->pr_io[(L - 1) & 1] + size_t(T - 1) * D; a.ldx = D;
+    a.gamma = p->final_norm; a.eps = d.rms_eps; a.y = out; a.ldy = d.vocab;
+    a.B = 1;
+    if ((st = run_kernel(tm, 5, s, [&] { return tasp::launch_gemv(tasp::GEMV_LMHEAD, a, s); })))
+      return st;
+  } else if (d.vocab) {
     tasp::PfArgs a = pf_base(p, T);
     a.w = p->lm_head; a.N = d.vocab; a.K = D; a.ld = D; a.x = p->pxd; a.ldx = p->ld_xd;
     a.plane = plane_d; a.ssq = p->pssq; a.y = out; a.ldy = d.vocab;
@@ -786,7 +796,8 @@ tasp_status prefill_impl(tasp_plan p, const float* x, int T, tasp_kv_cache* cach
 }
 
 tasp_status prefill_checked(tasp_plan p, const float* x, int32_t T, tasp_kv_cache* cache,
-                            int32_t pos0, float* out, void* stream, Timer* tm) {
+                            int32_t pos0, float* out, void* stream, Timer* tm,
+                            bool last_only = false) {
   if (!p) return fail(TASP_ERR_INVALID_ARG, "plan is NULL");
   if (!x || !out) return fail(TASP_ERR_INVALID_ARG, "x / out is NULL");
   tasp_status st = check_cache(p, cache);
@@ -798,13 +809,15 @@ tasp_status prefill_checked(tasp_plan p, const float* x, int32_t T, tasp_kv_cach
   if (pos0 > 0 && cache->plan_sig != p->sig)
     return fail(TASP_ERR_CACHE_PLAN_MISMATCH, "cache belongs to plan %016llx, not %016llx",
                 (unsigned long long)cache->plan_sig, (unsigned long long)p->sig);
-  const size_t out_elems = size_t(T) * (p->desc.vocab ? p->desc.vocab : p->desc.d_model);
+  if (last_only && p->desc.vocab < 1) return fail(TASP_ERR_UNSUPPORTED, "plan has no LM head");
+  const size_t out_elems = last_only ? size_t(p->desc.vocab)
+                                     : size_t(T) * (p->desc.vocab ? p->desc.vocab : p->desc.d_model);
   const char* xb = reinterpret_cast<const char*>(x);
   const char* ob = reinterpret_cast<const char*>(out);
   if (ob < xb + size_t(T) * p->desc.d_model * 4 && xb < ob + out_elems * 4)
     return fail(TASP_ERR_INVALID_ARG, "x and out overlap");
   if (pos0 == 0) cache->plan_sig = p->sig;             // a fresh sequence binds the cache
-  return prefill_impl(p, x, T, cache, pos0, out, static_cast<hipStream_t>(stream), tm);
+  return prefill_impl(p, x, T, cache, pos0, out, static_cast<hipStream_t>(stream), tm, last_only);
 }
 
 // one decode step of a shared-store plan (batch 1): the per-row kernels' sequence with the
@@ -1514,6 +1527,11 @@ tasp_status tasp_prefill(tasp_plan p, const float* x, int32_t T, tasp_kv_cache* 
   return prefill_checked(p, x, T, cache, pos0, out, stream, nullptr);
 }
 
+tasp_status tasp_prefill_last(tasp_plan p, const float* x, int32_t T, tasp_kv_cache* cache,
+                              int32_t pos0, float* out, void* stream) {
+  return prefill_checked(p, x, T, cache, pos0, out, stream, nullptr, true);
+}
+
 tasp_status tasp_prefill_timed(tasp_plan p, const float* x, int32_t T, tasp_kv_cache* cache,
                                int32_t pos0, float* out, void* stream, float* kernel_ms,
                                int32_t* kinds, int32_t cap, int32_t* n) {
@@ -1629,7 +1647,9 @@ tasp_status generate_impl(tasp_plan p, const int8_t* embed, const float* embed_s
   hipStream_t s = static_cast<hipStream_t>(stream);
   const int n = T - pos0;
   HIP_TRY(tasp::launch_embed(embed, embed_scale, d.vocab, d.d_model, prompt + pos0, n, x_scratch, s));
-  if ((st = prefill_checked(p, x_scratch, n, cache, pos0, logits, stream, nullptr)) != TASP_OK) return st;
+  if ((st = prefill_checked(p, x_scratch, n, cache, pos0, logits + size_t(n - 1) * d.vocab, stream,
+                           nullptr, true)) != TASP_OK)
+    return st;
   HIP_TRY(tasp::launch_argmax(logits + size_t(n - 1) * d.vocab, 1, d.vocab, out_ids, p->arg_part,
                               p->arg_cnt, s));
   for (int i = 0; i < n_new; ++i) {

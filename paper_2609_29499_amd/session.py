@@ -221,6 +221,11 @@ class Plan:
         B.tasp_prefill(self.handle, x.data_ptr(), T, cache.struct, pos0, out.data_ptr(),
                        stream if stream is not None else current_stream())
 
+    def prefill_last(self, x, T, cache, pos0, out, stream=None):
+        """The prefill with the last token's logits only: out is float32 [vocab]."""
+        B.tasp_prefill_last(self.handle, x.data_ptr(), T, cache.struct, pos0, out.data_ptr(),
+                            stream if stream is not None else current_stream())
+
     def generate(self, embed, embed_scale, prompt, n_new, cache, stream=None, scratch=None):
         """Prompt ids (device int32 [T]) -> n_new + 1 greedy ids (device int32). ``scratch`` may
         pass (x [T][d], logits [T][vocab]) float32 device tensors to reuse."""

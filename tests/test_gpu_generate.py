@@ -31,12 +31,13 @@ def _embed(table, scales, ids):
 
 def _stepped_logits(plan, desc, table, scales, prompt, ids, S_):
     """The plan's logits at every step of the request, stepped from the host: prefill of the
-    prompt, then one decode step per generated id (the device loop's kernels on the same inputs)."""
+    prompt (last token's logits only, as the device loop), then one decode step per generated id
+    (the device loop's kernels on the same inputs)."""
     T, V = len(prompt), desc.vocab
     cache = S.KVCache(desc, 1, S_)
-    out = torch.empty((T, V), device="cuda")
-    plan.prefill(torch.from_numpy(_embed(table, scales, prompt)).cuda(), T, cache, 0, out)
-    rows = [out[T - 1].clone()]
+    out = torch.empty((V,), device="cuda")
+    plan.prefill_last(torch.from_numpy(_embed(table, scales, prompt)).cuda(), T, cache, 0, out)
+    rows = [out.clone()]
     o1 = torch.empty((1, V), device="cuda")
     for s_, i in enumerate(ids[:-1]):
         plan.decode(torch.from_numpy(_embed(table, scales, [i])).cuda(), cache, T + s_, o1)

@@ -122,6 +122,38 @@ def test_prefill_stack_with_lm_head():
     assert (got.argmax(axis=1) == want.argmax(axis=1)).all()
 
 
+def test_prefill_last_logits():
+    """tasp_prefill_last: the last token's logits (the decode LM head over its final residual) at
+    parity with the full prefill's last row and the oracle's, with the same cache rows, bit for
+    bit; refused for a plan without an LM head."""
+    _flush("case prefill last logits")
+    sh = synth.tiny_shape(d=256, hq=8, hkv=2, dh=64, f=512, layers=3, vocab=3000)
+    for T, pos0 in ((40, 0), (130, 20)):
+        case = PrefillCase(sh, synth.raw_mask(sh, 6), T, pos0, max_seq=pos0 + T)
+        init = [(case.cache.bits("k", l).copy(), case.cache.bits("v", l).copy())
+                for l in range(sh.n_layers)]
+        full = case.run()
+        full_k = [case.cache.bits("k", l).copy() for l in range(sh.n_layers)]
+        full_v = [case.cache.bits("v", l).copy() for l in range(sh.n_layers)]
+        for l, (k0, v0) in enumerate(init):             # the cache as it was before the prefill
+            case.cache.load_layer(l, k0, v0)
+        last = torch.full((sh.vocab,), float("nan"), device="cuda")
+        case.plan.prefill_last(case.xd, T, case.cache, pos0, last)
+        torch.cuda.synchronize()
+        got = last.cpu().numpy().astype(np.float64)
+        for l in range(sh.n_layers):
+            assert np.array_equal(case.cache.bits("k", l), full_k[l])
+            assert np.array_equal(case.cache.bits("v", l), full_v[l])
+        want = case.oracle()[T - 1]
+        assert_parity(got, want, what=f"prefill last logits T={T}")
+        assert_parity(got, full[T - 1], what=f"prefill last vs full T={T}")
+        assert int(got.argmax()) == int(want.argmax())
+    nolm = PrefillCase(synth.tiny_shape(d=256, hq=8, hkv=2, dh=64, f=512, layers=1), None, 8, 0)
+    with pytest.raises(B.TaspError) as e:
+        nolm.plan.prefill_last(nolm.xd, 8, nolm.cache, 0, torch.empty(256, device="cuda"))
+    assert B.STATUS[e.value.status] == "TASP_ERR_UNSUPPORTED"
+
+
 def test_prefill_then_decode():
     """The cache a GPU prefill leaves is the one the decode path continues from: prefill 100
     tokens, then decode token 100 on the GPU; compare with the oracle doing the same."""
