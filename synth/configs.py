@@ -79,6 +79,9 @@ WORKLOADS = {
     # one 8B-shaped layer: the request's 2048-token prefill from an empty cache
     "llama3_8b_prefill2048": Workload("llama3_8b_prefill2048", LLAMA3_8B.with_layers(1, vocab=0),
                                       batch=1, pos=0, prefill_tokens=2048, mask_seeds=(1,)),
+    # one 70B-shaped layer: the request's 2048-token prefill from an empty cache
+    "llama3_70b_prefill2048": Workload("llama3_70b_prefill2048", LLAMA3_70B.with_layers(1, vocab=0),
+                                       batch=1, pos=0, prefill_tokens=2048, mask_seeds=(1,)),
     # the paper's timed request: 2048-token prompt, then 256 greedy decode steps, one plan
     "llama3_8b_request": Workload("llama3_8b_request", LLAMA3_8B, batch=1, pos=0,
                                   prefill_tokens=2048, kind="request", n_new=256),
