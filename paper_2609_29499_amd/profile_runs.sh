@@ -1,6 +1,6 @@
 #!/bin/bash
 # rocprofv3 runs behind the committed summaries in profiles/ (run from the repository root on
-# a GPU host; raw results go to gpurun_out/).
+# a GPU host; raw results go to $TASP_PROFILE_OUT, by default ./profile_out).
 #   decode_b1:  kernel trace of the default benchmark (8B layer, batch 1), then FETCH_SIZE and
 #               WRITE_SIZE passes of its sparse plan
 #   decode_b8:  kernel trace and FETCH_SIZE / WRITE_SIZE passes of the batch-8 benchmark
@@ -15,7 +15,7 @@
 set -o pipefail
 export TMPDIR=/tmp
 R=$(pwd)
-O=$R/gpurun_out
+O=${TASP_PROFILE_OUT:-$R/profile_out}
 mkdir -p $O
 which=${1:-decode_b1}
 case $which in
