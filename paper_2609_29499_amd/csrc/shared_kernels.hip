@@ -13,8 +13,8 @@
 // hence in one scale group: it loads the group's BF16 scale with them, forms the 16-byte dot
 // product in float32 (byte XOR 0x80 converted exactly to b + 128) and adds
 // scale * (dot - 128 * sum of the piece's 16 inputs); the piece sums are staged in LDS with the
-// input. The column map is staged in LDS; a kernel without one issues its first tile before
-// staging, as the per-row kernel does.
+// input. The column map is staged in LDS for all tiles but each wave's first, whose map entries
+// every lane loads itself.
 #include <algorithm>
 
 #include "device_common.hpp"
@@ -42,7 +42,8 @@ __device__ __forceinline__ float dot_bytes(uint32_t word, const float4& x, float
 }
 
 template <int MODE>
-__global__ __launch_bounds__(kBlock) void shared_gemv_kernel(SharedGemvArgs a) {
+__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) void shared_gemv_kernel(
+    SharedGemvArgs a) {
   constexpr bool NORM = (MODE != GEMV_RESID);
   extern __shared__ __attribute__((aligned(16))) float lds[];
   __shared__ float red[4];
@@ -72,7 +73,10 @@ __global__ __launch_bounds__(kBlock) void shared_gemv_kernel(SharedGemvArgs a) {
   auto row_of = [&](int gi, int r) {
     return (MODE == GEMV_GATEUP) ? gi * kCH + (r % kCH) : gi * kR + r;
   };
-  auto issue = [&](int t, int4 (&w)[kC][kR], uint32_t (&sv)[kC][kR]) {
+  // first: the column-map entries come from c_first (the lane's own, loaded from memory) instead
+  // of the staged map
+  auto issue = [&](int t, int4 (&w)[kC][kR], uint32_t (&sv)[kC][kR], const int (&c_first)[kC],
+                   bool first) {
     const bool ok_t = t < t_end;
     const int gi = ok_t ? t / KB : 0;
     const int kb = t - gi * KB;
@@ -85,7 +89,7 @@ __global__ __launch_bounds__(kBlock) void shared_gemv_kernel(SharedGemvArgs a) {
 #pragma unroll
     for (int u = 0; u < kC; ++u) {
       const int k = (kb * kC + u) * 1024 + lane * 16;
-      const int scol = (a.cols && k < K) ? cmap[k >> 4] : k;
+      const int scol = (a.cols && k < K) ? (first ? c_first[u] : cmap[k >> 4]) : k;
 #pragma unroll
       for (int r = 0; r < kR; ++r) {
         const bool ok = srow[r] >= 0 && k < K;
@@ -101,36 +105,81 @@ __global__ __launch_bounds__(kBlock) void shared_gemv_kernel(SharedGemvArgs a) {
 
   int4 wa[kC][kR], wb[kC][kR];
   uint32_t sa[kC][kR], sb[kC][kR];
-  if (!a.cols) issue(t_begin, wa, sa);                   // in flight during the staging
 
-  // stage x (times the gain) swizzled, the sums of its 16-column pieces and the column map
+  // Staging. The wave's first tile is issued between the first batch of input loads and their
+  // use: vector loads retire in issue order, so waiting for that batch then does not wait for
+  // the weights, and the weight stream starts one memory latency before the input is ready. A
+  // column-mapped kernel first loads each lane's map entries of that tile itself (ahead of the
+  // inputs, so that waiting for them does not wait for the inputs either); the rest of the map
+  // rides with the input batches. Every load of a batch is issued (out-of-range offsets return
+  // zeros) and consumed, so that the wait counts are the same on every path.
+  const __amdgpu_buffer_rsrc_t rc = make_rsrc(a.cols, a.cols ? uint32_t(K >> 4) * 4u : 0u);
+  int c_first[kC];
   {
+    const int kb0 = t_begin - (t_begin / KB) * KB;
+#pragma unroll
+    for (int u = 0; u < kC; ++u) {
+      const int q = (kb0 * kC + u) * 64 + lane;
+      c_first[u] = __builtin_amdgcn_raw_buffer_load_b32(rc, t_begin < t_end ? q * 4 : int(kOOB), 0, 0);
+    }
+  }
+  {
+    // float4 loads per thread in flight: a second batch waits for the first tile as well (loads
+    // retire in order), so the gain-free kernels, with registers to spare, take 12 (the 8B
+    // down projection's retained channels in one batch)
+    constexpr int kSB = NORM ? 8 : 12;
     const int n4 = K >> 2;
-    const int npass = KP >> 10;
+    const int npass = KP >> 10;                          // one float4 per thread per pass
     const __amdgpu_buffer_rsrc_t rx = make_rsrc(a.x, uint32_t(n4) * 16u);
     const __amdgpu_buffer_rsrc_t rg = make_rsrc(a.gamma, uint32_t(NORM ? K : 0) * 2u);
     float ss = 0.0f;
-    for (int i = 0; i < npass; ++i) {
-      const int c4 = (i << 8) + tid;
-      float4 v = __builtin_bit_cast(float4, buf_load16(rx, c4 < n4 ? uint32_t(c4) * 16u : kOOB));
-      if (NORM) {
-        const int2 g = __builtin_bit_cast(int2, __builtin_amdgcn_raw_buffer_load_b64(
-                                                    rg, c4 < n4 ? int(uint32_t(c4) * 8u) : int(kOOB), 0, 0));
-        ss = fmaf(v.x, v.x, fmaf(v.y, v.y, fmaf(v.z, v.z, fmaf(v.w, v.w, ss))));
-        v.x *= bf16_lo(uint32_t(g.x));
-        v.y *= bf16_hi(uint32_t(g.x));
-        v.z *= bf16_lo(uint32_t(g.y));
-        v.w *= bf16_hi(uint32_t(g.y));
+    int4 xv[kSB];
+    int2 gv[NORM ? kSB : 1];
+    int cm[kSB];
+    auto load_batch = [&](int i0) {
+#pragma unroll
+      for (int u = 0; u < kSB; ++u) {
+        const int c4 = ((i0 + u) << 8) + tid;          // float4 slot; piece c4 / 4
+        const bool ok = i0 + u < npass && c4 < n4;
+        xv[u] = buf_load16(rx, ok ? uint32_t(c4) * 16u : kOOB);
+        if constexpr (NORM)
+          gv[u] = __builtin_bit_cast(int2, __builtin_amdgcn_raw_buffer_load_b64(
+                                               rg, ok ? int(uint32_t(c4) * 8u) : int(kOOB), 0, 0));
+        cm[u] = __builtin_amdgcn_raw_buffer_load_b32(rc, ok ? (c4 >> 2) * 4 : int(kOOB), 0, 0);
       }
-      const int k = c4 << 2;
-      *reinterpret_cast<float4*>(xs + xs_slot_i8(k)) = v;
-      // a piece is four consecutive float4 slots, held by four consecutive lanes
-      float p = (v.x + v.y) + (v.z + v.w);
-      p += dpp<kQuadXor1>(p);
-      p += dpp<kQuadXor2>(p);
-      if ((tid & 3) == 0) xsum[c4 >> 2] = p;
+    };
+    auto store_batch = [&](int i0) {
+#pragma unroll
+      for (int u = 0; u < kSB; ++u) {
+        const int c4 = ((i0 + u) << 8) + tid;
+        float4 v = __builtin_bit_cast(float4, xv[u]);
+        if constexpr (NORM) {
+          ss = fmaf(v.x, v.x, fmaf(v.y, v.y, fmaf(v.z, v.z, fmaf(v.w, v.w, ss))));
+          v.x *= bf16_lo(uint32_t(gv[u].x));
+          v.y *= bf16_hi(uint32_t(gv[u].x));
+          v.z *= bf16_lo(uint32_t(gv[u].y));
+          v.w *= bf16_hi(uint32_t(gv[u].y));
+        }
+        // a piece is four consecutive float4 slots, held by four consecutive lanes
+        float p = (v.x + v.y) + (v.z + v.w);
+        p += dpp<kQuadXor1>(p);
+        p += dpp<kQuadXor2>(p);
+        if (i0 + u < npass) {
+          *reinterpret_cast<float4*>(xs + xs_slot_i8(c4 << 2)) = v;
+          if ((tid & 3) == 0) {
+            xsum[c4 >> 2] = p;
+            cmap[c4 >> 2] = cm[u];
+          }
+        }
+      }
+    };
+    load_batch(0);
+    issue(t_begin, wa, sa, c_first, true);
+    store_batch(0);
+    for (int i0 = kSB; i0 < npass; i0 += kSB) {
+      load_batch(i0);
+      store_batch(i0);
     }
-    for (int q = tid; q < NP; q += kBlock) cmap[q] = (a.cols && q < (K >> 4)) ? a.cols[q] : (q << 4);
     if (NORM) {
       ss = wave_sum(ss);
       if (lane == 0) red[tid >> 6] = ss;
@@ -138,7 +187,6 @@ __global__ __launch_bounds__(kBlock) void shared_gemv_kernel(SharedGemvArgs a) {
     __syncthreads();
   }
   const float xscale = NORM ? rsqrtf((red[0] + red[1] + red[2] + red[3]) / float(K) + a.eps) : 1.0f;
-  if (a.cols) issue(t_begin, wa, sa);
 
   float acc[kR], res[kR];
   auto process = [&](const int4 (&w)[kC][kR], const uint32_t (&sv)[kC][kR], int t) {
@@ -193,9 +241,9 @@ __global__ __launch_bounds__(kBlock) void shared_gemv_kernel(SharedGemvArgs a) {
   };
 
   for (int t = t_begin; t < t_end; t += 2) {
-    issue(t + 1, wb, sb);
+    issue(t + 1, wb, sb, c_first, false);
     process(wa, sa, t);
-    issue(t + 2, wa, sa);
+    issue(t + 2, wa, sa, c_first, false);
     if (t + 1 < t_end) process(wb, sb, t + 1);
   }
 }
