@@ -75,6 +75,19 @@ def test_llama3_8b_layer_budget_mask():
     _check(Case(sh, synth.budget_mask(sh, 1), 1, 2048, shared=True))
 
 
+def test_wide_inputs_staged_in_several_batches():
+    """Inputs wider than one batch of staging loads: a gain-applying projection with K = 8320
+    (more than 8 float4 loads per thread) and a down projection with 12416 retained channels (more
+    than 12), dense and under a block mask, plus the dense 8B layer (down K = 14336)."""
+    sh = synth.tiny_shape(d=8320, hq=8, hkv=2, dh=128, f=12416, layers=1)
+    _flush("case shared wide inputs dense")
+    _check(Case(sh, None, 1, 37, shared=True))
+    _flush("case shared wide inputs block mask")
+    _check(Case(sh, synth.raw_mask(sh, 11, block=16), 1, 37, shared=True))
+    _flush("case shared 8B layer dense")
+    _check(Case(synth.LLAMA3_8B.with_layers(1, vocab=0), None, 1, 40, shared=True))
+
+
 def test_graph_replay_and_timed_kernels():
     _flush("case shared graph replay")
     sh = synth.tiny_shape(layers=2, **TINY)
