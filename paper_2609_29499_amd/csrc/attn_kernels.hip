@@ -479,12 +479,15 @@ __device__ __forceinline__ void attn_mfma_body(const AttnArgs& a, AttnMfmaSmem<D
   const int h0 = a.slot_start[j];
   const int t0 = s * a.chunk;
   const int t1 = (s == a.n_split - 1) ? a.pos + 1 : t0 + a.chunk;
-  const int n_tiles = (t1 - t0 + 15) / 16;
+  const bool has_new = (t1 == a.pos + 1);
+  // the tiles cover the split's cache rows [t0, tr); the new row (pos) of the last split is
+  // folded into its record after them, so that split runs as many tiles as the others
+  const int tr = has_new ? a.pos : t1;
+  const int n_tiles = (tr - t0 + 15) / 16;
   const float* qkv = a.qkv + size_t(b) * a.ld_qkv;
   const size_t row_base = (size_t(b) * a.Hkv + g) * a.S;
   uint16_t* kc = a.kc + row_base * DH;
   uint16_t* vc = a.vc + row_base * DH;
-  const bool has_new = (t1 == a.pos + 1);
   // this group's cache rows 0..pos-1 (row pos comes from LDS)
   const uint32_t group_bytes = uint32_t(a.pos) * DH * 2u;
   const __amdgpu_buffer_rsrc_t rk = make_rsrc(kc, group_bytes);
@@ -518,13 +521,13 @@ __device__ __forceinline__ void attn_mfma_body(const AttnArgs& a, AttnMfmaSmem<D
     const int tk = tb + r;
 #pragma unroll
     for (int kk = 0; kk < NKC; ++kk)
-      f.k[kk] = buf_load16_stream(rk, (ti < n_tiles && tk < t1)
+      f.k[kk] = buf_load16_stream(rk, (ti < n_tiles && tk < tr)
                                           ? uint32_t(tk) * (DH * 2u) + uint32_t(32 * kk + 8 * qq) * 2u
                                           : kOOB);
 #pragma unroll
     for (int u = 0; u < RPG; ++u) {
       const int tv = tb + rg * RPG + u;
-      f.v[u] = buf_load16_stream(rv, (ti < n_tiles && tv < t1)
+      f.v[u] = buf_load16_stream(rv, (ti < n_tiles && tv < tr)
                                          ? uint32_t(tv) * (DH * 2u) + uint32_t(c) * 16u : kOOB);
     }
   };
@@ -588,16 +591,9 @@ __device__ __forceinline__ void attn_mfma_body(const AttnArgs& a, AttnMfmaSmem<D
     const int tb = t0 + 16 * ti;
     // scores
     f32x4_t sc = {0.0f, 0.0f, 0.0f, 0.0f};
-    const bool knew_row = has_new && tb + r == a.pos;
 #pragma unroll
     for (int kk = 0; kk < NKC; ++kk) {
-      int4 kw = f.k[kk];
-      if (has_new) {                   // select values (a select of addresses would force f to memory)
-        const int4 kn = *reinterpret_cast<const int4*>(&sm.knew_b[32 * kk + 8 * qq]);
-        kw = make_int4(knew_row ? kn.x : kw.x, knew_row ? kn.y : kw.y, knew_row ? kn.z : kw.z,
-                       knew_row ? kn.w : kw.w);
-      }
-      const bf16x8_t af = __builtin_bit_cast(bf16x8_t, kw);
+      const bf16x8_t af = __builtin_bit_cast(bf16x8_t, f.k[kk]);
       sc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af, qh[kk], sc, 0, 0, 0);
       sc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af, ql[kk], sc, 0, 0, 0);
     }
@@ -605,15 +601,7 @@ __device__ __forceinline__ void attn_mfma_body(const AttnArgs& a, AttnMfmaSmem<D
     {
       int4 vw[RPG];
 #pragma unroll
-      for (int u = 0; u < RPG; ++u) {
-        vw[u] = f.v[u];
-        if (has_new) {
-          const bool vnew_row = tb + rg * RPG + u == a.pos;
-          const int4 vn = *reinterpret_cast<const int4*>(&sm.vnew_b[8 * c]);
-          vw[u] = make_int4(vnew_row ? vn.x : vw[u].x, vnew_row ? vn.y : vw[u].y,
-                            vnew_row ? vn.z : vw[u].z, vnew_row ? vn.w : vw[u].w);
-        }
-      }
+      for (int u = 0; u < RPG; ++u) vw[u] = f.v[u];
 #pragma unroll
       for (int dd = 0; dd < 8; ++dd) {
         const int dim = 8 * c + dd;
@@ -638,11 +626,11 @@ __device__ __forceinline__ void attn_mfma_body(const AttnArgs& a, AttnMfmaSmem<D
     float mx = -INFINITY;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      if (tb + 4 * qq + i >= t1) sc[i] = -INFINITY;
+      if (tb + 4 * qq + i >= tr) sc[i] = -INFINITY;
       mx = fmaxf(mx, sc[i]);
     }
     mx = col_max4(mx);
-    const float mn = fmaxf(m_run, mx);           // finite: row tb < t1 is in the tile
+    const float mn = fmaxf(m_run, mx);           // finite: row tb < tr is in the tile
     const float al = __builtin_amdgcn_exp2f(m_run - mn);
     float pr[4], ps = 0.0f;
 #pragma unroll
@@ -721,11 +709,33 @@ __device__ __forceinline__ void attn_mfma_body(const AttnArgs& a, AttnMfmaSmem<D
     for (int w = 0; w < 4; ++w) M = fmaxf(M, sm.wm[w][h]);
 #pragma unroll
     for (int w = 0; w < 4; ++w) {
-      const float sw = exp2f(sm.wm[w][h] - M);    // 0 for a wave without rows
+      // 0 for a wave without rows (and for every wave when the split has no cache rows)
+      const float sw = (M == -INFINITY) ? 0.0f : exp2f(sm.wm[w][h] - M);
       L = fmaf(sm.wl[w][h], sw, L);
       const float4 v = reinterpret_cast<const float4*>(&sm.wacc[w][h][0])[e4];
       A.x = fmaf(v.x, sw, A.x); A.y = fmaf(v.y, sw, A.y);
       A.z = fmaf(v.z, sw, A.z); A.w = fmaf(v.w, sw, A.w);
+    }
+  }
+  if (has_new) {
+    // the new row: its score against head h (the pre-scaled q times the BF16 key, this thread's
+    // 4 dims summed over the head's Q4 consecutive threads), then one online-softmax step
+    float p = 0.0f;
+    if (item) {
+      const float4 qv = reinterpret_cast<const float4*>(sm.q_s[h])[e4];
+      const uint2 kb = *reinterpret_cast<const uint2*>(&sm.knew_b[4 * e4]);
+      p = fmaf(qv.x, bf16_lo(kb.x), fmaf(qv.y, bf16_hi(kb.x), fmaf(qv.z, bf16_lo(kb.y), qv.w * bf16_hi(kb.y))));
+    }
+#pragma unroll
+    for (int off = 1; off < Q4; off <<= 1) p += __shfl_xor(p, off, kWave);
+    if (item) {
+      const uint2 vb = *reinterpret_cast<const uint2*>(&sm.vnew_b[4 * e4]);
+      const float Mn = fmaxf(M, p);
+      const float co = exp2f(M - Mn), cn = exp2f(p - Mn);     // co = 0 when M = -inf
+      L = fmaf(L, co, cn);
+      A.x = fmaf(A.x, co, cn * bf16_lo(vb.x)); A.y = fmaf(A.y, co, cn * bf16_hi(vb.x));
+      A.z = fmaf(A.z, co, cn * bf16_lo(vb.y)); A.w = fmaf(A.w, co, cn * bf16_hi(vb.y));
+      M = Mn;
     }
   }
   auto store4 = [&](const float4& v) {
