@@ -423,9 +423,8 @@ struct AttnMfmaSmem {
   uint2 vt[4][DH * 4];                 // per wave: units (dim, row group of 4) of the tile's V
   float wm[4][NHM], wl[4][NHM];
   float wacc[4][NHM][DH];              // per wave: unnormalised outputs
-  float mw[kMfmaMaxSplit][NHM];        // merge: per (split, head) max, then weight
-  float mlw[kMfmaMaxSplit][NHM];       // merge: per (split, head) weighted sum
-  float mmax[NHM];
+  float mw[kMfmaMaxSplit][NHM];        // merge: per (split, head) weight
+  float mlsum[NHM];                    // merge: per head, the weighted sum of the splits' sums
   float4 mpart[kBlock];                // merge: per-thread partial outputs
   int last;
 };
@@ -778,20 +777,25 @@ __device__ __forceinline__ void attn_mfma_body(const AttnArgs& a, AttnMfmaSmem<D
   __syncthreads();
   if (!sm.last) return;
   if (tid == 0) __hip_atomic_store(cnt, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  // merge (n_split <= kMfmaMaxSplit): (1) thread (split, head) reads that record's (max, sum); the
-  // per-head maximum M and every split's weight exp2(max - M) go to LDS; (2) thread (part, head,
-  // 4 dims) sums weighted accumulators over splits part, part + NPARTS, ... with all of its record
-  // loads in flight at once; (3) the parts and the weighted sums are added and divided.
+  // merge (n_split <= kMfmaMaxSplit): (1) thread (head, split) reads that record's (max, sum); the
+  // head's maximum M and the total of the sums weighted by exp2(max - M) are lane reductions, and
+  // every split's weight goes to LDS; (2) thread (part, head, 4 dims) sums weighted accumulators
+  // over splits part, part + NPARTS, ... with all of its record loads in flight at once; (3) the
+  // parts are added and divided by the head's total.
   constexpr int ITEMS = NH * Q4;
   constexpr int NPARTS = ITEMS * 4 <= kBlock ? 4 : (ITEMS * 2 <= kBlock ? 2 : 1);
   constexpr int PER_PART = kMfmaMaxSplit / NPARTS;
-  static_assert(kMfmaMaxSplit * NHM <= kBlock, "one (max, sum) per thread");
+  static_assert(kMfmaMaxSplit * NHM <= kBlock && kMfmaMaxSplit <= kWave &&
+                    (kMfmaMaxSplit & (kMfmaMaxSplit - 1)) == 0,
+                "one (max, sum) per thread, a head's records in one wave");
   const int part = tid / ITEMS, it = tid % ITEMS, mh = it / Q4, me4 = it % Q4;
   float4 av[PER_PART];
   {
-    // every record load of the merge is issued before the first use of any of them
-    const int ms = tid / NH, mhl = tid % NH;
-    const bool mi = ms < a.n_split;
+    // every record load of the merge is issued before the first use of any of them; thread
+    // (head mhl, split ms) = (tid / 32, tid % 32) takes that record's (max, sum), so each head's
+    // records sit in 32 consecutive lanes and their maximum and weighted sum are lane reductions
+    const int ms = tid & (kMfmaMaxSplit - 1), mhl = tid / kMfmaMaxSplit;
+    const bool mi = ms < a.n_split && mhl < NH;
     const float2 ml = __builtin_bit_cast(
         float2, buf_load8_device(rp, mi ? uint32_t((ms * kMaxHeads + mhl) * PS * 4) : kOOB));
 #pragma unroll
@@ -802,19 +806,15 @@ __device__ __forceinline__ void attn_mfma_body(const AttnArgs& a, AttnMfmaSmem<D
                                             ? uint32_t((mq * kMaxHeads + mh) * PS * 4 + 16 + me4 * 16)
                                             : kOOB));
     }
-    if (mi) sm.mw[ms][mhl] = ml.x;
-    __syncthreads();
-    if (tid < NH) {
-      float mm = -INFINITY;
-      for (int q = 0; q < a.n_split; ++q) mm = fmaxf(mm, sm.mw[q][tid]);
-      sm.mmax[tid] = mm;
-    }
-    __syncthreads();
-    if (mi) {
-      const float w = exp2f(ml.x - sm.mmax[mhl]);
-      sm.mw[ms][mhl] = w;
-      sm.mlw[ms][mhl] = ml.y * w;
-    }
+    float mm = mi ? ml.x : -INFINITY;
+#pragma unroll
+    for (int off = 1; off < kMfmaMaxSplit; off <<= 1) mm = fmaxf(mm, __shfl_xor(mm, off, kWave));
+    const float w = mi ? exp2f(ml.x - mm) : 0.0f;        // every split has rows: mm is finite
+    float lw = ml.y * w;
+#pragma unroll
+    for (int off = 1; off < kMfmaMaxSplit; off <<= 1) lw += __shfl_xor(lw, off, kWave);
+    if (mi) sm.mw[ms][mhl] = w;
+    if (ms == 0 && mhl < NH) sm.mlsum[mhl] = lw;
     __syncthreads();
   }
   if (part < NPARTS) {
@@ -836,9 +836,7 @@ __device__ __forceinline__ void attn_mfma_body(const AttnArgs& a, AttnMfmaSmem<D
       const float4 u = sm.mpart[pp * ITEMS + tid];
       v.x += u.x; v.y += u.y; v.z += u.z; v.w += u.w;
     }
-    float lsum = 0.0f;
-    for (int q = 0; q < a.n_split; ++q) lsum += sm.mlw[q][mh];
-    const float inv = 1.0f / lsum;
+    const float inv = 1.0f / sm.mlsum[mh];
     store4(make_float4(v.x * inv, v.y * inv, v.z * inv, v.w * inv));   // h == mh, e4 == me4 here
   }
 }
