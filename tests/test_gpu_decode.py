@@ -180,9 +180,9 @@ def test_positions_and_split_boundaries(pos):
 
 @pytest.mark.parametrize("pos", [1087, 1088, 1500, 2047, 2175, 3000, 4095, 4097])
 def test_long_context_splits(pos):
-    """Past 32 splits of 64 rows the batch-1 attention takes splits of multiples of 128 rows,
-    the remainder in the last split: ragged last splits, 17 to 32 splits, one to three tiles per
-    wave, head_dim 64 and 128. The new token's row is folded into the last split after its tiles,
+    """From 256 rows on the batch-1 attention takes splits of at least 128 rows (multiples of 64,
+    at most 32 splits), the remainder in the last split: ragged last splits, 17 to 32 splits, two
+    to four tiles per wave, head_dim 64 and 128. The new token's row is folded into the last split after its tiles,
     whether the cached rows fill those tiles (4095: 127 rows) or spill into one more (4097)."""
     _flush(f"case long context pos={pos}")
     for sh in (SMALL, synth.tiny_shape(d=512, hq=8, hkv=2, dh=128, f=1024, layers=1)):
