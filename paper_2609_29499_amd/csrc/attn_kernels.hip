@@ -959,8 +959,27 @@ void attn_mfma_split(int total, int* chunk, int* n_split) {
   *chunk = kMfmaChunk * k;
   *n_split = std::max(1, total / *chunk);
 }
+void attn_mfma_split_batched(int total, int units, int* chunk, int* n_split) {
+  // a batch: about one workgroup per CU over all (sequence, group slot) units. The cache rows
+  // (total - 1; the new one is folded into the last split) are cut into splits of a multiple of
+  // 64 rows, at least 128 once the context holds 256, the last one shorter. At 8 sequences of
+  // 8192 positions: 4 splits of 2048 rows.
+  const int cached = total - 1;
+  const int n64 = total / kMfmaChunk;
+  if (n64 <= 1 || units >= kNumCu) {
+    attn_mfma_split(total, chunk, n_split);
+    return;
+  }
+  const int target = std::max(1, std::min(kNumCu / std::max(units, 1), kMfmaTargetSplits));
+  int rows = (cached + target - 1) / target;
+  rows = (rows + kMfmaChunk - 1) / kMfmaChunk * kMfmaChunk;
+  if (rows < 2 * kMfmaChunk && n64 >= 4) rows = 2 * kMfmaChunk;
+  *chunk = rows;
+  *n_split = std::max(1, (cached + rows - 1) / rows);
+}
 int attn_mfma_max_split(int max_seq) {
-  return std::max(1, std::min(max_seq / kMfmaChunk, kMfmaTargetSplits));
+  // both rules split total <= max_seq rows into at most ceil(total / 64) and at most 32 splits
+  return std::max(1, std::min((max_seq + kMfmaChunk - 1) / kMfmaChunk, kMfmaTargetSplits));
 }
 int attn_max_split() { return kMaxSplit; }
 int attn_resident_blocks(int dh, int nhm) {

@@ -248,8 +248,10 @@ constexpr int kAttnMfma = 1;       // matrix-core scores, short splits (attn_mfm
 // finish merges the partials into o by log-sum-exp (n_split == 1 writes o directly).
 hipError_t launch_attn_decode(const AttnArgs& a, hipStream_t s);
 int attn_min_chunk();   // rows per split are a multiple of this
-// split rows and count of the matrix-core kernel for total = pos + 1 attended rows
+// split rows and count of the matrix-core kernel for total = pos + 1 attended rows: one sequence,
+// and `units` (sequences x retained group slots) of a batch
 void attn_mfma_split(int total, int* chunk, int* n_split);
+void attn_mfma_split_batched(int total, int units, int* chunk, int* n_split);
 int attn_mfma_max_split(int max_seq);   // largest split count it uses for up to max_seq rows
 int attn_max_split();
 // decode-attention workgroups resident on the chip at once when the largest retained group of

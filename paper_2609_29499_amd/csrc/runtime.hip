@@ -555,11 +555,13 @@ tasp::AttnArgs attn_args(const tasp_plan_s* p, int l, const tasp_kv_cache* cache
   a.rope_sin = p->rope_sin; a.pos = pos; a.part = p->part; a.cnt = p->acnt;
   a.o = p->o_buf; a.ld_o = p->ld_obuf; a.B = B;
   if (hl) { a.o_hl = p->xo; a.ld_ohl = p->ld_xo; }
-  if (B == 1) {
-    // one sequence: the matrix-core kernel with short splits (many more workgroups than group
-    // slots x resident splits of the VALU kernel)
+  {
+    // the matrix-core kernel: one sequence with short splits (many more workgroups than group
+    // slots x resident splits of the VALU kernel); a batch with about one workgroup per CU over
+    // its (sequence, group slot) units
     int chunk = 0, n_split = 0;
-    tasp::attn_mfma_split(total, &chunk, &n_split);
+    if (B == 1) tasp::attn_mfma_split(total, &chunk, &n_split);
+    else tasp::attn_mfma_split_batched(total, B * P.m_kv, &chunk, &n_split);
     a.kernel = tasp::kAttnMfma;
     a.chunk = chunk;
     a.n_split = n_split;
