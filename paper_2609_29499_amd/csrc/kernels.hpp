@@ -240,23 +240,15 @@ struct AttnArgs {
   float* o; int ld_o;              // [B][ld_o] retained heads in ascending order
   uint16_t* o_hl; int ld_ohl;      // when set: o as the hi/lo BF16 operand [16][ld_ohl] instead
   int B;
-  int kernel;                      // kAttnValu or kAttnMfma (split rules: attn_mfma_split)
 };
-constexpr int kAttnValu = 0;       // VALU scores, splits of multiples of attn_min_chunk() rows
-constexpr int kAttnMfma = 1;       // matrix-core scores, short splits (attn_mfma_split)
-// Split-KV partial attention; for n_split > 1 the last split of each (group slot, sequence) to
-// finish merges the partials into o by log-sum-exp (n_split == 1 writes o directly).
+// Split-KV attention on the matrix cores; for n_split > 1 the last split of each (group slot,
+// sequence) to finish merges the partials into o by log-sum-exp (n_split == 1 writes o directly).
 hipError_t launch_attn_decode(const AttnArgs& a, hipStream_t s);
-int attn_min_chunk();   // rows per split are a multiple of this
 // split rows and count of the matrix-core kernel for total = pos + 1 attended rows: one sequence,
 // and `units` (sequences x retained group slots) of a batch
 void attn_mfma_split(int total, int* chunk, int* n_split);
 void attn_mfma_split_batched(int total, int units, int* chunk, int* n_split);
 int attn_mfma_max_split(int max_seq);   // largest split count it uses for up to max_seq rows
-int attn_max_split();
-// decode-attention workgroups resident on the chip at once when the largest retained group of
-// the launch keeps nhm query heads (head dimension dh)
-int attn_resident_blocks(int dh, int nhm);
 
 // ----------------------------------------------------------------- router
 

@@ -164,9 +164,7 @@ template <class Take>
 void scratch_layout(Layout& Y, const tasp_model_desc* d, Take&& take, size_t& off) {
   const int D = d->d_model, Hq = d->n_q_heads, Hkv = d->n_kv_heads;
   const int dh = d->head_dim, F = d->d_ffn, B = d->max_batch;
-  Y.n_split_max = std::max(std::min((d->max_seq + tasp::attn_min_chunk() - 1) / tasp::attn_min_chunk(),
-                                    tasp::attn_max_split()),
-                           tasp::attn_mfma_max_split(d->max_seq));
+  Y.n_split_max = tasp::attn_mfma_max_split(d->max_seq);
   Y.ld_qkv = (Hq + 2 * Hkv) * dh;
   Y.ld_obuf = Hq * dh;
   Y.ld_h = round_up16(F);
@@ -555,42 +553,10 @@ tasp::AttnArgs attn_args(const tasp_plan_s* p, int l, const tasp_kv_cache* cache
   a.rope_sin = p->rope_sin; a.pos = pos; a.part = p->part; a.cnt = p->acnt;
   a.o = p->o_buf; a.ld_o = p->ld_obuf; a.B = B;
   if (hl) { a.o_hl = p->xo; a.ld_ohl = p->ld_xo; }
-  {
-    // the matrix-core kernel: one sequence with short splits (many more workgroups than group
-    // slots x resident splits of the VALU kernel); a batch with about one workgroup per CU over
-    // its (sequence, group slot) units
-    int chunk = 0, n_split = 0;
-    if (B == 1) tasp::attn_mfma_split(total, &chunk, &n_split);
-    else tasp::attn_mfma_split_batched(total, B * P.m_kv, &chunk, &n_split);
-    a.kernel = tasp::kAttnMfma;
-    a.chunk = chunk;
-    a.n_split = n_split;
-    return a;
-  }
-  // Batches, VALU kernel. Split rows: as short as keeps every workgroup of the launch resident at
-  // once (a workgroup that waits for a free slot runs a whole split after the others), in
-  // multiples of the kernel's sub-block pair, within the merge's split limit. Two ways to cover
-  // the rows: the last split takes the remainder on its own (ceil), or the remainder joins the
-  // last full split (floor); the one with the shorter longest split is taken, the separate
-  // remainder on a tie.
-  const long sub = tasp::attn_min_chunk();
-  int nhm = 1;
-  for (int q = 0; q < P.m_kv; ++q) nhm = std::max(nhm, P.slot_start[q + 1] - P.slot_start[q]);
-  const long per_split = std::max<long>(1, long(P.m_kv) * B);
-  const long smax = std::max<long>(
-      1, std::min<long>(tasp::attn_resident_blocks(d.head_dim, nhm) / per_split,
-                        tasp::attn_max_split()));
-  auto round_up = [&](long r) { return (std::max(r, sub) + sub - 1) / sub * sub; };
-  const long chunk_c = round_up((total + smax - 1) / smax);       // ceil(total / chunk) <= smax
-  const long chunk_f = round_up(total / (smax + 1) + 1);          // floor(total / chunk) <= smax
-  const long split_f = std::max<long>(1, total / chunk_f);
-  const long longest_f = total - (split_f - 1) * chunk_f;
-  const bool floor_wins = longest_f < std::min<long>(chunk_c, total);
-  const long chunk = floor_wins ? chunk_f : chunk_c;
-  const long n_split = floor_wins ? split_f : (total + chunk_c - 1) / chunk_c;
-  a.kernel = tasp::kAttnValu;
-  a.chunk = int(chunk);
-  a.n_split = int(n_split);
+  // one sequence: short splits (many more workgroups than group slots); a batch: about one
+  // workgroup per CU over its (sequence, group slot) units
+  if (B == 1) tasp::attn_mfma_split(total, &a.chunk, &a.n_split);
+  else tasp::attn_mfma_split_batched(total, B * P.m_kv, &a.chunk, &a.n_split);
   return a;
 }
 

@@ -28,7 +28,7 @@ COPY_BYTES = 1 << 30
 
 def kind_of(name: str) -> str | None:
     rules = [
-        (r"attn_decode_kernel|attn_mfma_kernel", "attention"),
+        (r"attn_mfma_kernel", "attention"),
         (r"pf_attn_kernel", "prefill_attention"),
         (r"pf_rope_kernel", "rope_append"),
         (r"pf_prep_kernel|mfma_prep_kernel", "operand_prep"),
