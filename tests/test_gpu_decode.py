@@ -212,6 +212,19 @@ def test_batched_tiny_layer(batch):
     _check_cache_rows(case)
 
 
+@pytest.mark.parametrize("batch,pos", [(2, 255), (2, 256), (3, 1000), (5, 2049), (7, 3001), (2, 4096)])
+def test_batched_attention_splits(batch, pos):
+    """Batched attention splits the cache rows over about one workgroup per CU: split lengths of
+    64-row multiples with a short last split (or none besides the new row), from one split to
+    32, head_dim 64 and 128."""
+    for sh in (SMALL, SMALL128):
+        _flush(f"case batched splits batch={batch} pos={pos} dh={sh.head_dim}")
+        case, got, want = _decode_case(sh, synth.raw_mask(sh, 12, p_q=0.7, p_kv=0.9), batch, pos,
+                                       max_seq=pos + 1)
+        assert_parity(got, want, what=f"batched splits {batch} x {pos} dh {sh.head_dim}")
+        _check_cache_rows(case)
+
+
 @pytest.mark.parametrize("pos", [0, 1, 129, 511])
 def test_batched_positions(pos):
     _flush(f"case batched pos={pos}")
