@@ -246,6 +246,102 @@ def device_layer(torch, sh, gen):
     return out
 
 
+def device_group_layer(torch, sh, gen):
+    """One decoder layer of the groupwise store drawn on the GPU: N(0, 0.02) weights quantised to
+    INT8 with one BF16 scale per row and 128 inputs (max |w| of the group / 127, rounded to BF16
+    before quantising), BF16(1 + 0.1 N(0, 1)) gains; scales as int16 bit patterns."""
+    qd, kd, d, f = sh.n_q_heads * sh.head_dim, sh.n_kv_heads * sh.head_dim, sh.d_model, sh.d_ffn
+    out = {}
+    for name, (rows, cols) in (("wq", (qd, d)), ("wk", (kd, d)), ("wv", (kd, d)), ("wo", (d, qd)),
+                               ("wg", (f, d)), ("wu", (f, d)), ("wd", (d, f))):
+        w = (torch.randn(rows, cols, generator=gen, device="cuda") * 0.02).view(rows, cols // 128, 128)
+        s = (w.abs().amax(dim=2) / 127.0).clamp_min(1e-30).to(torch.bfloat16)
+        q = torch.round(w / s.float()[:, :, None]).clamp_(-127, 127).to(torch.int8).view(rows, cols)
+        out[name] = (q, s.view(torch.int16).contiguous())
+        del w
+    for name in ("attn_norm", "ffn_norm"):
+        g = (1.0 + 0.1 * torch.randn(d, generator=gen, device="cuda")).to(torch.bfloat16)
+        out[name] = g.view(torch.int16)
+    return out
+
+
+def bench_shared_stack(args, wl):
+    """Batch-1 decode of a full stack from one shared groupwise store: every plan (the seed mask,
+    then the dense plan) indexes the same store through its maps and owns no weight bytes. Per
+    plan: args.warmup graph replays, args.steps timed, then args.blocks blocks of
+    args.block_warmup + args.block_steps replays."""
+    import torch
+    import synth
+    from paper_2609_29499_amd import binding as B
+    from paper_2609_29499_amd import session as S
+    sh, pos = wl.shape, wl.pos
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(0)
+    t0 = time.time()
+    layers = [device_group_layer(torch, sh, gen) for _ in range(sh.n_layers)]
+    fnorm = (1.0 + 0.1 * torch.randn(sh.d_model, generator=gen, device="cuda")).to(torch.bfloat16).view(torch.int16)
+    lm = (0.02 * torch.randn(sh.vocab, sh.d_model, generator=gen, device="cuda")).to(torch.bfloat16).view(torch.int16)
+    store = S.GroupStore(layers, fnorm, lm)
+    del layers
+    desc = S.desc_from_shape(sh, max_batch=1, max_seq=pos + 1)
+    torch.cuda.synchronize()
+    print(f"[bench] {wl.name}: store {store.nbytes() / 1e9:.1f} GB drawn in {time.time() - t0:.1f}s",
+          file=sys.stderr, flush=True)
+    x = torch.randn(1, sh.d_model, generator=gen, device="cuda").to(torch.bfloat16).float()
+    out = torch.empty(1, sh.vocab, device="cuda")
+    scratch = S.SharedScratch(desc)
+    plans = [(f"mask{sd}", synth.budget_mask(sh, sd)) for sd in wl.mask_seeds] + [("dense", None)]
+    rows = []
+    for name, m in plans:
+        plan = S.Plan.shared(desc, store, m, scratch=scratch)
+        cache = S.KVCache(desc, 1, pos + 1)
+        for l in range(sh.n_layers):
+            cache.k[l, :, :, :pos].normal_(generator=gen)
+            cache.v[l, :, :, :pos].normal_(generator=gen)
+        plan.bind(cache)
+        for _ in range(3):
+            plan.decode(x, cache, pos, out)
+        torch.cuda.synchronize()
+        g = _graph_of(torch, S, plan, x, cache, pos, out)
+        for _ in range(args.warmup):
+            g.replay()
+        ms = _time_replays(torch, g, args.steps)
+        blocks = []
+        for _ in range(args.blocks):
+            for _ in range(args.block_warmup):
+                g.replay()
+            blocks.append(_time_replays(torch, g, args.block_steps))
+        bmean = float(np.mean(blocks)) if blocks else ms
+        rows.append({"plan": name, "ms_per_token": round(bmean, 5), "ms_per_step": round(ms, 5),
+                     "blocks_ms": [round(b, 5) for b in blocks],
+                     "plan_workspace_MB": round(plan.ws_bytes / 1e6, 3),
+                     "active_flop_ratio": round(plan.ledger()["active_flop_ratio"], 4)})
+        print(f"[bench] {name}: {bmean:.4f} ms/token (blocks), {ms:.4f} (timed steps)",
+              file=sys.stderr, flush=True)
+        del cache, g, plan
+        torch.cuda.empty_cache()
+    sp, dn = rows[0], rows[-1]
+    line = {
+        "metric": METRIC, "value": sp["ms_per_token"], "unit": "ms/token", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": sp["ms_per_step"],
+        "higher_is_better": False, "scaling": "weak", "vs_baseline": None, "dtype": "int8w-g128-f32",
+        "data": "synthetic",
+        "config": {"workload": wl.name, "d_model": sh.d_model, "layers": sh.n_layers, "batch": 1,
+                   "pos": pos, "mask_seed": wl.mask_seeds[0], "vocab": sh.vocab,
+                   "scales": "BF16 per 128 inputs"},
+        "dense_ms_per_token": dn["ms_per_token"],
+        "speedup_vs_dense": round(dn["ms_per_token"] / sp["ms_per_token"], 4),
+        "plans": rows,
+        "memory_GB": {"store_with_scales_gains_and_lm_head": round(store.nbytes() / 1e9, 2),
+                      "shared_scratch": round(scratch.bytes / 1e9, 3)},
+        "roofline": None, "cpu_baseline": None,
+        "paper_context": "one packed store serves every mask; a mask owns no weight bytes (appendix "
+                         "'Backing-store semantics')",
+        "manifest": run_manifest(),
+    }
+    print(json.dumps(line), flush=True)
+
+
 def _graph_of(torch, S, plan, x, cache, pos, out):
     """A HIP graph holding one decode step of `plan` (captured on a side stream after a warm
     launch)."""
@@ -1113,7 +1209,7 @@ def main():
         bench_router(args, wl)
         return
     if wl.kind == "shared":
-        bench_shared(args, wl)
+        (bench_shared_stack if sh.n_layers > 1 else bench_shared)(args, wl)
         return
     if sh.n_layers > 1 and wl.batch == 1 and wl.prefill_tokens == 0:
         bench_stack(args, wl)

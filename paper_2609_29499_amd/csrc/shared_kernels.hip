@@ -41,12 +41,15 @@ __device__ __forceinline__ float dot_bytes(uint32_t word, const float4& x, float
   return acc;
 }
 
-template <int MODE>
-__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) void shared_gemv_kernel(
+// NW waves per workgroup: 4, or 8 where the staged input leaves room for fewer than four
+// workgroups per CU (the same waves per CU with half the staging)
+template <int MODE, int NW>
+__global__ __launch_bounds__(NW * kWave) __attribute__((amdgpu_waves_per_eu(4))) void shared_gemv_kernel(
     SharedGemvArgs a) {
   constexpr bool NORM = (MODE != GEMV_RESID);
   extern __shared__ __attribute__((aligned(16))) float lds[];
-  __shared__ float red[4];
+  __shared__ float red[NW];
+  constexpr int NT = NW * kWave;
   const int K = a.K, N = a.N;
   const int KP = (K + 1023) & ~1023;
   const int NP = KP >> 4;                                 // pieces staged
@@ -54,8 +57,8 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) voi
   float* xsum = lds + KP;                                 // [NP] sums of the pieces' inputs
   int* cmap = reinterpret_cast<int*>(xsum + NP);          // [NP] store column of each piece
   const int tid = threadIdx.x, lane = tid & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(blockIdx.x * (kBlock / kWave) + (tid >> 6));
-  const int nwaves = gridDim.x * (kBlock / kWave);
+  const int wave = __builtin_amdgcn_readfirstlane(blockIdx.x * NW + (tid >> 6));
+  const int nwaves = gridDim.x * NW;
   const int nchunks = (K + 1023) >> 10;
   const int KB = max(1, (nchunks + kC - 1) / kC);
   const int per_group = (MODE == GEMV_GATEUP) ? kCH : kR;
@@ -129,7 +132,8 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) voi
     // down projection's retained channels in one batch)
     constexpr int kSB = NORM ? 8 : 12;
     const int n4 = K >> 2;
-    const int npass = KP >> 10;                          // one float4 per thread per pass
+    const int n4p = KP >> 2;                             // float4 slots staged
+    const int npass = (n4p + NT - 1) / NT;               // one float4 per thread per pass
     const __amdgpu_buffer_rsrc_t rx = make_rsrc(a.x, uint32_t(n4) * 16u);
     const __amdgpu_buffer_rsrc_t rg = make_rsrc(a.gamma, uint32_t(NORM ? K : 0) * 2u);
     float ss = 0.0f;
@@ -139,7 +143,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) voi
     auto load_batch = [&](int i0) {
 #pragma unroll
       for (int u = 0; u < kSB; ++u) {
-        const int c4 = ((i0 + u) << 8) + tid;          // float4 slot; piece c4 / 4
+        const int c4 = (i0 + u) * NT + tid;            // float4 slot; piece c4 / 4
         const bool ok = i0 + u < npass && c4 < n4;
         xv[u] = buf_load16(rx, ok ? uint32_t(c4) * 16u : kOOB);
         if constexpr (NORM)
@@ -151,7 +155,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) voi
     auto store_batch = [&](int i0) {
 #pragma unroll
       for (int u = 0; u < kSB; ++u) {
-        const int c4 = ((i0 + u) << 8) + tid;
+        const int c4 = (i0 + u) * NT + tid;
         float4 v = __builtin_bit_cast(float4, xv[u]);
         if constexpr (NORM) {
           ss = fmaf(v.x, v.x, fmaf(v.y, v.y, fmaf(v.z, v.z, fmaf(v.w, v.w, ss))));
@@ -164,7 +168,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) voi
         float p = (v.x + v.y) + (v.z + v.w);
         p += dpp<kQuadXor1>(p);
         p += dpp<kQuadXor2>(p);
-        if (i0 + u < npass) {
+        if (i0 + u < npass && (NT == 256 || c4 < n4p)) {   // 256 threads: passes end at KP
           *reinterpret_cast<float4*>(xs + xs_slot_i8(c4 << 2)) = v;
           if ((tid & 3) == 0) {
             xsum[c4 >> 2] = p;
@@ -186,7 +190,10 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) voi
     }
     __syncthreads();
   }
-  const float xscale = NORM ? rsqrtf((red[0] + red[1] + red[2] + red[3]) / float(K) + a.eps) : 1.0f;
+  float red_sum = 0.0f;
+#pragma unroll
+  for (int w = 0; w < NW; ++w) red_sum += red[w];
+  const float xscale = NORM ? rsqrtf(red_sum / float(K) + a.eps) : 1.0f;
 
   float acc[kR], res[kR];
   auto process = [&](const int4 (&w)[kC][kR], const uint32_t (&sv)[kC][kR], int t) {
@@ -248,14 +255,23 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) voi
   }
 }
 
-template <int MODE>
-hipError_t launch_shared_mode(const SharedGemvArgs& a, int grid, size_t lds, hipStream_t s) {
+template <int MODE, int NW>
+hipError_t launch_shared_nw(const SharedGemvArgs& a, int grid, size_t lds, hipStream_t s) {
   static const hipError_t attr = hipFuncSetAttribute(
-      reinterpret_cast<const void*>(&shared_gemv_kernel<MODE>),
+      reinterpret_cast<const void*>(&shared_gemv_kernel<MODE, NW>),
       hipFuncAttributeMaxDynamicSharedMemorySize, int(kMaxSharedGemvLds));
   if (attr != hipSuccess) return attr;
-  hipLaunchKernelGGL((shared_gemv_kernel<MODE>), dim3(grid), dim3(kBlock), lds, s, a);
+  hipLaunchKernelGGL((shared_gemv_kernel<MODE, NW>), dim3(grid), dim3(NW * kWave), lds, s, a);
   return hipGetLastError();
+}
+
+template <int MODE>
+hipError_t launch_shared_mode(const SharedGemvArgs& a, int groups, int per_cu, size_t lds, hipStream_t s) {
+  // one wave per group up to the workgroups resident at once; past that, waves take several
+  // groups each
+  const int nw = per_cu < kWgPerCu ? 8 : 4;
+  const int grid = std::max(1, std::min((groups + nw - 1) / nw, kNumCu * per_cu));
+  return nw == 8 ? launch_shared_nw<MODE, 8>(a, grid, lds, s) : launch_shared_nw<MODE, 4>(a, grid, lds, s);
 }
 
 // the retained rows and column pieces of every layer in store coordinates (one workgroup per
@@ -297,15 +313,13 @@ hipError_t launch_shared_gemv(GemvMode mode, const SharedGemvArgs& a, hipStream_
   const size_t lds = shared_gemv_lds_bytes(a.K);
   if (lds > kMaxSharedGemvLds) return hipErrorInvalidValue;
   const int per_group = (mode == GEMV_GATEUP) ? kCH : kR;
-  // one wave per group up to the workgroups resident at once (fewer when the staged input limits
-  // them to less than kWgPerCu per CU); past that, waves take several groups each
+  // workgroups resident per CU: kWgPerCu, fewer when the staged input limits them
   const int groups = (a.N + per_group - 1) / per_group;
   const int per_cu = std::max(1, std::min(kWgPerCu, int((160 * 1024) / (lds + 64))));
-  const int grid = std::max(1, std::min((groups + 3) / 4, kNumCu * per_cu));
   switch (mode) {
-    case GEMV_QKV: return launch_shared_mode<GEMV_QKV>(a, grid, lds, s);
-    case GEMV_RESID: return launch_shared_mode<GEMV_RESID>(a, grid, lds, s);
-    case GEMV_GATEUP: return launch_shared_mode<GEMV_GATEUP>(a, grid, lds, s);
+    case GEMV_QKV: return launch_shared_mode<GEMV_QKV>(a, groups, per_cu, lds, s);
+    case GEMV_RESID: return launch_shared_mode<GEMV_RESID>(a, groups, per_cu, lds, s);
+    case GEMV_GATEUP: return launch_shared_mode<GEMV_GATEUP>(a, groups, per_cu, lds, s);
     default: return hipErrorInvalidValue;
   }
 }

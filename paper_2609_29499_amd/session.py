@@ -68,27 +68,35 @@ class DeviceStore:
 class GroupStore:
     """The packed groupwise store on the device. ``layers`` is a list of dicts ``name: (int8
     [out][in], BF16 scale bits uint16 [out][in / 128])`` for wq, wk, wv, wo, wg, wu, wd plus the
-    two gains; wq, wk and wv are stacked into the store's QKV matrix (layout only)."""
+    two gains; wq, wk and wv are stacked into the store's QKV matrix (layout only). A layer may
+    also be given as device tensors with the same keys (scale bits as int16)."""
 
     def __init__(self, layers, final_norm=None, lm_head=None, device="cuda"):
         self.tensors = []
         arr = (B.tasp_glayer * len(layers))()
         for i, lay in enumerate(layers):
             keep = {}
-            qkv = (np.concatenate([lay["wq"][0], lay["wk"][0], lay["wv"][0]]),
-                   np.concatenate([lay["wq"][1], lay["wk"][1], lay["wv"][1]]))
+            on_dev = torch.is_tensor(lay["wq"][0])
+            cat = torch.cat if on_dev else np.concatenate
+            qkv = (cat([lay["wq"][0], lay["wk"][0], lay["wv"][0]]),
+                   cat([lay["wq"][1], lay["wk"][1], lay["wv"][1]]))
             for n, (w, sc) in (("wqkv", qkv), ("wo", lay["wo"]), ("wg", lay["wg"]),
                                ("wu", lay["wu"]), ("wd", lay["wd"])):
-                w, sc = _dev(w, device), _dev(np.ascontiguousarray(sc, np.uint16).view(np.int16), device)
+                if on_dev:
+                    w, sc = w.contiguous(), sc.contiguous().view(torch.int16)
+                else:
+                    w, sc = _dev(w, device), _dev(np.ascontiguousarray(sc, np.uint16).view(np.int16), device)
                 keep[n] = (w, sc)
                 setattr(arr[i], n, B.tasp_gqmat(w.data_ptr(), sc.data_ptr()))
             for n in ("attn_norm", "ffn_norm"):
-                g = _dev(lay[n], device)
+                g = lay[n] if torch.is_tensor(lay[n]) else _dev(lay[n], device)
                 keep[n] = g
                 setattr(arr[i], n, g.data_ptr())
             self.tensors.append(keep)
-        self.final_norm = None if final_norm is None else _dev(final_norm, device)
-        self.lm_head = None if lm_head is None else _dev(lm_head, device)
+        self.final_norm = None if final_norm is None else (
+            final_norm if torch.is_tensor(final_norm) else _dev(final_norm, device))
+        self.lm_head = None if lm_head is None else (
+            lm_head if torch.is_tensor(lm_head) else _dev(lm_head, device))
         self._layers = arr
         self.struct = B.tasp_gstore(arr, self.final_norm.data_ptr() if self.final_norm is not None else None,
                                     self.lm_head.data_ptr() if self.lm_head is not None else None)

@@ -100,6 +100,10 @@ WORKLOADS = {
     # 2048 prior positions, seed-1 mask
     "llama3_8b_layer_shared": Workload("llama3_8b_layer_shared", LLAMA3_8B.with_layers(1, vocab=0),
                                        batch=1, pos=2048, mask_seeds=(1,), kind="shared"),
+    # the 80-layer 70B-shaped stack from one shared groupwise store (plans own no weight bytes),
+    # batch 1, 4096 prior positions: seed-1 mask and the dense plan
+    "llama3_70b_stack_shared": Workload("llama3_70b_stack_shared", LLAMA3_70B, batch=1, pos=4096,
+                                        mask_seeds=(1,), kind="shared"),
     # one 8B-shaped layer: batch-8 decode, every sequence at 8192 prior positions
     "llama3_8b_batch8": Workload("llama3_8b_batch8", LLAMA3_8B.with_layers(1, vocab=0),
                                  batch=8, pos=8192, mask_seeds=(1,)),
