@@ -36,9 +36,9 @@ def kind_of(name: str) -> str | None:
         (r"gemv_kernel<1, 2[,>]", "gateup_gemv"),
         (r"gemv_kernel<1, 1[,>]", "resid_gemv"),
         (r"gemv_kernel<1, 3[,>]", "lmhead_gemv"),
-        (r"shared_gemv_kernel<0>", "qkv_shared"),
-        (r"shared_gemv_kernel<2>", "gateup_shared"),
-        (r"shared_gemv_kernel<1>", "resid_shared"),
+        (r"shared_gemv_kernel<0[,>]", "qkv_shared"),
+        (r"shared_gemv_kernel<2[,>]", "gateup_shared"),
+        (r"shared_gemv_kernel<1[,>]", "resid_shared"),
         (r"shared_maps_kernel", "shared_maps"),
         (r"mfma_gemv_kernel<0,", "qkv_mfma"),
         (r"mfma_gemv_kernel<2,", "gateup_mfma"),
