@@ -251,11 +251,10 @@ def test_batched_tall_panels():
 
 @pytest.mark.parametrize("pos", [511, 512, 640])
 def test_attention_splits_sized_to_residency(pos):
-    """Eight sequences over eight groups of eight heads (head dimension 128): 64 attention
-    workgroups per split index, so the residency bound, not the 128-row minimum, sets the split
-    length. With 256 resident workgroups (one per CU at this kernel's register use), 512 rows
-    fill four splits exactly, 513 rows put the extra row into the last split (129 rows), and
-    641 rows take three 256-row splits, the last one short."""
+    """Eight sequences over eight groups of eight heads (head dimension 128): 64 (sequence, group)
+    units, so the batched split rule takes four splits (about one workgroup per CU). 511 cache
+    rows make four 128-row splits, the last one short; 512 fill them exactly (the new row folded
+    into the last); 640 take three 192-row splits and a 64-row one."""
     _flush(f"case attention splits pos={pos}")
     sh = synth.tiny_shape(d=8192, hq=64, hkv=8, dh=128, f=512, theta=500000.0)
     q, kv, f = synth.all_kept_mask(sh)
